@@ -1,0 +1,190 @@
+"""Test infrastructure only: ctypes wrapper around the plain C oracle.
+
+Only tests/, ``__graft_entry__.smoke()`` and the bench's CPU-baseline leg may import
+this package. The product path (``paper_2404_09267_amd``) never does, and the two
+share no code: the only common module is the seeded input generator, which holds
+none of the method's arithmetic.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle.so")
+SOURCES = [os.path.join(HERE, "tg_oracle.c")]
+
+SHELF_FFDH, SHELF_ARRIVAL, GUILLOTINE_BSSF = 0, 1, 2
+OK, E_INVAL, E_ROI_OOB, E_ROI_TOO_LARGE, E_RANGE = 0, 1, 2, 3, 4
+ERROR_NAMES = {OK: "ok", E_INVAL: "inval", E_ROI_OOB: "roi_oob",
+               E_ROI_TOO_LARGE: "roi_too_large", E_RANGE: "range"}
+
+DET_DTYPE = np.dtype([("box", "<i4"), ("roi", "<i4"), ("frame", "<i4"),
+                      ("x1", "<f4"), ("y1", "<f4"), ("x2", "<f4"), ("y2", "<f4")])
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (always, when ``force``)."""
+    if force or not os.path.exists(LIB_PATH):
+        cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC",
+               "-shared", "-Wall", "-Wextra", "-o", LIB_PATH + ".tmp", *SOURCES, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    return LIB_PATH
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        _lib = ctypes.CDLL(LIB_PATH)
+        _declare(_lib)
+    return _lib
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+
+
+def _declare(L):
+    L.oracle_half_from_double.argtypes = [ctypes.c_double]
+    L.oracle_half_from_double.restype = ctypes.c_uint16
+    L.oracle_norm_table.argtypes = [_P, _P, _P]
+    L.oracle_norm_table.restype = None
+    L.oracle_pack.argtypes = [_P, _I32, _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P]
+    L.oracle_pack.restype = ctypes.c_int
+    L.oracle_guillotine_free.argtypes = [_P, _I32, _I32, _I32, _P, _I32]
+    L.oracle_guillotine_free.restype = _I32
+    L.oracle_check_plan.argtypes = [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _I32]
+    L.oracle_check_plan.restype = ctypes.c_int
+    L.oracle_stitch.argtypes = [_P, _I64, _I32, _P, _P, _P, _P, _I32, _I32, _I32, _I32, _I32,
+                                _P, _P, _P, _P]
+    L.oracle_stitch.restype = ctypes.c_int
+    L.oracle_pixel_sources.argtypes = [_P, _P, _P, _P, _I32, _I64, _I32, _P, _I32, _P]
+    L.oracle_pixel_sources.restype = None
+    L.oracle_unstitch.argtypes = [_P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P]
+    L.oracle_unstitch.restype = ctypes.c_int
+    L.oracle_threads.argtypes = []
+    L.oracle_threads.restype = _I32
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def half_from_double(v: float) -> int:
+    return int(lib().oracle_half_from_double(float(v)))
+
+
+def norm_table(mean, std) -> np.ndarray:
+    """uint16 [3, 256]: binary16 bits of (x - mean_k) / std_k."""
+    m = np.ascontiguousarray(mean, dtype=np.float32)
+    s = np.ascontiguousarray(std, dtype=np.float32)
+    t = np.zeros((3, 256), dtype=np.uint16)
+    lib().oracle_norm_table(_ptr(m), _ptr(s), _ptr(t))
+    return t
+
+
+class Plan:
+    def __init__(self, place, order, canvas_begin, n_canvases):
+        self.place = place
+        self.order = order
+        self.canvas_begin = canvas_begin
+        self.n_canvases = n_canvases
+
+
+def pack(rois, canvas_w, canvas_h, frame_w, frame_h, n_frames, policy=SHELF_FFDH):
+    """Returns (code, bad_index, Plan or None)."""
+    r = _i32(rois).reshape(-1, 5)
+    n = r.shape[0]
+    place = np.zeros((n, 3), dtype=np.int32)
+    order = np.zeros(n, dtype=np.int32)
+    cbeg = np.zeros(n + 1, dtype=np.int32)
+    J = np.zeros(1, dtype=np.int32)
+    bad = np.full(1, -1, dtype=np.int32)
+    rc = lib().oracle_pack(_ptr(r), n, canvas_w, canvas_h, frame_w, frame_h, n_frames, policy,
+                           _ptr(place), _ptr(order), _ptr(cbeg), _ptr(J), _ptr(bad))
+    if rc != OK:
+        return rc, int(bad[0]), None
+    j = int(J[0])
+    return rc, -1, Plan(place, order, cbeg[: j + 1].copy(), j)
+
+
+def guillotine_free(rois, canvas_w, canvas_h) -> np.ndarray:
+    r = _i32(rois).reshape(-1, 5)
+    cap = 2 * r.shape[0] + 2
+    out = np.zeros((cap, 5), dtype=np.int32)
+    m = lib().oracle_guillotine_free(_ptr(r), r.shape[0], canvas_w, canvas_h, _ptr(out), cap)
+    if m < 0:
+        raise ValueError("invalid input to guillotine_free")
+    return out[:m].copy()
+
+
+def check_plan(rois, canvas_w, canvas_h, policy, place, order, canvas_begin, n_canvases) -> int:
+    r = _i32(rois).reshape(-1, 5)
+    pl, od, cb = _i32(place).reshape(-1, 3), _i32(order), _i32(canvas_begin)
+    return int(lib().oracle_check_plan(_ptr(r), r.shape[0], canvas_w, canvas_h, policy,
+                                       _ptr(pl), _ptr(od), _ptr(cb), int(n_canvases)))
+
+
+def stitch(frames: np.ndarray, rois, plan: Plan, first, count, canvas_w, canvas_h,
+           mean, std, pad, frame_stride=None, row_pitch=None) -> np.ndarray:
+    """frames: uint8 [F, H, W, 3] (or a flat buffer with explicit strides)."""
+    fr = np.ascontiguousarray(frames)
+    if frame_stride is None:
+        frame_stride = fr.shape[1] * fr.shape[2] * 3
+        row_pitch = fr.shape[2] * 3
+    r = _i32(rois).reshape(-1, 5)
+    out = np.empty((count, 3, canvas_h, canvas_w), dtype=np.uint16)
+    m = np.ascontiguousarray(mean, dtype=np.float32)
+    s = np.ascontiguousarray(std, dtype=np.float32)
+    p = np.ascontiguousarray(pad, dtype=np.uint8)
+    rc = lib().oracle_stitch(_ptr(fr), frame_stride, row_pitch, _ptr(r), _ptr(_i32(plan.place)),
+                             _ptr(_i32(plan.order)), _ptr(_i32(plan.canvas_begin)),
+                             plan.n_canvases, first, count, canvas_w, canvas_h,
+                             _ptr(m), _ptr(s), _ptr(p), _ptr(out))
+    if rc != OK:
+        raise ValueError(f"oracle_stitch: {ERROR_NAMES.get(rc, rc)}")
+    return out
+
+
+def pixel_sources(rois, plan: Plan, frame_stride, row_pitch, pts) -> np.ndarray:
+    """int64 byte offsets of channel 0 for sample points {canvas, X, Y}; -1 = pad."""
+    q = _i32(pts).reshape(-1, 3)
+    src = np.empty(q.shape[0], dtype=np.int64)
+    lib().oracle_pixel_sources(_ptr(_i32(rois).reshape(-1, 5)), _ptr(_i32(plan.place)),
+                               _ptr(_i32(plan.order)), _ptr(_i32(plan.canvas_begin)),
+                               plan.n_canvases, frame_stride, row_pitch, _ptr(q), q.shape[0],
+                               _ptr(src))
+    return src
+
+
+def unstitch(boxes, box_canvas, rois, plan: Plan, clip=1):
+    """Returns (roi_of_box int32 [n], dets DET_DTYPE [n_out])."""
+    bx = np.ascontiguousarray(boxes, dtype=np.float32).reshape(-1, 4)
+    bc = _i32(box_canvas)
+    n = bx.shape[0]
+    rob = np.empty(n, dtype=np.int32)
+    dets = np.zeros(n, dtype=DET_DTYPE)
+    n_out = np.zeros(1, dtype=np.int32)
+    lib().oracle_unstitch(_ptr(bx), _ptr(bc), n, _ptr(_i32(rois).reshape(-1, 5)),
+                          _ptr(_i32(plan.place)), _ptr(_i32(plan.order)),
+                          _ptr(_i32(plan.canvas_begin)), plan.n_canvases, int(clip),
+                          _ptr(rob), _ptr(dets), _ptr(n_out))
+    return rob, dets[: int(n_out[0])].copy()
+
+
+def threads() -> int:
+    return int(lib().oracle_threads())
