@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Throughput of the patch-stitching path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  tg_plan_pack (host C++) -> plan uploaded to HBM -> tg_stitch once per batch of
+  canvases -> tg_unstitch of every detector box.
+Frames, the RoI table and the boxes are resident in HBM before timing starts. The
+host plan of step s+1 overlaps the GPU work of step s (double-buffered pinned
+staging), as a serving loop would run it.
+
+Prints one JSON line. `value` is stitched canvas Mpixel/s over whole steps; the
+roofline object covers the dominant kernel (tg_stitch) measured with HIP events on
+the stream it runs on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+METRIC = "stitched canvas Mpixel/s and achieved HBM GB/s (% of peak), 20-cam 4K"
+STITCH_SRC = os.path.join(ROOT, "paper_2404_09267_amd", "csrc", "stitch.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "stitch_cam20_4k_counters.json")
+
+
+def source_hash(path=STITCH_SRC) -> str:
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="cam20_4k")
+    ap.add_argument("--policy", type=int, default=0, help="0 shelf FFDH, 1 shelf arrival, 2 guillotine")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum wall time of the oracle's CPU sample")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="instead of the bench, run plain device copies of this size "
+                         "(counter calibration for rocprofv3 --pmc)")
+    return ap.parse_args()
+
+
+def calib_copy(mb: int, steps: int):
+    import torch
+
+    n = mb << 20
+    src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calib_copy_bytes": n, "launches": steps}), flush=True)
+
+
+def stitch_bytes(rois, plan, first, count, canvas) -> int:
+    """Algorithmic bytes of one tg_stitch launch: fp16 canvases written, source
+    pixels read once, and 36 bytes of plan per patch (tg_roi, tg_place, order)."""
+    lo, hi = int(plan.canvas_begin[first]), int(plan.canvas_begin[first + count])
+    ids = plan.order[lo:hi]
+    px = int((rois[ids, 3].astype(np.int64) * rois[ids, 4]).sum())
+    return int(count) * canvas * canvas * 6 + 3 * px + 36 * (hi - lo)
+
+
+def cpu_baseline(wl, rois, frames_np, boxes, canv, min_seconds: float):
+    """The oracle, untuned, on a bounded sample of the same workload: the full plan,
+    the first canvases' stitch and those canvases' boxes, repeated until at least
+    `min_seconds` of wall time have passed."""
+    import oracle
+
+    sample_canvases = 4
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        rc, _, oplan = oracle.pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h,
+                                   wl.n_frames, 0)
+        oracle.stitch(frames_np, rois, oplan, 0, sample_canvases, wl.canvas, wl.canvas,
+                      _W.MEAN, _W.STD, _W.PAD)
+        sel = canv < sample_canvases
+        oracle.unstitch(boxes[sel], canv[sel], rois, oplan, 1)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    px = reps * sample_canvases * wl.canvas * wl.canvas
+    return {"value": round(px / el / 1e6, 3), "unit": "Mpixel/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"{reps} x (plan of all {len(rois)} RoIs + stitch of canvases 0-"
+                      f"{sample_canvases - 1} ({sample_canvases} x {wl.canvas}x{wl.canvas}) + "
+                      f"unstitch of their {int((canv < sample_canvases).sum())} boxes), "
+                      f"{el:.1f} s wall",
+            "host_threads_available": len(os.sched_getaffinity(0))}
+
+
+_W = None
+
+
+def main():
+    global _W
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; run with --gpus 1"}),
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2404_09267_amd import tg
+    from paper_2404_09267_amd import workload as W
+
+    _W = W
+    if args.calib_copy_mb:
+        calib_copy(args.calib_copy_mb, args.steps)
+        return
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    tg.lib()
+    wl = W.WORKLOADS[args.workload]
+    dev = torch.device("cuda")
+    stream = torch.cuda.current_stream()
+
+    # ---- resident inputs -------------------------------------------------------
+    rois = W.make_rois(wl)
+    frames_d = W.make_frames(wl, dev)
+    plan0 = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames,
+                         args.policy)
+    J = plan0.n_canvases
+    boxes, canv = W.make_boxes(wl, J)
+    n_rois, n_boxes = len(rois), len(boxes)
+    rois_d = torch.from_numpy(rois).to(dev)
+    boxes_d = torch.from_numpy(boxes).to(dev)
+    canv_d = torch.from_numpy(canv).to(dev)
+    out = torch.empty((J, 3, wl.canvas, wl.canvas), dtype=torch.float16, device=dev)
+    ubufs = tg.UnstitchBuffers(n_boxes)
+    batches = [tg.batch_range(J, wl.batch_cap, k) for k in range(tg.batch_count(J, wl.batch_cap))]
+
+    # device plan arrays, refreshed every step from double-buffered pinned staging
+    words = n_rois * 3 + n_rois + (n_rois + 1)
+    staging = [torch.empty(words, dtype=torch.int32, pin_memory=True) for _ in range(2)]
+    staging_np = [s.numpy() for s in staging]
+    plan_d = torch.zeros(words, dtype=torch.int32, device=dev)
+    dplan = tg.DevicePlan.from_tensors(rois_d, plan_d[: 3 * n_rois].view(n_rois, 3),
+                                       plan_d[3 * n_rois: 4 * n_rois],
+                                       plan_d[4 * n_rois: 4 * n_rois + J + 1], J)
+    upload_done = [None, None]
+    J_buf = np.zeros(1, np.int32)
+    bad_buf = np.zeros(1, np.int32)
+    params = tg.PackParams(wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, args.policy)
+    # argument blocks are built once: no pointer changes between steps
+    stitch_args = [tg.stitch_args(frames_d, dplan, first, count, wl.canvas, wl.canvas,
+                                  W.MEAN, W.STD, W.PAD, out[first:first + count])
+                   for first, count in batches]
+
+    def make_uargs():
+        return tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
+
+    uargs = make_uargs()
+    stitch_events = []
+    timing = {"on": False}
+
+    def step(s: int):
+        buf = s & 1
+        if upload_done[buf] is not None:
+            upload_done[buf].synchronize()  # staging of step s-2 has reached the GPU
+        st = staging_np[buf]
+        place = st[: 3 * n_rois].reshape(n_rois, 3)
+        order = st[3 * n_rois: 4 * n_rois]
+        cbeg = st[4 * n_rois:]
+        rc = tg.lib().tg_plan_pack(rois.ctypes.data, n_rois, tg.ctypes.byref(params),
+                                   place.ctypes.data, order.ctypes.data, cbeg.ctypes.data,
+                                   J_buf.ctypes.data, bad_buf.ctypes.data)
+        if rc != tg.OK or J_buf[0] != J:
+            raise tg.TgError("tg_plan_pack", rc)
+        plan_d.copy_(staging[buf], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        upload_done[buf] = ev
+        h = tg._vp(stream.cuda_stream)
+        for a in stitch_args:
+            if timing["on"]:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            rc = tg.lib().tg_stitch(tg.ctypes.byref(a), h)
+            if rc != tg.OK:
+                raise tg.TgError("tg_stitch", rc)
+            if timing["on"]:
+                e1.record(stream)
+                stitch_events.append((e0, e1, a.canvas_first, a.canvas_count))
+        rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
+        if rc != tg.OK:
+            raise tg.TgError("tg_unstitch", rc)
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    # sanity: the plan the steps recompute equals the one the buffers were sized for
+    chk = plan_d.cpu().numpy()
+    assert np.array_equal(chk[: 3 * n_rois].reshape(n_rois, 3), plan0.place)
+    timing["on"] = True
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.warmup, args.warmup + args.steps):
+        step(s)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    timing["on"] = False
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    canvas_px = J * wl.canvas * wl.canvas
+    value = canvas_px / (ms_per_step * 1e-3) / 1e6
+
+    # ---- dominant kernel: tg_stitch ------------------------------------------------
+    tot_ms, tot_bytes = 0.0, 0
+    per_batch_bytes = {(f, c): stitch_bytes(rois, plan0, f, c, wl.canvas) for f, c in batches}
+    for e0, e1, f, c in stitch_events:
+        tot_ms += e0.elapsed_time(e1)
+        tot_bytes += per_batch_bytes[(f, c)]
+    n_launch = len(stitch_events)
+    avg_ms = tot_ms / n_launch
+    avg_bytes = tot_bytes / n_launch
+    achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(COUNTERS):
+        with open(COUNTERS) as f:
+            cnt = json.load(f)
+        if cnt.get("stitch_source_sha256_16") == source_hash() and \
+                cnt.get("workload") == wl.name:
+            traffic = cnt.get("hbm_bytes_per_launch")
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "stitch_kernel<true>", "launches": n_launch,
+                "avg_launch_us": round(avg_ms * 1e3, 2),
+                "algorithmic_bytes_per_launch": int(avg_bytes)}
+
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "Mpixel/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.n_frames} x {wl.frame_w}x{wl.frame_h} u8 RGB "
+                               f"frames, {n_rois} RoIs ({wl.roi_dist} {wl.roi_lo}..{wl.roi_hi} px),"
+                               f" {wl.canvas}x{wl.canvas} canvases, batch cap {wl.batch_cap}, "
+                               f"{n_boxes} boxes",
+                   "canvases": J, "batches": len(batches), "policy": args.policy,
+                   "canvas_efficiency": round(float((rois[:, 3].astype(np.int64) *
+                                                     rois[:, 4]).sum()) / canvas_px, 4)},
+        "roofline": roofline,
+        "stitch_gbs": round(achieved, 1),
+        "stitch_pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
+    }
+    if not args.no_cpu_baseline:
+        frames_np = frames_d.cpu().numpy()
+        result["cpu_baseline"] = cpu_baseline(wl, rois, frames_np, boxes, canv, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

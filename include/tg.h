@@ -1,0 +1,235 @@
+/*
+ * tg.h -- C ABI of the MI355X patch-stitching library (libtg.so).
+ *
+ * Tangram (arXiv 2404.09267) batches variable-size RoI patches from many cameras
+ * by stitching them, unresized, onto fixed-size canvases so that a detector sees one
+ * fixed-shape batch (Sec. I; Sec. III-B; Sec. III-C, Patch-stitching Solver), and
+ * its accuracy is scored per frame (Sec. V-D). This library is that data path:
+ *
+ *   tg_plan_pack   host:   place RoI rectangles on canvases (no HIP calls)
+ *   tg_stitch      device: scatter uint8 RGB crops into fp16 NCHW canvases,
+ *                          normalise per channel, fill the rest with the pad value
+ *   tg_unstitch    device: map detector boxes from canvas back to frame pixels
+ *
+ * Conventions for every call:
+ *  - Pixels: origin top-left, x right, y down; integer rectangles are half-open,
+ *    [x, x+w) x [y, y+h).
+ *  - Ownership: the caller owns every buffer. The library allocates no device memory
+ *    and keeps no global state; tg_plan_pack frees its host temporaries before it
+ *    returns.
+ *  - Asynchrony: tg_stitch and tg_unstitch only enqueue work on `stream` (a
+ *    hipStream_t; NULL is the default stream) and never synchronise. Inputs must stay
+ *    valid, and outputs untouched, until the stream has passed the call.
+ *  - Errors: every int-returning call returns TG_OK (0) or a negative TG_E_* code and
+ *    never lets a C++ exception cross the ABI. A device call that returns an error
+ *    has enqueued nothing.
+ *  - Device buffers need only their natural alignment (4 bytes for int32/float, 2 for
+ *    fp16); tg_stitch takes a faster path when `out` is 16-byte aligned and canvas_w
+ *    is a multiple of 8.
+ */
+#ifndef TG_H
+#define TG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A source rectangle: RoI/patch `i` is [x, x+w) x [y, y+h) of frame `frame`.
+ * The paper's patch information carries the patch size (Sec. III-C, Alg. 2 input
+ * P_i = {w_i, h_i, t_ddl_i}); the frame id and offset are what the cloud needs to
+ * cut the pixels and to send detections back. 20 bytes. */
+typedef struct {
+  int32_t frame, x, y, w, h;
+} tg_roi;
+
+/* Where RoI i sits: canvas id and top-left corner on that canvas. Indexed like the
+ * RoI table (the paper's assignment x_i^j, Sec. III-B). 12 bytes. */
+typedef struct {
+  int32_t canvas, x, y;
+} tg_place;
+
+/* A detector box in canvas pixels, continuous coordinates. 16 bytes. */
+typedef struct {
+  float x1, y1, x2, y2;
+} tg_box;
+
+/* A kept box mapped back to its frame: input box index, RoI index, frame id and the
+ * box in frame pixels. 28 bytes. */
+typedef struct {
+  int32_t box, roi, frame;
+  float x1, y1, x2, y2;
+} tg_det;
+
+enum tg_status {
+  TG_OK = 0,
+  TG_E_INVAL = -1,         /* null pointer, negative count, bad size/policy/std,
+                              or an RoI with w < 1 or h < 1 */
+  TG_E_ROI_TOO_LARGE = -2, /* RoI wider or taller than the canvas: patches are never
+                              resized (Sec. III-C), so it cannot be placed */
+  TG_E_ROI_OOB = -3,       /* RoI not inside its frame, or frame id out of range */
+  TG_E_RANGE = -4,         /* canvas range outside [0, n_canvases) */
+  TG_E_WORKSPACE = -5,     /* workspace missing or smaller than required */
+  TG_E_HIP = -6,           /* the HIP runtime refused a launch */
+  TG_E_INTERNAL = -7       /* host allocation failure or other internal error */
+};
+
+enum tg_policy {
+  /* First-fit decreasing height shelves: RoIs sorted by height, taller first (ties
+   * keep input order); each goes on the first shelf of the current canvas that is
+   * tall enough and has room, else on a new shelf under the last, else on a new
+   * canvas. Closed canvases are not revisited. */
+  TG_PACK_SHELF_FFDH = 0,
+  /* The same shelves, RoIs taken in input (arrival) order. */
+  TG_PACK_SHELF_ARRIVAL = 1,
+  /* The paper's Patch-stitching Solver (Sec. III-C, Alg. 2): RoIs in input order;
+   * among free rectangles that fit, the one leaving the smallest short-side leftover
+   * min(w_c - w_i, h_c - h_i) (ties: smaller long-side leftover, then earlier in the
+   * free list); the RoI goes to that rectangle's corner nearest the canvas origin;
+   * the leftover is split in two along the free rectangle's shorter side; with no
+   * fitting rectangle a new blank canvas is started. */
+  TG_PACK_GUILLOTINE_BSSF = 2
+};
+
+typedef struct {
+  int32_t canvas_w, canvas_h; /* canvas M x N of the paper (Sec. III-C), >= 1 */
+  int32_t frame_w, frame_h;   /* every source frame's size, >= 1 */
+  int32_t n_frames;           /* valid frame ids are [0, n_frames) */
+  int32_t policy;             /* enum tg_policy */
+} tg_pack_params;
+
+/*
+ * Pack n RoIs onto canvases of canvas_w x canvas_h (host only; makes no HIP call).
+ *
+ * Every RoI is placed exactly once, unrotated and unresized, with the rectangles on
+ * one canvas pairwise disjoint and inside the canvas (Sec. III-B, constraints (3)
+ * and (4); Sec. III-C). Canvases are opened one after another.
+ *
+ * In:  rois[n] (host). n >= 0.
+ * Out (host, caller-allocated):
+ *   place[n]            placement of RoI i
+ *   order[n]            RoI ids in placement sequence; canvas-major
+ *   canvas_begin[n+1]   order[canvas_begin[j] .. canvas_begin[j+1]) lie on canvas j;
+ *                       entries 0 .. *n_canvases are written
+ *   *n_canvases         J, the number of canvases (0 when n == 0)
+ *   *bad_index          -1, or the first RoI that failed validation
+ * RoIs are validated in index order; the first failure decides the code: w or h < 1
+ * -> TG_E_INVAL; outside its frame or frame id not in [0, n_frames) -> TG_E_ROI_OOB;
+ * larger than the canvas -> TG_E_ROI_TOO_LARGE. Outputs are unspecified on error.
+ */
+int tg_plan_pack(const tg_roi *rois, int32_t n, const tg_pack_params *params,
+                 tg_place *place, int32_t *order, int32_t *canvas_begin,
+                 int32_t *n_canvases, int32_t *bad_index);
+
+/*
+ * Batch split: the paper caps the canvases per function invocation by the GPU memory
+ * one canvas takes (Sec. III-B, constraint (5)). Batch k holds canvases
+ * [k * batch_cap, min((k+1) * batch_cap, n_canvases)); batch_cap <= 0 means one batch
+ * holding every canvas.
+ * tg_batch_count returns the number of batches (0 for no canvases).
+ * tg_batch_range writes batch k's first canvas and count; TG_E_RANGE if k is not a
+ * batch, TG_E_INVAL on null pointers.
+ */
+int32_t tg_batch_count(int32_t n_canvases, int32_t batch_cap);
+int tg_batch_range(int32_t n_canvases, int32_t batch_cap, int32_t k, int32_t *first,
+                   int32_t *count);
+
+typedef struct {
+  /* Source frames, device, uint8 HWC RGB: pixel (x, y) of frame f, channel k, is
+   * frames[f * frame_stride + y * row_pitch + 3 * x + k]. row_pitch >= 3 * frame_w,
+   * frame_stride >= frame_h * row_pitch. */
+  const uint8_t *frames;
+  int64_t frame_stride;
+  int32_t n_frames, frame_w, frame_h, row_pitch;
+  /* The plan, device copies of tg_plan_pack's outputs for n_rois RoIs and
+   * n_canvases canvases. */
+  const tg_roi *rois;
+  const tg_place *place;
+  const int32_t *order;
+  const int32_t *canvas_begin; /* n_canvases + 1 entries */
+  int32_t n_rois, n_canvases;
+  /* Canvases [canvas_first, canvas_first + canvas_count) are written. */
+  int32_t canvas_first, canvas_count;
+  int32_t canvas_w, canvas_h;
+  /* Per-channel normalisation in uint8 units, channels R, G, B: a source byte x of
+   * channel k becomes binary16((x - mean[k]) / std[k]), the quotient taken in double
+   * and rounded once to nearest-even binary16. std[k] must be finite and > 0, mean[k]
+   * finite. Canvas pixels outside every patch get the same transform of pad[k]. */
+  float mean[3], std[3];
+  uint8_t pad[3];
+  /* Output, device, binary16 bit patterns, [canvas_count][3][canvas_h][canvas_w]
+   * contiguous: out[((c * 3 + k) * canvas_h + Y) * canvas_w + X] holds canvas
+   * canvas_first + c. Every element is written exactly once. */
+  uint16_t *out;
+} tg_stitch_args;
+
+/*
+ * Stitch: for every canvas c in range, pixel (X, Y) and channel k, the output is the
+ * normalised byte frames[f][Y - dy + sy][X - dx + sx][k] when (X, Y) lies in the
+ * placed rectangle of an RoI on c (source (f, sx, sy), destination (dx, dy)), and the
+ * normalised pad byte otherwise. The paper copies patches onto canvases without
+ * resizing (Sec. I; Sec. III-C) but specifies no pixel mechanism; the transform above
+ * is the detector input.
+ *
+ * The kernel trusts no plan entry: RoI ids outside [0, n_rois), RoIs whose place names
+ * another canvas, and RoIs whose source or destination rectangle falls outside the
+ * frame or canvas are skipped (their pixels read as pad), so a corrupt plan cannot make
+ * it read or write outside the buffers described here.
+ * Returns TG_E_INVAL for null pointers (unless canvas_count == 0), non-positive sizes,
+ * row_pitch < 3 * frame_w, frame_stride < frame_h * row_pitch, or a bad mean/std;
+ * TG_E_RANGE when the canvas range leaves [0, n_canvases); TG_E_HIP on launch failure.
+ * canvas_count == 0 enqueues nothing and returns TG_OK.
+ */
+int tg_stitch(const tg_stitch_args *args, void *stream);
+
+typedef struct {
+  const tg_box *boxes;        /* device [n_boxes] */
+  const int32_t *box_canvas;  /* device [n_boxes], canvas id of each box */
+  int32_t n_boxes;
+  const tg_roi *rois;         /* device plan, as for tg_stitch */
+  const tg_place *place;
+  const int32_t *order;
+  const int32_t *canvas_begin;
+  int32_t n_rois, n_canvases;
+  int32_t clip;               /* nonzero: clip each kept box to its patch */
+  int32_t *roi_of_box;        /* device out [n_boxes]: RoI id or -1 */
+  tg_det *dets;               /* device out [n_boxes]: kept boxes, first *n_out valid */
+  int32_t *n_out;             /* device out, one int32 */
+  void *workspace;            /* device scratch, >= tg_unstitch_workspace_bytes(n_boxes) */
+  size_t workspace_bytes;
+} tg_unstitch_args;
+
+/* Device scratch tg_unstitch needs for n_boxes boxes (0 when n_boxes <= 0). */
+size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
+
+/*
+ * Unstitch: box b with canvas c = box_canvas[b]; its centre is
+ * cx = (x1 + x2) * 0.5f, cy = (y1 + y2) * 0.5f in fp32 (no fused multiply-add).
+ * It belongs to the RoI p on c with (float)dx <= cx < (float)(dx + w) and
+ * (float)dy <= cy < (float)(dy + h) -- at most one, as placed rectangles are
+ * disjoint. Boxes with no such RoI (centre on pad, NaN coordinate, or c outside
+ * [0, n_canvases)) get roi_of_box[b] = -1 and are dropped. A kept box is clipped,
+ * when `clip`, to [dx, dx+w] x [dy, dy+h] coordinate by coordinate (v < lo -> lo,
+ * v > hi -> hi), then moved to frame pixels by adding (float)(sx - dx) to x1, x2 and
+ * (float)(sy - dy) to y1, y2 (one fp32 add each). Kept boxes are written to dets in
+ * increasing b (a stable compaction), and their count to *n_out. The paper scores
+ * detections per frame (Sec. V-D) without stating this mapping; the centre rule is
+ * this library's reading.
+ * Returns TG_E_INVAL on null pointers (unless n_boxes == 0, which only writes
+ * *n_out = 0) or n_boxes < 0, TG_E_WORKSPACE when the workspace is too small,
+ * TG_E_HIP on launch failure.
+ */
+int tg_unstitch(const tg_unstitch_args *args, void *stream);
+
+/* Static description of a status code. */
+const char *tg_strerror(int code);
+
+/* ABI version: bumped whenever a struct or signature above changes. */
+int32_t tg_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TG_H */

@@ -1,0 +1,235 @@
+// tg_unstitch: map detector boxes from canvas pixels back to frame pixels.
+//
+// The paper scores detections per source frame (Sec. V-D) after inferring stitched
+// canvases (Sec. III-C) but does not say how a detection finds its patch. This
+// library's rule: a box belongs to the patch holding its centre (half-open on the
+// right and bottom edges); it is optionally clipped to that patch and shifted by the
+// patch's frame offset minus its canvas offset.
+//
+// Two launches on the caller's stream:
+//  1. assign: LPB lanes per box test the box canvas's patches LPB at a time; a wave
+//     ballot picks the (unique) patch containing the centre and roi_of_box[b] is
+//     written. The same launch clears the look-back state of launch 2.
+//  2. emit: one thread per box, 256 boxes per workgroup. Kept boxes are ranked inside
+//     the workgroup with ballot + mbcnt, the workgroup's offset comes from a
+//     single-pass decoupled look-back over earlier workgroups (workgroup order is
+//     taken from an atomic ticket, so every workgroup a block waits on has already
+//     started), and kept boxes are written in increasing box index -- a stable
+//     compaction whose output does not depend on scheduling.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "tg.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr uint64_t kAggregate = uint64_t(1) << 32;  // state: value = this block's count
+constexpr uint64_t kInclusive = uint64_t(2) << 32;  // state: value = count of blocks 0..i
+constexpr uint32_t kSpinLimit = 1u << 26;           // bounded wait; never reached in practice
+
+struct UnstitchParams {
+  const tg_box *boxes;
+  const int32_t *box_canvas;
+  int32_t n_boxes;
+  const tg_roi *rois;
+  const tg_place *place;
+  const int32_t *order;
+  const int32_t *canvas_begin;
+  int32_t n_rois, n_canvases, clip;
+  int32_t *roi_of_box;
+  tg_det *dets;
+  int32_t *n_out;
+  uint32_t *ticket;
+  uint64_t *state;  // one word per emit workgroup
+  int32_t n_state_words;  // ticket word + state words, in uint64 units
+};
+
+template <int LPB>
+__global__ __launch_bounds__(kThreads) void assign_kernel(const UnstitchParams P) {
+  const int gtid = blockIdx.x * kThreads + threadIdx.x;
+  if (gtid < P.n_state_words) reinterpret_cast<uint64_t *>(P.ticket)[gtid] = 0;
+
+  constexpr int kBoxesPerBlock = kThreads / LPB;
+  const int lane = threadIdx.x & 63;
+  const int sub = threadIdx.x / LPB;
+  const int sl = threadIdx.x % LPB;
+  const int seg_shift = lane - sl;  // first lane of this box's segment within the wave
+  const uint64_t seg_mask = LPB == 64 ? ~uint64_t(0) : ((uint64_t(1) << LPB) - 1);
+  const int b = blockIdx.x * kBoxesPerBlock + sub;
+  if (b >= P.n_boxes) return;  // whole segments leave together
+
+  const int c = P.box_canvas[b];
+  const tg_box box = P.boxes[b];
+  const float cx = (box.x1 + box.x2) * 0.5f;
+  const float cy = (box.y1 + box.y2) * 0.5f;
+  int k_lo = 0, k_hi = 0;
+  if (c >= 0 && c < P.n_canvases) {
+    k_lo = min(max(P.canvas_begin[c], 0), P.n_rois);
+    k_hi = min(max(P.canvas_begin[c + 1], k_lo), P.n_rois);
+  }
+  for (int base = k_lo; base < k_hi; base += LPB) {
+    const int k = base + sl;
+    bool hit = false;
+    int id = -1;
+    if (k < k_hi) {
+      id = P.order[k];
+      if (id >= 0 && id < P.n_rois) {
+        const tg_place pl = P.place[id];
+        const tg_roi r = P.rois[id];
+        hit = pl.canvas == c && float(pl.x) <= cx && cx < float(pl.x + r.w) &&
+              float(pl.y) <= cy && cy < float(pl.y + r.h);
+      }
+    }
+    const uint64_t m = (__ballot(hit) >> seg_shift) & seg_mask;
+    if (m) {
+      if (sl == __builtin_ctzll(m)) P.roi_of_box[b] = id;  // lowest k wins
+      return;
+    }
+  }
+  if (sl == 0) P.roi_of_box[b] = -1;
+}
+
+__device__ __forceinline__ uint64_t load_state(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_state(uint64_t *p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ __launch_bounds__(kThreads) void emit_kernel(const UnstitchParams P) {
+  __shared__ int s_blk, s_prefix;
+  __shared__ int s_wave[kThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0)
+    s_blk = static_cast<int>(__hip_atomic_fetch_add(P.ticket, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT));
+  __syncthreads();
+  const int blk = s_blk;
+  const int b = blk * kThreads + tid;
+  const int roi = b < P.n_boxes ? P.roi_of_box[b] : -1;
+  const bool kept = roi >= 0;
+  const uint64_t ballot = __ballot(kept);
+  if (lane == 0) s_wave[wave] = __popcll(ballot);
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int w = 0; w < kThreads / 64; ++w) {
+    if (w < wave) before += s_wave[w];
+    total += s_wave[w];
+  }
+  if (tid == 0) {
+    int prefix = 0;
+    if (blk == 0) {
+      store_state(&P.state[0], kInclusive | uint32_t(total));
+    } else {
+      store_state(&P.state[blk], kAggregate | uint32_t(total));
+      for (int j = blk - 1; j >= 0; --j) {
+        uint64_t s = load_state(&P.state[j]);
+        for (uint32_t spin = 0; (s >> 32) == 0 && spin < kSpinLimit; ++spin)
+          s = load_state(&P.state[j]);
+        prefix += static_cast<int>(static_cast<uint32_t>(s));
+        if ((s >> 32) != (kAggregate >> 32)) break;  // inclusive (or a timed-out wait)
+      }
+      store_state(&P.state[blk], kInclusive | uint32_t(prefix + total));
+    }
+    s_prefix = prefix;
+    if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = prefix + total;
+  }
+  __syncthreads();
+  if (!kept) return;
+  const int pos = s_prefix + before +
+                  static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                      static_cast<uint32_t>(ballot >> 32),
+                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(ballot), 0u)));
+  const tg_roi r = P.rois[roi];
+  const tg_place pl = P.place[roi];
+  const tg_box box = P.boxes[b];
+  float v[4] = {box.x1, box.y1, box.x2, box.y2};
+  if (P.clip) {
+    const float lo[2] = {float(pl.x), float(pl.y)};
+    const float hi[2] = {float(pl.x + r.w), float(pl.y + r.h)};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (v[q] < lo[q & 1]) v[q] = lo[q & 1];
+      if (v[q] > hi[q & 1]) v[q] = hi[q & 1];
+    }
+  }
+  const float ox = float(r.x - pl.x), oy = float(r.y - pl.y);
+  tg_det d;
+  d.box = b;
+  d.roi = roi;
+  d.frame = r.frame;
+  d.x1 = v[0] + ox;
+  d.y1 = v[1] + oy;
+  d.x2 = v[2] + ox;
+  d.y2 = v[3] + oy;
+  P.dets[pos] = d;
+}
+
+__global__ void zero_count_kernel(int32_t *n_out) { *n_out = 0; }
+
+int emit_blocks(int32_t n) { return (n + kThreads - 1) / kThreads; }
+
+}  // namespace
+
+extern "C" size_t tg_unstitch_workspace_bytes(int32_t n_boxes) {
+  if (n_boxes <= 0) return 0;
+  return sizeof(uint64_t) * (1 + static_cast<size_t>(emit_blocks(n_boxes)));
+}
+
+extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
+  if (!a || a->n_boxes < 0 || a->n_rois < 0 || a->n_canvases < 0) return TG_E_INVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!a->n_out) return TG_E_INVAL;
+  if (a->n_boxes == 0) {
+    hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(1), 0, s, a->n_out);
+    return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
+  }
+  if (!a->boxes || !a->box_canvas || !a->roi_of_box || !a->dets) return TG_E_INVAL;
+  if (a->n_canvases > 0 && !a->canvas_begin) return TG_E_INVAL;
+  if (a->n_rois > 0 && (!a->rois || !a->place || !a->order)) return TG_E_INVAL;
+  const size_t need = tg_unstitch_workspace_bytes(a->n_boxes);
+  if (!a->workspace || a->workspace_bytes < need ||
+      reinterpret_cast<uintptr_t>(a->workspace) % 8 != 0)
+    return TG_E_WORKSPACE;
+
+  UnstitchParams P;
+  P.boxes = a->boxes;
+  P.box_canvas = a->box_canvas;
+  P.n_boxes = a->n_boxes;
+  P.rois = a->rois;
+  P.place = a->place;
+  P.order = a->order;
+  P.canvas_begin = a->canvas_begin;
+  P.n_rois = a->n_rois;
+  P.n_canvases = a->n_canvases;
+  P.clip = a->clip;
+  P.roi_of_box = a->roi_of_box;
+  P.dets = a->dets;
+  P.n_out = a->n_out;
+  P.ticket = static_cast<uint32_t *>(a->workspace);
+  P.state = static_cast<uint64_t *>(a->workspace) + 1;
+  P.n_state_words = 1 + emit_blocks(a->n_boxes);
+
+  // Lanes per box: about the mean number of patches per canvas, so one ballot round
+  // usually settles a box.
+  const int64_t per_canvas = a->n_canvases > 0 ? (int64_t(a->n_rois) + a->n_canvases - 1) /
+                                                     a->n_canvases
+                                               : 1;
+  const int lpb = per_canvas <= 16 ? 16 : per_canvas <= 32 ? 32 : 64;
+  const int64_t boxes_per_block = kThreads / lpb;
+  const int64_t assign_blocks = (int64_t(a->n_boxes) + boxes_per_block - 1) / boxes_per_block;
+  if (assign_blocks > 0x7FFFFFFF) return TG_E_INVAL;
+  const dim3 g1(static_cast<uint32_t>(assign_blocks));
+  if (lpb == 16)
+    hipLaunchKernelGGL(assign_kernel<16>, g1, dim3(kThreads), 0, s, P);
+  else if (lpb == 32)
+    hipLaunchKernelGGL(assign_kernel<32>, g1, dim3(kThreads), 0, s, P);
+  else
+    hipLaunchKernelGGL(assign_kernel<64>, g1, dim3(kThreads), 0, s, P);
+  if (hipGetLastError() != hipSuccess) return TG_E_HIP;
+  hipLaunchKernelGGL(emit_kernel, dim3(static_cast<uint32_t>(emit_blocks(a->n_boxes))),
+                     dim3(kThreads), 0, s, P);
+  return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
+}

@@ -1,0 +1,300 @@
+"""Python binding of libtg.so (include/tg.h): argument marshalling only.
+
+Every step of the path runs in the native library: packing in its host C++ code,
+stitch and unstitch in its HIP kernels. PyTorch supplies device memory and the
+stream. There is no fallback: if libtg.so is missing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtg.so")
+
+SHELF_FFDH, SHELF_ARRIVAL, GUILLOTINE_BSSF = 0, 1, 2
+OK = 0
+E_INVAL, E_ROI_TOO_LARGE, E_ROI_OOB, E_RANGE, E_WORKSPACE, E_HIP, E_INTERNAL = range(-1, -8, -1)
+
+ROI_DTYPE = np.dtype([("frame", "<i4"), ("x", "<i4"), ("y", "<i4"), ("w", "<i4"), ("h", "<i4")])
+DET_DTYPE = np.dtype([("box", "<i4"), ("roi", "<i4"), ("frame", "<i4"),
+                      ("x1", "<f4"), ("y1", "<f4"), ("x2", "<f4"), ("y2", "<f4")])
+DET_WORDS = 7  # int32 words per tg_det
+
+_i32, _i64, _f32, _u8, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint8,
+                              ctypes.c_void_p)
+
+
+class PackParams(ctypes.Structure):
+    _fields_ = [("canvas_w", _i32), ("canvas_h", _i32), ("frame_w", _i32), ("frame_h", _i32),
+                ("n_frames", _i32), ("policy", _i32)]
+
+
+class StitchArgs(ctypes.Structure):
+    _fields_ = [("frames", _vp), ("frame_stride", _i64), ("n_frames", _i32), ("frame_w", _i32),
+                ("frame_h", _i32), ("row_pitch", _i32), ("rois", _vp), ("place", _vp),
+                ("order", _vp), ("canvas_begin", _vp), ("n_rois", _i32), ("n_canvases", _i32),
+                ("canvas_first", _i32), ("canvas_count", _i32), ("canvas_w", _i32),
+                ("canvas_h", _i32), ("mean", _f32 * 3), ("std", _f32 * 3), ("pad", _u8 * 3),
+                ("out", _vp)]
+
+
+class UnstitchArgs(ctypes.Structure):
+    _fields_ = [("boxes", _vp), ("box_canvas", _vp), ("n_boxes", _i32), ("rois", _vp),
+                ("place", _vp), ("order", _vp), ("canvas_begin", _vp), ("n_rois", _i32),
+                ("n_canvases", _i32), ("clip", _i32), ("roi_of_box", _vp), ("dets", _vp),
+                ("n_out", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
+
+
+EXPORTS = ["tg_plan_pack", "tg_batch_count", "tg_batch_range", "tg_stitch",
+           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror", "tg_abi_version"]
+
+_lib = None
+
+
+class TgError(RuntimeError):
+    def __init__(self, call, code, bad_index=-1):
+        msg = f"{call}: {strerror(code)} ({code})"
+        if bad_index >= 0:
+            msg += f", first bad RoI {bad_index}"
+        super().__init__(msg)
+        self.code = code
+        self.bad_index = bad_index
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2404_09267_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.tg_plan_pack.argtypes = [_vp, _i32, ctypes.POINTER(PackParams), _vp, _vp, _vp, _vp, _vp]
+        L.tg_plan_pack.restype = ctypes.c_int
+        L.tg_batch_count.argtypes = [_i32, _i32]
+        L.tg_batch_count.restype = _i32
+        L.tg_batch_range.argtypes = [_i32, _i32, _i32, _vp, _vp]
+        L.tg_batch_range.restype = ctypes.c_int
+        L.tg_stitch.argtypes = [ctypes.POINTER(StitchArgs), _vp]
+        L.tg_stitch.restype = ctypes.c_int
+        L.tg_unstitch_workspace_bytes.argtypes = [_i32]
+        L.tg_unstitch_workspace_bytes.restype = ctypes.c_size_t
+        L.tg_unstitch.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
+        L.tg_unstitch.restype = ctypes.c_int
+        L.tg_strerror.argtypes = [ctypes.c_int]
+        L.tg_strerror.restype = ctypes.c_char_p
+        L.tg_abi_version.argtypes = []
+        L.tg_abi_version.restype = _i32
+        _lib = L
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return lib().tg_strerror(int(code)).decode()
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(_vp)
+
+
+# --------------------------------------------------------------------------- planning
+
+@dataclass
+class Plan:
+    """Host outputs of tg_plan_pack."""
+    place: np.ndarray         # int32 [n, 3] = {canvas, x, y}
+    order: np.ndarray         # int32 [n]
+    canvas_begin: np.ndarray  # int32 [J + 1]
+    n_canvases: int
+
+
+def plan_pack(rois: np.ndarray, canvas_w: int, canvas_h: int, frame_w: int, frame_h: int,
+              n_frames: int, policy: int = SHELF_FFDH) -> Plan:
+    r = np.ascontiguousarray(rois, dtype=np.int32).reshape(-1, 5)
+    n = r.shape[0]
+    place = np.empty((n, 3), dtype=np.int32)
+    order = np.empty(n, dtype=np.int32)
+    cbeg = np.empty(n + 1, dtype=np.int32)
+    J = np.zeros(1, dtype=np.int32)
+    bad = np.full(1, -1, dtype=np.int32)
+    p = PackParams(canvas_w, canvas_h, frame_w, frame_h, n_frames, policy)
+    rc = lib().tg_plan_pack(_np_ptr(r), n, ctypes.byref(p), _np_ptr(place), _np_ptr(order),
+                            _np_ptr(cbeg), _np_ptr(J), _np_ptr(bad))
+    if rc != OK:
+        raise TgError("tg_plan_pack", rc, int(bad[0]))
+    j = int(J[0])
+    return Plan(place, order, cbeg[: j + 1].copy(), j)
+
+
+def plan_pack_raw(rois: np.ndarray, params: PackParams, place, order, cbeg, J, bad) -> int:
+    """Unchecked call on caller-provided numpy buffers (for tests of error codes)."""
+    r = np.ascontiguousarray(rois, dtype=np.int32).reshape(-1, 5)
+    return lib().tg_plan_pack(_np_ptr(r), r.shape[0], ctypes.byref(params), _np_ptr(place),
+                              _np_ptr(order), _np_ptr(cbeg), _np_ptr(J), _np_ptr(bad))
+
+
+def batch_count(n_canvases: int, batch_cap: int) -> int:
+    return int(lib().tg_batch_count(n_canvases, batch_cap))
+
+
+def batch_range(n_canvases: int, batch_cap: int, k: int):
+    first = np.zeros(1, dtype=np.int32)
+    count = np.zeros(1, dtype=np.int32)
+    rc = lib().tg_batch_range(n_canvases, batch_cap, k, _np_ptr(first), _np_ptr(count))
+    if rc != OK:
+        raise TgError("tg_batch_range", rc)
+    return int(first[0]), int(count[0])
+
+
+# --------------------------------------------------------------------------- device side
+
+def _stream_handle(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return _vp(s.cuda_stream)
+
+
+def _check(t, dtype, shape=None, name="tensor"):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+class DevicePlan:
+    """Device copies of a plan's arrays (int32, contiguous) for tg_stitch/tg_unstitch."""
+
+    def __init__(self, rois: np.ndarray, plan: Plan, device="cuda"):
+        import torch
+
+        r = np.ascontiguousarray(rois, dtype=np.int32).reshape(-1, 5)
+        self.n_rois = r.shape[0]
+        self.n_canvases = plan.n_canvases
+        self.rois = torch.from_numpy(r).to(device)
+        self.place = torch.from_numpy(np.ascontiguousarray(plan.place, np.int32)).to(device)
+        self.order = torch.from_numpy(np.ascontiguousarray(plan.order, np.int32)).to(device)
+        self.canvas_begin = torch.from_numpy(
+            np.ascontiguousarray(plan.canvas_begin, np.int32)).to(device)
+
+    @classmethod
+    def from_tensors(cls, rois, place, order, canvas_begin, n_canvases: int) -> "DevicePlan":
+        """Wrap existing device tensors (e.g. views of one staging-backed buffer)."""
+        self = cls.__new__(cls)
+        self.n_rois = int(rois.shape[0])
+        self.n_canvases = int(n_canvases)
+        self.rois, self.place, self.order, self.canvas_begin = rois, place, order, canvas_begin
+        self.check()
+        return self
+
+    def check(self):
+        import torch
+
+        _check(self.rois, torch.int32, (self.n_rois, 5), "rois")
+        _check(self.place, torch.int32, (self.n_rois, 3), "place")
+        _check(self.order, torch.int32, (self.n_rois,), "order")
+        _check(self.canvas_begin, torch.int32, (self.n_canvases + 1,), "canvas_begin")
+
+
+def stitch_args(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w, canvas_h,
+                mean, std, pad, out) -> StitchArgs:
+    import torch
+
+    dplan.check()
+    if frames.dim() != 4 or frames.shape[3] != 3:
+        raise ValueError("frames must be uint8 [F, H, W, 3]")
+    _check(frames, torch.uint8, name="frames")
+    if out.dtype not in (torch.float16, torch.int16):
+        raise ValueError("out must be float16 (or int16 bit patterns)")
+    _check(out, out.dtype, (canvas_count, 3, canvas_h, canvas_w), "out")
+    F, H, W, _ = frames.shape
+    a = StitchArgs()
+    a.frames = frames.data_ptr()
+    a.frame_stride = H * W * 3
+    a.n_frames, a.frame_w, a.frame_h, a.row_pitch = F, W, H, W * 3
+    a.rois, a.place = dplan.rois.data_ptr(), dplan.place.data_ptr()
+    a.order, a.canvas_begin = dplan.order.data_ptr(), dplan.canvas_begin.data_ptr()
+    a.n_rois, a.n_canvases = dplan.n_rois, dplan.n_canvases
+    a.canvas_first, a.canvas_count = canvas_first, canvas_count
+    a.canvas_w, a.canvas_h = canvas_w, canvas_h
+    a.mean[:] = [float(v) for v in mean]
+    a.std[:] = [float(v) for v in std]
+    a.pad[:] = [int(v) for v in pad]
+    a.out = out.data_ptr()
+    return a
+
+
+def stitch(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w, canvas_h,
+           mean, std, pad, out, stream=None) -> None:
+    """Enqueue tg_stitch for canvases [canvas_first, +canvas_count) into `out`."""
+    a = stitch_args(frames, dplan, canvas_first, canvas_count, canvas_w, canvas_h,
+                    mean, std, pad, out)
+    rc = lib().tg_stitch(ctypes.byref(a), _stream_handle(stream))
+    if rc != OK:
+        raise TgError("tg_stitch", rc)
+
+
+def stitch_raw(args: StitchArgs, stream=None) -> int:
+    return int(lib().tg_stitch(ctypes.byref(args), _stream_handle(stream)))
+
+
+def unstitch_workspace_bytes(n_boxes: int) -> int:
+    return int(lib().tg_unstitch_workspace_bytes(n_boxes))
+
+
+class UnstitchBuffers:
+    """Caller-owned device outputs and scratch for tg_unstitch."""
+
+    def __init__(self, n_boxes: int, device="cuda"):
+        import torch
+
+        self.n_boxes = n_boxes
+        self.roi_of_box = torch.empty(n_boxes, dtype=torch.int32, device=device)
+        self.dets = torch.empty((n_boxes, DET_WORDS), dtype=torch.int32, device=device)
+        self.n_out = torch.empty(1, dtype=torch.int32, device=device)
+        ws = unstitch_workspace_bytes(n_boxes)
+        self.workspace = torch.empty(max(ws, 8), dtype=torch.uint8, device=device)
+        self.workspace_bytes = ws
+
+    def dets_numpy(self) -> np.ndarray:
+        n = int(self.n_out.item())
+        return self.dets[:n].cpu().numpy().view(DET_DTYPE).reshape(-1)
+
+
+def unstitch_args(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers) -> UnstitchArgs:
+    import torch
+
+    dplan.check()
+    n = bufs.n_boxes
+    _check(boxes, torch.float32, (n, 4), "boxes")
+    _check(box_canvas, torch.int32, (n,), "box_canvas")
+    a = UnstitchArgs()
+    a.boxes, a.box_canvas, a.n_boxes = boxes.data_ptr(), box_canvas.data_ptr(), n
+    a.rois, a.place = dplan.rois.data_ptr(), dplan.place.data_ptr()
+    a.order, a.canvas_begin = dplan.order.data_ptr(), dplan.canvas_begin.data_ptr()
+    a.n_rois, a.n_canvases, a.clip = dplan.n_rois, dplan.n_canvases, int(bool(clip))
+    a.roi_of_box, a.dets, a.n_out = (bufs.roi_of_box.data_ptr(), bufs.dets.data_ptr(),
+                                     bufs.n_out.data_ptr())
+    a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    return a
+
+
+def unstitch(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers,
+             stream=None) -> None:
+    """Enqueue tg_unstitch; results land in `bufs`."""
+    a = unstitch_args(boxes, box_canvas, dplan, clip, bufs)
+    rc = lib().tg_unstitch(ctypes.byref(a), _stream_handle(stream))
+    if rc != OK:
+        raise TgError("tg_unstitch", rc)
+
+
+def unstitch_raw(args: UnstitchArgs, stream=None) -> int:
+    return int(lib().tg_unstitch(ctypes.byref(args), _stream_handle(stream)))

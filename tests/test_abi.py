@@ -1,0 +1,169 @@
+"""The C ABI: the library loads, exports every function tg.h declares, the ctypes
+structs match the header's layout, and argument validation rejects bad calls before
+any HIP work (so these run without a GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2404_09267_amd import tg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tg.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tg_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == set(tg.EXPORTS)
+    L = tg.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_abi_version():
+    assert tg.lib().tg_abi_version() == 1
+
+
+def test_strerror():
+    for code in range(0, -8, -1):
+        assert tg.strerror(code) not in ("", "unknown status")
+    assert tg.strerror(-99) == "unknown status"
+
+
+def _c_layout(tmp_path):
+    src = tmp_path / "layout.c"
+    src.write_text(r"""
+#include <stdio.h>
+#include <stddef.h>
+#include "tg.h"
+#define F(T, m) printf(#T "." #m " %zu\n", offsetof(T, m))
+int main(void) {
+  printf("tg_roi %zu\ntg_place %zu\ntg_box %zu\ntg_det %zu\ntg_pack_params %zu\n",
+         sizeof(tg_roi), sizeof(tg_place), sizeof(tg_box), sizeof(tg_det), sizeof(tg_pack_params));
+  printf("tg_stitch_args %zu\ntg_unstitch_args %zu\n", sizeof(tg_stitch_args), sizeof(tg_unstitch_args));
+  F(tg_stitch_args, frames); F(tg_stitch_args, frame_stride); F(tg_stitch_args, n_frames);
+  F(tg_stitch_args, row_pitch); F(tg_stitch_args, rois); F(tg_stitch_args, canvas_begin);
+  F(tg_stitch_args, n_rois); F(tg_stitch_args, canvas_first); F(tg_stitch_args, canvas_h);
+  F(tg_stitch_args, mean); F(tg_stitch_args, std); F(tg_stitch_args, pad); F(tg_stitch_args, out);
+  F(tg_unstitch_args, boxes); F(tg_unstitch_args, n_boxes); F(tg_unstitch_args, rois);
+  F(tg_unstitch_args, n_rois); F(tg_unstitch_args, clip); F(tg_unstitch_args, roi_of_box);
+  F(tg_unstitch_args, n_out); F(tg_unstitch_args, workspace); F(tg_unstitch_args, workspace_bytes);
+  return 0;
+}
+""")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    return dict(line.rsplit(" ", 1) for line in out.strip().splitlines())
+
+
+def test_struct_layout_matches_header(tmp_path):
+    c = {k: int(v) for k, v in _c_layout(tmp_path).items()}
+    assert c["tg_roi"] == 20 and c["tg_place"] == 12 and c["tg_box"] == 16 and c["tg_det"] == 28
+    assert c["tg_roi"] == tg.ROI_DTYPE.itemsize and c["tg_det"] == tg.DET_DTYPE.itemsize
+    assert c["tg_pack_params"] == ctypes.sizeof(tg.PackParams)
+    assert c["tg_stitch_args"] == ctypes.sizeof(tg.StitchArgs)
+    assert c["tg_unstitch_args"] == ctypes.sizeof(tg.UnstitchArgs)
+    for key, off in c.items():
+        if "." not in key:
+            continue
+        struct, field = key.split(".")
+        py = tg.StitchArgs if struct == "tg_stitch_args" else tg.UnstitchArgs
+        assert getattr(py, field).offset == off, key
+
+
+def _valid_stitch_args():
+    a = tg.StitchArgs()
+    a.frames = 0x1000
+    a.frame_stride = 64 * 64 * 3
+    a.n_frames, a.frame_w, a.frame_h, a.row_pitch = 1, 64, 64, 192
+    a.rois = a.place = a.order = a.canvas_begin = 0x2000
+    a.n_rois, a.n_canvases, a.canvas_first, a.canvas_count = 4, 2, 0, 0
+    a.canvas_w = a.canvas_h = 32
+    a.mean[:] = [0.0, 0.0, 0.0]
+    a.std[:] = [1.0, 1.0, 1.0]
+    a.out = 0x3000
+    return a
+
+
+def _raw_stitch(a):
+    return int(tg.lib().tg_stitch(ctypes.byref(a), None))
+
+
+def test_stitch_validation_without_gpu():
+    """Every rejection happens before any HIP call; canvas_count == 0 is a no-op."""
+    a = _valid_stitch_args()
+    assert _raw_stitch(a) == tg.OK  # nothing to do
+    assert int(tg.lib().tg_stitch(None, None)) == tg.E_INVAL
+    cases = [("canvas_w", 0, tg.E_INVAL), ("frame_h", 0, tg.E_INVAL),
+             ("row_pitch", 191, tg.E_INVAL), ("frame_stride", 100, tg.E_INVAL),
+             ("canvas_count", -1, tg.E_INVAL), ("canvas_first", -1, tg.E_INVAL),
+             ("n_rois", -1, tg.E_INVAL)]
+    for field, val, code in cases:
+        b = _valid_stitch_args()
+        setattr(b, field, val)
+        assert _raw_stitch(b) == code, field
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        b = _valid_stitch_args()
+        b.std[1] = bad
+        assert _raw_stitch(b) == tg.E_INVAL
+    b = _valid_stitch_args()
+    b.mean[2] = float("nan")
+    assert _raw_stitch(b) == tg.E_INVAL
+    b = _valid_stitch_args()
+    b.canvas_first, b.canvas_count = 1, 2
+    assert _raw_stitch(b) == tg.E_RANGE
+    b = _valid_stitch_args()
+    b.canvas_count = 1
+    b.out = None
+    assert _raw_stitch(b) == tg.E_INVAL
+
+
+def test_unstitch_validation_without_gpu():
+    a = tg.UnstitchArgs()
+    a.n_boxes = -1
+    a.n_out = 0x1000
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_INVAL
+    a.n_boxes = 10
+    a.n_out = None
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_INVAL
+    a.n_out = 0x1000
+    a.boxes = a.box_canvas = a.roi_of_box = a.dets = 0x2000
+    a.rois = a.place = a.order = a.canvas_begin = 0x3000
+    a.n_rois, a.n_canvases = 3, 1
+    a.workspace, a.workspace_bytes = 0x4000, tg.unstitch_workspace_bytes(10) - 1
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.workspace = None
+    a.workspace_bytes = 1 << 20
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.workspace = 0x4004  # misaligned
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.workspace = 0x4000
+    a.rois = None
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_INVAL
+
+
+def test_workspace_sizes():
+    assert tg.unstitch_workspace_bytes(0) == 0
+    assert tg.unstitch_workspace_bytes(-5) == 0
+    assert tg.unstitch_workspace_bytes(1) == 16
+    assert tg.unstitch_workspace_bytes(256) == 16
+    assert tg.unstitch_workspace_bytes(257) == 24
+    assert tg.unstitch_workspace_bytes(200000) == 8 * (1 + 782)
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(tg, "LIB_PATH", str(tmp_path / "nope.so"))
+    monkeypatch.setattr(tg, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        tg.lib()

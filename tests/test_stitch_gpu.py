@@ -1,0 +1,247 @@
+"""tg_stitch on the GPU against the oracle (pixels within 1 fp16 ulp, pad bit-exact;
+the library's table design makes it bit-exact everywhere, which is checked too)."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_helpers import (SENTINEL, assert_stitch_parity, coverage, oracle_plan, run_stitch,
+                         say)
+from paper_2404_09267_amd import tg
+from paper_2404_09267_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    tg.lib()
+    return torch
+
+
+def _case(torch, rng, n_frames, fh, fw, cw, ch, n, lo, hi_w, hi_h, policy, mean=W.MEAN,
+          std=W.STD, pad=W.PAD):
+    rois = W.random_rois(rng, n, n_frames, fw, fh, lo, min(hi_w, cw), min(hi_h, ch))
+    frames = W.random_frames_np(n_frames, fh, fw, int(rng.integers(1 << 30)))
+    plan = tg.plan_pack(rois, cw, ch, fw, fh, n_frames, policy)
+    frames_d = torch.from_numpy(frames).cuda()
+    got = run_stitch(frames_d, rois, plan, 0, plan.n_canvases, cw, ch, mean, std, pad)
+    want = oracle.stitch(frames, rois, oracle_plan(plan), 0, plan.n_canvases, cw, ch,
+                         mean, std, pad)
+    cov = coverage(plan, rois, 0, plan.n_canvases, cw, ch)
+    assert_stitch_parity(got, want, cov)
+    np.testing.assert_array_equal(got, want)  # bit-exact by design
+    return plan
+
+
+@pytest.mark.parametrize("cw,ch", [(64, 48), (256, 32), (264, 40), (8, 8), (300, 70),
+                                   (37, 29), (1, 1), (513, 33), (5, 300)])
+def test_small_random_plans(torch, cw, ch):
+    rng = np.random.default_rng(cw * 1000 + ch)
+    for policy in (0, 1, 2):
+        say("small", cw, ch, "policy", policy)
+        _case(torch, rng, 3, 70, 91, cw, ch, 60, 1, 40, 40, policy)
+
+
+def test_odd_frame_widths_and_mean_std(torch):
+    rng = np.random.default_rng(77)
+    for fw in (1, 2, 3, 5, 37, 101):
+        say("frame width", fw)
+        _case(torch, rng, 2, 23, fw, 72, 40, 30, 1, 16, 16, 0, mean=(0, 0, 0),
+              std=(255, 255, 255), pad=(0, 128, 255))
+        _case(torch, rng, 2, 23, fw, 72, 40, 30, 1, 16, 16, 2, mean=(10.5, 300.0, -7.25),
+              std=(0.01, 1000.0, 3.5), pad=(255, 0, 7))
+
+
+def test_many_patches_per_tile_take_extra_passes(torch):
+    """Over 253 patches touching one tile: tiny RoIs, including 1 x 1."""
+    rng = np.random.default_rng(5)
+    for cw, ch, n, lo, hi, pol in [(64, 64, 3000, 1, 1, 0), (64, 64, 1500, 1, 3, 0),
+                                   (256, 32, 2000, 1, 4, 2), (300, 64, 600, 1, 2, 1),
+                                   (64, 8, 254, 1, 1, 1), (64, 8, 253, 1, 1, 1),
+                                   (256, 32, 8192, 1, 1, 1)]:
+        say("dense", cw, ch, n, lo, hi, pol)
+        plan = _case(torch, rng, 2, 50, 60, cw, ch, n, lo, hi, hi, pol)
+        assert np.diff(plan.canvas_begin).max() >= min(n, 253)
+
+
+def test_roi_at_end_of_frame_buffer(torch):
+    """Patches that end on the frame buffer's last byte (no over-read past it)."""
+    for fw, fh in [(40, 30), (41, 30), (42, 31), (43, 17)]:
+        rois = np.array([[1, fw - 9, fh - 5, 9, 5], [1, fw - 17, fh - 1, 17, 1],
+                         [0, 0, 0, 8, 8], [1, fw - 1, fh - 1, 1, 1]])
+        frames = W.random_frames_np(2, fh, fw, fw)
+        for policy in (0, 2):
+            say("end of buffer", fw, fh, policy)
+            plan = tg.plan_pack(rois, 24, 24, fw, fh, 2, policy)
+            got = run_stitch(torch.from_numpy(frames).cuda(), rois, plan, 0, plan.n_canvases,
+                             24, 24)
+            want = oracle.stitch(frames, rois, oracle_plan(plan), 0, plan.n_canvases, 24, 24,
+                                 W.MEAN, W.STD, W.PAD)
+            np.testing.assert_array_equal(got, want)
+
+
+def test_whole_frame_is_plain_normalise(torch):
+    """One patch = whole frame = canvas: torch's own normalise, within 1 ulp."""
+    from gpu_helpers import half_ord
+
+    say("whole frame")
+    frames = torch.randint(0, 256, (2, 96, 160, 3), dtype=torch.uint8, device="cuda",
+                           generator=torch.Generator(device="cuda").manual_seed(9))
+    rois = np.array([[1, 0, 0, 160, 96]])
+    plan = tg.plan_pack(rois, 160, 96, 160, 96, 2, 0)
+    got = run_stitch(frames, rois, plan, 0, 1, 160, 96)[0]
+    mean = torch.tensor(W.MEAN, device="cuda").view(3, 1, 1)
+    std = torch.tensor(W.STD, device="cuda").view(3, 1, 1)
+    ref = ((frames[1].permute(2, 0, 1).float() - mean) / std).half()
+    ref = ref.cpu().numpy().view(np.uint16)
+    assert np.abs(half_ord(got) - half_ord(ref)).max() <= 1
+
+
+def test_canvas_ranges_and_misaligned_output(torch):
+    rng = np.random.default_rng(12)
+    rois = W.random_rois(rng, 400, 2, 500, 400, 8, 120, 120)
+    frames = W.random_frames_np(2, 400, 500, 3)
+    frames_d = torch.from_numpy(frames).cuda()
+    plan = tg.plan_pack(rois, 256, 256, 500, 400, 2, 0)
+    assert plan.n_canvases >= 4
+    want = oracle.stitch(frames, rois, oracle_plan(plan), 0, plan.n_canvases, 256, 256,
+                         W.MEAN, W.STD, W.PAD)
+    dplan = tg.DevicePlan(rois, plan)
+    for first, count in [(0, 1), (1, 2), (plan.n_canvases - 1, 1), (0, plan.n_canvases)]:
+        say("range", first, count)
+        got = run_stitch(frames_d, rois, plan, first, count, 256, 256, dplan=dplan)
+        np.testing.assert_array_equal(got, want[first:first + count])
+    say("count 0")
+    empty = torch.empty((0, 3, 256, 256), dtype=torch.int16, device="cuda")
+    tg.stitch(frames_d, dplan, 0, 0, 256, 256, W.MEAN, W.STD, W.PAD, empty)
+    with pytest.raises(tg.TgError):
+        tg.stitch(frames_d, dplan, plan.n_canvases, 1, 256, 256, W.MEAN, W.STD, W.PAD,
+                  torch.empty((1, 3, 256, 256), dtype=torch.int16, device="cuda"))
+    say("misaligned out")  # element offset 1: 2-byte aligned only -> generic path
+    buf = torch.full((2 * 3 * 256 * 256 + 1,), SENTINEL, dtype=torch.int16, device="cuda")
+    out = buf[1:].view(2, 3, 256, 256)
+    tg.stitch(frames_d, dplan, 1, 2, 256, 256, W.MEAN, W.STD, W.PAD, out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint16), want[1:3])
+    assert buf[0].item() == SENTINEL  # nothing written before the view
+
+
+def test_corrupt_plan_entries_are_skipped(torch):
+    """Out-of-range ids, wrong canvas, rects leaving canvas or frame: read as pad."""
+    rng = np.random.default_rng(6)
+    rois = W.random_rois(rng, 60, 2, 120, 90, 4, 30, 30)
+    frames = W.random_frames_np(2, 90, 120, 4)
+    plan = tg.plan_pack(rois, 128, 128, 120, 90, 2, 0)
+    assert plan.canvas_begin[1] >= 5
+    bad_rois, bad_place, bad_order = rois.copy(), plan.place.copy(), plan.order.copy()
+    victims = plan.order[plan.canvas_begin[0]:plan.canvas_begin[1]][:5]
+    bad_order[plan.canvas_begin[0]] = 10_000            # id out of range
+    bad_place[victims[1], 0] = 99                        # names another canvas
+    bad_place[victims[2], 1] = 128 - rois[victims[2], 3] + 1  # leaves the canvas
+    bad_rois[victims[3], 0] = 5                          # frame id out of range
+    bad_rois[victims[4], 1] = 120 - rois[victims[4], 3] + 1  # leaves the frame
+    skipped = set(victims.tolist())
+    keep = [i for i in plan.order if i not in skipped]
+    # the oracle's answer for the plan without the corrupt entries
+    cb = [0]
+    for j in range(plan.n_canvases):
+        seg = [i for i in plan.order[plan.canvas_begin[j]:plan.canvas_begin[j + 1]]
+               if i not in skipped]
+        cb.append(cb[-1] + len(seg))
+    clean = oracle.Plan(plan.place, np.array(keep, np.int32), np.array(cb, np.int32),
+                        plan.n_canvases)
+    want = oracle.stitch(frames, rois, clean, 0, plan.n_canvases, 128, 128, W.MEAN, W.STD,
+                         W.PAD)
+    say("corrupt plan")
+    corrupt = tg.Plan(bad_place, bad_order, plan.canvas_begin, plan.n_canvases)
+    got = run_stitch(torch.from_numpy(frames).cuda(), bad_rois, corrupt, 0, plan.n_canvases,
+                     128, 128)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_empty_canvas_is_all_pad(torch):
+    rois = np.array([[0, 0, 0, 4, 4], [0, 4, 4, 4, 4]])
+    place = np.array([[0, 0, 0], [2, 3, 3]], np.int32)
+    plan = tg.Plan(place, np.array([0, 1], np.int32), np.array([0, 1, 1, 2], np.int32), 3)
+    frames = W.random_frames_np(1, 8, 8, 1)
+    say("empty canvas")
+    got = run_stitch(torch.from_numpy(frames).cuda(), rois, plan, 0, 3, 16, 16)
+    want = oracle.stitch(frames, rois, oracle_plan(plan), 0, 3, 16, 16, W.MEAN, W.STD, W.PAD)
+    np.testing.assert_array_equal(got, want)
+    table = oracle.norm_table(W.MEAN, W.STD)
+    for k in range(3):
+        assert np.all(got[1, k] == table[k][W.PAD[k]])
+
+
+def test_deterministic(torch):
+    wl = W.WORKLOADS["cam5_4k"]
+    rois = W.make_rois(wl)
+    frames_d = W.make_frames(wl, "cuda")
+    plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
+    say("determinism")
+    a = run_stitch(frames_d, rois, plan, 0, plan.n_canvases, wl.canvas, wl.canvas)
+    b = run_stitch(frames_d, rois, plan, 0, plan.n_canvases, wl.canvas, wl.canvas,
+                   sentinel=False)
+    np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("name,policy", [("cam1_1080p", 0), ("cam5_4k", 0), ("cam20_4k", 0),
+                                         ("cam20_4k", 2), ("small_roi_8cam", 0),
+                                         ("small_roi_8cam", 1)])
+def test_workload_full_parity(torch, name, policy):
+    """Whole workloads, batch by batch as the bench launches them, against the oracle."""
+    wl = W.WORKLOADS[name]
+    say("workload", name, "policy", policy)
+    rois = W.make_rois(wl)
+    frames_d = W.make_frames(wl, "cuda")
+    plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, policy)
+    dplan = tg.DevicePlan(rois, plan)
+    frames = frames_d.cpu().numpy()
+    for k in range(tg.batch_count(plan.n_canvases, wl.batch_cap)):
+        first, count = tg.batch_range(plan.n_canvases, wl.batch_cap, k)
+        say("  batch", k, first, count)
+        got = run_stitch(frames_d, rois, plan, first, count, wl.canvas, wl.canvas, dplan=dplan)
+        want = oracle.stitch(frames, rois, oracle_plan(plan), first, count, wl.canvas,
+                             wl.canvas, W.MEAN, W.STD, W.PAD)
+        cov = coverage(plan, rois, first, count, wl.canvas, wl.canvas)
+        assert_stitch_parity(got, want, cov)
+        np.testing.assert_array_equal(got, want)
+
+
+def test_window_sampled_batches(torch):
+    """The 64-camera x 30-frame window (about 48 GB of frames resident): first, middle
+    and last batch. Every patch is read back against the oracle's normalisation of
+    its crop, and every uncovered pixel must be the pad value."""
+    wl = W.WORKLOADS["window_64x30"]
+    say("window: plan + frames")
+    rois = W.make_rois(wl)
+    plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
+    rc, _, oplan = oracle.pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h,
+                               wl.n_frames, 0)
+    np.testing.assert_array_equal(plan.place, oplan.place)
+    frames_d = W.make_frames(wl, "cuda")
+    dplan = tg.DevicePlan(rois, plan)
+    table = oracle.norm_table(W.MEAN, W.STD)
+    nb = tg.batch_count(plan.n_canvases, wl.batch_cap)
+    for k in sorted({0, nb // 2, nb - 1}):
+        first, count = tg.batch_range(plan.n_canvases, wl.batch_cap, k)
+        say("window batch", k, first, count)
+        got = run_stitch(frames_d, rois, plan, first, count, wl.canvas, wl.canvas, dplan=dplan)
+        assert not np.any(got == SENTINEL)
+        cov = np.zeros((count, wl.canvas, wl.canvas), dtype=bool)
+        for j in range(first, first + count):
+            for i in plan.order[plan.canvas_begin[j]:plan.canvas_begin[j + 1]]:
+                f, sx, sy, w, h = rois[i]
+                _, dx, dy = plan.place[i]
+                crop = frames_d[f, sy:sy + h, sx:sx + w].cpu().numpy()
+                for ch in range(3):
+                    np.testing.assert_array_equal(got[j - first, ch, dy:dy + h, dx:dx + w],
+                                                  table[ch][crop[..., ch]])
+                cov[j - first, dy:dy + h, dx:dx + w] = True
+        for ch in range(3):
+            assert np.all(got[:, ch][~cov] == table[ch][W.PAD[ch]])
+    del frames_d
+    torch.cuda.empty_cache()
