@@ -5,16 +5,19 @@
 // pixel is either the normalised byte of the one patch that covers it or the
 // normalised pad byte.
 //
-// Design for gfx950 (wave64, 160 KB LDS per CU, HBM-bound):
+// Design for gfx950 (wave64, 160 KB LDS per CU, HBM-bound, write-dominated):
 //  - One 256-thread workgroup per TILE_H x TILE_W canvas tile; grid = tiles x canvases.
 //  - The workgroup lists the patches of its canvas that touch the tile with a wave
-//    ballot and an mbcnt prefix (at most SLOTS per pass; more take extra passes), and
-//    paints a per-pixel owner map (one byte per pixel) in LDS.
-//  - Each thread then owns 8-pixel groups of a tile row. A group owned by one patch
-//    reads its 24 source bytes as 4-byte-aligned dwords realigned in registers, turns
-//    every byte into binary16 through a 3 x 256 table in LDS, and writes three 16-byte
-//    stores (one per plane); pad groups store the pad constants. Mixed groups fall
-//    back to per-pixel byte loads.
+//    ballot and an mbcnt prefix (at most kSlots per pass; more take extra passes), and
+//    paints a one-byte-per-pixel owner map of the tile in LDS, one thread per
+//    (patch, row) pair.
+//  - Each thread owns four 8-pixel groups of the tile. A group owned by one patch reads
+//    its 24 source bytes as 4-byte-aligned dwords realigned in registers, turns every
+//    byte into binary16 through a 3 x 256 table in LDS and writes three 16-byte
+//    nontemporal stores; a pad group stores the pad constants.
+//  - Groups that straddle a patch edge are queued in LDS and finished afterwards by
+//    the whole workgroup, one pixel per lane, so per-pixel loads run with full lanes
+//    instead of serialising every wave that holds one such group.
 //  - The table holds the correctly rounded binary16 of (x - mean_k) / std_k for each
 //    byte x, computed on the host in double; the kernel is therefore bit-exact for
 //    patch pixels and pad alike.
@@ -60,6 +63,15 @@ __device__ __forceinline__ uint32_t lane_rank(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
+// Paint owner bytes [a, b) of one tile row with `id`: single bytes up to 16-byte
+// alignment, then 16-byte stores, then the tail.
+__device__ __forceinline__ void paint(uint8_t *row, int a, int b, uint32_t id) {
+  const uint32_t v = id * 0x01010101u;
+  while (a < b && (a & 15)) row[a++] = static_cast<uint8_t>(id);
+  for (; a + 16 <= b; a += 16) *reinterpret_cast<u32x4 *>(row + a) = u32x4{v, v, v, v};
+  while (a < b) row[a++] = static_cast<uint8_t>(id);
+}
+
 // One group of 8 pixels: the three planes' eight halves packed two per dword.
 struct Group {
   uint32_t p[3][4];
@@ -96,6 +108,8 @@ __global__ __launch_bounds__(kThreads) void stitch_kernel(const StitchParams P) 
   __shared__ int16_t s_rect[kSlots][4];  // tile-local x0, y0, x1, y1 (half-open)
   __shared__ int32_t s_wave_hits[kThreads / 64];
   __shared__ int32_t s_resume;
+  __shared__ int16_t s_mixed[kGroups];
+  __shared__ int32_t s_n_mixed;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -194,110 +208,92 @@ __global__ __launch_bounds__(kThreads) void stitch_kernel(const StitchParams P) 
       own32[i] = v;
     }
     __syncthreads();
-    {
-      // Work items are (slot, 8-row block), dealt round-robin to the four waves; a
-      // wave paints its item as lanes over (row, dword column).
-      int q = 0;
-      for (int s = 0; s < n_slots; ++s) {
-        const int x0 = s_rect[s][0], y0 = s_rect[s][1], x1 = s_rect[s][2], y1 = s_rect[s][3];
-        const uint32_t id = static_cast<uint32_t>(s + 1);
-        const int d0 = x0 >> 2, d1 = (x1 - 1) >> 2;
-        const int nd = d1 - d0 + 1;
-        int lg = 0;
-        while ((1 << lg) < nd) ++lg;
-        const int rows_per_step = 64 >> lg;
-        for (int yb = y0; yb < y1; yb += 8, ++q) {
-          if ((q & 3) != wave) continue;
-          const int ye = min(yb + 8, y1);
-          const int dcol = lane & ((1 << lg) - 1);
-          if (dcol >= nd) continue;
-          const int d = d0 + dcol;
-          const int bx0 = max(x0, 4 * d), bx1 = min(x1, 4 * d + 4);
-          for (int y = yb + (lane >> lg); y < ye; y += rows_per_step) {
-            uint8_t *row = s_owner + y * kTileW;
-            if (bx1 - bx0 == 4) {
-              *reinterpret_cast<uint32_t *>(row + 4 * d) = id * 0x01010101u;
-            } else {
-              for (int x = bx0; x < bx1; ++x) row[x] = static_cast<uint8_t>(id);
-            }
-          }
-        }
-      }
+    for (int t = tid; t < n_slots * kTileH; t += kThreads) {
+      const int sl = t / kTileH, y = t % kTileH;
+      if (y < s_rect[sl][1] || y >= s_rect[sl][3]) continue;
+      paint(s_owner + y * kTileW, s_rect[sl][0], s_rect[sl][2], static_cast<uint32_t>(sl + 1));
     }
     __syncthreads();
 
-    // ---- write the tile ---------------------------------------------------------
+    // ---- write the tile: whole groups now, groups straddling an edge queued --------
+    if (tid == 0) s_n_mixed = 0;
+    __syncthreads();
     for (int g = tid; g < kGroups; g += kThreads) {
       const int r = g / kGroupsX;
       const int X0l = (g % kGroupsX) * 8;
       if (r >= th || X0l >= tw) continue;
-      const int Y = Y_t + r, X0 = X_t + X0l;
       const uint64_t own = *reinterpret_cast<const uint64_t *>(s_owner + r * kTileW + X0l);
       const uint32_t lo = static_cast<uint32_t>(own), hi = static_cast<uint32_t>(own >> 32);
       const uint32_t o0 = lo & 0xFFu;
+      if (!(lo == hi && lo == o0 * 0x01010101u)) {
+        s_mixed[atomicAdd(&s_n_mixed, 1)] = static_cast<int16_t>(g);
+        continue;
+      }
+      if (o0 == kDone || (o0 == 0 && !final_pass)) continue;
+      const int Y = Y_t + r, X0 = X_t + X0l;
       Group G;
-      uint32_t mask = 0xFFu;
-      if (lo == hi && lo == o0 * 0x01010101u) {
-        if (o0 == kDone || (o0 == 0 && !final_pass)) continue;
-        if (o0 == 0) {
-#pragma unroll
-          for (int k = 0; k < 3; ++k)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) G.p[k][j] = P.pad2[k];
-        } else {
-          const int64_t a = s_base[o0 - 1] + static_cast<int64_t>(Y) * P.row_pitch + 3 * X0;
-          // Realign through pointer arithmetic (not an integer round trip) so the
-          // loads stay in the global address space.
-          const uint8_t *src = P.frames + a;
-          const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(src) & 3u);
-          const uint32_t *q = reinterpret_cast<const uint32_t *>(src - sh);
-          const u32x4a4 v0 = *reinterpret_cast<const u32x4a4 *>(q);
-          const u32x2a4 v1 = *reinterpret_cast<const u32x2a4 *>(q + 4);
-          // The 7th dword holds a wanted byte only when the start is unaligned;
-          // reading it otherwise could step past the end of the frame buffer.
-          const uint32_t d6 = sh ? q[6] : 0u;
-          const uint32_t d[7] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, d6};
-          uint32_t e[6];
-#pragma unroll
-          for (int j = 0; j < 6; ++j) e[j] = __builtin_amdgcn_alignbyte(d[j + 1], d[j], sh);
-#pragma unroll
-          for (int k = 0; k < 3; ++k) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int b0 = 3 * (2 * j) + k, b1 = 3 * (2 * j + 1) + k;
-              const uint32_t x0 = (e[b0 >> 2] >> (8 * (b0 & 3))) & 0xFFu;
-              const uint32_t x1 = (e[b1 >> 2] >> (8 * (b1 & 3))) & 0xFFu;
-              G.p[k][j] = uint32_t(s_lut[k * 256 + x0]) | (uint32_t(s_lut[k * 256 + x1]) << 16);
-            }
-          }
-        }
-      } else {
-        mask = 0;
+      if (o0 == 0) {
 #pragma unroll
         for (int k = 0; k < 3; ++k)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) G.p[k][j] = 0;
+          for (int j = 0; j < 4; ++j) G.p[k][j] = P.pad2[k];
+      } else {
+        // Realign through pointer arithmetic (not an integer round trip) so the loads
+        // stay in the global address space.
+        const uint8_t *src = P.frames + s_base[o0 - 1] + static_cast<int64_t>(Y) * P.row_pitch +
+                             3 * X0;
+        const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(src) & 3u);
+        const uint32_t *q = reinterpret_cast<const uint32_t *>(src - sh);
+        const u32x4a4 v0 = *reinterpret_cast<const u32x4a4 *>(q);
+        const u32x2a4 v1 = *reinterpret_cast<const u32x2a4 *>(q + 4);
+        // The 7th dword holds a wanted byte only when the start is unaligned; reading it
+        // otherwise could step past the end of the frame buffer.
+        const uint32_t d6 = sh ? q[6] : 0u;
+        const uint32_t d[7] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, d6};
+        uint32_t e[6];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t o = static_cast<uint32_t>(own >> (8 * i)) & 0xFFu;
-          uint32_t h[3];
-          if (o == kDone || (o == 0 && !final_pass)) continue;
-          if (o == 0) {
+        for (int j = 0; j < 6; ++j) e[j] = __builtin_amdgcn_alignbyte(d[j + 1], d[j], sh);
 #pragma unroll
-            for (int k = 0; k < 3; ++k) h[k] = P.pad2[k] & 0xFFFFu;
-          } else {
-            const uint8_t *px = P.frames + s_base[o - 1] + static_cast<int64_t>(Y) * P.row_pitch +
-                                3 * static_cast<int64_t>(X0 + i);
+        for (int k = 0; k < 3; ++k) {
 #pragma unroll
-            for (int k = 0; k < 3; ++k) h[k] = s_lut[k * 256 + px[k]];
+          for (int j = 0; j < 4; ++j) {
+            const int b0 = 3 * (2 * j) + k, b1 = 3 * (2 * j + 1) + k;
+            const uint32_t x0 = (e[b0 >> 2] >> (8 * (b0 & 3))) & 0xFFu;
+            const uint32_t x1 = (e[b1 >> 2] >> (8 * (b1 & 3))) & 0xFFu;
+            G.p[k][j] = uint32_t(s_lut[k * 256 + x0]) | (uint32_t(s_lut[k * 256 + x1]) << 16);
           }
-          mask |= 1u << i;
-#pragma unroll
-          for (int k = 0; k < 3; ++k) G.p[k][i >> 1] |= h[k] << ((i & 1) * 16);
         }
-        if (!mask) continue;
       }
-      store_group<kVec>(P, c_local, Y, X0, G, mask);
+      store_group<kVec>(P, c_local, Y, X0, G, 0xFFu);
+    }
+    __syncthreads();
+    // Queued groups, one pixel per lane: eight consecutive lanes cover one group, so
+    // their 2-byte stores form one contiguous 16-byte run per plane.
+    {
+      const int n_units = s_n_mixed * 8;
+      const int64_t plane = static_cast<int64_t>(P.canvas_h) * P.canvas_w;
+      uint16_t *obase = P.out + static_cast<int64_t>(c_local) * 3 * plane;
+      for (int u = tid; u < n_units; u += kThreads) {
+        const int g = s_mixed[u >> 3], i = u & 7;
+        const int r = g / kGroupsX, x = (g % kGroupsX) * 8 + i;
+        if (x >= tw) continue;
+        const uint32_t o = s_owner[r * kTileW + x];
+        if (o == kDone || (o == 0 && !final_pass)) continue;
+        const int Y = Y_t + r, X = X_t + x;
+        uint32_t h[3];
+        if (o == 0) {
+#pragma unroll
+          for (int k = 0; k < 3; ++k) h[k] = P.pad2[k] & 0xFFFFu;
+        } else {
+          const uint8_t *px = P.frames + s_base[o - 1] + static_cast<int64_t>(Y) * P.row_pitch +
+                              3 * static_cast<int64_t>(X);
+#pragma unroll
+          for (int k = 0; k < 3; ++k) h[k] = s_lut[k * 256 + px[k]];
+        }
+        uint16_t *dst = obase + static_cast<int64_t>(Y) * P.canvas_w + X;
+#pragma unroll
+        for (int k = 0; k < 3; ++k) dst[k * plane] = static_cast<uint16_t>(h[k]);
+      }
     }
     if (final_pass) break;
     first_pass = false;
