@@ -11,13 +11,14 @@
 //    ballot and an mbcnt prefix (at most kSlots per pass; more take extra passes), and
 //    paints a one-byte-per-pixel owner map of the tile in LDS, one thread per
 //    (patch, row) pair.
-//  - Each thread owns four 8-pixel groups of the tile. A group owned by one patch reads
-//    its 24 source bytes as 4-byte-aligned dwords realigned in registers, turns every
-//    byte into binary16 through a 3 x 256 table in LDS and writes three 16-byte
-//    nontemporal stores; a pad group stores the pad constants.
-//  - Groups that straddle a patch edge are queued in LDS and finished afterwards by
-//    the whole workgroup, one pixel per lane, so per-pixel loads run with full lanes
-//    instead of serialising every wave that holds one such group.
+//  - Each thread owns four 8-pixel groups of the tile. A group's pixels come from at
+//    most two patches or the pad: it reads the 24 source bytes of each patch as one
+//    16-byte and one 12-byte load of 4-byte-aligned dwords, realigned in registers,
+//    picks each pixel's byte (the pad byte for pad pixels), turns every byte into
+//    binary16 through a 3 x 256 table in LDS and writes three 16-byte nontemporal
+//    stores.
+//  - Groups with three or more patches, or whose window would leave the frame buffer,
+//    go to a per-wave queue in LDS that the same wave finishes one pixel per lane.
 //  - The table holds the correctly rounded binary16 of (x - mean_k) / std_k for each
 //    byte x, computed on the host in double; the kernel is therefore bit-exact for
 //    patch pixels and pad alike.
@@ -50,12 +51,19 @@ struct StitchParams {
   int32_t n_rois, canvas_first, canvas_w, canvas_h;
   int32_t tiles_x;
   uint16_t *out;
+  // Highest address at which a 28-byte source window may start: the last dword holding
+  // a valid frame byte ends 28 bytes later. Windows are clamped to it so that no load
+  // touches a dword without a valid byte.
+  const uint8_t *window_limit;
+  const uint8_t *window_base;  // first dword holding a frame byte
+  int32_t window_ok;
   uint32_t pad2[3];    // pad value of each channel, replicated in both halves
+  uint32_t pad_byte[3];
   uint32_t lut[384];   // channel k, byte x -> half bits at lut16[k * 256 + x]
 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2a4 __attribute__((ext_vector_type(2), aligned(4)));
+typedef uint32_t u32x3a4 __attribute__((ext_vector_type(3), aligned(4)));
 typedef uint32_t u32x4a4 __attribute__((ext_vector_type(4), aligned(4)));
 
 __device__ __forceinline__ uint32_t lane_rank(uint64_t mask) {
@@ -70,6 +78,37 @@ __device__ __forceinline__ void paint(uint8_t *row, int a, int b, uint32_t id) {
   while (a < b && (a & 15)) row[a++] = static_cast<uint8_t>(id);
   for (; a + 16 <= b; a += 16) *reinterpret_cast<u32x4 *>(row + a) = u32x4{v, v, v, v};
   while (a < b) row[a++] = static_cast<uint8_t>(id);
+}
+
+// The 24 source bytes of eight pixels starting at `src`, realigned into e[0..5]. They
+// lie in the 7 dwords from the one holding the first byte, read as one 16-byte and one
+// 12-byte load. Near the end of the frame buffer the window slides back one dword (only
+// possible when the start is aligned). A window whose dwords would not all hold frame
+// bytes is refused (returns false); windows of pixels that all lie in one patch are
+// never refused.
+__device__ __forceinline__ bool load_window(const StitchParams &P, const uint8_t *src,
+                                            uint32_t e[6]) {
+  const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(src) & 3u);
+  const uint8_t *a0 = src - sh;  // pointer arithmetic keeps the global address space
+  const bool slid = a0 > P.window_limit;
+  if (a0 < P.window_base || (slid && (sh != 0 || a0 > P.window_limit + 4))) return false;
+  const uint32_t *q = reinterpret_cast<const uint32_t *>(slid ? a0 - 4 : a0);
+  const u32x4a4 v0 = *reinterpret_cast<const u32x4a4 *>(q);
+  const u32x3a4 v1 = *reinterpret_cast<const u32x3a4 *>(q + 4);
+  const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, 0u};
+  // Blend with a mask rather than `slid ? w[j + 1] : w[j]`, which the compiler turns
+  // into an indexed private array (scratch memory).
+  const uint32_t m = slid ? ~0u : 0u;
+  uint32_t d[7];
+#pragma unroll
+  for (int j = 0; j < 7; ++j) d[j] = (w[j] & ~m) | (w[j + 1] & m);
+#pragma unroll
+  for (int j = 0; j < 6; ++j) e[j] = __builtin_amdgcn_alignbyte(d[j + 1], d[j], sh);
+  return true;
+}
+
+__device__ __forceinline__ uint32_t byte_of(const uint32_t e[6], int b) {
+  return (e[b >> 2] >> (8 * (b & 3))) & 0xFFu;
 }
 
 // One group of 8 pixels: the three planes' eight halves packed two per dword.
@@ -108,8 +147,7 @@ __global__ __launch_bounds__(kThreads) void stitch_kernel(const StitchParams P) 
   __shared__ int16_t s_rect[kSlots][4];  // tile-local x0, y0, x1, y1 (half-open)
   __shared__ int32_t s_wave_hits[kThreads / 64];
   __shared__ int32_t s_resume;
-  __shared__ int16_t s_mixed[kGroups];
-  __shared__ int32_t s_n_mixed;
+  __shared__ int16_t s_wq[kThreads / 64][kGroups / (kThreads / 64)];  // per-wave queues
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -215,66 +253,86 @@ __global__ __launch_bounds__(kThreads) void stitch_kernel(const StitchParams P) 
     }
     __syncthreads();
 
-    // ---- write the tile: whole groups now, groups straddling an edge queued --------
-    if (tid == 0) s_n_mixed = 0;
-    __syncthreads();
+    // ---- write the tile ------------------------------------------------------------
+    // Each lane takes its 8-pixel groups in turn. A group's pixels come from at most two
+    // patches (A, B) or the pad value: one source window per patch, then per pixel the
+    // byte of its owner (the pad byte for pad pixels: the table maps it to the pad
+    // value). Groups with three or more patches, or whose window would leave the frame
+    // buffer, go to the wave's own queue and are finished by the same wave one pixel
+    // per lane.
+    int n_queued = 0;
+#pragma unroll 1
     for (int g = tid; g < kGroups; g += kThreads) {
       const int r = g / kGroupsX;
       const int X0l = (g % kGroupsX) * 8;
-      if (r >= th || X0l >= tw) continue;
-      const uint64_t own = *reinterpret_cast<const uint64_t *>(s_owner + r * kTileW + X0l);
-      const uint32_t lo = static_cast<uint32_t>(own), hi = static_cast<uint32_t>(own >> 32);
-      const uint32_t o0 = lo & 0xFFu;
-      if (!(lo == hi && lo == o0 * 0x01010101u)) {
-        s_mixed[atomicAdd(&s_n_mixed, 1)] = static_cast<int16_t>(g);
-        continue;
-      }
-      if (o0 == kDone || (o0 == 0 && !final_pass)) continue;
+      // Groups outside the canvas read as all done; every lane still reaches the ballot
+      // below, which keeps the queue count wave-uniform.
+      const bool inside = r < th && X0l < tw;
+      const uint64_t own =
+          inside ? *reinterpret_cast<const uint64_t *>(s_owner + r * kTileW + X0l) : ~uint64_t(0);
       const int Y = Y_t + r, X0 = X_t + X0l;
-      Group G;
-      if (o0 == 0) {
+      uint32_t wmask = 0, A = 0, B = 0, from_b = 0, is_pad = 0;
+      bool queue = false;
 #pragma unroll
-        for (int k = 0; k < 3; ++k)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) G.p[k][j] = P.pad2[k];
-      } else {
-        // Realign through pointer arithmetic (not an integer round trip) so the loads
-        // stay in the global address space.
-        const uint8_t *src = P.frames + s_base[o0 - 1] + static_cast<int64_t>(Y) * P.row_pitch +
-                             3 * X0;
-        const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(src) & 3u);
-        const uint32_t *q = reinterpret_cast<const uint32_t *>(src - sh);
-        const u32x4a4 v0 = *reinterpret_cast<const u32x4a4 *>(q);
-        const u32x2a4 v1 = *reinterpret_cast<const u32x2a4 *>(q + 4);
-        // The 7th dword holds a wanted byte only when the start is unaligned; reading it
-        // otherwise could step past the end of the frame buffer.
-        const uint32_t d6 = sh ? q[6] : 0u;
-        const uint32_t d[7] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, d6};
-        uint32_t e[6];
-#pragma unroll
-        for (int j = 0; j < 6; ++j) e[j] = __builtin_amdgcn_alignbyte(d[j + 1], d[j], sh);
-#pragma unroll
-        for (int k = 0; k < 3; ++k) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int b0 = 3 * (2 * j) + k, b1 = 3 * (2 * j + 1) + k;
-            const uint32_t x0 = (e[b0 >> 2] >> (8 * (b0 & 3))) & 0xFFu;
-            const uint32_t x1 = (e[b1 >> 2] >> (8 * (b1 & 3))) & 0xFFu;
-            G.p[k][j] = uint32_t(s_lut[k * 256 + x0]) | (uint32_t(s_lut[k * 256 + x1]) << 16);
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t o = static_cast<uint32_t>(own >> (8 * i)) & 0xFFu;
+        if (o == kDone) continue;
+        if (o == 0) {
+          if (final_pass) {
+            wmask |= 1u << i;
+            is_pad |= 1u << i;
           }
+          continue;
+        }
+        wmask |= 1u << i;
+        if (A == 0 || o == A) {
+          A = o;
+        } else if (B == 0 || o == B) {
+          B = o;
+          from_b |= 1u << i;
+        } else {
+          queue = true;
         }
       }
-      store_group<kVec>(P, c_local, Y, X0, G, 0xFFu);
+      if (!kVec && X0 + 8 > P.canvas_w) wmask &= (1u << (P.canvas_w - X0)) - 1u;
+      uint32_t eA[6] = {0, 0, 0, 0, 0, 0}, eB[6] = {0, 0, 0, 0, 0, 0};
+      const int64_t row_off = static_cast<int64_t>(Y) * P.row_pitch + 3 * X0;
+      if (!queue && A) queue = !load_window(P, P.frames + s_base[A - 1] + row_off, eA);
+      if (!queue && B) queue = !load_window(P, P.frames + s_base[B - 1] + row_off, eB);
+      if (!P.window_ok && (A || B)) queue = true;
+      const uint64_t qb = __ballot(queue && wmask);
+      if (queue && wmask)
+        s_wq[wave][n_queued + static_cast<int>(lane_rank(qb))] = static_cast<int16_t>(g);
+      n_queued += __popcll(qb);
+      if (queue || !wmask) continue;
+      Group G;
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const uint32_t pk = P.pad_byte[k];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          uint32_t x[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int i = 2 * j + h, b = 3 * i + k;
+            const uint32_t xa = byte_of(eA, b), xb = byte_of(eB, b);
+            x[h] = (is_pad >> i) & 1u ? pk : ((from_b >> i) & 1u ? xb : xa);
+          }
+          G.p[k][j] = uint32_t(s_lut[k * 256 + x[0]]) | (uint32_t(s_lut[k * 256 + x[1]]) << 16);
+        }
+      }
+      store_group<kVec>(P, c_local, Y, X0, G, wmask);
     }
-    __syncthreads();
-    // Queued groups, one pixel per lane: eight consecutive lanes cover one group, so
-    // their 2-byte stores form one contiguous 16-byte run per plane.
-    {
-      const int n_units = s_n_mixed * 8;
+    // The wave's queue: one pixel per lane, eight consecutive lanes per group, so the
+    // 2-byte stores of a group form one contiguous 16-byte run per plane.
+    if (n_queued) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       const int64_t plane = static_cast<int64_t>(P.canvas_h) * P.canvas_w;
       uint16_t *obase = P.out + static_cast<int64_t>(c_local) * 3 * plane;
-      for (int u = tid; u < n_units; u += kThreads) {
-        const int g = s_mixed[u >> 3], i = u & 7;
+      for (int u = lane; u < n_queued * 8; u += 64) {
+        const int g = s_wq[wave][u >> 3], i = u & 7;
         const int r = g / kGroupsX, x = (g % kGroupsX) * 8 + i;
         if (x >= tw) continue;
         const uint32_t o = s_owner[r * kTileW + x];
@@ -363,6 +421,16 @@ extern "C" int tg_stitch(const tg_stitch_args *a, void *stream) {
   P.canvas_h = a->canvas_h;
   P.tiles_x = (a->canvas_w + kTileW - 1) / kTileW;
   P.out = a->out;
+  // One past the last valid frame byte, rounded up to a dword; windows start at most
+  // 28 bytes before it. Frame buffers too small for one window take the per-pixel path.
+  const int64_t valid_end = int64_t(a->n_frames - 1) * a->frame_stride +
+                            int64_t(a->frame_h - 1) * a->row_pitch + 3 * int64_t(a->frame_w);
+  const uintptr_t end4 = (reinterpret_cast<uintptr_t>(a->frames) + uintptr_t(valid_end) + 3) &
+                         ~uintptr_t(3);
+  const uintptr_t begin4 = reinterpret_cast<uintptr_t>(a->frames) & ~uintptr_t(3);
+  P.window_limit = a->frames + (int64_t(end4 - 28) - int64_t(reinterpret_cast<uintptr_t>(a->frames)));
+  P.window_base = a->frames - (reinterpret_cast<uintptr_t>(a->frames) - begin4);
+  P.window_ok = a->n_frames > 0 && end4 >= begin4 + 32;
   uint16_t lut16[768];
   for (int k = 0; k < 3; ++k)
     for (int x = 0; x < 256; ++x)
@@ -371,6 +439,7 @@ extern "C" int tg_stitch(const tg_stitch_args *a, void *stream) {
   for (int k = 0; k < 3; ++k) {
     const uint32_t pv = lut16[k * 256 + a->pad[k]];
     P.pad2[k] = pv | (pv << 16);
+    P.pad_byte[k] = a->pad[k];
   }
   const int tiles_y = (a->canvas_h + kTileH - 1) / kTileH;
   const int64_t tiles = int64_t(P.tiles_x) * tiles_y;
