@@ -5,20 +5,21 @@
 // pixel is either the normalised byte of the one patch that covers it or the
 // normalised pad byte.
 //
-// Design for gfx950 (wave64, 160 KB LDS per CU, HBM-bound, write-dominated):
-//  - One 256-thread workgroup per TILE_H x TILE_W canvas tile; grid = tiles x canvases.
-//  - The workgroup lists the patches of its canvas that touch the tile with a wave
-//    ballot and an mbcnt prefix (at most kSlots per pass; more take extra passes), and
-//    paints a one-byte-per-pixel owner map of the tile in LDS, one thread per
-//    (patch, row) pair.
-//  - Each thread owns four 8-pixel groups of the tile. A group's pixels come from at
-//    most two patches or the pad: it reads the 24 source bytes of each patch as one
-//    16-byte and one 12-byte load of 4-byte-aligned dwords, realigned in registers,
-//    picks each pixel's byte (the pad byte for pad pixels), turns every byte into
-//    binary16 through a 3 x 256 table in LDS and writes three 16-byte nontemporal
-//    stores.
-//  - Groups with three or more patches, or whose window would leave the frame buffer,
-//    go to a per-wave queue in LDS that the same wave finishes one pixel per lane.
+// Design for gfx950 (wave64, 160 KB LDS per CU, 8 XCDs, HBM-bound, write-dominated):
+//  - One 256-thread workgroup per TILE_H x TILE_W canvas tile. Workgroup ids are
+//    remapped so that each XCD (which takes every eighth workgroup) works through a
+//    contiguous range of tiles: horizontally adjacent tiles read the two halves of the
+//    same source lines, which then meet in one L2.
+//  - The tile's pixels are staged in LDS as u8 RGB rows, prefilled with the pad bytes.
+//  - The workgroup lists its canvas's patches that meet the tile with a wave ballot and
+//    an mbcnt prefix (kRecs at a time), and enumerates every (patch, tile row, 16-byte
+//    LDS chunk) triple with a block-wide prefix sum. Each lane copies its chunks: one
+//    16-byte + one 4-byte load of aligned dwords per chunk, realigned with v_alignbyte,
+//    several chunks in flight per lane; chunks at a patch's left or right edge write
+//    only their own bytes.
+//  - Every lane then converts 8-pixel groups from LDS: each byte goes through a 3 x 256
+//    binary16 table in LDS (RGB interleaved in, planar out) and the group leaves as
+//    three 16-byte nontemporal stores, one per plane.
 //  - The table holds the correctly rounded binary16 of (x - mean_k) / std_k for each
 //    byte x, computed on the host in double; the kernel is therefore bit-exact for
 //    patch pixels and pad alike.
@@ -33,12 +34,16 @@
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTileW = 256;   // pixels; 32 groups of 8
+constexpr int kWaves = kThreads / 64;
+constexpr int kTileW = 256;            // pixels
 constexpr int kTileH = 32;
+constexpr int kRowBytes = 3 * kTileW;  // one staged tile row, u8 RGB
+constexpr int kChunksPerRow = kRowBytes / 16;
 constexpr int kGroupsX = kTileW / 8;
 constexpr int kGroups = kGroupsX * kTileH;
-constexpr int kSlots = 253;   // owner ids 1..253; 0 = not covered yet; 255 = written earlier
-constexpr uint8_t kDone = 255;
+constexpr int kRecs = 256;             // patches listed per round
+constexpr int kInFlight = 4;           // chunks whose loads a lane issues before writing
+constexpr int kXcds = 8;
 
 struct StitchParams {
   const uint8_t *frames;
@@ -48,22 +53,20 @@ struct StitchParams {
   const tg_place *place;
   const int32_t *order;
   const int32_t *canvas_begin;
-  int32_t n_rois, canvas_first, canvas_w, canvas_h;
-  int32_t tiles_x;
+  int32_t n_rois, canvas_first, canvas_count, canvas_w, canvas_h;
+  int32_t tiles_x, tiles_per_canvas, n_tiles;
   uint16_t *out;
-  // Highest address at which a 28-byte source window may start: the last dword holding
-  // a valid frame byte ends 28 bytes later. Windows are clamped to it so that no load
-  // touches a dword without a valid byte.
+  // 20-byte source windows start on a dword at or after window_base and at or before
+  // window_limit, so that every dword they touch holds a frame byte. Chunks whose
+  // window would not fit (only at the two ends of the frame buffer) copy byte by byte.
+  const uint8_t *window_base;
   const uint8_t *window_limit;
-  const uint8_t *window_base;  // first dword holding a frame byte
-  int32_t window_ok;
-  uint32_t pad2[3];    // pad value of each channel, replicated in both halves
-  uint32_t pad_byte[3];
+  uint32_t pad_dw[3];  // the pad bytes repeated over 12 bytes (4 pixels), as 3 dwords
   uint32_t lut[384];   // channel k, byte x -> half bits at lut16[k * 256 + x]
 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x3a4 __attribute__((ext_vector_type(3), aligned(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4a4 __attribute__((ext_vector_type(4), aligned(4)));
 
 __device__ __forceinline__ uint32_t lane_rank(uint64_t mask) {
@@ -71,44 +74,15 @@ __device__ __forceinline__ uint32_t lane_rank(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-// Paint owner bytes [a, b) of one tile row with `id`: single bytes up to 16-byte
-// alignment, then 16-byte stores, then the tail.
-__device__ __forceinline__ void paint(uint8_t *row, int a, int b, uint32_t id) {
-  const uint32_t v = id * 0x01010101u;
-  while (a < b && (a & 15)) row[a++] = static_cast<uint8_t>(id);
-  for (; a + 16 <= b; a += 16) *reinterpret_cast<u32x4 *>(row + a) = u32x4{v, v, v, v};
-  while (a < b) row[a++] = static_cast<uint8_t>(id);
-}
-
-// The 24 source bytes of eight pixels starting at `src`, realigned into e[0..5]. They
-// lie in the 7 dwords from the one holding the first byte, read as one 16-byte and one
-// 12-byte load. Near the end of the frame buffer the window slides back one dword (only
-// possible when the start is aligned). A window whose dwords would not all hold frame
-// bytes is refused (returns false); windows of pixels that all lie in one patch are
-// never refused.
-__device__ __forceinline__ bool load_window(const StitchParams &P, const uint8_t *src,
-                                            uint32_t e[6]) {
-  const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(src) & 3u);
-  const uint8_t *a0 = src - sh;  // pointer arithmetic keeps the global address space
-  const bool slid = a0 > P.window_limit;
-  if (a0 < P.window_base || (slid && (sh != 0 || a0 > P.window_limit + 4))) return false;
-  const uint32_t *q = reinterpret_cast<const uint32_t *>(slid ? a0 - 4 : a0);
-  const u32x4a4 v0 = *reinterpret_cast<const u32x4a4 *>(q);
-  const u32x3a4 v1 = *reinterpret_cast<const u32x3a4 *>(q + 4);
-  const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, 0u};
-  // Blend with a mask rather than `slid ? w[j + 1] : w[j]`, which the compiler turns
-  // into an indexed private array (scratch memory).
-  const uint32_t m = slid ? ~0u : 0u;
-  uint32_t d[7];
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int j = 0; j < 7; ++j) d[j] = (w[j] & ~m) | (w[j + 1] & m);
-#pragma unroll
-  for (int j = 0; j < 6; ++j) e[j] = __builtin_amdgcn_alignbyte(d[j + 1], d[j], sh);
-  return true;
-}
-
-__device__ __forceinline__ uint32_t byte_of(const uint32_t e[6], int b) {
-  return (e[b >> 2] >> (8 * (b & 3))) & 0xFFu;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d, 64);
+    if (lane >= d) v += u;
+  }
+  return v;
 }
 
 // One group of 8 pixels: the three planes' eight halves packed two per dword.
@@ -118,11 +92,11 @@ struct Group {
 
 template <bool kVec>
 __device__ __forceinline__ void store_group(const StitchParams &P, int c_local, int Y, int X0,
-                                            const Group &g, uint32_t mask) {
+                                            const Group &g) {
   const int64_t plane = static_cast<int64_t>(P.canvas_h) * P.canvas_w;
   uint16_t *base = P.out + (static_cast<int64_t>(c_local) * 3) * plane +
                    static_cast<int64_t>(Y) * P.canvas_w + X0;
-  if (kVec && mask == 0xFFu) {
+  if (kVec) {  // canvas_w % 8 == 0 and a 16-byte aligned output: whole groups only
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
       u32x4 v = {g.p[k][0], g.p[k][1], g.p[k][2], g.p[k][3]};
@@ -132,50 +106,64 @@ __device__ __forceinline__ void store_group(const StitchParams &P, int c_local, 
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    if (!(mask & (1u << i)) || X0 + i >= P.canvas_w) continue;
+    if (X0 + i >= P.canvas_w) continue;
 #pragma unroll
     for (int k = 0; k < 3; ++k)
       base[k * plane + i] = static_cast<uint16_t>(g.p[k][i >> 1] >> ((i & 1) * 16));
   }
 }
 
+struct Shared {
+  uint16_t lut[3 * 256];
+  int64_t src[kRecs];        // frame offset of the patch's bytes for tile pixel (0, 0)
+  int32_t start[kRecs + 1];  // exclusive prefix of the records' chunk counts
+  int16_t rect[kRecs][4];    // tile-local byte range [b0, b1) of a row; rows [y0, y1)
+  int32_t wave_sum[kWaves];
+  int32_t resume;
+};
+
 template <bool kVec>
 __global__ __launch_bounds__(kThreads) void stitch_kernel(const StitchParams P) {
-  __shared__ uint16_t s_lut[3 * 256];
-  __shared__ __attribute__((aligned(16))) uint8_t s_owner[kTileH * kTileW];
-  __shared__ int64_t s_base[kSlots];
-  __shared__ int16_t s_rect[kSlots][4];  // tile-local x0, y0, x1, y1 (half-open)
-  __shared__ int32_t s_wave_hits[kThreads / 64];
-  __shared__ int32_t s_resume;
-  __shared__ int16_t s_wq[kThreads / 64][kGroups / (kThreads / 64)];  // per-wave queues
+  __shared__ __attribute__((aligned(16))) uint8_t s_px[kTileH * kRowBytes];
+  __shared__ Shared S;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int c_local = blockIdx.y;
+
+  // XCD-aware order: the workgroups of XCD x (ids x, x + 8, ...) take consecutive tiles.
+  const int w = blockIdx.x;
+  const int per = P.n_tiles / kXcds, extra = P.n_tiles % kXcds;
+  const int xcd = w % kXcds;
+  const int L = xcd * per + min(xcd, extra) + w / kXcds;
+  const int c_local = L / P.tiles_per_canvas;
+  const int t_in = L % P.tiles_per_canvas;
   const int canvas = P.canvas_first + c_local;
-  const int tx = blockIdx.x % P.tiles_x;
-  const int ty = blockIdx.x / P.tiles_x;
-  const int X_t = tx * kTileW, Y_t = ty * kTileH;
+  const int X_t = (t_in % P.tiles_x) * kTileW, Y_t = (t_in / P.tiles_x) * kTileH;
   const int tw = min(kTileW, P.canvas_w - X_t);
   const int th = min(kTileH, P.canvas_h - Y_t);
 
-  for (int i = tid; i < 384; i += kThreads) reinterpret_cast<uint32_t *>(s_lut)[i] = P.lut[i];
+  for (int i = tid; i < 384; i += kThreads) reinterpret_cast<uint32_t *>(S.lut)[i] = P.lut[i];
+  // Pad prefill: 16-byte chunk j of a row starts at dword 4j, whose phase in the 3-dword
+  // pad pattern is (4j) mod 3 = j mod 3.
+  for (int i = tid; i < kTileH * kChunksPerRow; i += kThreads) {
+    const int ph = (i % kChunksPerRow) % 3;
+    const u32x4 v = {P.pad_dw[ph], P.pad_dw[(ph + 1) % 3], P.pad_dw[(ph + 2) % 3], P.pad_dw[ph]};
+    *reinterpret_cast<u32x4 *>(s_px + 16 * i) = v;
+  }
 
   // Clamp the canvas's segment of `order` so a corrupt plan cannot index outside it.
   const int k_lo = min(max(P.canvas_begin[canvas], 0), P.n_rois);
   const int k_hi = min(max(P.canvas_begin[canvas + 1], k_lo), P.n_rois);
 
-  int scan = k_lo;
-  bool first_pass = true;
-  for (;;) {
-    // ---- list the patches touching this tile (up to kSlots) -------------------
-    int n_slots = 0;
-    bool overflow = false;
-    while (scan < k_hi && !overflow) {
+  for (int scan = k_lo; scan < k_hi;) {
+    // ---- list up to kRecs patches that meet the tile, in plan order -----------------
+    int n = 0;
+    int resume = k_hi;
+    while (scan < k_hi) {
       const int k = scan + tid;
       bool hit = false;
-      int64_t base = 0;
+      int64_t src = 0;
       int x0 = 0, y0 = 0, x1 = 0, y1 = 0;
       if (k < k_hi) {
         const int id = P.order[k];
@@ -193,169 +181,158 @@ __global__ __launch_bounds__(kThreads) void stitch_kernel(const StitchParams P) 
             x1 = min(pl.x + r.w, X_t + tw) - X_t;
             y1 = min(pl.y + r.h, Y_t + th) - Y_t;
             hit = x0 < x1 && y0 < y1;
-            base = static_cast<int64_t>(r.frame) * P.frame_stride +
-                   static_cast<int64_t>(r.y - pl.y) * P.row_pitch +
-                   3 * static_cast<int64_t>(r.x - pl.x);
+            // canvas pixel (X, Y) of this patch, channel k, is frame byte
+            // src + (Y - Y_t) * row_pitch + 3 * (X - X_t) + k
+            src = static_cast<int64_t>(r.frame) * P.frame_stride +
+                  static_cast<int64_t>(r.y - pl.y + Y_t) * P.row_pitch +
+                  3 * static_cast<int64_t>(r.x - pl.x + X_t);
           }
         }
       }
       const uint64_t ballot = __ballot(hit);
-      if (lane == 0) s_wave_hits[wave] = __popcll(ballot);
-      if (tid == 0) s_resume = -1;
+      if (lane == 0) S.wave_sum[wave] = __popcll(ballot);
+      if (tid == 0) S.resume = k_hi;
       __syncthreads();
-      int before = n_slots, total = 0;
-      for (int w = 0; w < kThreads / 64; ++w) {
-        if (w < wave) before += s_wave_hits[w];
-        total += s_wave_hits[w];
+      int before = n, total = 0;
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) {
+        if (v < wave) before += S.wave_sum[v];
+        total += S.wave_sum[v];
       }
       if (hit) {
         const int slot = before + static_cast<int>(lane_rank(ballot));
-        if (slot < kSlots) {
-          s_base[slot] = base;
-          s_rect[slot][0] = static_cast<int16_t>(x0);
-          s_rect[slot][1] = static_cast<int16_t>(y0);
-          s_rect[slot][2] = static_cast<int16_t>(x1);
-          s_rect[slot][3] = static_cast<int16_t>(y1);
-        } else if (slot == kSlots) {
-          s_resume = k;  // first patch that did not fit: the next pass starts here
+        if (slot < kRecs) {
+          S.src[slot] = src;
+          S.rect[slot][0] = static_cast<int16_t>(3 * x0);
+          S.rect[slot][1] = static_cast<int16_t>(3 * x1);
+          S.rect[slot][2] = static_cast<int16_t>(y0);
+          S.rect[slot][3] = static_cast<int16_t>(y1);
+        } else if (slot == kRecs) {
+          S.resume = k;  // first patch that did not fit: the next round starts here
         }
       }
       __syncthreads();
-      if (n_slots + total > kSlots) {
-        overflow = true;
-        n_slots = kSlots;
-        scan = s_resume;
-      } else {
-        n_slots += total;
-        scan += kThreads;
+      const bool full = n + total > kRecs;
+      resume = S.resume;
+      __syncthreads();  // wave_sum / resume are rewritten by the next round
+      if (full) {
+        n = kRecs;
+        break;
       }
-      __syncthreads();  // s_wave_hits / s_resume are rewritten by the next round
+      n += total;
+      scan += kThreads;
     }
-    const bool final_pass = scan >= k_hi;
+    scan = resume;  // k_hi unless the list filled up
 
-    // ---- owner map: 0 = pad so far, 1..kSlots = slot + 1, kDone = written -------
-    uint32_t *own32 = reinterpret_cast<uint32_t *>(s_owner);
-    for (int i = tid; i < kTileH * kTileW / 4; i += kThreads) {
-      uint32_t v = 0;
-      if (!first_pass) {  // mark every byte painted in an earlier pass as done
-        const uint32_t o = own32[i];
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-          if ((o >> (8 * b)) & 0xFFu) v |= uint32_t(kDone) << (8 * b);
-      }
-      own32[i] = v;
+    // ---- chunk counts and their block-wide exclusive prefix -------------------------
+    int cnt = 0;
+    if (tid < n) {
+      const int b0 = S.rect[tid][0], b1 = S.rect[tid][1];
+      cnt = (S.rect[tid][3] - S.rect[tid][2]) * (((b1 - 1) >> 4) - (b0 >> 4) + 1);
     }
+    const int incl = wave_inclusive_sum(cnt);
+    if (lane == 63) S.wave_sum[wave] = incl;
     __syncthreads();
-    for (int t = tid; t < n_slots * kTileH; t += kThreads) {
-      const int sl = t / kTileH, y = t % kTileH;
-      if (y < s_rect[sl][1] || y >= s_rect[sl][3]) continue;
-      paint(s_owner + y * kTileW, s_rect[sl][0], s_rect[sl][2], static_cast<uint32_t>(sl + 1));
+    int offset = 0, total = 0;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+      if (v < wave) offset += S.wave_sum[v];
+      total += S.wave_sum[v];
     }
+    if (tid < n) S.start[tid] = offset + incl - cnt;
+    if (tid == 0) S.start[n] = total;
     __syncthreads();
 
-    // ---- write the tile ------------------------------------------------------------
-    // Each lane takes its 8-pixel groups in turn. A group's pixels come from at most two
-    // patches (A, B) or the pad value: one source window per patch, then per pixel the
-    // byte of its owner (the pad byte for pad pixels: the table maps it to the pad
-    // value). Groups with three or more patches, or whose window would leave the frame
-    // buffer, go to the wave's own queue and are finished by the same wave one pixel
-    // per lane.
-    int n_queued = 0;
-#pragma unroll 1
-    for (int g = tid; g < kGroups; g += kThreads) {
-      const int r = g / kGroupsX;
-      const int X0l = (g % kGroupsX) * 8;
-      // Groups outside the canvas read as all done; every lane still reaches the ballot
-      // below, which keeps the queue count wave-uniform.
-      const bool inside = r < th && X0l < tw;
-      const uint64_t own =
-          inside ? *reinterpret_cast<const uint64_t *>(s_owner + r * kTileW + X0l) : ~uint64_t(0);
-      const int Y = Y_t + r, X0 = X_t + X0l;
-      uint32_t wmask = 0, A = 0, B = 0, from_b = 0, is_pad = 0;
-      bool queue = false;
+    // ---- copy the patches' rows into the staged tile ---------------------------------
+    for (int base = 0; base < total; base += kThreads * kInFlight) {
+      uint32_t win[kInFlight][5];
+      int dst[kInFlight], lo[kInFlight], hi[kInFlight];
+      const uint8_t *sp[kInFlight];
+      bool fast[kInFlight];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const uint32_t o = static_cast<uint32_t>(own >> (8 * i)) & 0xFFu;
-        if (o == kDone) continue;
-        if (o == 0) {
-          if (final_pass) {
-            wmask |= 1u << i;
-            is_pad |= 1u << i;
+      for (int j = 0; j < kInFlight; ++j) {
+        const int i = base + j * kThreads + tid;
+        dst[j] = -1;
+        lo[j] = hi[j] = 0;
+        sp[j] = P.frames;
+        fast[j] = false;
+        if (i < total) {
+          // the record whose chunk range holds i: the largest r with start[r] <= i
+          int a = 0, b = n - 1;
+          while (a < b) {
+            const int m = (a + b + 1) >> 1;
+            if (S.start[m] <= i)
+              a = m;
+            else
+              b = m - 1;
           }
-          continue;
-        }
-        wmask |= 1u << i;
-        if (A == 0 || o == A) {
-          A = o;
-        } else if (B == 0 || o == B) {
-          B = o;
-          from_b |= 1u << i;
-        } else {
-          queue = true;
+          const int b0 = S.rect[a][0], b1 = S.rect[a][1];
+          const int q0 = b0 >> 4, nq = ((b1 - 1) >> 4) - q0 + 1;
+          const int local = i - S.start[a];
+          const int row = S.rect[a][2] + local / nq;
+          const int q = q0 + local % nq;
+          dst[j] = row * kRowBytes + 16 * q;
+          lo[j] = max(b0 - 16 * q, 0);
+          hi[j] = min(b1 - 16 * q, 16);
+          // staged byte 16q + t of this row comes from frame byte sp + t
+          sp[j] = P.frames + S.src[a] + static_cast<int64_t>(row) * P.row_pitch + 16 * q;
+          const uint8_t *a0 = sp[j] - (reinterpret_cast<uintptr_t>(sp[j]) & 3u);
+          fast[j] = a0 >= P.window_base && a0 <= P.window_limit;
+          if (fast[j]) {
+            const u32x4a4 v = *reinterpret_cast<const u32x4a4 *>(a0);
+            win[j][0] = v.x;
+            win[j][1] = v.y;
+            win[j][2] = v.z;
+            win[j][3] = v.w;
+            win[j][4] = *reinterpret_cast<const uint32_t *>(a0 + 16);
+          }
         }
       }
-      if (!kVec && X0 + 8 > P.canvas_w) wmask &= (1u << (P.canvas_w - X0)) - 1u;
-      uint32_t eA[6] = {0, 0, 0, 0, 0, 0}, eB[6] = {0, 0, 0, 0, 0, 0};
-      const int64_t row_off = static_cast<int64_t>(Y) * P.row_pitch + 3 * X0;
-      if (!queue && A) queue = !load_window(P, P.frames + s_base[A - 1] + row_off, eA);
-      if (!queue && B) queue = !load_window(P, P.frames + s_base[B - 1] + row_off, eB);
-      if (!P.window_ok && (A || B)) queue = true;
-      const uint64_t qb = __ballot(queue && wmask);
-      if (queue && wmask)
-        s_wq[wave][n_queued + static_cast<int>(lane_rank(qb))] = static_cast<int16_t>(g);
-      n_queued += __popcll(qb);
-      if (queue || !wmask) continue;
-      Group G;
 #pragma unroll
-      for (int k = 0; k < 3; ++k) {
-        const uint32_t pk = P.pad_byte[k];
+      for (int j = 0; j < kInFlight; ++j) {
+        if (dst[j] < 0) continue;
+        uint8_t *d = s_px + dst[j];
+        if (fast[j]) {
+          const uint32_t sh = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(sp[j]) & 3u);
+          uint32_t e[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          uint32_t x[2];
+          for (int t = 0; t < 4; ++t)
+            e[t] = __builtin_amdgcn_alignbyte(win[j][t + 1], win[j][t], sh);
+          if (lo[j] == 0 && hi[j] == 16) {
+            *reinterpret_cast<u32x4 *>(d) = u32x4{e[0], e[1], e[2], e[3]};
+          } else {
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int i = 2 * j + h, b = 3 * i + k;
-            const uint32_t xa = byte_of(eA, b), xb = byte_of(eB, b);
-            x[h] = (is_pad >> i) & 1u ? pk : ((from_b >> i) & 1u ? xb : xa);
+            for (int t = 0; t < 16; ++t)
+              if (t >= lo[j] && t < hi[j]) d[t] = static_cast<uint8_t>(e[t >> 2] >> (8 * (t & 3)));
           }
-          G.p[k][j] = uint32_t(s_lut[k * 256 + x[0]]) | (uint32_t(s_lut[k * 256 + x[1]]) << 16);
-        }
-      }
-      store_group<kVec>(P, c_local, Y, X0, G, wmask);
-    }
-    // The wave's queue: one pixel per lane, eight consecutive lanes per group, so the
-    // 2-byte stores of a group form one contiguous 16-byte run per plane.
-    if (n_queued) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      const int64_t plane = static_cast<int64_t>(P.canvas_h) * P.canvas_w;
-      uint16_t *obase = P.out + static_cast<int64_t>(c_local) * 3 * plane;
-      for (int u = lane; u < n_queued * 8; u += 64) {
-        const int g = s_wq[wave][u >> 3], i = u & 7;
-        const int r = g / kGroupsX, x = (g % kGroupsX) * 8 + i;
-        if (x >= tw) continue;
-        const uint32_t o = s_owner[r * kTileW + x];
-        if (o == kDone || (o == 0 && !final_pass)) continue;
-        const int Y = Y_t + r, X = X_t + x;
-        uint32_t h[3];
-        if (o == 0) {
-#pragma unroll
-          for (int k = 0; k < 3; ++k) h[k] = P.pad2[k] & 0xFFFFu;
         } else {
-          const uint8_t *px = P.frames + s_base[o - 1] + static_cast<int64_t>(Y) * P.row_pitch +
-                              3 * static_cast<int64_t>(X);
-#pragma unroll
-          for (int k = 0; k < 3; ++k) h[k] = s_lut[k * 256 + px[k]];
+          for (int t = lo[j]; t < hi[j]; ++t) d[t] = sp[j][t];
         }
-        uint16_t *dst = obase + static_cast<int64_t>(Y) * P.canvas_w + X;
-#pragma unroll
-        for (int k = 0; k < 3; ++k) dst[k * plane] = static_cast<uint16_t>(h[k]);
       }
     }
-    if (final_pass) break;
-    first_pass = false;
-    __syncthreads();  // the next pass rewrites slots and the owner map
+    __syncthreads();  // records are rewritten by the next round; staging is complete
+  }
+  __syncthreads();  // the prefill is complete when the canvas has no patch at all
+
+  // ---- convert and store: RGB interleaved in LDS -> three fp16 planes -----------------
+#pragma unroll 2
+  for (int g = tid; g < kGroups; g += kThreads) {
+    const int r = g / kGroupsX, X0l = (g % kGroupsX) * 8;
+    if (r >= th || X0l >= tw) continue;
+    const u32x2 *p = reinterpret_cast<const u32x2 *>(s_px + r * kRowBytes + 3 * X0l);
+    const u32x2 v0 = p[0], v1 = p[1], v2 = p[2];
+    const uint32_t e[6] = {v0.x, v0.y, v1.x, v1.y, v2.x, v2.y};
+    Group G;
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int b0 = 3 * (2 * j) + k, b1 = 3 * (2 * j + 1) + k;
+        const uint32_t x0 = (e[b0 >> 2] >> (8 * (b0 & 3))) & 0xFFu;
+        const uint32_t x1 = (e[b1 >> 2] >> (8 * (b1 & 3))) & 0xFFu;
+        G.p[k][j] = uint32_t(S.lut[k * 256 + x0]) | (uint32_t(S.lut[k * 256 + x1]) << 16);
+      }
+    store_group<kVec>(P, c_local, Y_t + r, X_t + X0l, G);
   }
 }
 
@@ -417,36 +394,41 @@ extern "C" int tg_stitch(const tg_stitch_args *a, void *stream) {
   P.canvas_begin = a->canvas_begin;
   P.n_rois = a->n_rois;
   P.canvas_first = a->canvas_first;
+  P.canvas_count = a->canvas_count;
   P.canvas_w = a->canvas_w;
   P.canvas_h = a->canvas_h;
   P.tiles_x = (a->canvas_w + kTileW - 1) / kTileW;
+  const int64_t tiles_pc = int64_t(P.tiles_x) * ((a->canvas_h + kTileH - 1) / kTileH);
+  const int64_t n_tiles = tiles_pc * a->canvas_count;
+  if (n_tiles > 0x7FFFFFFF) return TG_E_INVAL;
+  P.tiles_per_canvas = static_cast<int32_t>(tiles_pc);
+  P.n_tiles = static_cast<int32_t>(n_tiles);
   P.out = a->out;
-  // One past the last valid frame byte, rounded up to a dword; windows start at most
-  // 28 bytes before it. Frame buffers too small for one window take the per-pixel path.
-  const int64_t valid_end = int64_t(a->n_frames - 1) * a->frame_stride +
-                            int64_t(a->frame_h - 1) * a->row_pitch + 3 * int64_t(a->frame_w);
-  const uintptr_t end4 = (reinterpret_cast<uintptr_t>(a->frames) + uintptr_t(valid_end) + 3) &
-                         ~uintptr_t(3);
-  const uintptr_t begin4 = reinterpret_cast<uintptr_t>(a->frames) & ~uintptr_t(3);
-  P.window_limit = a->frames + (int64_t(end4 - 28) - int64_t(reinterpret_cast<uintptr_t>(a->frames)));
-  P.window_base = a->frames - (reinterpret_cast<uintptr_t>(a->frames) - begin4);
-  P.window_ok = a->n_frames > 0 && end4 >= begin4 + 32;
+  // A 20-byte window may start on any dword from the one holding the first frame byte
+  // up to the one 20 bytes before the end of the dword holding the last valid byte.
+  // With n_frames == 0 no patch is sane and no window is formed.
+  const int64_t valid_end = a->n_frames > 0 ? int64_t(a->n_frames - 1) * a->frame_stride +
+                                                  int64_t(a->frame_h - 1) * a->row_pitch +
+                                                  3 * int64_t(a->frame_w)
+                                            : 0;
+  const uintptr_t f0 = reinterpret_cast<uintptr_t>(a->frames);
+  const uintptr_t begin4 = f0 & ~uintptr_t(3);
+  const uintptr_t end4 = (f0 + uintptr_t(valid_end) + 3) & ~uintptr_t(3);
+  P.window_base = a->frames - (f0 - begin4);
+  // below window_base (no fast window at all) when the buffer holds under 20 bytes
+  P.window_limit = a->frames + (int64_t(end4) - 20 - int64_t(f0));
   uint16_t lut16[768];
   for (int k = 0; k < 3; ++k)
     for (int x = 0; x < 256; ++x)
       lut16[k * 256 + x] = half_bits_rne((double(x) - double(a->mean[k])) / double(a->std[k]));
   std::memcpy(P.lut, lut16, sizeof lut16);
-  for (int k = 0; k < 3; ++k) {
-    const uint32_t pv = lut16[k * 256 + a->pad[k]];
-    P.pad2[k] = pv | (pv << 16);
-    P.pad_byte[k] = a->pad[k];
-  }
-  const int tiles_y = (a->canvas_h + kTileH - 1) / kTileH;
-  const int64_t tiles = int64_t(P.tiles_x) * tiles_y;
-  if (tiles > 0x7FFFFFFF || a->canvas_count > 65535) return TG_E_INVAL;
-  const dim3 grid(static_cast<uint32_t>(tiles), static_cast<uint32_t>(a->canvas_count));
+  uint8_t pat[12];
+  for (int i = 0; i < 12; ++i) pat[i] = a->pad[i % 3];
+  std::memcpy(P.pad_dw, pat, sizeof pat);
+
   const bool vec = (a->canvas_w % 8 == 0) && (reinterpret_cast<uintptr_t>(a->out) % 16 == 0);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 grid(static_cast<uint32_t>(n_tiles));
   if (vec)
     hipLaunchKernelGGL(stitch_kernel<true>, grid, dim3(kThreads), 0, s, P);
   else
