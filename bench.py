@@ -2,8 +2,8 @@
 """Throughput of the patch-stitching path on one MI355X.
 
 One step = one pass of the whole path over one batch of synthetic input:
-  tg_plan_pack (host C++) -> plan uploaded to HBM -> tg_stitch once per batch of
-  canvases -> tg_unstitch of every detector box.
+  tg_plan_pack and tg_stitch_schedule (host C++) -> plan and unit orders uploaded
+  to HBM -> tg_stitch once per batch of canvases -> tg_unstitch of every detector box.
 Frames, the RoI table and the boxes are resident in HBM before timing starts. The
 host plan of step s+1 overlaps the GPU work of step s (double-buffered pinned
 staging), as a serving loop would run it.
@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="cam20_4k")
     ap.add_argument("--policy", type=int, default=0, help="0 shelf FFDH, 1 shelf arrival, 2 guillotine")
+    ap.add_argument("--unit-order", choices=["heavy", "natural"], default="heavy",
+                    help="tg_stitch launch order: heaviest units first (tg_stitch_schedule) "
+                         "or canvas order")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum wall time of the oracle's CPU sample")
@@ -145,8 +148,12 @@ def main():
     ubufs = tg.UnstitchBuffers(n_boxes)
     batches = [tg.batch_range(J, wl.batch_cap, k) for k in range(tg.batch_count(J, wl.batch_cap))]
 
-    # device plan arrays, refreshed every step from double-buffered pinned staging
-    words = n_rois * 3 + n_rois + (n_rois + 1)
+    # device plan arrays and per-batch unit orders, refreshed every step from
+    # double-buffered pinned staging
+    scheduled = args.unit_order == "heavy"
+    n_units = [tg.stitch_units(wl.canvas, wl.canvas, c) if scheduled else 0 for _, c in batches]
+    unit_off = np.concatenate([[0], np.cumsum(n_units)]).astype(np.int64) + 5 * n_rois + 1
+    words = int(unit_off[-1])
     staging = [torch.empty(words, dtype=torch.int32, pin_memory=True) for _ in range(2)]
     staging_np = [s.numpy() for s in staging]
     plan_d = torch.zeros(words, dtype=torch.int32, device=dev)
@@ -159,8 +166,10 @@ def main():
     params = tg.PackParams(wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, args.policy)
     # argument blocks are built once: no pointer changes between steps
     stitch_args = [tg.stitch_args(frames_d, dplan, first, count, wl.canvas, wl.canvas,
-                                  W.MEAN, W.STD, W.PAD, out[first:first + count])
-                   for first, count in batches]
+                                  W.MEAN, W.STD, W.PAD, out[first:first + count],
+                                  unit_order=plan_d[unit_off[k]:unit_off[k + 1]]
+                                  if scheduled else None)
+                   for k, (first, count) in enumerate(batches)]
 
     def make_uargs():
         return tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
@@ -176,12 +185,20 @@ def main():
         st = staging_np[buf]
         place = st[: 3 * n_rois].reshape(n_rois, 3)
         order = st[3 * n_rois: 4 * n_rois]
-        cbeg = st[4 * n_rois:]
+        cbeg = st[4 * n_rois: 5 * n_rois + 1]
         rc = tg.lib().tg_plan_pack(rois.ctypes.data, n_rois, tg.ctypes.byref(params),
                                    place.ctypes.data, order.ctypes.data, cbeg.ctypes.data,
                                    J_buf.ctypes.data, bad_buf.ctypes.data)
         if rc != tg.OK or J_buf[0] != J:
             raise tg.TgError("tg_plan_pack", rc)
+        if scheduled:
+            for k, (first, count) in enumerate(batches):
+                rc = tg.lib().tg_stitch_schedule(
+                    rois.ctypes.data, place.ctypes.data, order.ctypes.data, cbeg.ctypes.data,
+                    n_rois, J, first, count, wl.canvas, wl.canvas,
+                    st[unit_off[k]:].ctypes.data)
+                if rc != tg.OK:
+                    raise tg.TgError("tg_stitch_schedule", rc)
         plan_d.copy_(staging[buf], non_blocking=True)
         ev = torch.cuda.Event()
         ev.record(stream)
@@ -207,6 +224,11 @@ def main():
     # sanity: the plan the steps recompute equals the one the buffers were sized for
     chk = plan_d.cpu().numpy()
     assert np.array_equal(chk[: 3 * n_rois].reshape(n_rois, 3), plan0.place)
+    for k, (first, count) in enumerate(batches):
+        if scheduled:
+            assert np.array_equal(chk[unit_off[k]:unit_off[k + 1]],
+                                  tg.stitch_schedule(rois, plan0, first, count, wl.canvas,
+                                                     wl.canvas))
     timing["on"] = True
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -239,7 +261,7 @@ def main():
             traffic = cnt.get("hbm_bytes_per_launch")
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "stitch_kernel<true>", "launches": n_launch,
+                "kernel": "stitch_kernel<true, false>", "launches": n_launch,
                 "avg_launch_us": round(avg_ms * 1e3, 2),
                 "algorithmic_bytes_per_launch": int(avg_bytes)}
 
@@ -253,6 +275,7 @@ def main():
                                f" {wl.canvas}x{wl.canvas} canvases, batch cap {wl.batch_cap}, "
                                f"{n_boxes} boxes",
                    "canvases": J, "batches": len(batches), "policy": args.policy,
+                   "unit_order": args.unit_order,
                    "canvas_efficiency": round(float((rois[:, 3].astype(np.int64) *
                                                      rois[:, 4]).sum()) / canvas_px, 4)},
         "roofline": roofline,

@@ -163,6 +163,13 @@ typedef struct {
    * contiguous: out[((c * 3 + k) * canvas_h + Y) * canvas_w + X] holds canvas
    * canvas_first + c. Every element is written exactly once. */
   uint16_t *out;
+  /* Optional launch order of the work units, device, int32
+   * [tg_stitch_units(canvas_w, canvas_h, canvas_count)]: a permutation of the unit ids,
+   * normally from tg_stitch_schedule for the same plan and canvas range. NULL runs the
+   * units in id order. The order changes only speed, never the output -- provided it
+   * is a permutation: an id missing from it leaves that unit's canvas region unwritten,
+   * a repeated id writes it twice (same values), ids outside the range are ignored. */
+  const int32_t *unit_order;
 } tg_stitch_args;
 
 /*
@@ -183,6 +190,45 @@ typedef struct {
  * canvas_count == 0 enqueues nothing and returns TG_OK.
  */
 int tg_stitch(const tg_stitch_args *args, void *stream);
+
+/*
+ * Which exact normalisation tg_stitch uses for (mean, std) (host only): 0 when fp32
+ * constants (a_k, c_k) exist with binary16(fma(x, a_k, c_k)) equal to the correctly
+ * rounded binary16((x - mean[k]) / std[k]) for every byte x and channel k, so the kernel
+ * computes each value; 1 when it looks values up in a 3 x 256 table instead. Both give
+ * the same bits. TG_E_INVAL for null pointers or a bad mean/std (as tg_stitch).
+ */
+int32_t tg_stitch_norm_uses_table(const float mean[3], const float std[3]);
+
+/*
+ * Work units of one tg_stitch launch (host only). A canvas is cut into tiles of at most
+ * 1280 columns and each tile into bands of rows; one unit = one band of one tile of one
+ * canvas, run by one workgroup. Unit k is canvas canvas_first + k / (bands * tiles),
+ * band (k / tiles) % bands, tile k % tiles.
+ * Returns the number of units for canvas_count canvases of canvas_w x canvas_h (0 when
+ * canvas_count == 0), or TG_E_INVAL for non-positive sizes or a negative count.
+ */
+int32_t tg_stitch_units(int32_t canvas_w, int32_t canvas_h, int32_t canvas_count);
+
+/*
+ * A launch order for tg_stitch's units (host only): heaviest first, weight = canvas
+ * pixels of the unit that patches cover (ties keep unit order). Run last, the lightest
+ * units fill the tail of the launch, which otherwise waits on a few heavy ones.
+ *
+ * In: the plan as tg_plan_pack wrote it (host arrays; n_rois RoIs, n_canvases
+ * canvases), the canvas range and canvas size of the tg_stitch call.
+ * Out: unit_order[tg_stitch_units(canvas_w, canvas_h, canvas_count)] (host), a
+ * permutation of the unit ids; upload it and pass it as tg_stitch_args.unit_order.
+ * Plan entries that tg_stitch would skip (ids out of range, a place on another canvas,
+ * rectangles outside the canvas) add no weight.
+ * Returns TG_E_INVAL for null pointers or bad sizes, TG_E_RANGE when the canvas range
+ * leaves [0, n_canvases), TG_E_INTERNAL on host allocation failure; canvas_count == 0
+ * writes nothing and returns TG_OK.
+ */
+int tg_stitch_schedule(const tg_roi *rois, const tg_place *place, const int32_t *order,
+                       const int32_t *canvas_begin, int32_t n_rois, int32_t n_canvases,
+                       int32_t canvas_first, int32_t canvas_count, int32_t canvas_w,
+                       int32_t canvas_h, int32_t *unit_order);
 
 typedef struct {
   const tg_box *boxes;        /* device [n_boxes] */

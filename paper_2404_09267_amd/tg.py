@@ -38,7 +38,7 @@ class StitchArgs(ctypes.Structure):
                 ("order", _vp), ("canvas_begin", _vp), ("n_rois", _i32), ("n_canvases", _i32),
                 ("canvas_first", _i32), ("canvas_count", _i32), ("canvas_w", _i32),
                 ("canvas_h", _i32), ("mean", _f32 * 3), ("std", _f32 * 3), ("pad", _u8 * 3),
-                ("out", _vp)]
+                ("out", _vp), ("unit_order", _vp)]
 
 
 class UnstitchArgs(ctypes.Structure):
@@ -48,8 +48,9 @@ class UnstitchArgs(ctypes.Structure):
                 ("n_out", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
 
 
-EXPORTS = ["tg_plan_pack", "tg_batch_count", "tg_batch_range", "tg_stitch",
-           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror", "tg_abi_version"]
+EXPORTS = ["tg_plan_pack", "tg_batch_count", "tg_batch_range", "tg_stitch", "tg_stitch_units",
+           "tg_stitch_schedule", "tg_stitch_norm_uses_table", "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror",
+           "tg_abi_version"]
 
 _lib = None
 
@@ -79,6 +80,13 @@ def lib() -> ctypes.CDLL:
         L.tg_batch_range.restype = ctypes.c_int
         L.tg_stitch.argtypes = [ctypes.POINTER(StitchArgs), _vp]
         L.tg_stitch.restype = ctypes.c_int
+        L.tg_stitch_norm_uses_table.argtypes = [ctypes.POINTER(_f32), ctypes.POINTER(_f32)]
+        L.tg_stitch_norm_uses_table.restype = _i32
+        L.tg_stitch_units.argtypes = [_i32, _i32, _i32]
+        L.tg_stitch_units.restype = _i32
+        L.tg_stitch_schedule.argtypes = [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32,
+                                         _vp]
+        L.tg_stitch_schedule.restype = ctypes.c_int
         L.tg_unstitch_workspace_bytes.argtypes = [_i32]
         L.tg_unstitch_workspace_bytes.restype = ctypes.c_size_t
         L.tg_unstitch.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
@@ -204,8 +212,47 @@ class DevicePlan:
         _check(self.canvas_begin, torch.int32, (self.n_canvases + 1,), "canvas_begin")
 
 
+def stitch_norm_uses_table(mean, std) -> bool:
+    """True when tg_stitch normalises through its binary16 table (no exact fp32 fma
+    constants exist for this mean/std), False when it computes each value."""
+    m = (_f32 * 3)(*[float(v) for v in mean])
+    s = (_f32 * 3)(*[float(v) for v in std])
+    rc = int(lib().tg_stitch_norm_uses_table(m, s))
+    if rc < 0:
+        raise TgError("tg_stitch_norm_uses_table", rc)
+    return bool(rc)
+
+
+def stitch_units(canvas_w: int, canvas_h: int, canvas_count: int) -> int:
+    """Number of work units of one tg_stitch launch (the length of a unit order)."""
+    n = int(lib().tg_stitch_units(canvas_w, canvas_h, canvas_count))
+    if n < 0:
+        raise TgError("tg_stitch_units", n)
+    return n
+
+
+def stitch_schedule(rois: np.ndarray, plan: Plan, canvas_first: int, canvas_count: int,
+                    canvas_w: int, canvas_h: int, out: np.ndarray | None = None) -> np.ndarray:
+    """Host: heaviest-first launch order of the units of one tg_stitch call (int32)."""
+    r = np.ascontiguousarray(rois, dtype=np.int32).reshape(-1, 5)
+    place = np.ascontiguousarray(plan.place, dtype=np.int32)
+    order = np.ascontiguousarray(plan.order, dtype=np.int32)
+    cbeg = np.ascontiguousarray(plan.canvas_begin, dtype=np.int32)
+    n_units = stitch_units(canvas_w, canvas_h, canvas_count)
+    if out is None:
+        out = np.empty(n_units, dtype=np.int32)
+    if out.dtype != np.int32 or not out.flags.c_contiguous or out.size < n_units:
+        raise ValueError(f"unit order buffer must be contiguous int32 with >= {n_units} entries")
+    rc = lib().tg_stitch_schedule(_np_ptr(r), _np_ptr(place), _np_ptr(order), _np_ptr(cbeg),
+                                  r.shape[0], plan.n_canvases, canvas_first, canvas_count,
+                                  canvas_w, canvas_h, _np_ptr(out))
+    if rc != OK:
+        raise TgError("tg_stitch_schedule", rc)
+    return out[:n_units]
+
+
 def stitch_args(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w, canvas_h,
-                mean, std, pad, out) -> StitchArgs:
+                mean, std, pad, out, unit_order=None) -> StitchArgs:
     import torch
 
     dplan.check()
@@ -229,14 +276,22 @@ def stitch_args(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w,
     a.std[:] = [float(v) for v in std]
     a.pad[:] = [int(v) for v in pad]
     a.out = out.data_ptr()
+    a.unit_order = None
+    if unit_order is not None:
+        n_units = stitch_units(canvas_w, canvas_h, canvas_count) if canvas_count > 0 else 0
+        _check(unit_order, torch.int32, name="unit_order")
+        if unit_order.numel() < n_units:
+            raise ValueError(f"unit_order must hold {n_units} unit ids")
+        a.unit_order = unit_order.data_ptr()
     return a
 
 
 def stitch(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w, canvas_h,
-           mean, std, pad, out, stream=None) -> None:
-    """Enqueue tg_stitch for canvases [canvas_first, +canvas_count) into `out`."""
+           mean, std, pad, out, stream=None, unit_order=None) -> None:
+    """Enqueue tg_stitch for canvases [canvas_first, +canvas_count) into `out`
+    (`unit_order`: optional device int32 launch order from stitch_schedule)."""
     a = stitch_args(frames, dplan, canvas_first, canvas_count, canvas_w, canvas_h,
-                    mean, std, pad, out)
+                    mean, std, pad, out, unit_order)
     rc = lib().tg_stitch(ctypes.byref(a), _stream_handle(stream))
     if rc != OK:
         raise TgError("tg_stitch", rc)

@@ -46,14 +46,14 @@ def coverage(plan, rois, first, count, cw, ch) -> np.ndarray:
 
 
 def run_stitch(frames_d, rois, plan, first, count, cw, ch, mean=W.MEAN, std=W.STD, pad=W.PAD,
-               dplan=None, sentinel=True):
+               dplan=None, sentinel=True, unit_order=None):
     import torch
 
     dplan = dplan or tg.DevicePlan(rois, plan)
     out = torch.empty((count, 3, ch, cw), dtype=torch.int16, device="cuda")
     if sentinel:
         out.fill_(SENTINEL)
-    tg.stitch(frames_d, dplan, first, count, cw, ch, mean, std, pad, out)
+    tg.stitch(frames_d, dplan, first, count, cw, ch, mean, std, pad, out, unit_order=unit_order)
     torch.cuda.synchronize()
     return out.cpu().numpy().view(np.uint16)
 

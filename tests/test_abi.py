@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version():
-    assert tg.lib().tg_abi_version() == 1
+    assert tg.lib().tg_abi_version() == 2
 
 
 def test_strerror():
@@ -54,6 +54,7 @@ int main(void) {
   F(tg_stitch_args, row_pitch); F(tg_stitch_args, rois); F(tg_stitch_args, canvas_begin);
   F(tg_stitch_args, n_rois); F(tg_stitch_args, canvas_first); F(tg_stitch_args, canvas_h);
   F(tg_stitch_args, mean); F(tg_stitch_args, std); F(tg_stitch_args, pad); F(tg_stitch_args, out);
+  F(tg_stitch_args, unit_order);
   F(tg_unstitch_args, boxes); F(tg_unstitch_args, n_boxes); F(tg_unstitch_args, rois);
   F(tg_unstitch_args, n_rois); F(tg_unstitch_args, clip); F(tg_unstitch_args, roi_of_box);
   F(tg_unstitch_args, n_out); F(tg_unstitch_args, workspace); F(tg_unstitch_args, workspace_bytes);

@@ -6,6 +6,7 @@ import pytest
 import oracle
 from gpu_helpers import (SENTINEL, assert_stitch_parity, coverage, oracle_plan, run_stitch,
                          say)
+from stitch_geometry import geometry
 from paper_2404_09267_amd import tg
 from paper_2404_09267_amd import workload as W
 
@@ -188,13 +189,16 @@ def test_deterministic(torch):
     np.testing.assert_array_equal(a, b)
 
 
-@pytest.mark.parametrize("name,policy", [("cam1_1080p", 0), ("cam5_4k", 0), ("cam20_4k", 0),
-                                         ("cam20_4k", 2), ("small_roi_8cam", 0),
-                                         ("small_roi_8cam", 1)])
-def test_workload_full_parity(torch, name, policy):
-    """Whole workloads, batch by batch as the bench launches them, against the oracle."""
+@pytest.mark.parametrize("name,policy,scheduled", [("cam1_1080p", 0, True), ("cam5_4k", 0, True),
+                                                   ("cam20_4k", 0, True), ("cam20_4k", 0, False),
+                                                   ("cam20_4k", 2, True),
+                                                   ("small_roi_8cam", 0, True),
+                                                   ("small_roi_8cam", 1, False)])
+def test_workload_full_parity(torch, name, policy, scheduled):
+    """Whole workloads, batch by batch as the bench launches them (with the host's
+    heaviest-first unit order, or units in id order), against the oracle."""
     wl = W.WORKLOADS[name]
-    say("workload", name, "policy", policy)
+    say("workload", name, "policy", policy, "scheduled", scheduled)
     rois = W.make_rois(wl)
     frames_d = W.make_frames(wl, "cuda")
     plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, policy)
@@ -203,7 +207,12 @@ def test_workload_full_parity(torch, name, policy):
     for k in range(tg.batch_count(plan.n_canvases, wl.batch_cap)):
         first, count = tg.batch_range(plan.n_canvases, wl.batch_cap, k)
         say("  batch", k, first, count)
-        got = run_stitch(frames_d, rois, plan, first, count, wl.canvas, wl.canvas, dplan=dplan)
+        unit_order = None
+        if scheduled:
+            unit_order = torch.from_numpy(
+                tg.stitch_schedule(rois, plan, first, count, wl.canvas, wl.canvas)).cuda()
+        got = run_stitch(frames_d, rois, plan, first, count, wl.canvas, wl.canvas, dplan=dplan,
+                         unit_order=unit_order)
         want = oracle.stitch(frames, rois, oracle_plan(plan), first, count, wl.canvas,
                              wl.canvas, W.MEAN, W.STD, W.PAD)
         cov = coverage(plan, rois, first, count, wl.canvas, wl.canvas)
@@ -245,3 +254,69 @@ def test_window_sampled_batches(torch):
             assert np.all(got[:, ch][~cov] == table[ch][W.PAD[ch]])
     del frames_d
     torch.cuda.empty_cache()
+
+
+# mean/std for which tg_stitch normalises through its binary16 table (no fp32 fma
+# constants reproduce every correctly rounded value); the CPU tests pin that choice
+TABLE_MEAN = (174.00369262695312, 189.9988250732422, 150.99696350097656)
+TABLE_STD = (0.031708136200904846, 1.5641870498657227, 1.5637657642364502)
+
+
+def test_table_path_parity(torch):
+    """The table path: small plans of every policy and a whole workload, bit-exact."""
+    assert tg.stitch_norm_uses_table(TABLE_MEAN, TABLE_STD)
+    rng = np.random.default_rng(31)
+    for cw, ch in [(64, 48), (300, 70), (37, 29)]:
+        for policy in (0, 1, 2):
+            say("table path", cw, ch, policy)
+            _case(torch, rng, 3, 70, 91, cw, ch, 60, 1, 40, 40, policy, mean=TABLE_MEAN,
+                  std=TABLE_STD, pad=(3, 200, 90))
+    wl = W.WORKLOADS["cam5_4k"]
+    rois = W.make_rois(wl)
+    frames_d = W.make_frames(wl, "cuda")
+    plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
+    say("table path cam5_4k")
+    got = run_stitch(frames_d, rois, plan, 0, plan.n_canvases, wl.canvas, wl.canvas,
+                     TABLE_MEAN, TABLE_STD, (3, 200, 90))
+    want = oracle.stitch(frames_d.cpu().numpy(), rois, oracle_plan(plan), 0, plan.n_canvases,
+                         wl.canvas, wl.canvas, TABLE_MEAN, TABLE_STD, (3, 200, 90))
+    np.testing.assert_array_equal(got, want)
+
+
+def test_unit_order_that_is_not_a_permutation(torch):
+    """Ids outside the unit range are ignored, a repeated id rewrites the same values, a
+    missing id leaves its region unwritten -- and nothing outside `out` is touched."""
+    rng = np.random.default_rng(8)
+    cw = ch = 256
+    rois = W.random_rois(rng, 80, 2, 400, 300, 8, 120, 120)
+    frames = W.random_frames_np(2, 300, 400, 6)
+    plan = tg.plan_pack(rois, cw, ch, 400, 300, 2, 0)
+    count = min(plan.n_canvases, 2)
+    n_units = tg.stitch_units(cw, ch, count)
+    want = oracle.stitch(frames, rois, oracle_plan(plan), 0, count, cw, ch, W.MEAN, W.STD,
+                         W.PAD)
+    order = np.full(n_units, -1, np.int32)
+    order[0] = order[1] = 0        # unit 0 twice
+    order[2] = n_units             # out of range
+    order[3] = n_units - 1         # the last unit
+    order[4] = 2 ** 31 - 1
+    say("unit order not a permutation", n_units)
+    buf = torch.full((count * 3 * ch * cw + 64,), SENTINEL, dtype=torch.int16, device="cuda")
+    out = buf[:count * 3 * ch * cw].view(count, 3, ch, cw)
+    tg.stitch(torch.from_numpy(frames).cuda(), tg.DevicePlan(rois, plan), 0, count, cw, ch,
+              W.MEAN, W.STD, W.PAD, out, unit_order=torch.from_numpy(order).cuda())
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint16)
+    assert np.all(buf[count * 3 * ch * cw:].cpu().numpy().view(np.uint16) == SENTINEL)
+    tiles, band_rows, bands, _ = geometry(cw, ch, count)
+    assert tiles == 1
+    written = np.zeros((count, ch), bool)
+    for u in (0, n_units - 1):
+        c, b = divmod(u, bands)
+        written[c, b * band_rows:(b + 1) * band_rows] = True
+    for c in range(count):
+        for y in range(ch):
+            if written[c, y]:
+                np.testing.assert_array_equal(got[c, :, y], want[c, :, y])
+            else:
+                assert np.all(got[c, :, y] == SENTINEL), (c, y)
