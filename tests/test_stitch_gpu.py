@@ -6,7 +6,7 @@ import pytest
 import oracle
 from gpu_helpers import (SENTINEL, assert_stitch_parity, coverage, oracle_plan, run_stitch,
                          say)
-from stitch_geometry import geometry
+from stitch_geometry import geometry, records_per_unit
 from paper_2404_09267_amd import tg
 from paper_2404_09267_amd import workload as W
 
@@ -23,7 +23,7 @@ def torch():
 
 
 def _case(torch, rng, n_frames, fh, fw, cw, ch, n, lo, hi_w, hi_h, policy, mean=W.MEAN,
-          std=W.STD, pad=W.PAD):
+          std=W.STD, pad=W.PAD, with_rois=False):
     rois = W.random_rois(rng, n, n_frames, fw, fh, lo, min(hi_w, cw), min(hi_h, ch))
     frames = W.random_frames_np(n_frames, fh, fw, int(rng.integers(1 << 30)))
     plan = tg.plan_pack(rois, cw, ch, fw, fh, n_frames, policy)
@@ -34,7 +34,7 @@ def _case(torch, rng, n_frames, fh, fw, cw, ch, n, lo, hi_w, hi_h, policy, mean=
     cov = coverage(plan, rois, 0, plan.n_canvases, cw, ch)
     assert_stitch_parity(got, want, cov)
     np.testing.assert_array_equal(got, want)  # bit-exact by design
-    return plan
+    return (plan, rois) if with_rois else plan
 
 
 @pytest.mark.parametrize("cw,ch", [(64, 48), (256, 32), (264, 40), (8, 8), (300, 70),
@@ -56,16 +56,25 @@ def test_odd_frame_widths_and_mean_std(torch):
               std=(0.01, 1000.0, 3.5), pad=(255, 0, 7))
 
 
-def test_many_patches_per_tile_take_extra_passes(torch):
-    """Over 253 patches touching one tile: tiny RoIs, including 1 x 1."""
+def test_many_patches_per_band_take_the_slow_path(torch):
+    """More than 192 patches meeting one unit (the fast path's list size) and exactly 192:
+    tiny RoIs, including 1 x 1."""
     rng = np.random.default_rng(5)
-    for cw, ch, n, lo, hi, pol in [(64, 64, 3000, 1, 1, 0), (64, 64, 1500, 1, 3, 0),
-                                   (256, 32, 2000, 1, 4, 2), (300, 64, 600, 1, 2, 1),
-                                   (64, 8, 254, 1, 1, 1), (64, 8, 253, 1, 1, 1),
-                                   (256, 32, 8192, 1, 1, 1)]:
+    # expect: the exact maximum of patches per unit, or ">" (over 192), or "<=" (192 or fewer)
+    for cw, ch, n, lo, hi, pol, expect in [
+            (256, 3, 193, 1, 1, 1, 193), (256, 3, 192, 1, 1, 1, 192),
+            (256, 32, 8192, 1, 1, 1, ">"), (256, 32, 3000, 1, 4, 2, ">"),
+            (64, 64, 1500, 1, 3, 0, "<="), (300, 64, 600, 1, 2, 1, ">"),
+            (1300, 6, 900, 1, 2, 0, ">")]:
         say("dense", cw, ch, n, lo, hi, pol)
-        plan = _case(torch, rng, 2, 50, 60, cw, ch, n, lo, hi, hi, pol)
-        assert np.diff(plan.canvas_begin).max() >= min(n, 253)
+        plan, rois = _case(torch, rng, 2, 50, 60, cw, ch, n, lo, hi, hi, pol, with_rois=True)
+        most = max(records_per_unit(rois, plan, 0, plan.n_canvases, cw, ch))
+        if expect == ">":
+            assert most > 192
+        elif expect == "<=":
+            assert most <= 192
+        else:
+            assert most == expect
 
 
 def test_roi_at_end_of_frame_buffer(torch):
