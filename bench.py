@@ -170,11 +170,7 @@ def main():
                                   unit_order=plan_d[unit_off[k]:unit_off[k + 1]]
                                   if scheduled else None)
                    for k, (first, count) in enumerate(batches)]
-
-    def make_uargs():
-        return tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
-
-    uargs = make_uargs()
+    uargs = tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
     stitch_events = []
     timing = {"on": False}
 
@@ -200,20 +196,19 @@ def main():
                 if rc != tg.OK:
                     raise tg.TgError("tg_stitch_schedule", rc)
         plan_d.copy_(staging[buf], non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record(stream)
-        upload_done[buf] = ev
+        # One timing event before each tg_stitch launch and one after the last: launch k
+        # runs between events k and k + 1. The first also marks the staging upload as done.
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(stitch_args) + 1)]
+        evs[0].record(stream)
+        upload_done[buf] = evs[0]
         h = tg._vp(stream.cuda_stream)
-        for a in stitch_args:
-            if timing["on"]:
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
+        for k, a in enumerate(stitch_args):
             rc = tg.lib().tg_stitch(tg.ctypes.byref(a), h)
             if rc != tg.OK:
                 raise tg.TgError("tg_stitch", rc)
+            evs[k + 1].record(stream)
             if timing["on"]:
-                e1.record(stream)
-                stitch_events.append((e0, e1, a.canvas_first, a.canvas_count))
+                stitch_events.append((evs[k], evs[k + 1], a.canvas_first, a.canvas_count))
         rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
         if rc != tg.OK:
             raise tg.TgError("tg_unstitch", rc)

@@ -10,12 +10,12 @@
 //  1. assign: LPB lanes per box test the box canvas's patches LPB at a time; a wave
 //     ballot picks the (unique) patch containing the centre and roi_of_box[b] is
 //     written. The same launch clears the look-back state of launch 2.
-//  2. emit: one thread per box, 256 boxes per workgroup. Kept boxes are ranked inside
-//     the workgroup with ballot + mbcnt, the workgroup's offset comes from a
-//     single-pass decoupled look-back over earlier workgroups (workgroup order is
-//     taken from an atomic ticket, so every workgroup a block waits on has already
-//     started), and kept boxes are written in increasing box index -- a stable
-//     compaction whose output does not depend on scheduling.
+//  2. emit: four consecutive boxes per thread, 1024 per workgroup. Kept boxes are
+//     ranked inside the workgroup with a wave prefix sum of per-thread counts, the
+//     workgroup's offset comes from a single-pass decoupled look-back over earlier
+//     workgroups (workgroup order is taken from an atomic ticket, so every workgroup a
+//     block waits on has already started), and kept boxes are written in increasing
+//     box index -- a stable compaction whose output does not depend on scheduling.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -25,6 +25,8 @@
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kBoxesPerThread = 4;                  // emit: consecutive boxes per thread
+constexpr int kEmitBoxes = kThreads * kBoxesPerThread;
 constexpr uint64_t kAggregate = uint64_t(1) << 32;  // state: value = this block's count
 constexpr uint64_t kInclusive = uint64_t(2) << 32;  // state: value = count of blocks 0..i
 constexpr uint32_t kSpinLimit = 1u << 26;           // bounded wait; never reached in practice
@@ -98,50 +100,19 @@ __device__ __forceinline__ void store_state(uint64_t *p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__global__ __launch_bounds__(kThreads) void emit_kernel(const UnstitchParams P) {
-  __shared__ int s_blk, s_prefix;
-  __shared__ int s_wave[kThreads / 64];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0)
-    s_blk = static_cast<int>(__hip_atomic_fetch_add(P.ticket, 1u, __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT));
-  __syncthreads();
-  const int blk = s_blk;
-  const int b = blk * kThreads + tid;
-  const int roi = b < P.n_boxes ? P.roi_of_box[b] : -1;
-  const bool kept = roi >= 0;
-  const uint64_t ballot = __ballot(kept);
-  if (lane == 0) s_wave[wave] = __popcll(ballot);
-  __syncthreads();
-  int before = 0, total = 0;
-  for (int w = 0; w < kThreads / 64; ++w) {
-    if (w < wave) before += s_wave[w];
-    total += s_wave[w];
-  }
-  if (tid == 0) {
-    int prefix = 0;
-    if (blk == 0) {
-      store_state(&P.state[0], kInclusive | uint32_t(total));
-    } else {
-      store_state(&P.state[blk], kAggregate | uint32_t(total));
-      for (int j = blk - 1; j >= 0; --j) {
-        uint64_t s = load_state(&P.state[j]);
-        for (uint32_t spin = 0; (s >> 32) == 0 && spin < kSpinLimit; ++spin)
-          s = load_state(&P.state[j]);
-        prefix += static_cast<int>(static_cast<uint32_t>(s));
-        if ((s >> 32) != (kAggregate >> 32)) break;  // inclusive (or a timed-out wait)
-      }
-      store_state(&P.state[blk], kInclusive | uint32_t(prefix + total));
-    }
-    s_prefix = prefix;
-    if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = prefix + total;
-  }
-  __syncthreads();
-  if (!kept) return;
-  const int pos = s_prefix + before +
-                  static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                      static_cast<uint32_t>(ballot >> 32),
-                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(ballot), 0u)));
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row broadcasts).
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
+// Writes the detection of kept box b (patch roi) at position pos.
+__device__ __forceinline__ void write_det(const UnstitchParams &P, int b, int roi, int pos) {
   const tg_roi r = P.rois[roi];
   const tg_place pl = P.place[roi];
   const tg_box box = P.boxes[b];
@@ -167,9 +138,59 @@ __global__ __launch_bounds__(kThreads) void emit_kernel(const UnstitchParams P) 
   P.dets[pos] = d;
 }
 
+__global__ __launch_bounds__(kThreads) void emit_kernel(const UnstitchParams P) {
+  __shared__ int s_blk, s_prefix;
+  __shared__ int s_wave[kThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0)
+    s_blk = static_cast<int>(__hip_atomic_fetch_add(P.ticket, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT));
+  __syncthreads();
+  const int blk = s_blk;
+  const int b0 = blk * kEmitBoxes + kBoxesPerThread * tid;  // this thread's first box
+  int roi[kBoxesPerThread];
+#pragma unroll
+  for (int j = 0; j < kBoxesPerThread; ++j)
+    roi[j] = b0 + j < P.n_boxes ? P.roi_of_box[b0 + j] : -1;
+  int cnt = 0;
+#pragma unroll
+  for (int j = 0; j < kBoxesPerThread; ++j) cnt += roi[j] >= 0;
+  const int incl = wave_inclusive_sum(cnt);
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int w = 0; w < kThreads / 64; ++w) {
+    if (w < wave) before += s_wave[w];
+    total += s_wave[w];
+  }
+  if (tid == 0) {
+    int prefix = 0;
+    if (blk == 0) {
+      store_state(&P.state[0], kInclusive | uint32_t(total));
+    } else {
+      store_state(&P.state[blk], kAggregate | uint32_t(total));
+      for (int j = blk - 1; j >= 0; --j) {
+        uint64_t s = load_state(&P.state[j]);
+        for (uint32_t spin = 0; (s >> 32) == 0 && spin < kSpinLimit; ++spin)
+          s = load_state(&P.state[j]);
+        prefix += static_cast<int>(static_cast<uint32_t>(s));
+        if ((s >> 32) != (kAggregate >> 32)) break;  // inclusive (or a timed-out wait)
+      }
+      store_state(&P.state[blk], kInclusive | uint32_t(prefix + total));
+    }
+    s_prefix = prefix;
+    if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = prefix + total;
+  }
+  __syncthreads();
+  int pos = s_prefix + before + incl - cnt;
+#pragma unroll
+  for (int j = 0; j < kBoxesPerThread; ++j)
+    if (roi[j] >= 0) write_det(P, b0 + j, roi[j], pos++);
+}
+
 __global__ void zero_count_kernel(int32_t *n_out) { *n_out = 0; }
 
-int emit_blocks(int32_t n) { return (n + kThreads - 1) / kThreads; }
+int emit_blocks(int32_t n) { return (n + kEmitBoxes - 1) / kEmitBoxes; }
 
 }  // namespace
 

@@ -157,10 +157,11 @@ def test_unstitch_validation_without_gpu():
 def test_workspace_sizes():
     assert tg.unstitch_workspace_bytes(0) == 0
     assert tg.unstitch_workspace_bytes(-5) == 0
+    # one ticket word and one look-back word per 1024 boxes
     assert tg.unstitch_workspace_bytes(1) == 16
-    assert tg.unstitch_workspace_bytes(256) == 16
-    assert tg.unstitch_workspace_bytes(257) == 24
-    assert tg.unstitch_workspace_bytes(200000) == 8 * (1 + 782)
+    assert tg.unstitch_workspace_bytes(1024) == 16
+    assert tg.unstitch_workspace_bytes(1025) == 24
+    assert tg.unstitch_workspace_bytes(200000) == 8 * (1 + 196)
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
