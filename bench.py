@@ -57,15 +57,28 @@ def parse():
 
 
 def calib_copy(mb: int, steps: int):
+    """Plain device copies of `mb` MiB, alternating between two source and two destination
+    buffers so that no copy finds its bytes in the memory-side cache. Used to scale the
+    rocprofv3 traffic counters (one copy moves a known byte count) and as the practical
+    read + write streaming rate of the part."""
     import torch
 
     n = mb << 20
-    src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
-    dst = torch.empty_like(src)
-    for _ in range(steps):
-        dst.copy_(src)
+    src = [torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda") for _ in range(2)]
+    dst = [torch.empty_like(src[0]) for _ in range(2)]
+    stream = torch.cuda.current_stream()
+    for i in range(2):
+        dst[i].copy_(src[i])
     torch.cuda.synchronize()
-    print(json.dumps({"calib_copy_bytes": n, "launches": steps}), flush=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record(stream)
+    for i in range(steps):
+        dst[i & 1].copy_(src[i & 1])
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(steps)) * 1e3 / steps
+    print(json.dumps({"calib_copy_bytes": n, "launches": steps + 2, "avg_copy_us": round(us, 2),
+                      "read_plus_write_gbs": round(2 * n / us / 1e3, 1)}), flush=True)
 
 
 def stitch_bytes(rois, plan, first, count, canvas) -> int:
