@@ -120,6 +120,39 @@ def cpu_baseline(wl, rois, frames_np, boxes, canv, min_seconds: float):
             "host_threads_available": len(os.sched_getaffinity(0))}
 
 
+def invoker_cost(tg, W, with_oracle: bool):
+    """Host cost of the SLO-aware batching invoker (tg_slo_replay, incremental packing)
+    per patch arrival on a camera trace of cam20_4k's patches, next to the oracle's
+    literal form (the whole queue re-packed on every arrival)."""
+    wl = W.WORKLOADS["cam20_4k"]
+    w, h, t, ddl, mean, std = W.camera_arrival_trace(wl)
+    pt = tg.slo_patches(w, h, t, ddl)
+    n = len(pt)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        r = tg.slo_replay(pt, wl.canvas, wl.canvas, tg.GUILLOTINE_BSSF, len(mean), mean, std)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= 0.2:
+            break
+    reasons = np.bincount(r.invocations["reason"], minlength=3)
+    out = {"trace": f"{n} patches of cam20_4k, 20 cameras at 30 fps, two rounds 0.3 s apart "
+                    f"with SLO 0.5 s and 0.25 s, {wl.canvas}x{wl.canvas} canvases, "
+                    f"guillotine, at most {len(mean)} canvases per invocation",
+           "arrivals": n, "invocations": len(r.invocations),
+           "fired_by": {"deadline": int(reasons[0]), "slo": int(reasons[1]),
+                        "memory": int(reasons[2])},
+           "us_per_arrival": round(el / reps / n * 1e6, 4)}
+    if with_oracle:
+        from oracle import slo
+
+        t0 = time.perf_counter()
+        slo.replay(w.tolist(), h.tolist(), t.tolist(), ddl.tolist(), wl.canvas, wl.canvas,
+                   tg.GUILLOTINE_BSSF, len(mean), list(mean), list(std))
+        out["oracle_us_per_arrival"] = round((time.perf_counter() - t0) / n * 1e6, 2)
+    return out
+
+
 _W = None
 
 
@@ -290,6 +323,7 @@ def main():
         "stitch_gbs": round(achieved, 1),
         "stitch_pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
     }
+    result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         frames_np = frames_d.cpu().numpy()
         result["cpu_baseline"] = cpu_baseline(wl, rois, frames_np, boxes, canv, args.cpu_seconds)

@@ -136,6 +136,68 @@ int32_t tg_batch_count(int32_t n_canvases, int32_t batch_cap);
 int tg_batch_range(int32_t n_canvases, int32_t batch_cap, int32_t k, int32_t *first,
                    int32_t *count);
 
+/* ---- Online SLO-aware batching invoker (Sec. III-C, Alg. 2; Latency Estimator) ---- */
+
+/* A patch as the scheduler receives it: its size, the time it arrives and its deadline
+ * (generation time plus SLO). Times are in any one unit (seconds, say), finite. */
+typedef struct {
+  int32_t w, h;
+  double t_arrive;
+  double t_ddl;
+} tg_slo_patch;
+
+typedef struct {
+  int32_t canvas_w, canvas_h;
+  int32_t policy;          /* TG_PACK_GUILLOTINE_BSSF (the paper's solver) or
+                              TG_PACK_SHELF_ARRIVAL: packers that keep arrival order */
+  int32_t max_canvases;    /* memory cap: canvases one invocation may hold (>= 1) */
+  int32_t n_lat;           /* rows of the latency table, >= max_canvases */
+  const double *lat_mean;  /* host [n_lat]: mean inference time of b canvases at row b-1 */
+  const double *lat_std;   /* host [n_lat]: its standard deviation */
+} tg_slo_params;
+
+enum tg_fire_reason {
+  TG_FIRE_DEADLINE = 0, /* the clock reached t_remain = t_DDL - T_slack */
+  TG_FIRE_SLO = 1,      /* the next patch would have pushed t_remain before its arrival */
+  TG_FIRE_MEMORY = 2    /* the next patch would have needed more than max_canvases */
+};
+
+/* One invocation of the detector function. */
+typedef struct {
+  double t_fire;        /* when it is invoked */
+  double t_ddl;         /* earliest deadline among its patches (t_DDL) */
+  double t_slack;       /* Latency Estimator's conservative time for its batch */
+  int32_t first, count; /* its patches: order[first .. first+count), in arrival order */
+  int32_t n_canvases;
+  int32_t reason;       /* enum tg_fire_reason */
+} tg_invocation;
+
+/*
+ * Replays an arrival trace through the SLO-aware batching invoker of Alg. 2 (Sec. III-C):
+ * on each arrival the patch joins the queue, t_DDL becomes the earliest deadline of the
+ * queue, the queue is packed onto canvas_w x canvas_h canvases, the Latency Estimator
+ * gives T_slack = lat_mean[b-1] + 3 * lat_std[b-1] for the b canvases, and
+ * t_remain = t_DDL - T_slack. If t_remain falls before the arrival time, or b exceeds
+ * max_canvases, the queue without the new patch is invoked at the arrival time and the
+ * patch starts a new queue. Whenever the clock reaches t_remain (t >= t_remain), the queue
+ * is invoked at max(t_remain, the time it was last changed); a deadline firing that falls
+ * exactly on an arrival time happens before that arrival. After the last arrival the queue
+ * fires at its t_remain. The paper's pseudo-code tests `t_remain > t` where its text
+ * describes the opposite; this library reads it as stated above.
+ * The queue is packed incrementally, one placement per arrival: with an arrival-order
+ * packer that equals packing the whole queue afresh on every arrival, as Alg. 2 does.
+ * patches: host [n], sorted by t_arrive (non-decreasing). Outputs (host, caller-owned):
+ * order[n] (patch ids grouped by invocation), place[n] (indexed by patch id; canvas is
+ * the canvas index inside its invocation), inv[n] (invocations, *n_inv of them).
+ * Returns TG_E_INVAL (null pointer, n < 0, bad sizes or table, a policy that reorders,
+ * a non-finite time, arrivals out of order: *bad_index names the patch when one is at
+ * fault), TG_E_ROI_TOO_LARGE (patch larger than the canvas, *bad_index set),
+ * TG_E_INTERNAL (host allocation failure).
+ */
+int tg_slo_replay(const tg_slo_patch *patches, int32_t n, const tg_slo_params *params,
+                  int32_t *order, tg_place *place, tg_invocation *inv, int32_t *n_inv,
+                  int32_t *bad_index);
+
 typedef struct {
   /* Source frames, device, uint8 HWC RGB: pixel (x, y) of frame f, channel k, is
    * frames[f * frame_stride + y * row_pitch + 3 * x + k]. row_pitch >= 3 * frame_w,

@@ -20,7 +20,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtg.so")
 ARCH = "gfx950"
 
-HOST_SOURCES = ["plan.cpp", "norm.cpp"]
+HOST_SOURCES = ["plan.cpp", "norm.cpp", "invoker.cpp"]
 HIP_SOURCES = ["stitch.hip", "unstitch.hip"]
 
 # Packed FP32 instructions are kept out of every kernel; scalar code is all we need.

@@ -22,6 +22,11 @@ ROI_DTYPE = np.dtype([("frame", "<i4"), ("x", "<i4"), ("y", "<i4"), ("w", "<i4")
 DET_DTYPE = np.dtype([("box", "<i4"), ("roi", "<i4"), ("frame", "<i4"),
                       ("x1", "<f4"), ("y1", "<f4"), ("x2", "<f4"), ("y2", "<f4")])
 DET_WORDS = 7  # int32 words per tg_det
+SLO_PATCH_DTYPE = np.dtype([("w", "<i4"), ("h", "<i4"), ("t_arrive", "<f8"), ("t_ddl", "<f8")])
+INVOCATION_DTYPE = np.dtype([("t_fire", "<f8"), ("t_ddl", "<f8"), ("t_slack", "<f8"),
+                             ("first", "<i4"), ("count", "<i4"), ("n_canvases", "<i4"),
+                             ("reason", "<i4")])
+FIRE_DEADLINE, FIRE_SLO, FIRE_MEMORY = 0, 1, 2
 
 _i32, _i64, _f32, _u8, _vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint8,
                               ctypes.c_void_p)
@@ -48,9 +53,14 @@ class UnstitchArgs(ctypes.Structure):
                 ("n_out", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
 
 
-EXPORTS = ["tg_plan_pack", "tg_batch_count", "tg_batch_range", "tg_stitch", "tg_stitch_units",
-           "tg_stitch_schedule", "tg_stitch_norm_uses_table", "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror",
-           "tg_abi_version"]
+class SloParams(ctypes.Structure):
+    _fields_ = [("canvas_w", _i32), ("canvas_h", _i32), ("policy", _i32), ("max_canvases", _i32),
+                ("n_lat", _i32), ("lat_mean", _vp), ("lat_std", _vp)]
+
+
+EXPORTS = ["tg_plan_pack", "tg_batch_count", "tg_batch_range", "tg_slo_replay", "tg_stitch",
+           "tg_stitch_units", "tg_stitch_schedule", "tg_stitch_norm_uses_table",
+           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror", "tg_abi_version"]
 
 _lib = None
 
@@ -78,6 +88,9 @@ def lib() -> ctypes.CDLL:
         L.tg_batch_count.restype = _i32
         L.tg_batch_range.argtypes = [_i32, _i32, _i32, _vp, _vp]
         L.tg_batch_range.restype = ctypes.c_int
+        L.tg_slo_replay.argtypes = [_vp, _i32, ctypes.POINTER(SloParams), _vp, _vp, _vp, _vp,
+                                    _vp]
+        L.tg_slo_replay.restype = ctypes.c_int
         L.tg_stitch.argtypes = [ctypes.POINTER(StitchArgs), _vp]
         L.tg_stitch.restype = ctypes.c_int
         L.tg_stitch_norm_uses_table.argtypes = [ctypes.POINTER(_f32), ctypes.POINTER(_f32)]
@@ -154,6 +167,43 @@ def batch_range(n_canvases: int, batch_cap: int, k: int):
     if rc != OK:
         raise TgError("tg_batch_range", rc)
     return int(first[0]), int(count[0])
+
+
+@dataclass
+class SloReplay:
+    """Host outputs of tg_slo_replay."""
+    order: np.ndarray        # int32 [n]: patch ids grouped by invocation
+    place: np.ndarray        # int32 [n, 3]: {canvas inside its invocation, x, y} per patch
+    invocations: np.ndarray  # INVOCATION_DTYPE [n_inv]
+
+
+def slo_patches(w, h, t_arrive, t_ddl) -> np.ndarray:
+    """Packs per-patch arrays into tg_slo_patch records."""
+    out = np.zeros(len(w), dtype=SLO_PATCH_DTYPE)
+    out["w"], out["h"], out["t_arrive"], out["t_ddl"] = w, h, t_arrive, t_ddl
+    return out
+
+
+def slo_replay(patches: np.ndarray, canvas_w: int, canvas_h: int, policy: int, max_canvases: int,
+               lat_mean, lat_std) -> SloReplay:
+    pt = np.ascontiguousarray(patches, dtype=SLO_PATCH_DTYPE)
+    n = pt.shape[0]
+    mean = np.ascontiguousarray(lat_mean, dtype=np.float64)
+    sd = np.ascontiguousarray(lat_std, dtype=np.float64)
+    if mean.shape != sd.shape:
+        raise ValueError("latency mean and std tables differ in length")
+    p = SloParams(canvas_w, canvas_h, policy, max_canvases, mean.shape[0], _np_ptr(mean),
+                  _np_ptr(sd))
+    order = np.empty(n, dtype=np.int32)
+    place = np.empty((n, 3), dtype=np.int32)
+    inv = np.empty(max(n, 1), dtype=INVOCATION_DTYPE)
+    n_inv = np.zeros(1, dtype=np.int32)
+    bad = np.full(1, -1, dtype=np.int32)
+    rc = lib().tg_slo_replay(_np_ptr(pt), n, ctypes.byref(p), _np_ptr(order), _np_ptr(place),
+                             _np_ptr(inv), _np_ptr(n_inv), _np_ptr(bad))
+    if rc != OK:
+        raise TgError("tg_slo_replay", rc, int(bad[0]))
+    return SloReplay(order, place, inv[: int(n_inv[0])].copy())
 
 
 # --------------------------------------------------------------------------- device side

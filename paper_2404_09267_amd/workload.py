@@ -147,3 +147,23 @@ def random_rois(rng: np.random.Generator, n: int, n_frames: int, frame_w: int, f
     y = rng.integers(0, frame_h - h + 1)
     f = rng.integers(0, n_frames, size=n)
     return np.stack([f, x, y, w, h], axis=1).astype(np.int32)
+
+
+def camera_arrival_trace(wl: Workload, rounds=((0.0, 0.5), (0.3, 0.25)), fps: float = 30.0,
+                         cap: int = 32, seed: int = 5):
+    """An arrival trace for the SLO-aware invoker: the workload's RoIs as patches, frame
+    f of the round sent at offset + f / (fps * n_frames) plus up to 4 ms of jitter, with
+    deadline = arrival + the round's SLO; `rounds` lists (offset s, SLO s). Also returns a
+    synthetic latency table (mean, std per batch of 1..cap canvases) that grows with the
+    batch. Returns (w, h, t_arrive, t_ddl, lat_mean, lat_std) as numpy arrays."""
+    rois = make_rois(wl)
+    rng = np.random.default_rng(seed)
+    per = len(rois) // wl.n_frames
+    t = np.repeat(np.arange(wl.n_frames) * (1.0 / fps / wl.n_frames), per)
+    t = np.sort(t + rng.uniform(0, 0.004, len(t)))
+    w = np.concatenate([rois[: len(t), 3]] * len(rounds))
+    h = np.concatenate([rois[: len(t), 4]] * len(rounds))
+    t_arrive = np.concatenate([t + off for off, _ in rounds])
+    t_ddl = np.concatenate([t + off + slo for off, slo in rounds])
+    b = np.arange(1, cap + 1)
+    return w, h, t_arrive, t_ddl, 0.02 + 0.012 * b, 0.002 + 0.0005 * b

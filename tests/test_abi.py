@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version():
-    assert tg.lib().tg_abi_version() == 2
+    assert tg.lib().tg_abi_version() == 3
 
 
 def test_strerror():
@@ -50,6 +50,14 @@ int main(void) {
   printf("tg_roi %zu\ntg_place %zu\ntg_box %zu\ntg_det %zu\ntg_pack_params %zu\n",
          sizeof(tg_roi), sizeof(tg_place), sizeof(tg_box), sizeof(tg_det), sizeof(tg_pack_params));
   printf("tg_stitch_args %zu\ntg_unstitch_args %zu\n", sizeof(tg_stitch_args), sizeof(tg_unstitch_args));
+  printf("tg_slo_patch %zu\ntg_slo_params %zu\ntg_invocation %zu\n", sizeof(tg_slo_patch),
+         sizeof(tg_slo_params), sizeof(tg_invocation));
+  F(tg_slo_patch, w); F(tg_slo_patch, h); F(tg_slo_patch, t_arrive); F(tg_slo_patch, t_ddl);
+  F(tg_slo_params, canvas_w); F(tg_slo_params, policy); F(tg_slo_params, max_canvases);
+  F(tg_slo_params, n_lat); F(tg_slo_params, lat_mean); F(tg_slo_params, lat_std);
+  F(tg_invocation, t_fire); F(tg_invocation, t_ddl); F(tg_invocation, t_slack);
+  F(tg_invocation, first); F(tg_invocation, count); F(tg_invocation, n_canvases);
+  F(tg_invocation, reason);
   F(tg_stitch_args, frames); F(tg_stitch_args, frame_stride); F(tg_stitch_args, n_frames);
   F(tg_stitch_args, row_pitch); F(tg_stitch_args, rois); F(tg_stitch_args, canvas_begin);
   F(tg_stitch_args, n_rois); F(tg_stitch_args, canvas_first); F(tg_stitch_args, canvas_h);
@@ -75,12 +83,20 @@ def test_struct_layout_matches_header(tmp_path):
     assert c["tg_pack_params"] == ctypes.sizeof(tg.PackParams)
     assert c["tg_stitch_args"] == ctypes.sizeof(tg.StitchArgs)
     assert c["tg_unstitch_args"] == ctypes.sizeof(tg.UnstitchArgs)
+    assert c["tg_slo_patch"] == tg.SLO_PATCH_DTYPE.itemsize == 24
+    assert c["tg_slo_params"] == ctypes.sizeof(tg.SloParams)
+    assert c["tg_invocation"] == tg.INVOCATION_DTYPE.itemsize == 40
+    structs = {"tg_stitch_args": tg.StitchArgs, "tg_unstitch_args": tg.UnstitchArgs,
+               "tg_slo_params": tg.SloParams}
+    dtypes = {"tg_slo_patch": tg.SLO_PATCH_DTYPE, "tg_invocation": tg.INVOCATION_DTYPE}
     for key, off in c.items():
         if "." not in key:
             continue
         struct, field = key.split(".")
-        py = tg.StitchArgs if struct == "tg_stitch_args" else tg.UnstitchArgs
-        assert getattr(py, field).offset == off, key
+        if struct in dtypes:
+            assert dtypes[struct].fields[field][1] == off, key
+        else:
+            assert getattr(structs[struct], field).offset == off, key
 
 
 def _valid_stitch_args():
