@@ -136,6 +136,42 @@ int32_t tg_batch_count(int32_t n_canvases, int32_t batch_cap);
 int tg_batch_range(int32_t n_canvases, int32_t batch_cap, int32_t k, int32_t *first,
                    int32_t *count);
 
+/* ---- Adaptive frame partitioning (Sec. III-A, Alg. 1) ---- */
+
+typedef struct {
+  /* RoIs from the background model, device, grouped by frame: frame f's RoIs are
+   * boxes[frame_begin[f] .. frame_begin[f+1]) and have .frame == f. */
+  const tg_roi *boxes;
+  const int32_t *frame_begin;  /* device [n_frames + 1] */
+  int32_t n_boxes, n_frames, frame_w, frame_h;
+  int32_t zones_x, zones_y;    /* X x Y zones, X <= frame_w, Y <= frame_h, X * Y <= 1024 */
+  tg_roi *patches;             /* device out [n_boxes]: the first *n_patches are valid */
+  int32_t *zone_of_box;        /* device out [n_boxes], or null: zone r* of each RoI, -1 if
+                                  the RoI is skipped */
+  int32_t *n_patches;          /* device out, one int32 */
+  void *workspace;             /* device scratch, >= tg_partition_workspace_bytes(n_frames),
+                                  8-byte aligned */
+  size_t workspace_bytes;
+} tg_partition_args;
+
+/* Device scratch tg_partition needs for n_frames frames (0 when n_frames <= 0). */
+size_t tg_partition_workspace_bytes(int32_t n_frames);
+
+/*
+ * Adaptive frame partitioning (Sec. III-A, Alg. 1): each frame is divided into
+ * zones_x x zones_y zones; zone i of X spans columns [floor(i W / X), floor((i+1) W / X))
+ * and zone j of Y rows [floor(j H / Y), floor((j+1) H / Y)); zone r = j * X + i. Every
+ * RoI joins the zone with the largest overlap area (ties: the lowest r), and every zone
+ * with RoIs becomes one patch, the minimum rectangle enclosing its RoIs (not clipped to
+ * the zone). Patches are written frame by frame, zones in increasing r, as tg_roi records
+ * (frame, x, y, w, h), ready for tg_plan_pack; a patch may be larger than a canvas, which
+ * tg_plan_pack then reports. RoIs that are not inside the frame, have w or h < 1, or carry
+ * another frame id are skipped (zone -1). Enqueued on `stream`; the library allocates
+ * nothing. Returns TG_E_INVAL (null pointer, negative count, bad sizes, more than 1024
+ * zones), TG_E_WORKSPACE, TG_E_HIP. With n_frames == 0 only *n_patches = 0 is written.
+ */
+int tg_partition(const tg_partition_args *args, void *stream);
+
 /* ---- Online SLO-aware batching invoker (Sec. III-C, Alg. 2; Latency Estimator) ---- */
 
 /* A patch as the scheduler receives it: its size, the time it arrives and its deadline

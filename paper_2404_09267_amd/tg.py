@@ -53,12 +53,20 @@ class UnstitchArgs(ctypes.Structure):
                 ("n_out", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
 
 
+class PartitionArgs(ctypes.Structure):
+    _fields_ = [("boxes", _vp), ("frame_begin", _vp), ("n_boxes", _i32), ("n_frames", _i32),
+                ("frame_w", _i32), ("frame_h", _i32), ("zones_x", _i32), ("zones_y", _i32),
+                ("patches", _vp), ("zone_of_box", _vp), ("n_patches", _vp), ("workspace", _vp),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
 class SloParams(ctypes.Structure):
     _fields_ = [("canvas_w", _i32), ("canvas_h", _i32), ("policy", _i32), ("max_canvases", _i32),
                 ("n_lat", _i32), ("lat_mean", _vp), ("lat_std", _vp)]
 
 
-EXPORTS = ["tg_plan_pack", "tg_batch_count", "tg_batch_range", "tg_slo_replay", "tg_stitch",
+EXPORTS = ["tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
+           "tg_batch_range", "tg_slo_replay", "tg_stitch",
            "tg_stitch_units", "tg_stitch_schedule", "tg_stitch_norm_uses_table",
            "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror", "tg_abi_version"]
 
@@ -88,6 +96,10 @@ def lib() -> ctypes.CDLL:
         L.tg_batch_count.restype = _i32
         L.tg_batch_range.argtypes = [_i32, _i32, _i32, _vp, _vp]
         L.tg_batch_range.restype = ctypes.c_int
+        L.tg_partition_workspace_bytes.argtypes = [_i32]
+        L.tg_partition_workspace_bytes.restype = ctypes.c_size_t
+        L.tg_partition.argtypes = [ctypes.POINTER(PartitionArgs), _vp]
+        L.tg_partition.restype = ctypes.c_int
         L.tg_slo_replay.argtypes = [_vp, _i32, ctypes.POINTER(SloParams), _vp, _vp, _vp, _vp,
                                     _vp]
         L.tg_slo_replay.restype = ctypes.c_int
@@ -353,6 +365,51 @@ def stitch_raw(args: StitchArgs, stream=None) -> int:
 
 def unstitch_workspace_bytes(n_boxes: int) -> int:
     return int(lib().tg_unstitch_workspace_bytes(n_boxes))
+
+
+class PartitionBuffers:
+    """Caller-owned device outputs and scratch for tg_partition."""
+
+    def __init__(self, n_boxes: int, n_frames: int, device="cuda"):
+        import torch
+
+        self.n_boxes, self.n_frames = n_boxes, n_frames
+        self.patches = torch.empty((max(n_boxes, 1), 5), dtype=torch.int32, device=device)
+        self.zone_of_box = torch.empty(max(n_boxes, 1), dtype=torch.int32, device=device)
+        self.n_patches = torch.empty(1, dtype=torch.int32, device=device)
+        ws = int(lib().tg_partition_workspace_bytes(n_frames))
+        self.workspace = torch.empty(max(ws, 8), dtype=torch.uint8, device=device)
+        self.workspace_bytes = ws
+
+    def patches_numpy(self) -> np.ndarray:
+        n = int(self.n_patches.item())
+        return self.patches[:n].cpu().numpy()
+
+
+def partition_args(boxes, frame_begin, frame_w, frame_h, zones_x, zones_y,
+                   bufs: PartitionBuffers, zone_of_box=True) -> PartitionArgs:
+    import torch
+
+    _check(boxes, torch.int32, (bufs.n_boxes, 5), "boxes")
+    _check(frame_begin, torch.int32, (bufs.n_frames + 1,), "frame_begin")
+    a = PartitionArgs()
+    a.boxes, a.frame_begin = boxes.data_ptr(), frame_begin.data_ptr()
+    a.n_boxes, a.n_frames, a.frame_w, a.frame_h = bufs.n_boxes, bufs.n_frames, frame_w, frame_h
+    a.zones_x, a.zones_y = zones_x, zones_y
+    a.patches = bufs.patches.data_ptr()
+    a.zone_of_box = bufs.zone_of_box.data_ptr() if zone_of_box else None
+    a.n_patches = bufs.n_patches.data_ptr()
+    a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    return a
+
+
+def partition(boxes, frame_begin, frame_w, frame_h, zones_x, zones_y, bufs: PartitionBuffers,
+              stream=None, zone_of_box=True) -> None:
+    """Enqueue tg_partition; patches land in `bufs`."""
+    a = partition_args(boxes, frame_begin, frame_w, frame_h, zones_x, zones_y, bufs, zone_of_box)
+    rc = lib().tg_partition(ctypes.byref(a), _stream_handle(stream))
+    if rc != OK:
+        raise TgError("tg_partition", rc)
 
 
 class UnstitchBuffers:

@@ -167,3 +167,32 @@ def camera_arrival_trace(wl: Workload, rounds=((0.0, 0.5), (0.3, 0.25)), fps: fl
     t_ddl = np.concatenate([t + off + slo for off, slo in rounds])
     b = np.arange(1, cap + 1)
     return w, h, t_arrive, t_ddl, 0.02 + 0.012 * b, 0.002 + 0.0005 * b
+
+
+def make_gmm_boxes(n_frames: int, per_frame: int, frame_w: int, frame_h: int, seed: int,
+                   lo: int = 8, hi: int = 160, clusters: int = 4):
+    """Synthetic background-model RoIs (the input of adaptive frame partitioning), grouped
+    by frame: per frame a count uniform in [0, 2 * per_frame], sides log-uniform in
+    [lo, hi], 70 % of the boxes scattered around one of `clusters` centres (normal,
+    sigma = frame_w / 12) and the rest uniform, every box clamped inside the frame.
+    Returns (boxes int32 [n, 5] as (frame, x, y, w, h), frame_begin int32 [n_frames + 1])."""
+    rng = np.random.default_rng(seed)
+    counts = rng.integers(0, 2 * per_frame + 1, n_frames)
+    frame_begin = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    n = int(frame_begin[-1])
+    frame = np.repeat(np.arange(n_frames), counts)
+    w = np.rint(np.exp(rng.uniform(np.log(lo), np.log(hi), n))).astype(np.int64)
+    h = np.rint(np.exp(rng.uniform(np.log(lo), np.log(hi), n))).astype(np.int64)
+    w = np.clip(w, 1, frame_w)
+    h = np.clip(h, 1, frame_h)
+    cx = rng.uniform(0, frame_w, (n_frames, clusters))
+    cy = rng.uniform(0, frame_h, (n_frames, clusters))
+    pick = rng.integers(0, clusters, n)
+    near = rng.random(n) < 0.7
+    sd = frame_w / 12.0
+    x = np.where(near, cx[frame, pick] + rng.normal(0, sd, n), rng.uniform(0, frame_w, n))
+    y = np.where(near, cy[frame, pick] + rng.normal(0, sd, n), rng.uniform(0, frame_h, n))
+    x = np.clip(np.rint(x - w / 2), 0, frame_w - w).astype(np.int64)
+    y = np.clip(np.rint(y - h / 2), 0, frame_h - h).astype(np.int64)
+    boxes = np.stack([frame, x, y, w, h], 1).astype(np.int32)
+    return boxes, frame_begin
