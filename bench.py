@@ -153,6 +153,50 @@ def invoker_cost(tg, W, with_oracle: bool):
     return out
 
 
+def partition_cost(tg, W, torch, with_oracle: bool, launches: int = 50):
+    """tg_partition (Alg. 1) over a 64-camera x 30-frame window of 3840x2160 frames with
+    synthetic background-model RoIs and 4 x 4 zones, timed with HIP events on the stream
+    it runs on; the oracle on a sample of the same frames."""
+    import time as _t
+
+    frames, fw, fh, zx, zy = 1920, 3840, 2160, 4, 4
+    boxes, fb = W.make_gmm_boxes(frames, 30, fw, fh, seed=77)
+    bufs = tg.PartitionBuffers(len(boxes), frames)
+    boxes_d = torch.from_numpy(boxes).cuda()
+    fb_d = torch.from_numpy(fb).cuda()
+    a = tg.partition_args(boxes_d, fb_d, fw, fh, zx, zy, bufs, zone_of_box=False)
+    stream = torch.cuda.current_stream()
+    h = tg._vp(stream.cuda_stream)
+    for _ in range(3):
+        tg.lib().tg_partition(tg.ctypes.byref(a), h)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs[0].record(stream)
+    for i in range(launches):
+        rc = tg.lib().tg_partition(tg.ctypes.byref(a), h)
+        if rc != tg.OK:
+            raise tg.TgError("tg_partition", rc)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
+    n_patches = int(bufs.n_patches.item())
+    out = {"workload": f"{frames} frames {fw}x{fh} (64 cameras x 30), {len(boxes)} RoIs, "
+                       f"{zx}x{zy} zones", "patches": n_patches,
+           "us_per_launch": round(us, 2), "mroi_per_s": round(len(boxes) / us, 1),
+           "bound": "latency: 2 launches, one 256-thread workgroup per frame",
+           "algorithmic_bytes": int(20 * len(boxes) + 4 * (frames + 1) + 20 * n_patches)}
+    if with_oracle:
+        from oracle import partition
+
+        sample = frames  # the whole window: about a second
+        t0 = _t.perf_counter()
+        partition.partition(boxes[: fb[sample]].tolist(), fb[: sample + 1].tolist(), fw, fh, zx, zy)
+        el = _t.perf_counter() - t0
+        out["oracle_mroi_per_s"] = round(fb[sample] / el / 1e6, 4)
+        out["oracle_sample"] = f"first {sample} frames ({int(fb[sample])} RoIs), {el:.2f} s"
+    return out
+
+
 _W = None
 
 
@@ -324,6 +368,7 @@ def main():
         "stitch_pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
     }
     result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
+    result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         frames_np = frames_d.cpu().numpy()
         result["cpu_baseline"] = cpu_baseline(wl, rois, frames_np, boxes, canv, args.cpu_seconds)

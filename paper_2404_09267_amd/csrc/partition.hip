@@ -21,6 +21,7 @@
 #include <climits>
 #include <cstdint>
 
+#include "lookback.h"
 #include "tg.h"
 
 namespace {
@@ -28,9 +29,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxZones = 1024;                     // zones per frame, e.g. 32 x 32
-constexpr uint64_t kAggregate = uint64_t(1) << 32;  // state: value = this frame's patches
-constexpr uint64_t kInclusive = uint64_t(2) << 32;  // state: value = patches of frames 0..f
-constexpr uint32_t kSpinLimit = 1u << 26;           // bounded wait; never reached in practice
 
 struct PartitionParams {
   const tg_roi *boxes;
@@ -55,13 +53,6 @@ __device__ __forceinline__ int zone_of(int p, int n, int size) {
 __global__ void clear_kernel(uint64_t *words, int32_t n_words) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n_words) words[i] = 0;
-}
-
-__device__ __forceinline__ uint64_t load_state(const uint64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_state(uint64_t *p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __global__ __launch_bounds__(kThreads) void zone_kernel(const PartitionParams P) {
@@ -122,23 +113,12 @@ __global__ __launch_bounds__(kThreads) void zone_kernel(const PartitionParams P)
     for (int w = 0; w < kWaves; ++w) total += s_wave[w];
     __syncthreads();
   }
-  if (tid == 0) {
-    int prefix = 0;
-    if (f == 0) {
-      store_state(&P.state[0], kInclusive | uint32_t(total));
-    } else {
-      store_state(&P.state[f], kAggregate | uint32_t(total));
-      for (int j = f - 1; j >= 0; --j) {
-        uint64_t s = load_state(&P.state[j]);
-        for (uint32_t spin = 0; (s >> 32) == 0 && spin < kSpinLimit; ++spin)
-          s = load_state(&P.state[j]);
-        prefix += static_cast<int>(static_cast<uint32_t>(s));
-        if ((s >> 32) != (kAggregate >> 32)) break;  // inclusive (or a timed-out wait)
-      }
-      store_state(&P.state[f], kInclusive | uint32_t(prefix + total));
+  if (wave == 0) {
+    const int prefix = tg_detail::lookback_prefix(P.state, f, total);
+    if (lane == 0) {
+      s_prefix = prefix;
+      if (f == P.n_frames - 1) *P.n_patches = prefix + total;
     }
-    s_prefix = prefix;
-    if (f == P.n_frames - 1) *P.n_patches = prefix + total;
   }
   __syncthreads();
 

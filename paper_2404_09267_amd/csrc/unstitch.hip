@@ -20,6 +20,7 @@
 
 #include <cstdint>
 
+#include "lookback.h"
 #include "tg.h"
 
 namespace {
@@ -27,9 +28,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kBoxesPerThread = 4;                  // emit: consecutive boxes per thread
 constexpr int kEmitBoxes = kThreads * kBoxesPerThread;
-constexpr uint64_t kAggregate = uint64_t(1) << 32;  // state: value = this block's count
-constexpr uint64_t kInclusive = uint64_t(2) << 32;  // state: value = count of blocks 0..i
-constexpr uint32_t kSpinLimit = 1u << 26;           // bounded wait; never reached in practice
 
 struct UnstitchParams {
   const tg_box *boxes;
@@ -91,13 +89,6 @@ __global__ __launch_bounds__(kThreads) void assign_kernel(const UnstitchParams P
     }
   }
   if (sl == 0) P.roi_of_box[b] = -1;
-}
-
-__device__ __forceinline__ uint64_t load_state(const uint64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_state(uint64_t *p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row broadcasts).
@@ -163,23 +154,12 @@ __global__ __launch_bounds__(kThreads) void emit_kernel(const UnstitchParams P) 
     if (w < wave) before += s_wave[w];
     total += s_wave[w];
   }
-  if (tid == 0) {
-    int prefix = 0;
-    if (blk == 0) {
-      store_state(&P.state[0], kInclusive | uint32_t(total));
-    } else {
-      store_state(&P.state[blk], kAggregate | uint32_t(total));
-      for (int j = blk - 1; j >= 0; --j) {
-        uint64_t s = load_state(&P.state[j]);
-        for (uint32_t spin = 0; (s >> 32) == 0 && spin < kSpinLimit; ++spin)
-          s = load_state(&P.state[j]);
-        prefix += static_cast<int>(static_cast<uint32_t>(s));
-        if ((s >> 32) != (kAggregate >> 32)) break;  // inclusive (or a timed-out wait)
-      }
-      store_state(&P.state[blk], kInclusive | uint32_t(prefix + total));
+  if (wave == 0) {
+    const int prefix = tg_detail::lookback_prefix(P.state, blk, total);
+    if (lane == 0) {
+      s_prefix = prefix;
+      if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = prefix + total;
     }
-    s_prefix = prefix;
-    if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = prefix + total;
   }
   __syncthreads();
   int pos = s_prefix + before + incl - cnt;
