@@ -367,6 +367,49 @@ size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
  */
 int tg_unstitch(const tg_unstitch_args *args, void *stream);
 
+/* ---- Per-frame merge of detections after unstitch (Sec. III-A patches, Sec. V-D) ---- */
+
+typedef struct {
+  const tg_det *dets;       /* device [n_max]: tg_unstitch's output; box indices unique */
+  const int32_t *n_dets;    /* device: how many of dets are valid (tg_unstitch's n_out) */
+  int32_t n_max;            /* capacity of dets, keep and out */
+  const float *scores;      /* device [n_scores]: detector score of each box, by tg_det.box */
+  int32_t n_scores;
+  int32_t n_frames;         /* frames are 0 .. n_frames-1 */
+  float iou_threshold;
+  int32_t cross_only;       /* nonzero: only detections from different patches suppress */
+  int32_t *keep;            /* device out [n_max]: 1 kept, 0 dropped, for the first *n_dets */
+  tg_det *out;              /* device out [n_max]: kept detections in input order */
+  int32_t *n_kept;          /* device out, one int32 */
+  int32_t *n_overflow;      /* device out, one int32: frames with more than 2048 detections,
+                               left unmerged (all kept) */
+  void *workspace;          /* device scratch, >= tg_merge_workspace_bytes(n_max, n_frames),
+                               8-byte aligned */
+  size_t workspace_bytes;
+} tg_merge_args;
+
+/* Device scratch tg_merge needs (0 when n_max <= 0). */
+size_t tg_merge_workspace_bytes(int32_t n_max, int32_t n_frames);
+
+/*
+ * Per-frame duplicate suppression of mapped-back detections. Patches of one frame can
+ * overlap when a frame is cut into zone patches (Sec. III-A, Alg. 1), so one object can
+ * come back twice; the paper scores per frame (Sec. V-D) without spelling out a merge.
+ * This library's reading: a frame's detections are ranked by score (higher first; equal
+ * scores by box index, lower first; a NaN score, or a box index outside [0, n_scores),
+ * ranks as -infinity) and, walking the ranking, a detection is kept unless one kept
+ * before it in the same frame (with cross_only: from another patch, tg_det.roi) overlaps
+ * it by IoU > iou_threshold, decided in binary32 with every operation rounded on its own:
+ * w = max(0, min(x2a, x2b) - max(x1a, x1b)), h likewise, inter = w * h,
+ * area = max(0, x2 - x1) * max(0, y2 - y1), union = (area_a + area_b) - inter,
+ * suppressed when inter > iou_threshold * union. Detections whose frame is outside
+ * [0, n_frames) are dropped. Kept detections are written to out in input order and their
+ * count to *n_kept. Enqueued on `stream`; the library allocates nothing.
+ * Returns TG_E_INVAL (null pointer, negative size, NaN threshold), TG_E_WORKSPACE,
+ * TG_E_HIP. With n_max == 0 only *n_kept = *n_overflow = 0 is written.
+ */
+int tg_merge(const tg_merge_args *args, void *stream);
+
 /* Static description of a status code. */
 const char *tg_strerror(int code);
 

@@ -21,7 +21,7 @@ LIB = os.path.join(PKG, "libtg.so")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["plan.cpp", "norm.cpp", "invoker.cpp"]
-HIP_SOURCES = ["stitch.hip", "unstitch.hip", "partition.hip"]
+HIP_SOURCES = ["stitch.hip", "unstitch.hip", "partition.hip", "merge.hip"]
 
 # Packed FP32 instructions are kept out of every kernel; scalar code is all we need.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,

@@ -60,6 +60,13 @@ class PartitionArgs(ctypes.Structure):
                 ("workspace_bytes", ctypes.c_size_t)]
 
 
+class MergeArgs(ctypes.Structure):
+    _fields_ = [("dets", _vp), ("n_dets", _vp), ("n_max", _i32), ("scores", _vp),
+                ("n_scores", _i32), ("n_frames", _i32), ("iou_threshold", _f32),
+                ("cross_only", _i32), ("keep", _vp), ("out", _vp), ("n_kept", _vp),
+                ("n_overflow", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
+
+
 class SloParams(ctypes.Structure):
     _fields_ = [("canvas_w", _i32), ("canvas_h", _i32), ("policy", _i32), ("max_canvases", _i32),
                 ("n_lat", _i32), ("lat_mean", _vp), ("lat_std", _vp)]
@@ -68,7 +75,8 @@ class SloParams(ctypes.Structure):
 EXPORTS = ["tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
            "tg_batch_range", "tg_slo_replay", "tg_stitch",
            "tg_stitch_units", "tg_stitch_schedule", "tg_stitch_norm_uses_table",
-           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_strerror", "tg_abi_version"]
+           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_merge_workspace_bytes", "tg_merge",
+           "tg_strerror", "tg_abi_version"]
 
 _lib = None
 
@@ -116,6 +124,10 @@ def lib() -> ctypes.CDLL:
         L.tg_unstitch_workspace_bytes.restype = ctypes.c_size_t
         L.tg_unstitch.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
         L.tg_unstitch.restype = ctypes.c_int
+        L.tg_merge_workspace_bytes.argtypes = [_i32, _i32]
+        L.tg_merge_workspace_bytes.restype = ctypes.c_size_t
+        L.tg_merge.argtypes = [ctypes.POINTER(MergeArgs), _vp]
+        L.tg_merge.restype = ctypes.c_int
         L.tg_strerror.argtypes = [ctypes.c_int]
         L.tg_strerror.restype = ctypes.c_char_p
         L.tg_abi_version.argtypes = []
@@ -460,3 +472,51 @@ def unstitch(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers,
 
 def unstitch_raw(args: UnstitchArgs, stream=None) -> int:
     return int(lib().tg_unstitch(ctypes.byref(args), _stream_handle(stream)))
+
+
+class MergeBuffers:
+    """Caller-owned device outputs and scratch for tg_merge."""
+
+    def __init__(self, n_max: int, n_frames: int, device="cuda"):
+        import torch
+
+        self.n_max, self.n_frames = n_max, n_frames
+        self.keep = torch.empty(max(n_max, 1), dtype=torch.int32, device=device)
+        self.out = torch.empty((max(n_max, 1), DET_WORDS), dtype=torch.int32, device=device)
+        self.n_kept = torch.empty(1, dtype=torch.int32, device=device)
+        self.n_overflow = torch.empty(1, dtype=torch.int32, device=device)
+        ws = int(lib().tg_merge_workspace_bytes(n_max, n_frames))
+        self.workspace = torch.empty(max(ws, 8), dtype=torch.uint8, device=device)
+        self.workspace_bytes = ws
+
+    def kept_numpy(self) -> np.ndarray:
+        n = int(self.n_kept.item())
+        return self.out[:n].cpu().numpy().view(DET_DTYPE).reshape(-1)
+
+
+def merge_args(dets, n_dets, scores, n_frames, iou_threshold, cross_only,
+               bufs: MergeBuffers) -> MergeArgs:
+    """dets: int32 [n_max, 7] device tensor of tg_det (e.g. UnstitchBuffers.dets); n_dets:
+    device int32 [1] (e.g. UnstitchBuffers.n_out); scores: device float32 per box."""
+    import torch
+
+    _check(dets, torch.int32, (bufs.n_max, DET_WORDS), "dets")
+    _check(n_dets, torch.int32, (1,), "n_dets")
+    _check(scores, torch.float32, None, "scores")
+    a = MergeArgs()
+    a.dets, a.n_dets, a.n_max = dets.data_ptr(), n_dets.data_ptr(), bufs.n_max
+    a.scores, a.n_scores = scores.data_ptr(), scores.numel()
+    a.n_frames, a.iou_threshold, a.cross_only = n_frames, float(iou_threshold), int(bool(cross_only))
+    a.keep, a.out = bufs.keep.data_ptr(), bufs.out.data_ptr()
+    a.n_kept, a.n_overflow = bufs.n_kept.data_ptr(), bufs.n_overflow.data_ptr()
+    a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    return a
+
+
+def merge(dets, n_dets, scores, n_frames, iou_threshold, cross_only, bufs: MergeBuffers,
+          stream=None) -> None:
+    """Enqueue tg_merge; results land in `bufs`."""
+    a = merge_args(dets, n_dets, scores, n_frames, iou_threshold, cross_only, bufs)
+    rc = lib().tg_merge(ctypes.byref(a), _stream_handle(stream))
+    if rc != OK:
+        raise TgError("tg_merge", rc)

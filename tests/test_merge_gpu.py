@@ -1,0 +1,121 @@
+"""tg_merge on the GPU against the oracle: keep flags, kept detections and counts,
+bit-exact, through the C ABI, including the path fed directly by tg_unstitch."""
+import numpy as np
+import pytest
+
+from gpu_helpers import say
+from paper_2404_09267_amd import tg
+from paper_2404_09267_amd import workload as W
+from test_merge import golden_inputs, random_dets
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    tg.lib()
+    return torch
+
+
+def run_gpu(torch, dets, scores, n_frames, thr, cross_only, n_max=None):
+    n = len(dets)
+    n_max = n if n_max is None else n_max
+    host = np.zeros((max(n_max, 1), tg.DET_WORDS), np.int32)
+    host[:n] = dets.view(np.int32).reshape(n, tg.DET_WORDS)
+    bufs = tg.MergeBuffers(n_max, n_frames)
+    bufs.keep.fill_(-7)
+    d = torch.from_numpy(host).cuda()
+    if n_max == 0:
+        d = d[:0]
+    tg.merge(d, torch.tensor([n], dtype=torch.int32, device="cuda"),
+             torch.from_numpy(np.ascontiguousarray(scores, np.float32)).cuda(), n_frames, thr,
+             cross_only, bufs)
+    torch.cuda.synchronize()
+    return (bufs.keep[:n].cpu().numpy(), bufs.kept_numpy(), int(bufs.n_kept.item()),
+            int(bufs.n_overflow.item()))
+
+
+def check(torch, dets, scores, n_frames, thr, cross_only, **kw):
+    from oracle import merge
+
+    say("merge", len(dets), n_frames, thr, cross_only)
+    keep, kept, n_kept, over = run_gpu(torch, dets, scores, n_frames, thr, cross_only, **kw)
+    want_keep, want_kept = merge.merge(dets, scores, n_frames, thr, cross_only)
+    np.testing.assert_array_equal(keep, want_keep.astype(np.int32))
+    assert n_kept == len(want_kept)
+    np.testing.assert_array_equal(kept.view(np.int32), want_kept.view(np.int32))
+    assert over == 0
+    return keep
+
+
+@pytest.mark.parametrize("cross_only,key", [(True, "keep_cross_only"), (False, "keep_all_pairs")])
+def test_golden(torch, cross_only, key):
+    g, dets, scores = golden_inputs()
+    keep, _, _, _ = run_gpu(torch, dets, scores, g["n_frames"], g["threshold"], cross_only)
+    assert keep.tolist() == g[key]
+
+
+@pytest.mark.parametrize("cross_only,thr", [(True, 0.5), (False, 0.45), (True, 0.0), (False, 1.0)])
+def test_random(torch, cross_only, thr):
+    rng = np.random.default_rng(int(thr * 100) + cross_only)
+    dets, scores = random_dets(rng, 5000, 40, 30)
+    dets["frame"][rng.random(5000) < 0.02] = 40 + rng.integers(0, 5)  # outside [0, 40)
+    check(torch, dets, scores, 40, thr, cross_only)
+
+
+def test_after_unstitch_on_device(torch):
+    """tg_unstitch's device outputs feed tg_merge directly (no host copy in between)."""
+    from oracle import merge
+
+    wl = W.WORKLOADS["cam20_4k"]
+    rois = W.make_rois(wl)
+    plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
+    boxes, canv = W.make_boxes(wl, plan.n_canvases)
+    dplan = tg.DevicePlan(rois, plan)
+    ub = tg.UnstitchBuffers(len(boxes))
+    tg.unstitch(torch.from_numpy(boxes).cuda(), torch.from_numpy(canv).cuda(), dplan, 1, ub)
+    scores = np.random.default_rng(2).uniform(0, 1, len(boxes)).astype(np.float32)
+    mb = tg.MergeBuffers(len(boxes), wl.n_frames)
+    tg.merge(ub.dets, ub.n_out, torch.from_numpy(scores).cuda(), wl.n_frames, 0.5, True, mb)
+    torch.cuda.synchronize()
+    dets = ub.dets_numpy()
+    want_keep, want_kept = merge.merge(dets, scores, wl.n_frames, 0.5, True)
+    np.testing.assert_array_equal(mb.keep[: len(dets)].cpu().numpy(), want_keep.astype(np.int32))
+    np.testing.assert_array_equal(mb.kept_numpy().view(np.int32), want_kept.view(np.int32))
+    assert 0 < len(want_kept) < len(dets)
+
+
+def test_large_frames(torch):
+    rng = np.random.default_rng(9)
+    # exactly 2048 detections in frame 0, 300 in frame 1: merged
+    dets, scores = random_dets(rng, 2348, 2, 10, span=600.0)
+    dets["frame"] = np.r_[np.zeros(2048, np.int32), np.ones(300, np.int32)]
+    check(torch, dets, scores, 2, 0.5, True)
+    # 2049 in frame 0: left unmerged (all kept), frame 1 still merged
+    dets, scores = random_dets(rng, 2349, 2, 10, span=600.0)
+    dets["frame"] = np.r_[np.zeros(2049, np.int32), np.ones(300, np.int32)]
+    keep, kept, n_kept, over = run_gpu(torch, dets, scores, 2, 0.5, True)
+    assert over == 1 and keep[:2049].all()
+    from oracle import merge
+
+    want, _ = merge.merge(dets[2049:], scores, 2, 0.5, True)
+    np.testing.assert_array_equal(keep[2049:], want.astype(np.int32))
+
+
+def test_partial_count_and_empty(torch):
+    rng = np.random.default_rng(4)
+    dets, scores = random_dets(rng, 800, 5, 4)
+    # only the first 600 entries are valid (device count), capacity 800
+    from oracle import merge
+
+    keep, kept, n_kept, _ = run_gpu(torch, dets[:600], scores, 5, 0.5, True, n_max=800)
+    want_keep, want_kept = merge.merge(dets[:600], scores, 5, 0.5, True)
+    np.testing.assert_array_equal(keep, want_keep.astype(np.int32))
+    assert n_kept == len(want_kept)
+    _, _, n_kept, over = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=64)
+    assert n_kept == 0 and over == 0
+    _, _, n_kept, over = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=0)
+    assert n_kept == 0 and over == 0
