@@ -197,6 +197,45 @@ def partition_cost(tg, W, torch, with_oracle: bool, launches: int = 50):
     return out
 
 
+def merge_cost(tg, W, torch, uargs, ubufs, n_frames, with_oracle: bool, launches: int = 50):
+    """tg_merge on the bench's own tg_unstitch output (cam20_4k, 10,000 boxes, seeded
+    detector scores, IoU 0.5 across patches), timed with HIP events; the oracle beside."""
+    stream = torch.cuda.current_stream()
+    h = tg._vp(stream.cuda_stream)
+    rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
+    if rc != tg.OK:
+        raise tg.TgError("tg_unstitch", rc)
+    n_boxes = ubufs.n_boxes
+    scores = torch.from_numpy(np.random.default_rng(2).uniform(0, 1, n_boxes)
+                              .astype(np.float32)).cuda()
+    mb = tg.MergeBuffers(n_boxes, n_frames)
+    a = tg.merge_args(ubufs.dets, ubufs.n_out, scores, n_frames, 0.5, True, mb)
+    for _ in range(3):
+        tg.lib().tg_merge(tg.ctypes.byref(a), h)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs[0].record(stream)
+    for i in range(launches):
+        rc = tg.lib().tg_merge(tg.ctypes.byref(a), h)
+        if rc != tg.OK:
+            raise tg.TgError("tg_merge", rc)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
+    n_dets = int(ubufs.n_out.item())
+    out = {"input": f"tg_unstitch output of cam20_4k ({n_dets} detections, {n_frames} frames), "
+                    "IoU 0.5 across patches", "kept": int(mb.n_kept.item()),
+           "us_per_call": round(us, 2), "bound": "latency: 6 small launches"}
+    if with_oracle:
+        from oracle import merge
+
+        dets = ubufs.dets_numpy()
+        t0 = time.perf_counter()
+        merge.merge(dets, scores.cpu().numpy(), n_frames, 0.5, True)
+        out["oracle_us_per_call"] = round((time.perf_counter() - t0) * 1e6, 1)
+    return out
+
+
 _W = None
 
 
@@ -369,6 +408,7 @@ def main():
     }
     result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
     result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
+    result["merge"] = merge_cost(tg, W, torch, uargs, ubufs, wl.n_frames, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         frames_np = frames_d.cpu().numpy()
         result["cpu_baseline"] = cpu_baseline(wl, rois, frames_np, boxes, canv, args.cpu_seconds)

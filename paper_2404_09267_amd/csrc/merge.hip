@@ -12,13 +12,17 @@
 // Six launches on the caller's stream, all on device data (the detection count comes from
 // tg_unstitch's n_out on the device):
 //  1. clear the per-frame counters and look-back words;
-//  2. count detections per frame (atomics);
+//  2. count detections per frame (LDS histograms, one global atomic per frame and
+//     workgroup);
 //  3. exclusive scan of the counts (one workgroup);
-//  4. scatter detection indices into frame groups (a per-frame cursor; the order inside a
-//     group does not matter, the ranking below is a total order);
-//  5. one 256-thread workgroup per frame: bitonic sort of 64-bit keys (score, box) in LDS,
-//     then the greedy pass with one barrier per candidate; up to 2048 detections per
-//     frame, more are left unmerged (all kept) and counted in n_overflow;
+//  4. scatter detection indices into frame groups (ranks inside a workgroup from LDS, one
+//     range per frame and workgroup from a global cursor; the order inside a group does
+//     not matter, the ranking below is a total order);
+//  5. one 1024-thread workgroup per frame: bitonic sort of 64-bit keys (score, box) in LDS,
+//     then the greedy pass 64 candidates at a time (all threads test the chunk against the
+//     detections kept so far and fill the chunk's 64 x 64 suppression bits; one wave walks
+//     the chunk); up to 2048 detections per frame, more are left unmerged (all kept) and
+//     counted in n_overflow;
 //  6. stable compaction of the kept detections (decoupled look-back, 1024 per workgroup).
 #include <hip/hip_runtime.h>
 
@@ -68,14 +72,30 @@ __global__ void clear_kernel(MergeParams P, int32_t n_words32, int32_t n_words64
   if (i == 0) *P.n_overflow = 0;
 }
 
-__global__ void count_kernel(const MergeParams P) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= count_of(P)) return;
-  const int f = P.dets[i].frame;
-  if (f >= 0 && f < P.n_frames)
-    atomicAdd(&P.counts[f], 1);
-  else
-    P.keep[i] = 0;  // no frame to merge in: dropped
+// Detections per frame. Up to kHistMax frames a workgroup first counts in LDS and then
+// adds each non-empty bin to the global count once (many detections share few frames, so
+// direct global atomics would queue on the same words).
+constexpr int kHistMax = 4096;
+
+__global__ __launch_bounds__(kThreads) void count_kernel(const MergeParams P) {
+  __shared__ int hist[kHistMax];
+  const int tid = threadIdx.x;
+  const bool local = P.n_frames <= kHistMax;
+  if (local)
+    for (int f = tid; f < P.n_frames; f += kThreads) hist[f] = 0;
+  __syncthreads();
+  const int i = blockIdx.x * kThreads + tid;
+  if (i < count_of(P)) {
+    const int f = P.dets[i].frame;
+    if (f >= 0 && f < P.n_frames)
+      atomicAdd(local ? &hist[f] : &P.counts[f], 1);
+    else
+      P.keep[i] = 0;  // no frame to merge in: dropped
+  }
+  if (!local) return;
+  __syncthreads();
+  for (int f = tid; f < P.n_frames; f += kThreads)
+    if (hist[f]) atomicAdd(&P.counts[f], hist[f]);
 }
 
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const MergeParams P) {
@@ -104,12 +124,32 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const MergeParams P)
   if (tid == 0) P.frame_begin[P.n_frames] = carry;
 }
 
-__global__ void scatter_kernel(const MergeParams P) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= count_of(P)) return;
-  const int f = P.dets[i].frame;
-  if (f < 0 || f >= P.n_frames) return;
-  P.grouped[P.frame_begin[f] + atomicAdd(&P.cursor[f], 1)] = i;
+// Detection indices into frame groups. Up to kHistMax frames a workgroup ranks its
+// detections per frame in LDS and reserves one range per non-empty frame.
+__global__ __launch_bounds__(kThreads) void scatter_kernel(const MergeParams P) {
+  __shared__ int hist[kHistMax];
+  const int tid = threadIdx.x;
+  const bool local = P.n_frames <= kHistMax;
+  if (local)
+    for (int f = tid; f < P.n_frames; f += kThreads) hist[f] = 0;
+  __syncthreads();
+  const int i = blockIdx.x * kThreads + tid;
+  int f = -1, rank = 0;
+  if (i < count_of(P)) {
+    f = P.dets[i].frame;
+    if (f < 0 || f >= P.n_frames)
+      f = -1;
+    else if (local)
+      rank = atomicAdd(&hist[f], 1);
+    else
+      P.grouped[P.frame_begin[f] + atomicAdd(&P.cursor[f], 1)] = i;
+  }
+  if (!local) return;
+  __syncthreads();
+  for (int g = tid; g < P.n_frames; g += kThreads)  // this workgroup's range of frame g
+    if (hist[g]) hist[g] = P.frame_begin[g] + atomicAdd(&P.cursor[g], hist[g]);
+  __syncthreads();
+  if (f >= 0) P.grouped[hist[f] + rank] = i;
 }
 
 // Ranking key, ascending = higher score first, then lower box index. NaN ranks as -inf;
@@ -133,25 +173,46 @@ __device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
   return inter > __fmul_rn(thr, uni);
 }
 
-__global__ __launch_bounds__(kThreads) void frame_kernel(const MergeParams P) {
-  __shared__ uint64_t key[kMaxPerFrame];
-  __shared__ int32_t det[kMaxPerFrame];
-  __shared__ float4 box[kMaxPerFrame];
-  __shared__ int32_t roi[kMaxPerFrame];
-  __shared__ uint8_t alive[kMaxPerFrame];
-  const int tid = threadIdx.x;
+// LDS of one frame: ranking keys and detection ids for the sort, then the ranked boxes,
+// patches and flags, the list of detections kept so far and one chunk's bit matrix.
+constexpr int kChunk = 64;  // candidates decided per round
+constexpr int kFrameThreads = 1024;  // one workgroup per frame
+static_assert(kChunk * kChunk % kFrameThreads == 0 && 32 % (kChunk * kChunk / kFrameThreads) == 0,
+              "a thread's columns lie in one 32-bit word");
+constexpr size_t kOffKey = 0;                                          // u64 [2048]
+constexpr size_t kOffDet = kOffKey + sizeof(uint64_t) * kMaxPerFrame;  // i32 [2048]
+constexpr size_t kOffBox = kOffDet + sizeof(int32_t) * kMaxPerFrame;   // float4 [2048]
+constexpr size_t kOffRoi = kOffBox + sizeof(float4) * kMaxPerFrame;    // i32 [2048]
+constexpr size_t kOffKeptBox = kOffRoi + sizeof(int32_t) * kMaxPerFrame;  // float4 [2048]
+constexpr size_t kOffKeptRoi = kOffKeptBox + sizeof(float4) * kMaxPerFrame;  // i32 [2048]
+constexpr size_t kOffBits = kOffKeptRoi + sizeof(int32_t) * kMaxPerFrame;   // u32 [64][2]
+constexpr size_t kOffAlive = kOffBits + sizeof(uint32_t) * 2 * kChunk; // u8 [2048]
+constexpr size_t kLdsBytes = kOffAlive + kMaxPerFrame;
+
+__global__ __launch_bounds__(kFrameThreads) void frame_kernel(const MergeParams P) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
+  __shared__ int s_kept;
+  uint64_t *key = reinterpret_cast<uint64_t *>(lds + kOffKey);
+  int32_t *det = reinterpret_cast<int32_t *>(lds + kOffDet);
+  float4 *box = reinterpret_cast<float4 *>(lds + kOffBox);
+  int32_t *roi = reinterpret_cast<int32_t *>(lds + kOffRoi);
+  float4 *kept_box = reinterpret_cast<float4 *>(lds + kOffKeptBox);
+  int32_t *kept_roi = reinterpret_cast<int32_t *>(lds + kOffKeptRoi);
+  uint32_t *bits = reinterpret_cast<uint32_t *>(lds + kOffBits);  // row a: bits[2a], bits[2a+1]
+  uint8_t *alive = lds + kOffAlive;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int f = blockIdx.x;
   const int lo = P.frame_begin[f];
   const int n = P.frame_begin[f + 1] - lo;
   if (n <= 0) return;
   if (n > kMaxPerFrame) {  // left unmerged
-    for (int k = tid; k < n; k += kThreads) P.keep[P.grouped[lo + k]] = 1;
+    for (int k = tid; k < n; k += kFrameThreads) P.keep[P.grouped[lo + k]] = 1;
     if (tid == 0) atomicAdd(P.n_overflow, 1);
     return;
   }
   int pw = 1;
   while (pw < n) pw <<= 1;
-  for (int k = tid; k < pw; k += kThreads) {
+  for (int k = tid; k < pw; k += kFrameThreads) {
     if (k < n) {
       const int i = P.grouped[lo + k];
       const int32_t b = P.dets[i].box;
@@ -163,11 +224,12 @@ __global__ __launch_bounds__(kThreads) void frame_kernel(const MergeParams P) {
       det[k] = -1;
     }
   }
+  if (tid == 0) s_kept = 0;
   __syncthreads();
   // Bitonic sort of pw keys, ascending.
   for (int size = 2; size <= pw; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int t = tid; t < pw / 2; t += kThreads) {
+      for (int t = tid; t < pw / 2; t += kFrameThreads) {
         const int i = 2 * t - (t & (stride - 1));
         const int j = i + stride;
         const bool up = (i & size) == 0;
@@ -183,25 +245,73 @@ __global__ __launch_bounds__(kThreads) void frame_kernel(const MergeParams P) {
       __syncthreads();
     }
   }
-  for (int k = tid; k < n; k += kThreads) {
+  for (int k = tid; k < n; k += kFrameThreads) {
     const tg_det d = P.dets[det[k]];
     box[k] = make_float4(d.x1, d.y1, d.x2, d.y2);
     roi[k] = d.roi;
     alive[k] = 1;
   }
   __syncthreads();
-  // Greedy: the k-th ranked detection, if still alive, removes those after it it overlaps.
-  for (int k = 0; k < n; ++k) {
-    if (alive[k]) {
-      const float4 a = box[k];
-      const int ra = roi[k];
-      for (int j = k + 1 + tid; j < n; j += kThreads)
-        if (alive[j] && (!P.cross_only || roi[j] != ra) && suppresses(a, box[j], P.thr))
-          alive[j] = 0;
+  // Greedy over the ranking, kChunk candidates per round: (1) candidates overlapped by a
+  // detection kept in an earlier round die -- lane l of every wave holds candidate l, the
+  // waves share out the kept list; (2) the chunk's own suppression bits; (3) one wave walks
+  // the chunk in rank order with row a of the bits in lane a. Equal to walking candidate
+  // by candidate.
+  const int wave = tid >> 6;
+  for (int c0 = 0; c0 < n; c0 += kChunk) {
+    const int m = min(kChunk, n - c0);
+    const int K = s_kept;
+    if (lane < m) {
+      const float4 bj = box[c0 + lane];
+      const int rj = roi[c0 + lane];
+      bool dead = false;
+#pragma unroll 4
+      for (int e = wave; e < K; e += kFrameThreads / 64)
+        dead |= (!P.cross_only || kept_roi[e] != rj) && suppresses(kept_box[e], bj, P.thr);
+      if (dead) alive[c0 + lane] = 0;  // every writer stores 0
+    }
+    if (tid < 2 * kChunk) bits[tid] = 0;
+    __syncthreads();
+    {
+      constexpr int kCols = kChunk * kChunk / kFrameThreads;  // columns per thread
+      const int a = tid / (kChunk / kCols), q = tid % (kChunk / kCols);  // row a, columns
+      uint32_t part = 0;                                                 // [kCols q, +kCols)
+      if (a < m) {
+        const float4 ba = box[c0 + a];
+        const int ra = roi[c0 + a];
+        for (int b = max(kCols * q, a + 1); b < min(kCols * q + kCols, m); ++b)
+          if ((!P.cross_only || roi[c0 + b] != ra) && suppresses(ba, box[c0 + b], P.thr))
+            part |= 1u << (b & 31);
+        if (part) atomicOr(&bits[2 * a + ((kCols * q) >> 5)], part);
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const uint32_t row_lo = lane < m ? bits[2 * lane] : 0;
+      const uint32_t row_hi = lane < m ? bits[2 * lane + 1] : 0;
+      uint64_t removed = __ballot(lane < m && !alive[c0 + lane]) | (m < 64 ? ~uint64_t(0) << m : 0);
+      for (int a = 0; a < m; ++a) {
+        if ((removed >> a) & 1) continue;
+        // readlane returns int: widen through uint32_t so bit 31 does not sign-extend
+        const uint32_t lo32 = static_cast<uint32_t>(__builtin_amdgcn_readlane(row_lo, a));
+        const uint32_t hi32 = static_cast<uint32_t>(__builtin_amdgcn_readlane(row_hi, a));
+        removed |= (static_cast<uint64_t>(hi32) << 32) | lo32;
+      }
+      const bool keep_me = lane < m && !((removed >> lane) & 1);
+      const uint64_t kb = __ballot(keep_me);
+      if (keep_me) {
+        const int slot = K + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                 static_cast<uint32_t>(kb >> 32),
+                                 __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(kb), 0u)));
+        kept_box[slot] = box[c0 + lane];
+        kept_roi[slot] = roi[c0 + lane];
+      }
+      if (lane < m) alive[c0 + lane] = keep_me ? 1 : 0;
+      if (lane == 0) s_kept = K + __popcll(kb);
     }
     __syncthreads();
   }
-  for (int k = tid; k < n; k += kThreads) P.keep[det[k]] = alive[k];
+  for (int k = tid; k < n; k += kFrameThreads) P.keep[det[k]] = alive[k];
 }
 
 __global__ __launch_bounds__(kThreads) void compact_kernel(const MergeParams P) {
@@ -325,7 +435,7 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, s, P);
   hipLaunchKernelGGL(scatter_kernel, dim3(per), dim3(kThreads), 0, s, P);
   if (a->n_frames > 0)
-    hipLaunchKernelGGL(frame_kernel, dim3(static_cast<uint32_t>(a->n_frames)), dim3(kThreads), 0,
+    hipLaunchKernelGGL(frame_kernel, dim3(static_cast<uint32_t>(a->n_frames)), dim3(kFrameThreads), 0,
                        s, P);
   hipLaunchKernelGGL(compact_kernel, dim3(static_cast<uint32_t>(compact_blocks(a->n_max))),
                      dim3(kThreads), 0, s, P);

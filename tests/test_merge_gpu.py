@@ -105,6 +105,23 @@ def test_large_frames(torch):
     np.testing.assert_array_equal(keep[2049:], want.astype(np.int32))
 
 
+def test_frames_around_the_matrix_limit(torch):
+    """Frames of 437 and 439 detections (the bit matrix fits), 448 and 513 (it does not)."""
+    rng = np.random.default_rng(12)
+    sizes = [437, 439, 448, 513]
+    dets, scores = random_dets(rng, sum(sizes), len(sizes), 8, span=400.0)
+    dets["frame"] = np.repeat(np.arange(len(sizes)), sizes)
+    check(torch, dets, scores, len(sizes), 0.4, True)
+    check(torch, dets, scores, len(sizes), 0.6, False)
+
+
+def test_many_frames(torch):
+    """More frames than the LDS histograms hold (4096): direct global counters."""
+    rng = np.random.default_rng(13)
+    dets, scores = random_dets(rng, 20000, 5000, 6, span=100.0)
+    check(torch, dets, scores, 5000, 0.5, True)
+
+
 def test_partial_count_and_empty(torch):
     rng = np.random.default_rng(4)
     dets, scores = random_dets(rng, 800, 5, 4)
