@@ -343,6 +343,8 @@ typedef struct {
   int32_t *n_out;             /* device out, one int32 */
   void *workspace;            /* device scratch, >= tg_unstitch_workspace_bytes(n_boxes) */
   size_t workspace_bytes;
+  int32_t rule;               /* 0: the patch holding the box centre (default);
+                                 1: the patch the box overlaps most, see tg_unstitch */
 } tg_unstitch_args;
 
 /* Device scratch tg_unstitch needs for n_boxes boxes (0 when n_boxes <= 0). */
@@ -361,9 +363,14 @@ size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
  * increasing b (a stable compaction), and their count to *n_out. The paper scores
  * detections per frame (Sec. V-D) without stating this mapping; the centre rule is
  * this library's reading.
+ * With rule = 1 a box instead belongs to the RoI p on c that it overlaps most: area =
+ * ow * oh with ow = max(0, min(x2, dx+w) - max(x1, dx)) and oh likewise, binary32, one
+ * rounding per operation; the largest area > 0 wins, ties go to the lower RoI id, and a
+ * box with a NaN coordinate or no overlap is dropped (Alg. 1 assigns RoIs to zones by
+ * largest overlap in the same way, Sec. III-A).
  * Returns TG_E_INVAL on null pointers (unless n_boxes == 0, which only writes
  * *n_out = 0) or n_boxes < 0, TG_E_WORKSPACE when the workspace is too small,
- * TG_E_HIP on launch failure.
+ * TG_E_HIP on launch failure, TG_E_INVAL for a rule other than 0 or 1.
  */
 int tg_unstitch(const tg_unstitch_args *args, void *stream);
 

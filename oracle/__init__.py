@@ -70,7 +70,7 @@ def _declare(L):
     L.oracle_stitch.restype = ctypes.c_int
     L.oracle_pixel_sources.argtypes = [_P, _P, _P, _P, _I32, _I64, _I32, _P, _I32, _P]
     L.oracle_pixel_sources.restype = None
-    L.oracle_unstitch.argtypes = [_P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P]
+    L.oracle_unstitch.argtypes = [_P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _I32, _P, _P, _P]
     L.oracle_unstitch.restype = ctypes.c_int
     L.oracle_threads.argtypes = []
     L.oracle_threads.restype = _I32
@@ -171,8 +171,8 @@ def pixel_sources(rois, plan: Plan, frame_stride, row_pitch, pts) -> np.ndarray:
     return src
 
 
-def unstitch(boxes, box_canvas, rois, plan: Plan, clip=1):
-    """Returns (roi_of_box int32 [n], dets DET_DTYPE [n_out])."""
+def unstitch(boxes, box_canvas, rois, plan: Plan, clip=1, rule=0):
+    """Returns (roi_of_box int32 [n], dets DET_DTYPE [n_out]); rule 0 centre, 1 overlap."""
     bx = np.ascontiguousarray(boxes, dtype=np.float32).reshape(-1, 4)
     bc = _i32(box_canvas)
     n = bx.shape[0]
@@ -181,7 +181,7 @@ def unstitch(boxes, box_canvas, rois, plan: Plan, clip=1):
     n_out = np.zeros(1, dtype=np.int32)
     lib().oracle_unstitch(_ptr(bx), _ptr(bc), n, _ptr(_i32(rois).reshape(-1, 5)),
                           _ptr(_i32(plan.place)), _ptr(_i32(plan.order)),
-                          _ptr(_i32(plan.canvas_begin)), plan.n_canvases, int(clip),
+                          _ptr(_i32(plan.canvas_begin)), plan.n_canvases, int(clip), int(rule),
                           _ptr(rob), _ptr(dets), _ptr(n_out))
     return rob, dets[: int(n_out[0])].copy()
 

@@ -42,8 +42,18 @@ def stitch(frames, rois, place, first, count, canvas_w, canvas_h, mean, std, pad
     return out
 
 
-def unstitch(boxes, box_canvas, rois, place, n_canvases, clip=True):
-    """Per-box search over every RoI; returns (roi_of_box, list of det tuples)."""
+def overlap_area(box, rect):
+    """binary32 area of box (x1, y1, x2, y2) inside rect (x0, y0, x1, y1), one rounding per
+    operation, 0 when they do not overlap."""
+    f32 = np.float32
+    w = f32(min(box[2], rect[2]) - max(box[0], rect[0]))
+    h = f32(min(box[3], rect[3]) - max(box[1], rect[1]))
+    return f32(max(w, f32(0)) * max(h, f32(0)))
+
+
+def unstitch(boxes, box_canvas, rois, place, n_canvases, clip=True, rule=0):
+    """Per-box search over every RoI; returns (roi_of_box, list of det tuples). rule 0:
+    the RoI holding the centre; rule 1: the RoI overlapped most (ties: lower id)."""
     rois = np.asarray(rois).reshape(-1, 5)
     place = np.asarray(place).reshape(-1, 3)
     boxes = np.asarray(boxes, dtype=np.float32).reshape(-1, 4)
@@ -55,13 +65,27 @@ def unstitch(boxes, box_canvas, rois, place, n_canvases, clip=True):
         if not 0 <= c < n_canvases:
             continue
         x1, y1, x2, y2 = (f32(v) for v in boxes[b])
-        with np.errstate(invalid="ignore", over="ignore"):
-            cx = f32(f32(x1 + x2) * f32(0.5))
-            cy = f32(f32(y1 + y2) * f32(0.5))
-        hits = [i for i in range(rois.shape[0])
-                if place[i, 0] == c
-                and f32(place[i, 1]) <= cx < f32(place[i, 1] + rois[i, 3])
-                and f32(place[i, 2]) <= cy < f32(place[i, 2] + rois[i, 4])]
+        if rule == 1:
+            if np.isnan([x1, y1, x2, y2]).any():
+                continue
+            best, hits = f32(0), []
+            for i in range(rois.shape[0]):
+                if place[i, 0] != c:
+                    continue
+                with np.errstate(invalid="ignore", over="ignore"):
+                    a = overlap_area((x1, y1, x2, y2),
+                                     (f32(place[i, 1]), f32(place[i, 2]),
+                                      f32(place[i, 1] + rois[i, 3]), f32(place[i, 2] + rois[i, 4])))
+                if a > best:  # ascending ids: the first maximum is the lowest id
+                    best, hits = a, [i]
+        else:
+            with np.errstate(invalid="ignore", over="ignore"):
+                cx = f32(f32(x1 + x2) * f32(0.5))
+                cy = f32(f32(y1 + y2) * f32(0.5))
+            hits = [i for i in range(rois.shape[0])
+                    if place[i, 0] == c
+                    and f32(place[i, 1]) <= cx < f32(place[i, 1] + rois[i, 3])
+                    and f32(place[i, 2]) <= cy < f32(place[i, 2] + rois[i, 4])]
         assert len(hits) <= 1
         if not hits:
             continue

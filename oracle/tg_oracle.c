@@ -457,15 +457,39 @@ void oracle_pixel_sources(const int32_t *rois, const int32_t *place, const int32
  * canvas id is out of range, or that hold a NaN are dropped (roi_of_box = -1). The
  * paper evaluates per-frame detection accuracy (Sec. V-D) without stating this
  * mapping; this is the build's reading. */
+/* Length of [lo, hi] inside [p0, p1], at least 0 (binary32, one rounding). */
+static float overlap_1d(float lo, float hi, float p0, float p1) {
+  float a = (hi < p1 ? hi : p1) - (lo > p0 ? lo : p0);
+  return a > 0.0f ? a : 0.0f;
+}
+
 int oracle_unstitch(const float *boxes, const int32_t *box_canvas, int32_t n,
                     const int32_t *rois, const int32_t *place, const int32_t *order,
-                    const int32_t *cbeg, int32_t J, int32_t clip, int32_t *roi_of_box,
-                    orc_det *dets, int32_t *n_out) {
+                    const int32_t *cbeg, int32_t J, int32_t clip, int32_t rule,
+                    int32_t *roi_of_box, orc_det *dets, int32_t *n_out) {
 #pragma omp parallel for schedule(static)
   for (int32_t b = 0; b < n; ++b) {
     roi_of_box[b] = -1;
     int32_t c = box_canvas[b];
     if (c < 0 || c >= J) continue;
+    if (rule == 1) {
+      /* the patch of the canvas that the box overlaps most (area > 0); ties to the lower
+         RoI id; a NaN coordinate matches nothing */
+      const float *bx = boxes + 4 * b;
+      if (bx[0] != bx[0] || bx[1] != bx[1] || bx[2] != bx[2] || bx[3] != bx[3]) continue;
+      float best = 0.0f;
+      for (int32_t t = cbeg[c]; t < cbeg[c + 1]; ++t) {
+        int32_t i = order[t];
+        float x0 = (float)place[3 * i + 1], y0 = (float)place[3 * i + 2];
+        float x1 = (float)(place[3 * i + 1] + R_W(i)), y1 = (float)(place[3 * i + 2] + R_H(i));
+        float area = overlap_1d(bx[0], bx[2], x0, x1) * overlap_1d(bx[1], bx[3], y0, y1);
+        if (area > best || (area == best && area > 0.0f && i < roi_of_box[b])) {
+          best = area;
+          roi_of_box[b] = i;
+        }
+      }
+      continue;
+    }
     float cx = (boxes[4 * b + 0] + boxes[4 * b + 2]) * 0.5f;
     float cy = (boxes[4 * b + 1] + boxes[4 * b + 3]) * 0.5f;
     for (int32_t t = cbeg[c]; t < cbeg[c + 1]; ++t) {

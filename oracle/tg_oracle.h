@@ -80,10 +80,11 @@ void oracle_pixel_sources(const int32_t *rois, const int32_t *place, const int32
                           const int32_t *cbeg, int32_t n_canvases, int64_t fstride,
                           int32_t pitch, const int32_t *pts, int32_t m, int64_t *src);
 
-/* Box remapping; returns ORC_OK. */
+/* Box remapping; returns ORC_OK. rule 0: the patch holding the box centre; rule 1: the
+ * patch the box overlaps most (area > 0, ties to the lower RoI id, NaN matches nothing). */
 int oracle_unstitch(const float *boxes, const int32_t *box_canvas, int32_t n,
                     const int32_t *rois, const int32_t *place, const int32_t *order,
-                    const int32_t *cbeg, int32_t n_canvases, int32_t clip,
+                    const int32_t *cbeg, int32_t n_canvases, int32_t clip, int32_t rule,
                     int32_t *roi_of_box, orc_det *dets, int32_t *n_out);
 
 /* Threads OpenMP would use for the stitch/unstitch loops. */

@@ -9,7 +9,9 @@
 // Two launches on the caller's stream:
 //  1. assign: LPB lanes per box test the box canvas's patches LPB at a time; a wave
 //     ballot picks the (unique) patch containing the centre and roi_of_box[b] is
-//     written. The same launch clears the look-back state of launch 2.
+//     written. With the overlap rule each lane scores its patch's overlap area and the
+//     lanes of the box take the largest (ties: lower RoI id) with xor shuffles. The same
+//     launch clears the look-back state of launch 2.
 //  2. emit: four consecutive boxes per thread, 1024 per workgroup. Kept boxes are
 //     ranked inside the workgroup with a wave prefix sum of per-thread counts, the
 //     workgroup's offset comes from a single-pass decoupled look-back over earlier
@@ -37,7 +39,7 @@ struct UnstitchParams {
   const tg_place *place;
   const int32_t *order;
   const int32_t *canvas_begin;
-  int32_t n_rois, n_canvases, clip;
+  int32_t n_rois, n_canvases, clip, rule;
   int32_t *roi_of_box;
   tg_det *dets;
   int32_t *n_out;
@@ -68,6 +70,49 @@ __global__ __launch_bounds__(kThreads) void assign_kernel(const UnstitchParams P
   if (c >= 0 && c < P.n_canvases) {
     k_lo = min(max(P.canvas_begin[c], 0), P.n_rois);
     k_hi = min(max(P.canvas_begin[c + 1], k_lo), P.n_rois);
+  }
+  if (P.rule == 1) {
+    // Largest overlap area (> 0), ties to the lower RoI id: each lane scores one patch per
+    // round, the segment takes the best of its lanes (xor shuffles stay in the segment),
+    // and the best of the rounds is kept.
+    if (box.x1 != box.x1 || box.y1 != box.y1 || box.x2 != box.x2 || box.y2 != box.y2)
+      k_hi = k_lo;  // a NaN coordinate matches nothing
+    float best = 0.0f;
+    int best_id = -1;
+    for (int base = k_lo; base < k_hi; base += LPB) {
+      const int k = base + sl;
+      float a = 0.0f;
+      int id = -1;
+      if (k < k_hi) {
+        id = P.order[k];
+        if (id >= 0 && id < P.n_rois) {
+          const tg_place pl = P.place[id];
+          const tg_roi r = P.rois[id];
+          if (pl.canvas == c) {
+            const float ow = fmaxf(0.0f, __fsub_rn(fminf(box.x2, float(pl.x + r.w)),
+                                                   fmaxf(box.x1, float(pl.x))));
+            const float oh = fmaxf(0.0f, __fsub_rn(fminf(box.y2, float(pl.y + r.h)),
+                                                   fmaxf(box.y1, float(pl.y))));
+            a = __fmul_rn(ow, oh);
+          }
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < LPB; o <<= 1) {
+        const float a2 = __shfl_xor(a, o);
+        const int i2 = __shfl_xor(id, o);
+        if (a2 > a || (a2 == a && a2 > 0.0f && i2 < id)) {
+          a = a2;
+          id = i2;
+        }
+      }
+      if (a > best || (a == best && a > 0.0f && id < best_id)) {
+        best = a;
+        best_id = id;
+      }
+    }
+    if (sl == 0) P.roi_of_box[b] = best > 0.0f ? best_id : -1;
+    return;
   }
   for (int base = k_lo; base < k_hi; base += LPB) {
     const int k = base + sl;
@@ -181,6 +226,7 @@ extern "C" size_t tg_unstitch_workspace_bytes(int32_t n_boxes) {
 
 extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
   if (!a || a->n_boxes < 0 || a->n_rois < 0 || a->n_canvases < 0) return TG_E_INVAL;
+  if (a->rule != 0 && a->rule != 1) return TG_E_INVAL;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (!a->n_out) return TG_E_INVAL;
   if (a->n_boxes == 0) {
@@ -206,6 +252,7 @@ extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
   P.n_rois = a->n_rois;
   P.n_canvases = a->n_canvases;
   P.clip = a->clip;
+  P.rule = a->rule;
   P.roi_of_box = a->roi_of_box;
   P.dets = a->dets;
   P.n_out = a->n_out;

@@ -50,7 +50,8 @@ class UnstitchArgs(ctypes.Structure):
     _fields_ = [("boxes", _vp), ("box_canvas", _vp), ("n_boxes", _i32), ("rois", _vp),
                 ("place", _vp), ("order", _vp), ("canvas_begin", _vp), ("n_rois", _i32),
                 ("n_canvases", _i32), ("clip", _i32), ("roi_of_box", _vp), ("dets", _vp),
-                ("n_out", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
+                ("n_out", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t),
+                ("rule", _i32)]
 
 
 class PartitionArgs(ctypes.Structure):
@@ -443,7 +444,8 @@ class UnstitchBuffers:
         return self.dets[:n].cpu().numpy().view(DET_DTYPE).reshape(-1)
 
 
-def unstitch_args(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers) -> UnstitchArgs:
+def unstitch_args(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers,
+                  rule: int = 0) -> UnstitchArgs:
     import torch
 
     dplan.check()
@@ -458,13 +460,14 @@ def unstitch_args(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuff
     a.roi_of_box, a.dets, a.n_out = (bufs.roi_of_box.data_ptr(), bufs.dets.data_ptr(),
                                      bufs.n_out.data_ptr())
     a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    a.rule = int(rule)
     return a
 
 
 def unstitch(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers,
-             stream=None) -> None:
-    """Enqueue tg_unstitch; results land in `bufs`."""
-    a = unstitch_args(boxes, box_canvas, dplan, clip, bufs)
+             stream=None, rule: int = 0) -> None:
+    """Enqueue tg_unstitch; results land in `bufs` (rule 0 centre, 1 largest overlap)."""
+    a = unstitch_args(boxes, box_canvas, dplan, clip, bufs, rule)
     rc = lib().tg_unstitch(ctypes.byref(a), _stream_handle(stream))
     if rc != OK:
         raise TgError("tg_unstitch", rc)

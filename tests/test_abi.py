@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version():
-    assert tg.lib().tg_abi_version() == 3
+    assert tg.lib().tg_abi_version() == 4
 
 
 def test_strerror():
@@ -66,6 +66,7 @@ int main(void) {
   F(tg_unstitch_args, boxes); F(tg_unstitch_args, n_boxes); F(tg_unstitch_args, rois);
   F(tg_unstitch_args, n_rois); F(tg_unstitch_args, clip); F(tg_unstitch_args, roi_of_box);
   F(tg_unstitch_args, n_out); F(tg_unstitch_args, workspace); F(tg_unstitch_args, workspace_bytes);
+  F(tg_unstitch_args, rule);
   return 0;
 }
 """)

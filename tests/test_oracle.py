@@ -394,3 +394,63 @@ def test_workload_plans_are_valid(orc, name):
     assert rc == 0
     assert orc.check_plan(rois, wl.canvas, wl.canvas, 0, plan.place, plan.order,
                           plan.canvas_begin, plan.n_canvases) == 0
+
+
+# ---------------------------------------------------------------- unstitch, overlap rule
+
+def test_unstitch_overlap_rule_example(orc):
+    """Hand-worked: RoI 0 at (0,0), RoI 1 at (10,0), RoI 2 at (0,10), all 10 x 10.
+    A [4,2,16,8] overlaps RoI 0 and RoI 1 by 6x6 = 36 each: the tie goes to RoI 0 (its
+    centre x = 10 belongs to RoI 1). B [8,0,13,5]: 2x5 = 10 against 3x5 = 15: RoI 1.
+    C [-5,-5,2,2]: 2x2 = 4 with RoI 0 (its centre is on no patch). D overlaps nothing,
+    E has a NaN. F [2,8,8,14]: 6x2 = 12 with RoI 0, 6x4 = 24 with RoI 2: RoI 2."""
+    rois = np.array([[0, 100, 50, 10, 10], [1, 200, 0, 10, 10], [0, 0, 0, 10, 10]], np.int32)
+    plan = orc.Plan(np.array([[0, 0, 0], [0, 10, 0], [0, 0, 10]], np.int32),
+                    np.array([0, 1, 2], np.int32), np.array([0, 3], np.int32), 1)
+    boxes = np.array([[4, 2, 16, 8], [8, 0, 13, 5], [-5, -5, 2, 2], [30, 30, 40, 40],
+                      [np.nan, 0, 5, 5], [2, 8, 8, 14]], np.float32)
+    canv = np.zeros(6, np.int32)
+    rob, dets = orc.unstitch(boxes, canv, rois, plan, 1, rule=1)
+    assert rob.tolist() == [0, 1, 0, -1, -1, 2]
+    # A clipped to RoI 0 ([0,10] x [0,10]) and moved by (100, 50) on frame 0
+    assert tuple(dets[0])[:3] == (0, 0, 0) and tuple(dets[0])[3:] == (104, 52, 110, 58)
+    rob_c, _ = orc.unstitch(boxes, canv, rois, plan, 1, rule=0)
+    assert rob_c.tolist() == [1, 1, -1, -1, -1, 2]
+
+
+def test_unstitch_overlap_rule_matches_brute_force(orc):
+    from oracle import brute
+
+    rng = np.random.default_rng(41)
+    for _ in range(30):
+        rois = W.random_rois(rng, int(rng.integers(1, 40)), 3, 200, 100, 1, 40, 40)
+        rc, _, plan = orc.pack(rois, 64, 48, 200, 100, 3, int(rng.integers(0, 3)))
+        n = 300
+        cx, cy = rng.uniform(-4, 68, n), rng.uniform(-4, 52, n)
+        bw, bh = rng.uniform(0, 30, n), rng.uniform(0, 30, n)
+        boxes = np.stack([cx - bw / 2, cy - bh / 2, cx + bw / 2, cy + bh / 2], 1).astype(np.float32)
+        boxes[:80] = np.round(boxes[:80])  # integer corners: exact ties between patches
+        boxes[80:85, 2] = np.nan
+        boxes[85:90, 0] = -np.inf
+        canv = rng.integers(-1, plan.n_canvases + 1, n)
+        for clip in (0, 1):
+            rob, dets = orc.unstitch(boxes, canv, rois, plan, clip, rule=1)
+            rob_b, dets_b = brute.unstitch(boxes, canv, rois, plan.place, plan.n_canvases, clip,
+                                           rule=1)
+            np.testing.assert_array_equal(rob, rob_b)
+            assert [tuple(d) for d in dets.tolist()] == [tuple(d) for d in dets_b]
+
+
+def test_unstitch_rules_agree_inside_patches(orc):
+    """A box inside one patch overlaps only that patch and has its centre there."""
+    rng = np.random.default_rng(5)
+    rois = W.random_rois(rng, 200, 4, 800, 600, 8, 120, 120)
+    rc, _, plan = orc.pack(rois, 400, 400, 800, 600, 4, 0)
+    pl = plan.place
+    f = rng.uniform(0.1, 0.45, (200, 4))
+    x0 = pl[:, 1] + f[:, 0] * rois[:, 3]
+    y0 = pl[:, 2] + f[:, 1] * rois[:, 4]
+    boxes = np.stack([x0, y0, x0 + f[:, 2] * rois[:, 3], y0 + f[:, 3] * rois[:, 4]], 1).astype(np.float32)
+    r0, _ = orc.unstitch(boxes, pl[:, 0], rois, plan, 1, rule=0)
+    r1, _ = orc.unstitch(boxes, pl[:, 0], rois, plan, 1, rule=1)
+    assert r0.tolist() == r1.tolist() == list(range(200))

@@ -20,7 +20,7 @@ def torch():
     return torch
 
 
-def run_unstitch(torch, boxes, box_canvas, rois, plan, clip, dplan=None):
+def run_unstitch(torch, boxes, box_canvas, rois, plan, clip, dplan=None, rule=0):
     dplan = dplan or tg.DevicePlan(rois, plan)
     n = boxes.shape[0]
     b_d = torch.from_numpy(np.ascontiguousarray(boxes, np.float32).reshape(n, 4)).cuda()
@@ -28,14 +28,14 @@ def run_unstitch(torch, boxes, box_canvas, rois, plan, clip, dplan=None):
     bufs = tg.UnstitchBuffers(n)
     bufs.roi_of_box.fill_(-7)
     bufs.n_out.fill_(-7)
-    tg.unstitch(b_d, c_d, dplan, clip, bufs)
+    tg.unstitch(b_d, c_d, dplan, clip, bufs, rule=rule)
     torch.cuda.synchronize()
     return bufs.roi_of_box.cpu().numpy(), bufs.dets_numpy(), int(bufs.n_out.item())
 
 
-def check(torch, boxes, box_canvas, rois, plan, clip, dplan=None):
-    rob, dets, n_out = run_unstitch(torch, boxes, box_canvas, rois, plan, clip, dplan)
-    rob_o, dets_o = oracle.unstitch(boxes, box_canvas, rois, oracle_plan(plan), clip)
+def check(torch, boxes, box_canvas, rois, plan, clip, dplan=None, rule=0):
+    rob, dets, n_out = run_unstitch(torch, boxes, box_canvas, rois, plan, clip, dplan, rule)
+    rob_o, dets_o = oracle.unstitch(boxes, box_canvas, rois, oracle_plan(plan), clip, rule)
     np.testing.assert_array_equal(rob, rob_o)
     assert n_out == len(dets_o)
     # compare bit patterns (NaN-free by construction: kept boxes have finite sums)
@@ -78,9 +78,10 @@ def test_random_plans(torch, per_canvas):
         boxes[3000:3100, 0] = np.nan
         boxes[3100:3200, 3] = np.inf
         canv = rng.integers(-2, plan.n_canvases + 2, n).astype(np.int32)
-        for clip in (0, 1):
-            say("random", per_canvas, "policy", policy, "clip", clip)
-            check(torch, boxes, canv, rois, plan, clip)
+        boxes[3200:3400] = np.round(boxes[3200:3400])  # integer corners: overlap ties
+        for clip, rule in ((0, 0), (1, 0), (1, 1), (0, 1)):
+            say("random", per_canvas, "policy", policy, "clip", clip, "rule", rule)
+            check(torch, boxes, canv, rois, plan, clip, rule=rule)
 
 
 @pytest.mark.parametrize("name", W.ORDERED)
@@ -140,3 +141,25 @@ def test_deterministic(torch):
     b = run_unstitch(torch, boxes, canv, rois, plan, 1, dplan)
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_overlap_rule_example(torch):
+    """The hand-worked overlap example of the oracle tests, through the C ABI."""
+    rois = np.array([[0, 100, 50, 10, 10], [1, 200, 0, 10, 10], [0, 0, 0, 10, 10]], np.int32)
+    plan = tg.Plan(np.array([[0, 0, 0], [0, 10, 0], [0, 0, 10]], np.int32),
+                   np.array([0, 1, 2], np.int32), np.array([0, 3], np.int32), 1)
+    boxes = np.array([[4, 2, 16, 8], [8, 0, 13, 5], [-5, -5, 2, 2], [30, 30, 40, 40],
+                      [np.nan, 0, 5, 5], [2, 8, 8, 14]], np.float32)
+    rob, dets, n_out = run_unstitch(torch, boxes, np.zeros(6, np.int32), rois, plan, 1, rule=1)
+    assert rob.tolist() == [0, 1, 0, -1, -1, 2]
+    assert tuple(dets[0])[:3] == (0, 0, 0) and tuple(dets[0])[3:] == (104, 52, 110, 58)
+
+
+@pytest.mark.parametrize("name", ["cam5_4k", "cam20_4k", "small_roi_8cam"])
+def test_workload_boxes_overlap_rule(torch, name):
+    wl = W.WORKLOADS[name]
+    rois = W.make_rois(wl)
+    plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
+    boxes, canv = W.make_boxes(wl, plan.n_canvases)
+    say("workload overlap rule", name)
+    check(torch, boxes, canv, rois, plan, 1, rule=1)
