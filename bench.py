@@ -111,7 +111,30 @@ def cpu_baseline(wl, rois, frames_np, boxes, canv, min_seconds: float):
         if el >= min_seconds:
             break
     px = reps * sample_canvases * wl.canvas * wl.canvas
-    return {"value": round(px / el / 1e6, 3), "unit": "Mpixel/s", "cores": oracle.threads(),
+    threads = oracle.threads()
+    # the same sample on one thread, for at least a quarter of the time
+    oracle.set_threads(1)
+    t1, reps1 = time.perf_counter(), 0
+    while True:
+        rc, _, oplan = oracle.pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h,
+                                   wl.n_frames, 0)
+        oracle.stitch(frames_np, rois, oplan, 0, sample_canvases, wl.canvas, wl.canvas,
+                      _W.MEAN, _W.STD, _W.PAD)
+        oracle.unstitch(boxes[sel], canv[sel], rois, oplan, 1)
+        reps1 += 1
+        el1 = time.perf_counter() - t1
+        if el1 >= min_seconds / 4:
+            break
+    oracle.set_threads(threads)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+    return {"value": round(px / el / 1e6, 3), "unit": "Mpixel/s", "cores": threads,
+            "value_1_thread": round(reps1 * sample_canvases * wl.canvas * wl.canvas / el1 / 1e6, 3),
+            "cpu_model": model, "nproc": os.cpu_count(),
             "kind": "oracle",
             "sample": f"{reps} x (plan of all {len(rois)} RoIs + stitch of canvases 0-"
                       f"{sample_canvases - 1} ({sample_canvases} x {wl.canvas}x{wl.canvas}) + "
@@ -234,6 +257,71 @@ def merge_cost(tg, W, torch, uargs, ubufs, n_frames, with_oracle: bool, launches
         merge.merge(dets, scores.cpu().numpy(), n_frames, 0.5, True)
         out["oracle_us_per_call"] = round((time.perf_counter() - t0) * 1e6, 1)
     return out
+
+
+def stream_ceiling(torch, read_bytes: int, write_bytes: int, launches: int = 40):
+    """A plain streaming kernel (libtg_probe.so) moving the stitch launch's algorithmic
+    reads and writes, writes alternating between two outputs and reads cycling through a
+    pool of five read regions, as consecutive stitch batches do: what the memory system
+    gives a kernel with no work of its own for this mix. Swept over the bytes each
+    workgroup writes; the best rate is the ceiling."""
+    import ctypes
+
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2404_09267_amd", "libtg_probe.so"))
+    L.tg_probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                  ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    r = read_bytes // 4096 * 4096
+    w = write_bytes // 4096 * 4096
+    regions = 5
+    pool = torch.empty(regions * r, dtype=torch.uint8, device="cuda").fill_(1)
+    outs = [torch.empty(w, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    stream = torch.cuda.current_stream()
+    h = ctypes.c_void_p(stream.cuda_stream)
+    out = {"kernel": "plain stream, libtg_probe.so", "read_bytes": r, "write_bytes": w}
+    out["sweep"] = {}
+    for chunk in (8192, 16384, 32768, 49152, 131072):
+        def launch(i):
+            rc = L.tg_probe_stream(ctypes.c_void_p(pool.data_ptr() + (i % regions) * r), r,
+                                   ctypes.c_void_p(outs[i & 1].data_ptr()), w, chunk, h)
+            if rc != 0:
+                raise RuntimeError(f"tg_probe_stream: {rc}")
+        for i in range(4):
+            launch(i)
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+        evs[0].record(stream)
+        for i in range(launches):
+            launch(i)
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
+        out["sweep"][f"{chunk // 1024}k"] = {"us": round(us, 2), "gbs": round((r + w) / us / 1e3, 1)}
+    del pool, outs
+    best = max(out["sweep"], key=lambda k: out["sweep"][k]["gbs"])
+    out["best_chunk"] = best
+    out["gbs"] = out["sweep"][best]["gbs"]
+    return out
+
+
+def unstitch_cost(tg, torch, uargs, n_boxes, launches: int = 50):
+    """tg_unstitch alone (assign + emit), timed with HIP events after the timed steps."""
+    stream = torch.cuda.current_stream()
+    h = tg._vp(stream.cuda_stream)
+    for _ in range(3):
+        tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs[0].record(stream)
+    for i in range(launches):
+        rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
+        if rc != tg.OK:
+            raise tg.TgError("tg_unstitch", rc)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    t = sorted(evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(launches))
+    us = sum(t) / launches
+    return {"boxes": n_boxes, "us_per_call": round(us, 2), "median_us": round(t[launches // 2], 2),
+            "mboxes_per_s": round(n_boxes / us, 1), "bound": "latency: 2 launches, about 0.5 MB"}
 
 
 _W = None
@@ -373,6 +461,7 @@ def main():
         tot_ms += e0.elapsed_time(e1)
         tot_bytes += per_batch_bytes[(f, c)]
     n_launch = len(stitch_events)
+    launch_ms = sorted(e0.elapsed_time(e1) for e0, e1, _, _ in stitch_events)
     avg_ms = tot_ms / n_launch
     avg_bytes = tot_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
@@ -387,6 +476,7 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "stitch_kernel<true, false>", "launches": n_launch,
                 "avg_launch_us": round(avg_ms * 1e3, 2),
+                "median_launch_us": round(launch_ms[n_launch // 2] * 1e3, 2),
                 "algorithmic_bytes_per_launch": int(avg_bytes)}
 
     result = {
@@ -406,6 +496,11 @@ def main():
         "stitch_gbs": round(achieved, 1),
         "stitch_pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
     }
+    write_bytes = int(np.mean([c * wl.canvas * wl.canvas * 6 for _, c in batches]))
+    ceil = stream_ceiling(torch, int(avg_bytes) - write_bytes, write_bytes)
+    ceil["stitch_frac"] = round(achieved / ceil["gbs"], 4)
+    result["ceiling"] = ceil
+    result["unstitch"] = unstitch_cost(tg, torch, uargs, n_boxes)
     result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
     result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
     result["merge"] = merge_cost(tg, W, torch, uargs, ubufs, wl.n_frames, not args.no_cpu_baseline)

@@ -1,0 +1,30 @@
+/*
+ * libtg_probe.so: measurement helper of the benchmark, not part of the stitching path.
+ *
+ * A plain streaming kernel that reads `read_bytes` and writes `write_bytes` with 16-byte
+ * nontemporal stores, so that the stitch kernel's HBM rate can be set beside what the
+ * memory system delivers to a kernel with no work of its own for the same mix of reads
+ * and writes. Each workgroup reads one chunk and writes one chunk of `chunk` bytes (the
+ * read chunk scaled by read_bytes / write_bytes); workgroups take chunks in address order.
+ */
+#ifndef TG_PROBE_H
+#define TG_PROBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* src: device, >= read_bytes; dst: device, >= write_bytes; both 16-byte aligned, sizes
+ * multiples of 16, chunk a multiple of 4096. Enqueued on `stream`. Returns 0, or -1 for
+ * bad arguments, -2 when the launch fails. */
+int tg_probe_stream(const void *src, int64_t read_bytes, void *dst, int64_t write_bytes,
+                    int32_t chunk, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TG_PROBE_H */

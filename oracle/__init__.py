@@ -74,6 +74,8 @@ def _declare(L):
     L.oracle_unstitch.restype = ctypes.c_int
     L.oracle_threads.argtypes = []
     L.oracle_threads.restype = _I32
+    L.oracle_set_threads.argtypes = [_I32]
+    L.oracle_set_threads.restype = None
 
 
 def _ptr(a: np.ndarray):
@@ -188,3 +190,7 @@ def unstitch(boxes, box_canvas, rois, plan: Plan, clip=1, rule=0):
 
 def threads() -> int:
     return int(lib().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    lib().oracle_set_threads(int(n))

@@ -531,6 +531,14 @@ int oracle_unstitch(const float *boxes, const int32_t *box_canvas, int32_t n,
   return ORC_OK;
 }
 
+void oracle_set_threads(int32_t n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 int32_t oracle_threads(void) {
 #ifdef _OPENMP
   return (int32_t)omp_get_max_threads();

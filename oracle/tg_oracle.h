@@ -89,6 +89,8 @@ int oracle_unstitch(const float *boxes, const int32_t *box_canvas, int32_t n,
 
 /* Threads OpenMP would use for the stitch/unstitch loops. */
 int32_t oracle_threads(void);
+/* Threads for later OpenMP loops (n > 0). */
+void oracle_set_threads(int32_t n);
 
 #ifdef __cplusplus
 }

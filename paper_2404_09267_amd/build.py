@@ -18,6 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtg.so")
+PROBE_LIB = os.path.join(PKG, "libtg_probe.so")  # the benchmark's streaming probe only
+PROBE_SOURCES = ["probe.hip"]
 ARCH = "gfx950"
 
 HOST_SOURCES = ["plan.cpp", "norm.cpp", "invoker.cpp"]
@@ -58,6 +60,14 @@ def build(verbose_isa: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)
+    probe_objs = []
+    for src in PROBE_SOURCES:
+        obj = os.path.join(BUILD, src + ".o")
+        _run([cc, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        probe_objs.append(obj)
+    tmp = PROBE_LIB + ".tmp"
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *probe_objs])
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 

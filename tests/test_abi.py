@@ -186,3 +186,22 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(tg, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         tg.lib()
+
+
+def test_probe_library_exports_its_header():
+    """libtg_probe.so (the benchmark's streaming probe) exports what tg_probe.h declares
+    and rejects bad arguments before any HIP call."""
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "tg_probe.h")).read(),
+                  flags=re.S)
+    names = sorted(set(re.findall(r"\b(tg_\w+)\s*\(", text)))
+    assert names == ["tg_probe_stream"]
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2404_09267_amd", "libtg_probe.so"))
+    f = L.tg_probe_stream
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_int32, ctypes.c_void_p]
+    ok = ctypes.c_void_p(4096)
+    assert f(None, 4096, ok, 4096, 4096, None) == -1          # null source
+    assert f(ok, 4096, ok, 0, 4096, None) == -1               # nothing to write
+    assert f(ok, 4100, ok, 4096, 4096, None) == -1            # size not a multiple of 16
+    assert f(ok, 4096, ok, 4096, 1000, None) == -1            # chunk not whole pages
+    assert f(ctypes.c_void_p(4104), 4096, ok, 4096, 4096, None) == -1  # misaligned
