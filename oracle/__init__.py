@@ -15,7 +15,7 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liboracle.so")
-SOURCES = [os.path.join(HERE, "tg_oracle.c")]
+SOURCES = [os.path.join(HERE, "tg_oracle.c"), os.path.join(HERE, "gmm_oracle.c")]
 
 SHELF_FFDH, SHELF_ARRIVAL, GUILLOTINE_BSSF = 0, 1, 2
 OK, E_INVAL, E_ROI_OOB, E_ROI_TOO_LARGE, E_RANGE = 0, 1, 2, 3, 4
@@ -76,6 +76,12 @@ def _declare(L):
     L.oracle_threads.restype = _I32
     L.oracle_set_threads.argtypes = [_I32]
     L.oracle_set_threads.restype = None
+    L.oracle_gmm_pixel.argtypes = [_P, _P, _P, _P]
+    L.oracle_gmm_pixel.restype = ctypes.c_int
+    L.oracle_gmm_update.argtypes = [_P, _I64, _P, _P, _P, _P]
+    L.oracle_gmm_update.restype = ctypes.c_int
+    L.oracle_mask_rois.argtypes = [_P, _I32, _I32, _I32, _I32, _P, _P, _I64, _P]
+    L.oracle_mask_rois.restype = _I64
 
 
 def _ptr(a: np.ndarray):
@@ -194,3 +200,66 @@ def threads() -> int:
 
 def set_threads(n: int) -> None:
     lib().oracle_set_threads(int(n))
+
+
+class GmmParams(ctypes.Structure):
+    """orc_gmm_params (gmm_oracle.h)."""
+    _fields_ = [("n_mix", ctypes.c_int32), ("alpha", ctypes.c_float),
+                ("var_threshold", ctypes.c_float), ("var_threshold_gen", ctypes.c_float),
+                ("var_init", ctypes.c_float), ("var_min", ctypes.c_float),
+                ("var_max", ctypes.c_float), ("background_ratio", ctypes.c_float),
+                ("complexity_reduction", ctypes.c_float)]
+
+
+def gmm_params(n_mix=5, alpha=0.002, var_threshold=16.0, var_threshold_gen=9.0, var_init=15.0,
+               var_min=4.0, var_max=75.0, background_ratio=0.9, complexity_reduction=0.05):
+    return GmmParams(n_mix, alpha, var_threshold, var_threshold_gen, var_init, var_min,
+                     var_max, background_ratio, complexity_reduction)
+
+
+def gmm_state(n_px: int, n_mix: int):
+    """A fresh model: (state float32 [n_px][n_mix][5], modes uint8 [n_px])."""
+    return (np.zeros((n_px, n_mix, 5), dtype=np.float32), np.zeros(n_px, dtype=np.uint8))
+
+
+def gmm_update(frames, state, modes, params: GmmParams) -> np.ndarray:
+    """One sample per pixel (frames uint8 [..., 3], pixel-major); updates state and modes
+    in place and returns the foreground mask (uint8, frames' shape without the channel)."""
+    fr = np.ascontiguousarray(frames, dtype=np.uint8)
+    n = fr.size // 3
+    assert state.dtype == np.float32 and state.flags.c_contiguous
+    if 1 <= params.n_mix <= 8:  # other counts are refused by the C side before any access
+        assert state.shape == (n, params.n_mix, 5)
+    assert modes.dtype == np.uint8 and modes.flags.c_contiguous and modes.size == n
+    mask = np.empty(fr.shape[:-1], dtype=np.uint8)
+    rc = lib().oracle_gmm_update(_ptr(fr), n, _ptr(state), _ptr(modes), _ptr(mask),
+                                 ctypes.byref(params))
+    if rc != 0:
+        raise ValueError("oracle_gmm_update: bad parameters")
+    return mask
+
+
+def gmm_pixel(sample, state_px, modes_px, params: GmmParams) -> int:
+    """One sample of one pixel: state_px float32 [n_mix][5], modes_px uint8 [1]."""
+    x = np.ascontiguousarray(sample, dtype=np.uint8).reshape(3)
+    return int(lib().oracle_gmm_pixel(_ptr(x), _ptr(state_px), _ptr(modes_px),
+                                      ctypes.byref(params)))
+
+
+def mask_rois(mask, min_area=1):
+    """mask uint8 [F, H, W]. Returns (rows int32 [n][5] = frame, x, y, w, h; areas int64
+    [n]; frame_begin int32 [F + 1])."""
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    F, H, W = m.shape
+    fb = np.zeros(F + 1, dtype=np.int32)
+    cap = 1024
+    while True:
+        rows = np.zeros((cap, 5), dtype=np.int32)
+        areas = np.zeros(cap, dtype=np.int64)
+        n = lib().oracle_mask_rois(_ptr(m), F, W, H, int(min_area), _ptr(rows), _ptr(areas),
+                                   cap, _ptr(fb))
+        if n < 0:
+            raise ValueError("oracle_mask_rois: bad arguments")
+        if n <= cap:
+            return rows[:n].copy(), areas[:n].copy(), fb
+        cap = int(n)
