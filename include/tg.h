@@ -417,6 +417,100 @@ size_t tg_merge_workspace_bytes(int32_t n_max, int32_t n_frames);
  */
 int tg_merge(const tg_merge_args *args, void *stream);
 
+/* ---- Background model: the RoI source (Sec. III-A, step 1; Sec. V) ---- */
+
+/* Most mixture components per pixel the kernels hold in registers. */
+#define TG_GMM_MAX_MIX 5
+
+typedef struct {
+  int32_t n_mix;              /* K, components per pixel, 1 .. TG_GMM_MAX_MIX */
+  float alpha;                /* learning rate of this frame, (0, 1] */
+  float var_threshold;        /* background test: |x - mu|^2 < var_threshold * v */
+  float var_threshold_gen;    /* ownership test: |x - mu|^2 < var_threshold_gen * v */
+  float var_init;             /* variance of a new component, in [var_min, var_max] */
+  float var_min, var_max;     /* 0 < var_min <= var_max */
+  float background_ratio;     /* weight the background components cover (1 - c_f) */
+  float complexity_reduction; /* c_T, in [0, 1) */
+} tg_gmm_params;
+
+typedef struct {
+  const uint8_t *frames;  /* device [n_frames][height][width][3] RGB, packed, 4-byte aligned;
+                             frame f is camera f's next sample */
+  int32_t n_frames, width, height;
+  float *state;           /* device, tg_gmm_state_bytes(n_px, n_mix) bytes, 16-byte aligned:
+                             5 * n_mix planes of tg_gmm_plane_stride(n_px) floats, plane
+                             5 m + {0: weight, 1..3: mean r, g, b, 4: variance} of
+                             component m (heaviest first), pixel p = (f * height + y) *
+                             width + x; only the first modes[p] components are meaningful */
+  uint8_t *modes;         /* device [n_px], 4-byte aligned: components in use; all zero is a
+                             fresh model (state contents are then ignored) */
+  uint8_t *mask;          /* device out [n_px], 4-byte aligned: 1 foreground, 0 background */
+  tg_gmm_params params;
+} tg_gmm_args;
+
+/* Floats between two state planes: n_px rounded up to a multiple of 64. */
+int64_t tg_gmm_plane_stride(int64_t n_px);
+/* Bytes of model state for n_px pixels and n_mix components (0 for bad arguments). */
+size_t tg_gmm_state_bytes(int64_t n_px, int32_t n_mix);
+
+/*
+ * One frame per camera into each camera's per-pixel background model, n_px =
+ * n_frames * width * height pixels. The paper takes its RoIs from a Gaussian-mixture
+ * background model (Sec. III-A, step 1; Sec. V runs a MOG2-style subtractor); this is
+ * the adaptive mixture whose component count is chosen online (Zivkovic, ICPR 2004),
+ * with the background set of Stauffer and Grimson. Per pixel and sample x, in binary32
+ * with every operation rounded on its own:
+ *  1. components in order: d2 = |x - mu|^2 (r, g, b summed left to right); the first
+ *     with d2 < var_threshold_gen * v owns x; x is background if a component whose
+ *     predecessors' weights sum to at most background_ratio has d2 < var_threshold * v;
+ *  2. w = (w + alpha (o - w)) - alpha c_T for every component (o = 1 for the owner); the
+ *     owner, with rho = alpha / w: mu += rho (x - mu), v += rho (d2 - v), v clamped to
+ *     [var_min, var_max];
+ *  3. components with w < 0 are removed (the rest keep their order);
+ *  4. with no owner a component (alpha, x, var_init) is appended, or replaces the last
+ *     when n_mix are in use;
+ *  5. weights are divided by their sum (list order); 6. stable sort, heaviest first.
+ * mask[p] = 1 when x is not background. Enqueued on `stream`; allocates nothing.
+ * Returns TG_E_INVAL (null pointer, non-positive sizes, misalignment, bad parameters),
+ * TG_E_HIP. n_frames == 0 does nothing.
+ */
+int tg_gmm_update(const tg_gmm_args *args, void *stream);
+
+typedef struct {
+  const uint8_t *mask;      /* device [n_frames][height][width]: nonzero = foreground */
+  int32_t n_frames, width, height;
+  int32_t min_area;         /* components of fewer pixels are dropped */
+  tg_roi *rois;             /* device out [max_rois]: bounding boxes {frame, x, y, w, h} */
+  int32_t *areas;           /* device out [max_rois] or NULL: pixel count of each RoI */
+  int32_t max_rois;
+  int32_t *frame_begin;     /* device out [n_frames + 1]: RoIs of frame f are
+                               [frame_begin[f], frame_begin[f + 1]) */
+  int32_t *n_rois;          /* device out: kept components (more than max_rois: only the
+                               first max_rois are written) */
+  int32_t *n_components;    /* device out: all components; more than max_components means
+                               the ones past the cap (raster order) were not measured */
+  int32_t max_components;
+  void *workspace;          /* device scratch, >= tg_mask_rois_workspace_bytes(...),
+                               16-byte aligned */
+  size_t workspace_bytes;
+} tg_mask_rois_args;
+
+/* Device scratch tg_mask_rois needs (0 for bad arguments). */
+size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t height,
+                                    int32_t max_components);
+
+/*
+ * RoIs from a foreground mask: the bounding boxes of each frame's 8-connected
+ * foreground components of at least min_area pixels (the paper cuts its RoIs from the
+ * background model's foreground, Sec. III-A, step 1; the connectivity, the area rule
+ * and the order are this library's reading). RoIs are listed frame by frame, each
+ * frame's in raster order of the component's first pixel, ready for tg_partition.
+ * Enqueued on `stream`; allocates nothing. Returns TG_E_INVAL (null pointer,
+ * non-positive sizes, more than 65535 frames or tile rows, width * height >= 2^31,
+ * max_components < 1, max_rois < 0), TG_E_WORKSPACE, TG_E_HIP.
+ */
+int tg_mask_rois(const tg_mask_rois_args *args, void *stream);
+
 /* Static description of a status code. */
 const char *tg_strerror(int code);
 

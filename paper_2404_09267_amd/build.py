@@ -23,12 +23,17 @@ PROBE_SOURCES = ["probe.hip"]
 ARCH = "gfx950"
 
 HOST_SOURCES = ["plan.cpp", "norm.cpp", "invoker.cpp"]
-HIP_SOURCES = ["stitch.hip", "unstitch.hip", "partition.hip", "merge.hip"]
+HIP_SOURCES = ["stitch.hip", "unstitch.hip", "partition.hip", "merge.hip", "gmm.hip", "rois.hip"]
 
 # Packed FP32 instructions are kept out of every kernel; scalar code is all we need.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wall", "-Wno-unused-command-line-argument"]
+# Sources whose binary32 results decide integers (foreground flags, suppression, box
+# assignment): every operation rounded on its own, no multiply-add fusion. The rounded
+# intrinsics (__fmul_rn and the like) are plain operators in the clang headers, so only
+# the command-line switch reaches them.
+EXACT_FP32 = {"unstitch.hip", "merge.hip", "gmm.hip"}
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-I", INCLUDE, "-Wall", "-Wextra"]
 
 
@@ -55,6 +60,8 @@ def build(verbose_isa: bool = False) -> str:
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         extra = ["-save-temps=obj"] if verbose_isa else []
+        if src in EXACT_FP32:
+            extra.append("-ffp-contract=off")
         _run([cc, *HIP_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     tmp = LIB + ".tmp"

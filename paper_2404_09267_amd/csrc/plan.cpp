@@ -229,4 +229,4 @@ extern "C" int tg_stitch_schedule(const tg_roi *rois, const tg_place *place,
   }
 }
 
-extern "C" int32_t tg_abi_version(void) { return 4; }
+extern "C" int32_t tg_abi_version(void) { return 5; }

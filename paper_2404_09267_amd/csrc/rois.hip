@@ -1,0 +1,511 @@
+// tg_mask_rois: RoIs from a foreground mask, as the bounding boxes of 8-connected
+// components (the paper cuts its RoIs from the background model's foreground,
+// Sec. III-A, step 1).
+//
+// Connected components by union-find with atomic-min linking (a root always points to
+// the smallest index of its set, so every set ends rooted at its first pixel in raster
+// order), in seven launches on the caller's stream:
+//  1. clear:  zeroes the tickets and look-back words of launches 4 and 6.
+//  2. local:  one 256-thread workgroup per 32x32 tile labels the tile in LDS and writes,
+//             for each foreground pixel, the frame index of its tile-local root.
+//  3. merge:  one wave per tile joins its top-row and left-column pixels with their
+//             foreground neighbours in the tiles above and to the left (global atomics
+//             on the label array). Every 8-neighbour pair across a tile border is seen
+//             from the tile below or to the right of it.
+//  4. roots:  8192-pixel raster spans in ticket order find the pixels still labelled
+//             with their own index (the components), number them in raster order with a
+//             decoupled look-back, initialise each component's record and mark the root
+//             with its number.
+//  5. boxes:  per tile again, the tile's local components (relabelled in LDS) fold their
+//             pixels' extent and count in LDS; each local component then follows the
+//             label chain to its component number and folds its totals into the record
+//             with global atomics: one set of atomics per (tile, component).
+//  6. filter: components of at least min_area pixels, compacted in number order with a
+//             look-back, written as tg_roi rows.
+//  7. begin:  frame_begin by binary search over the kept rows' frames.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdint>
+
+#include "lookback.h"
+#include "tg.h"
+
+namespace {
+
+constexpr int kTile = 32;
+constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
+constexpr int kSpan = 8192;        // pixels per workgroup of the roots pass
+constexpr int kSpanThreads = 256;  // 32 pixels per thread
+constexpr int kSpanPix = kSpan / kSpanThreads;
+constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
+constexpr int kFilterThreads = 256;
+
+struct Comp {
+  int32_t frame, root, x0, y0, x1, y1, area, unused;
+};
+static_assert(sizeof(Comp) == 32, "component record is 32 bytes");
+
+struct Layout {
+  uint64_t *words;  // [0]: roots ticket, [1]: filter ticket, then the look-back words
+  uint64_t *root_state, *filter_state;
+  Comp *comp;
+  int32_t *kept_frame;
+  int32_t *label;
+  int64_t n_words;
+  size_t bytes;
+};
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+Layout layout(void *base, int64_t n_px, int32_t max_components) {
+  Layout L;
+  const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
+  const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
+  L.n_words = 2 + n_spans + n_filter;
+  const size_t o_comp = round_up(8 * static_cast<size_t>(L.n_words), 256);
+  const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
+  const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
+  L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
+  char *b = static_cast<char *>(base);
+  L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
+  L.root_state = b ? L.words + 2 : nullptr;
+  L.filter_state = b ? L.root_state + n_spans : nullptr;
+  L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
+  L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
+  L.label = b ? reinterpret_cast<int32_t *>(b + o_label) : nullptr;
+  return L;
+}
+
+// ---- union-find ---------------------------------------------------------------------
+
+__device__ __forceinline__ int lds_load(int *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ int lds_find(int *L, int i) {
+  for (int p = lds_load(&L[i]); p != i; p = lds_load(&L[i])) i = p;
+  return i;
+}
+// Joins the sets of a and b: the larger root is linked under the smaller with an atomic
+// min; if that root was relinked meanwhile, retry from what it now points to.
+__device__ __forceinline__ void lds_unite(int *L, int a, int b) {
+  for (;;) {
+    a = lds_find(L, a);
+    b = lds_find(L, b);
+    if (a == b) return;
+    if (a > b) {
+      const int t = a;
+      a = b;
+      b = t;
+    }
+    const int old = atomicMin(&L[b], a);
+    if (old == b) return;
+    b = old;
+  }
+}
+
+__device__ __forceinline__ int g_load(const int32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int g_find(int32_t *L, int i) {
+  for (int p = g_load(&L[i]); p != i; p = g_load(&L[i])) i = p;
+  return i;
+}
+__device__ __forceinline__ void g_unite(int32_t *L, int a, int b) {
+  for (;;) {
+    a = g_find(L, a);
+    b = g_find(L, b);
+    if (a == b) return;
+    if (a > b) {
+      const int t = a;
+      a = b;
+      b = t;
+    }
+    const int old =
+        __hip_atomic_fetch_min(&L[b], a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == b) return;
+    b = old;
+  }
+}
+
+// Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
+// within the tile). Thread t holds row t / 8, columns 4 (t % 8) .. + 3; fg[k] says which
+// of them are foreground. Returns false, uniformly, when the tile has no foreground.
+__device__ __forceinline__ bool label_tile(const uint8_t *mf, int W, int H, int tx0, int ty0,
+                                           int *L, bool fg[4]) {
+  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
+  bool any = false;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int x = tx0 + c0 + k;
+    fg[k] = y < H && x < W && mf[static_cast<int64_t>(y) * W + x] != 0;
+    L[r * kTile + c0 + k] = fg[k] ? r * kTile + c0 + k : -1;
+    any |= fg[k];
+  }
+  if (!__syncthreads_or(any)) return false;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (!fg[k]) continue;
+    const int c = c0 + k, i = r * kTile + c;
+    if (c > 0 && lds_load(&L[i - 1]) >= 0) lds_unite(L, i, i - 1);
+    if (r > 0) {
+      if (c > 0 && lds_load(&L[i - kTile - 1]) >= 0) lds_unite(L, i, i - kTile - 1);
+      if (lds_load(&L[i - kTile]) >= 0) lds_unite(L, i, i - kTile);
+      if (c + 1 < kTile && lds_load(&L[i - kTile + 1]) >= 0) lds_unite(L, i, i - kTile + 1);
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
+// ---- kernels ------------------------------------------------------------------------
+
+__global__ void clear_kernel(uint64_t *words, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) words[i] = 0;
+}
+
+__global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask, int W, int H,
+                                                             int64_t frame_px,
+                                                             int32_t *label) {
+  __shared__ int L[kTile * kTile];
+  const int64_t f = blockIdx.z;
+  const int tx0 = blockIdx.x * kTile, ty0 = blockIdx.y * kTile;
+  bool fg[4];
+  if (!label_tile(mask + f * frame_px, W, H, tx0, ty0, L, fg)) return;
+  int32_t *lf = label + f * frame_px;
+  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (!fg[k]) continue;
+    const int root = lds_find(L, r * kTile + c0 + k);
+    lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] =
+        (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
+  }
+}
+
+__global__ __launch_bounds__(64) void merge_kernel(const uint8_t *mask, int W, int H,
+                                                   int64_t frame_px, int32_t *label) {
+  const int64_t f = blockIdx.z;
+  const int tx0 = blockIdx.x * kTile, ty0 = blockIdx.y * kTile, lane = threadIdx.x;
+  const uint8_t *mf = mask + f * frame_px;
+  int32_t *lf = label + f * frame_px;
+  if (lane < kTile) {  // top row against the row above
+    const int x = tx0 + lane, y = ty0;
+    if (y > 0 && x < W && mf[y * W + x]) {
+      for (int dx = -1; dx <= 1; ++dx) {
+        const int nx = x + dx;
+        if (nx >= 0 && nx < W && mf[(y - 1) * W + nx]) g_unite(lf, y * W + x, (y - 1) * W + nx);
+      }
+    }
+  } else {  // left column against the column to the left
+    const int x = tx0, y = ty0 + lane - kTile;
+    if (x > 0 && y < H && mf[y * W + x]) {
+      for (int dy = -1; dy <= 1; ++dy) {
+        const int ny = y + dy;
+        if (ny >= 0 && ny < H && mf[ny * W + x - 1]) g_unite(lf, y * W + x, ny * W + x - 1);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kSpanThreads) void roots_kernel(
+    const uint8_t *mask, int64_t n_px, int64_t frame_px, int64_t n_spans, int32_t *label,
+    Comp *comp, int32_t max_components, uint64_t *words, uint64_t *state,
+    int32_t *n_components) {
+  __shared__ int s_span, s_base;
+  __shared__ int s_wave[kSpanThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0)
+    s_span = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words), 1u,
+                                                     __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT));
+  __syncthreads();
+  const int64_t span = s_span;
+  const int64_t p0 = span * kSpan + static_cast<int64_t>(tid) * kSpanPix;
+
+  // Which of this thread's 32 pixels are roots.
+  uint32_t roots = 0;
+  int64_t f0 = p0 / frame_px;
+  if (p0 < n_px) {
+    int64_t local = p0 - f0 * frame_px;
+#pragma unroll 4
+    for (int j = 0; j < kSpanPix; ++j) {
+      const int64_t P = p0 + j;
+      if (P >= n_px) break;
+      if (local == frame_px) local = 0;
+      if (mask[P] && label[P] == static_cast<int32_t>(local)) roots |= 1u << j;
+      ++local;
+    }
+  }
+
+  // Exclusive scan of the counts over the workgroup, then the look-back over spans.
+  const int cnt = __popc(roots);
+  int incl = cnt;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o);
+    if (lane >= o) incl += v;
+  }
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kSpanThreads / 64; ++w) {
+    if (w < wave) before += s_wave[w];
+    total += s_wave[w];
+  }
+  if (wave == 0) {
+    const int prefix = tg_detail::lookback_prefix(state, static_cast<int>(span), total);
+    if (lane == 0) {
+      s_base = prefix;
+      if (span == n_spans - 1) *n_components = prefix + total;
+    }
+  }
+  __syncthreads();
+
+  int id = s_base + before + incl - cnt;
+  if (roots) {
+    int64_t local = p0 - f0 * frame_px, f = f0;
+    for (int j = 0; j < kSpanPix; ++j) {
+      if (local == frame_px) {
+        local = 0;
+        ++f;
+      }
+      if (roots >> j & 1u) {
+        if (id < max_components) {
+          comp[id] = Comp{static_cast<int32_t>(f), static_cast<int32_t>(local), INT_MAX, INT_MAX,
+                          INT_MIN, INT_MIN, 0, 0};
+          label[p0 + j] = -(id + 1);
+        }
+        ++id;
+      }
+      ++local;
+    }
+  }
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_max(int v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_sum(int v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask, int W, int H,
+                                                             int64_t frame_px,
+                                                             const int32_t *label,
+                                                             Comp *comp) {
+  __shared__ int L[kTile * kTile];
+  __shared__ int bx0[kTile * kTile], by0[kTile * kTile], bx1[kTile * kTile],
+      by1[kTile * kTile], bn[kTile * kTile];
+  const int64_t f = blockIdx.z;
+  const int tx0 = blockIdx.x * kTile, ty0 = blockIdx.y * kTile;
+  bool fg[4];
+  if (!label_tile(mask + f * frame_px, W, H, tx0, ty0, L, fg)) return;
+  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
+  int root[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = r * kTile + c0 + k;
+    root[k] = fg[k] ? lds_find(L, i) : -1;
+    if (root[k] == i) {
+      bx0[i] = INT_MAX;
+      by0[i] = INT_MAX;
+      bx1[i] = INT_MIN;
+      by1[i] = INT_MIN;
+      bn[i] = 0;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int x = tx0 + c0 + k;
+    // When every foreground lane of the wave is in one local component, reduce across
+    // the wave first and fold once.
+    const uint64_t fgm = __ballot(fg[k]);
+    if (!fgm) continue;
+    const int lead = __shfl(root[k], __builtin_ctzll(fgm));
+    if (__ballot(fg[k] && root[k] != lead) == 0) {
+      const int mx0 = wave_min(fg[k] ? x : INT_MAX), my0 = wave_min(fg[k] ? y : INT_MAX);
+      const int mx1 = wave_max(fg[k] ? x : INT_MIN), my1 = wave_max(fg[k] ? y : INT_MIN);
+      const int n = wave_sum(fg[k] ? 1 : 0);
+      if ((threadIdx.x & 63) == 0) {
+        atomicMin(&bx0[lead], mx0);
+        atomicMin(&by0[lead], my0);
+        atomicMax(&bx1[lead], mx1);
+        atomicMax(&by1[lead], my1);
+        atomicAdd(&bn[lead], n);
+      }
+    } else if (fg[k]) {
+      atomicMin(&bx0[root[k]], x);
+      atomicMin(&by0[root[k]], y);
+      atomicMax(&bx1[root[k]], x);
+      atomicMax(&by1[root[k]], y);
+      atomicAdd(&bn[root[k]], 1);
+    }
+  }
+  __syncthreads();
+  const int32_t *lf = label + f * frame_px;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = r * kTile + c0 + k;
+    if (root[k] != i) continue;
+    int cur = y * W + tx0 + c0 + k;
+    int v = lf[cur];
+    while (v >= 0 && v != cur) {
+      cur = v;
+      v = lf[cur];
+    }
+    if (v >= 0) continue;  // a component past max_components: not measured
+    Comp *c = comp + (-v - 1);
+    atomicMin(&c->x0, bx0[i]);
+    atomicMin(&c->y0, by0[i]);
+    atomicMax(&c->x1, bx1[i]);
+    atomicMax(&c->y1, by1[i]);
+    atomicAdd(&c->area, bn[i]);
+  }
+}
+
+__global__ __launch_bounds__(kFilterThreads) void filter_kernel(
+    const Comp *comp, const int32_t *n_components, int32_t max_components, int32_t min_area,
+    tg_roi *rois, int32_t *areas, int32_t max_rois, int32_t *kept_frame, uint64_t *words,
+    uint64_t *state, int32_t *n_rois) {
+  __shared__ int s_blk, s_base;
+  __shared__ int s_wave[kFilterThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0)
+    s_blk = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words + 1), 1u,
+                                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  __syncthreads();
+  const int blk = s_blk;
+  const int n = min(*n_components, max_components);
+  const int start = blk * kFilterBlock;
+  if (start >= n && !(n == 0 && blk == 0)) return;  // uniform: later tickets lie further on
+
+  constexpr int kPer = kFilterBlock / kFilterThreads;
+  bool keep[kPer];
+  int cnt = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int id = start + tid * kPer + k;
+    keep[k] = id < n && comp[id].area >= min_area;
+    cnt += keep[k];
+  }
+  int incl = cnt;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o);
+    if (lane >= o) incl += v;
+  }
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kFilterThreads / 64; ++w) {
+    if (w < wave) before += s_wave[w];
+    total += s_wave[w];
+  }
+  if (wave == 0) {
+    const int prefix = tg_detail::lookback_prefix(state, blk, total);
+    if (lane == 0) {
+      s_base = prefix;
+      if ((start < n && n <= start + kFilterBlock) || n == 0) *n_rois = prefix + total;
+    }
+  }
+  __syncthreads();
+  int k_out = s_base + before + incl - cnt;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    if (!keep[k]) continue;
+    const Comp c = comp[start + tid * kPer + k];
+    kept_frame[k_out] = c.frame;
+    if (k_out < max_rois) {
+      rois[k_out] = tg_roi{c.frame, c.x0, c.y0, c.x1 - c.x0 + 1, c.y1 - c.y0 + 1};
+      if (areas) areas[k_out] = c.area;
+    }
+    ++k_out;
+  }
+}
+
+__global__ void begin_kernel(const int32_t *kept_frame, const int32_t *n_rois, int32_t n_frames,
+                             int32_t *frame_begin) {
+  const int f = blockIdx.x * blockDim.x + threadIdx.x;
+  if (f > n_frames) return;
+  int lo = 0, hi = *n_rois;  // first kept row whose frame is >= f
+  while (lo < hi) {
+    const int mid = lo + (hi - lo) / 2;
+    if (kept_frame[mid] < f)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  frame_begin[f] = lo;
+}
+
+__global__ void empty_kernel(int32_t *n_rois, int32_t *n_components, int32_t *frame_begin) {
+  *n_rois = 0;
+  *n_components = 0;
+  frame_begin[0] = 0;
+}
+
+bool sizes_ok(int32_t n_frames, int32_t width, int32_t height, int32_t max_components) {
+  if (n_frames < 0 || n_frames > 65535 || width < 1 || height < 1 || max_components < 1)
+    return false;
+  if (int64_t(width) * height >= (int64_t(1) << 31)) return false;
+  if ((int64_t(height) + kTile - 1) / kTile > 65535) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t height,
+                                               int32_t max_components) {
+  if (!sizes_ok(n_frames, width, height, max_components)) return 0;
+  return layout(nullptr, int64_t(n_frames) * width * height, max_components).bytes;
+}
+
+extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
+  if (!a || !sizes_ok(a->n_frames, a->width, a->height, a->max_components) || a->max_rois < 0 ||
+      !a->frame_begin || !a->n_rois || !a->n_components)
+    return TG_E_INVAL;
+  if (a->n_frames > 0 && !a->mask) return TG_E_INVAL;
+  if (a->max_rois > 0 && !a->rois) return TG_E_INVAL;
+  const int64_t frame_px = int64_t(a->width) * a->height, n_px = a->n_frames * frame_px;
+  const Layout L = layout(a->workspace, n_px, a->max_components);
+  if (!a->workspace || a->workspace_bytes < L.bytes ||
+      reinterpret_cast<uintptr_t>(a->workspace) % 16 != 0)
+    return TG_E_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int W = a->width, H = a->height;
+  const dim3 tiles((W + kTile - 1) / kTile, (H + kTile - 1) / kTile,
+                   static_cast<uint32_t>(a->n_frames));
+  const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
+  const int64_t n_filter = (a->max_components + kFilterBlock - 1) / kFilterBlock;
+
+  if (n_px == 0) {  // no frames: no components, no rows
+    hipLaunchKernelGGL(empty_kernel, dim3(1), dim3(1), 0, s, a->n_rois, a->n_components,
+                       a->frame_begin);
+    return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
+  }
+  hipLaunchKernelGGL(clear_kernel, dim3(static_cast<uint32_t>((L.n_words + 255) / 256)),
+                     dim3(256), 0, s, L.words, L.n_words);
+  hipLaunchKernelGGL(local_kernel, tiles, dim3(kTileThreads), 0, s, a->mask, W, H, frame_px,
+                     L.label);
+  hipLaunchKernelGGL(merge_kernel, tiles, dim3(64), 0, s, a->mask, W, H, frame_px, L.label);
+  hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_spans)), dim3(kSpanThreads), 0,
+                     s, a->mask, n_px, frame_px, n_spans, L.label, L.comp, a->max_components,
+                     L.words, L.root_state, a->n_components);
+  hipLaunchKernelGGL(boxes_kernel, tiles, dim3(kTileThreads), 0, s, a->mask, W, H, frame_px,
+                     L.label, L.comp);
+  hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
+                     0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,
+                     a->areas, a->max_rois, L.kept_frame, L.words, L.filter_state, a->n_rois);
+  hipLaunchKernelGGL(begin_kernel, dim3(static_cast<uint32_t>((a->n_frames + 1 + 255) / 256)),
+                     dim3(256), 0, s, L.kept_frame, a->n_rois, a->n_frames, a->frame_begin);
+  return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
+}

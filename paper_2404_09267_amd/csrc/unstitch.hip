@@ -25,6 +25,10 @@
 #include "lookback.h"
 #include "tg.h"
 
+// Built with -ffp-contract=off: every binary32 operation here is rounded on its own (no
+// multiply-add fusion), so decisions taken in floating point match any plain IEEE
+// implementation of the same steps.
+
 namespace {
 
 constexpr int kThreads = 256;

@@ -73,7 +73,29 @@ class SloParams(ctypes.Structure):
                 ("n_lat", _i32), ("lat_mean", _vp), ("lat_std", _vp)]
 
 
-EXPORTS = ["tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
+class GmmParams(ctypes.Structure):
+    _fields_ = [("n_mix", _i32), ("alpha", _f32), ("var_threshold", _f32),
+                ("var_threshold_gen", _f32), ("var_init", _f32), ("var_min", _f32),
+                ("var_max", _f32), ("background_ratio", _f32), ("complexity_reduction", _f32)]
+
+
+class GmmArgs(ctypes.Structure):
+    _fields_ = [("frames", _vp), ("n_frames", _i32), ("width", _i32), ("height", _i32),
+                ("state", _vp), ("modes", _vp), ("mask", _vp), ("params", GmmParams)]
+
+
+class MaskRoisArgs(ctypes.Structure):
+    _fields_ = [("mask", _vp), ("n_frames", _i32), ("width", _i32), ("height", _i32),
+                ("min_area", _i32), ("rois", _vp), ("areas", _vp), ("max_rois", _i32),
+                ("frame_begin", _vp), ("n_rois", _vp), ("n_components", _vp),
+                ("max_components", _i32), ("workspace", _vp),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
+GMM_MAX_MIX = 5
+
+EXPORTS = ["tg_gmm_plane_stride", "tg_gmm_state_bytes", "tg_gmm_update",
+           "tg_mask_rois_workspace_bytes", "tg_mask_rois", "tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
            "tg_batch_range", "tg_slo_replay", "tg_stitch",
            "tg_stitch_units", "tg_stitch_schedule", "tg_stitch_norm_uses_table",
            "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_merge_workspace_bytes", "tg_merge",
@@ -129,6 +151,16 @@ def lib() -> ctypes.CDLL:
         L.tg_merge_workspace_bytes.restype = ctypes.c_size_t
         L.tg_merge.argtypes = [ctypes.POINTER(MergeArgs), _vp]
         L.tg_merge.restype = ctypes.c_int
+        L.tg_gmm_plane_stride.argtypes = [ctypes.c_int64]
+        L.tg_gmm_plane_stride.restype = ctypes.c_int64
+        L.tg_gmm_state_bytes.argtypes = [ctypes.c_int64, _i32]
+        L.tg_gmm_state_bytes.restype = ctypes.c_size_t
+        L.tg_gmm_update.argtypes = [ctypes.POINTER(GmmArgs), _vp]
+        L.tg_gmm_update.restype = ctypes.c_int
+        L.tg_mask_rois_workspace_bytes.argtypes = [_i32, _i32, _i32, _i32]
+        L.tg_mask_rois_workspace_bytes.restype = ctypes.c_size_t
+        L.tg_mask_rois.argtypes = [ctypes.POINTER(MaskRoisArgs), _vp]
+        L.tg_mask_rois.restype = ctypes.c_int
         L.tg_strerror.argtypes = [ctypes.c_int]
         L.tg_strerror.restype = ctypes.c_char_p
         L.tg_abi_version.argtypes = []
@@ -523,3 +555,112 @@ def merge(dets, n_dets, scores, n_frames, iou_threshold, cross_only, bufs: Merge
     rc = lib().tg_merge(ctypes.byref(a), _stream_handle(stream))
     if rc != OK:
         raise TgError("tg_merge", rc)
+
+
+# ---- background model and mask -> RoIs --------------------------------------------
+
+def gmm_params(n_mix=5, alpha=0.002, var_threshold=16.0, var_threshold_gen=9.0, var_init=15.0,
+               var_min=4.0, var_max=75.0, background_ratio=0.9,
+               complexity_reduction=0.05) -> GmmParams:
+    return GmmParams(n_mix, alpha, var_threshold, var_threshold_gen, var_init, var_min, var_max,
+                     background_ratio, complexity_reduction)
+
+
+class GmmModel:
+    """Device state of the per-pixel background model of n_frames cameras (tg_gmm_update):
+    5 n_mix planes of `stride` floats, the component counts and the last mask."""
+
+    def __init__(self, n_frames: int, width: int, height: int, n_mix: int, device="cuda"):
+        import torch
+
+        self.n_frames, self.width, self.height, self.n_mix = n_frames, width, height, n_mix
+        self.n_px = n_frames * width * height
+        self.stride = int(lib().tg_gmm_plane_stride(self.n_px))
+        nbytes = int(lib().tg_gmm_state_bytes(self.n_px, n_mix))
+        if nbytes == 0:
+            raise ValueError("bad model size")
+        self.state = torch.zeros(nbytes // 4, dtype=torch.float32, device=device)
+        self.modes = torch.zeros(max(self.n_px, 4), dtype=torch.uint8, device=device)
+        self.mask = torch.zeros(max(self.n_px, 4), dtype=torch.uint8, device=device)
+
+    def planes(self):
+        """State as [n_mix, 5, n_px] (a view): weight, mean r, g, b, variance."""
+        return self.state.view(self.n_mix, 5, self.stride)[:, :, : self.n_px]
+
+    def reset(self):
+        self.modes.zero_()
+
+
+def gmm_args(frames, model: GmmModel, params: GmmParams) -> GmmArgs:
+    import torch
+
+    _check(frames, torch.uint8, (model.n_frames, model.height, model.width, 3), "frames")
+    if params.n_mix != model.n_mix:
+        raise ValueError("params.n_mix differs from the model's")
+    a = GmmArgs()
+    a.frames = frames.data_ptr()
+    a.n_frames, a.width, a.height = model.n_frames, model.width, model.height
+    a.state, a.modes, a.mask = model.state.data_ptr(), model.modes.data_ptr(), model.mask.data_ptr()
+    a.params = params
+    return a
+
+
+def gmm_update(frames, model: GmmModel, params: GmmParams, stream=None) -> None:
+    """Enqueue tg_gmm_update: one frame per camera; the mask lands in model.mask."""
+    a = gmm_args(frames, model, params)
+    rc = lib().tg_gmm_update(ctypes.byref(a), _stream_handle(stream))
+    if rc != OK:
+        raise TgError("tg_gmm_update", rc)
+
+
+class MaskRoisBuffers:
+    """Caller-owned device outputs and scratch for tg_mask_rois."""
+
+    def __init__(self, n_frames: int, width: int, height: int, max_rois: int,
+                 max_components: int, device="cuda"):
+        import torch
+
+        self.n_frames, self.width, self.height = n_frames, width, height
+        self.max_rois, self.max_components = max_rois, max_components
+        self.rois = torch.empty((max(max_rois, 1), 5), dtype=torch.int32, device=device)
+        self.areas = torch.empty(max(max_rois, 1), dtype=torch.int32, device=device)
+        self.frame_begin = torch.empty(n_frames + 1, dtype=torch.int32, device=device)
+        self.counts = torch.empty(2, dtype=torch.int32, device=device)  # n_rois, n_components
+        ws = int(lib().tg_mask_rois_workspace_bytes(n_frames, width, height, max_components))
+        if ws == 0:
+            raise ValueError("bad mask size or max_components")
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
+        self.workspace_bytes = ws
+
+    def result(self):
+        """(rois int32 [n][5], areas int32 [n], frame_begin, n_rois, n_components)."""
+        n_rois, n_comp = (int(v) for v in self.counts.cpu().tolist())
+        n = min(n_rois, self.max_rois)
+        return (self.rois[:n].cpu().numpy(), self.areas[:n].cpu().numpy(),
+                self.frame_begin.cpu().numpy(), n_rois, n_comp)
+
+
+def mask_rois_args(mask, bufs: MaskRoisBuffers, min_area: int) -> MaskRoisArgs:
+    import torch
+
+    _check(mask, torch.uint8, None, "mask")
+    if mask.numel() < bufs.n_frames * bufs.width * bufs.height:
+        raise ValueError("mask smaller than n_frames * height * width")
+    a = MaskRoisArgs()
+    a.mask = mask.data_ptr()
+    a.n_frames, a.width, a.height, a.min_area = bufs.n_frames, bufs.width, bufs.height, min_area
+    a.rois, a.areas, a.max_rois = bufs.rois.data_ptr(), bufs.areas.data_ptr(), bufs.max_rois
+    a.frame_begin = bufs.frame_begin.data_ptr()
+    a.n_rois = bufs.counts.data_ptr()
+    a.n_components = bufs.counts.data_ptr() + 4
+    a.max_components = bufs.max_components
+    a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    return a
+
+
+def mask_rois(mask, bufs: MaskRoisBuffers, min_area: int = 1, stream=None) -> None:
+    """Enqueue tg_mask_rois; RoIs land in `bufs`."""
+    a = mask_rois_args(mask, bufs, min_area)
+    rc = lib().tg_mask_rois(ctypes.byref(a), _stream_handle(stream))
+    if rc != OK:
+        raise TgError("tg_mask_rois", rc)

@@ -196,3 +196,66 @@ def make_gmm_boxes(n_frames: int, per_frame: int, frame_w: int, frame_h: int, se
     y = np.clip(np.rint(y - h / 2), 0, frame_h - h).astype(np.int64)
     boxes = np.stack([frame, x, y, w, h], 1).astype(np.int32)
     return boxes, frame_begin
+
+
+class SyntheticVideo:
+    """Seeded stand-in for the paper's fixed high-resolution cameras (PANDA4K video is not
+    available), the input of the background model. Per camera: a static background of
+    16 x 16-pixel cells of random RGB levels in [40, 200), integer sensor noise in [-noise, noise]
+    (random bytes spread evenly over the range) redrawn every frame (slices of one seeded bank), and `objects` solid
+    RGB rectangles with log-uniform sides in [lo, hi] moving at constant velocity (each
+    axis uniform in [-max_speed, max_speed] px per frame) and bouncing off the frame edges.
+    frame(t) returns uint8 [cameras, height, width, 3]."""
+
+    def __init__(self, cameras: int, width: int, height: int, objects: int = 40, lo: int = 16,
+                 hi: int = 256, max_speed: float = 8.0, noise: int = 3, seed: int = 0):
+        rng = np.random.default_rng(seed)
+        self.cameras, self.width, self.height, self.noise = cameras, width, height, noise
+        cell = 16
+        gh, gw = -(-height // cell), -(-width // cell)
+        coarse = rng.integers(40, 200, (cameras, gh, gw, 3), dtype=np.uint8)
+        # stored lowered by `noise`, so that adding a bank value in [0, 2 noise] stays in uint8
+        bg = np.repeat(np.repeat(coarse - np.uint8(noise), cell, axis=1), cell, axis=2)
+        self.bg = np.ascontiguousarray(bg[:, :height, :width])
+        self.n = cameras * height * width * 3
+        self.bank_slack = 1 << 20
+        # random bytes mapped onto [0, 2 noise] by (b * (2 noise + 1)) >> 8
+        lut = ((np.arange(256) * (2 * noise + 1)) >> 8).astype(np.uint8)
+        self.bank = lut[np.frombuffer(rng.bytes(self.n + self.bank_slack), dtype=np.uint8)]
+        k = cameras * objects
+        self.obj_cam = np.repeat(np.arange(cameras), objects)
+        self.obj_w = np.clip(np.rint(np.exp(rng.uniform(np.log(lo), np.log(hi), k))), 1, width).astype(np.int64)
+        self.obj_h = np.clip(np.rint(np.exp(rng.uniform(np.log(lo), np.log(hi), k))), 1, height).astype(np.int64)
+        self.obj_x = rng.uniform(0, 1, k) * (width - self.obj_w)
+        self.obj_y = rng.uniform(0, 1, k) * (height - self.obj_h)
+        self.obj_vx = rng.uniform(-max_speed, max_speed, k)
+        self.obj_vy = rng.uniform(-max_speed, max_speed, k)
+        self.obj_rgb = rng.integers(0, 256, (k, 3), dtype=np.uint8)
+
+    @staticmethod
+    def _bounce(p0, v, t, span):
+        if span <= 0:
+            return 0
+        m = (p0 + v * t) % (2 * span)
+        return int(m if m <= span else 2 * span - m)
+
+    def frame(self, t: int) -> np.ndarray:
+        off = (t * 1_000_003) % self.bank_slack
+        f = self.bg + self.bank[off: off + self.n].reshape(self.bg.shape)
+        for i in range(len(self.obj_cam)):
+            w, h = int(self.obj_w[i]), int(self.obj_h[i])
+            x = self._bounce(self.obj_x[i], self.obj_vx[i], t, self.width - w)
+            y = self._bounce(self.obj_y[i], self.obj_vy[i], t, self.height - h)
+            f[self.obj_cam[i], y: y + h, x: x + w] = self.obj_rgb[i]
+        return f
+
+
+def gmm_alpha(t: int, history: int = 500) -> float:
+    """Learning rate handed to the background model for frame t: 1 / (t + 1) while the
+    model warms up, then 1 / history (a running mean of the first frames, then an
+    exponential window of `history` frames)."""
+    return 1.0 / min(t + 1, history)
+
+
+# The background-model workload of the bench: the 20 cameras of cam20_4k, 5 components.
+GMM_BENCH = dict(cameras=20, width=3840, height=2160, n_mix=5, objects=40, seed=7)

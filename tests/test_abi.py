@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version():
-    assert tg.lib().tg_abi_version() == 4
+    assert tg.lib().tg_abi_version() == 5
 
 
 def test_strerror():
@@ -67,6 +67,17 @@ int main(void) {
   F(tg_unstitch_args, n_rois); F(tg_unstitch_args, clip); F(tg_unstitch_args, roi_of_box);
   F(tg_unstitch_args, n_out); F(tg_unstitch_args, workspace); F(tg_unstitch_args, workspace_bytes);
   F(tg_unstitch_args, rule);
+  printf("tg_gmm_params %zu\ntg_gmm_args %zu\ntg_mask_rois_args %zu\n", sizeof(tg_gmm_params),
+         sizeof(tg_gmm_args), sizeof(tg_mask_rois_args));
+  F(tg_gmm_params, alpha); F(tg_gmm_params, var_threshold_gen); F(tg_gmm_params, var_max);
+  F(tg_gmm_params, complexity_reduction);
+  F(tg_gmm_args, frames); F(tg_gmm_args, n_frames); F(tg_gmm_args, height); F(tg_gmm_args, state);
+  F(tg_gmm_args, modes); F(tg_gmm_args, mask); F(tg_gmm_args, params);
+  F(tg_mask_rois_args, mask); F(tg_mask_rois_args, min_area); F(tg_mask_rois_args, rois);
+  F(tg_mask_rois_args, areas); F(tg_mask_rois_args, max_rois); F(tg_mask_rois_args, frame_begin);
+  F(tg_mask_rois_args, n_rois); F(tg_mask_rois_args, n_components);
+  F(tg_mask_rois_args, max_components); F(tg_mask_rois_args, workspace);
+  F(tg_mask_rois_args, workspace_bytes);
   return 0;
 }
 """)
@@ -87,8 +98,12 @@ def test_struct_layout_matches_header(tmp_path):
     assert c["tg_slo_patch"] == tg.SLO_PATCH_DTYPE.itemsize == 24
     assert c["tg_slo_params"] == ctypes.sizeof(tg.SloParams)
     assert c["tg_invocation"] == tg.INVOCATION_DTYPE.itemsize == 40
+    assert c["tg_gmm_params"] == ctypes.sizeof(tg.GmmParams) == 36
+    assert c["tg_gmm_args"] == ctypes.sizeof(tg.GmmArgs)
+    assert c["tg_mask_rois_args"] == ctypes.sizeof(tg.MaskRoisArgs)
     structs = {"tg_stitch_args": tg.StitchArgs, "tg_unstitch_args": tg.UnstitchArgs,
-               "tg_slo_params": tg.SloParams}
+               "tg_slo_params": tg.SloParams, "tg_gmm_params": tg.GmmParams,
+               "tg_gmm_args": tg.GmmArgs, "tg_mask_rois_args": tg.MaskRoisArgs}
     dtypes = {"tg_slo_patch": tg.SLO_PATCH_DTYPE, "tg_invocation": tg.INVOCATION_DTYPE}
     for key, off in c.items():
         if "." not in key:
@@ -179,6 +194,52 @@ def test_workspace_sizes():
     assert tg.unstitch_workspace_bytes(1024) == 16
     assert tg.unstitch_workspace_bytes(1025) == 24
     assert tg.unstitch_workspace_bytes(200000) == 8 * (1 + 196)
+
+
+def test_gmm_and_mask_rois_validation_without_gpu():
+    L = tg.lib()
+    assert L.tg_gmm_plane_stride(1) == 64 and L.tg_gmm_plane_stride(64) == 64
+    assert L.tg_gmm_plane_stride(65) == 128 and L.tg_gmm_plane_stride(0) == 0
+    assert L.tg_gmm_state_bytes(100, 3) == 4 * 5 * 3 * 128
+    assert L.tg_gmm_state_bytes(100, 0) == 0 and L.tg_gmm_state_bytes(100, 6) == 0
+    a = tg.GmmArgs()
+    a.frames = a.state = a.modes = a.mask = 0x1000
+    a.n_frames, a.width, a.height = 1, 8, 8
+    a.params = tg.gmm_params(n_mix=3)
+    for field, bad in (("n_mix", 0), ("n_mix", 6), ("alpha", 0.0), ("alpha", 2.0),
+                       ("var_min", 0.0), ("complexity_reduction", 1.0),
+                       ("background_ratio", float("nan"))):
+        b = tg.GmmArgs.from_buffer_copy(a)
+        setattr(b.params, field, bad)
+        assert L.tg_gmm_update(ctypes.byref(b), None) == tg.E_INVAL, field
+    b = tg.GmmArgs.from_buffer_copy(a)
+    b.state = 0x1004  # not 16-byte aligned
+    assert L.tg_gmm_update(ctypes.byref(b), None) == tg.E_INVAL
+    b = tg.GmmArgs.from_buffer_copy(a)
+    b.n_frames = 0
+    assert L.tg_gmm_update(ctypes.byref(b), None) == tg.OK  # nothing to do, no launch
+    assert L.tg_gmm_update(None, None) == tg.E_INVAL
+
+    assert L.tg_mask_rois_workspace_bytes(1, 8, 8, 0) == 0
+    assert L.tg_mask_rois_workspace_bytes(70000, 8, 8, 4) == 0
+    assert L.tg_mask_rois_workspace_bytes(1, 1 << 16, 1 << 15, 4) == 0
+    ws = L.tg_mask_rois_workspace_bytes(2, 100, 50, 1000)
+    assert ws >= 4 * 2 * 100 * 50 + 32 * 1000 + 4 * 1000 and ws % 256 == 0
+    m = tg.MaskRoisArgs()
+    m.mask = m.rois = m.areas = m.frame_begin = m.n_rois = m.n_components = 0x1000
+    m.n_frames, m.width, m.height, m.min_area, m.max_rois, m.max_components = 2, 100, 50, 1, 10, 1000
+    m.workspace, m.workspace_bytes = 0x2000, ws - 1
+    assert L.tg_mask_rois(ctypes.byref(m), None) == tg.E_WORKSPACE
+    m.workspace = 0x2008
+    m.workspace_bytes = ws
+    assert L.tg_mask_rois(ctypes.byref(m), None) == tg.E_WORKSPACE  # misaligned
+    for field, bad in (("max_components", 0), ("max_rois", -1), ("width", 0), ("n_frames", -1)):
+        b = tg.MaskRoisArgs.from_buffer_copy(m)
+        setattr(b, field, bad)
+        assert L.tg_mask_rois(ctypes.byref(b), None) == tg.E_INVAL, field
+    b = tg.MaskRoisArgs.from_buffer_copy(m)
+    b.n_rois = None
+    assert L.tg_mask_rois(ctypes.byref(b), None) == tg.E_INVAL
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
