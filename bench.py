@@ -259,6 +259,88 @@ def merge_cost(tg, W, torch, uargs, ubufs, n_frames, with_oracle: bool, launches
     return out
 
 
+def gmm_cost(tg, W, torch, with_oracle: bool, warm: int = 8, launches: int = 8):
+    """tg_gmm_update on the 20-camera 3840x2160 background model (5 components) fed seeded
+    synthetic video, then tg_mask_rois on its mask; HIP events on the stream they run on.
+    Algorithmic bytes of an update: per pixel 3 sample bytes, the component count read and
+    written, the mask byte, and 20 bytes per component in use before (read) and after
+    (written) the frame."""
+    cfg = W.GMM_BENCH
+    cams, fw, fh, K = cfg["cameras"], cfg["width"], cfg["height"], cfg["n_mix"]
+    video = W.SyntheticVideo(cams, fw, fh, objects=cfg["objects"], seed=cfg["seed"])
+    n_video = warm + launches  # every update sees a new frame: objects keep moving
+    frames = [torch.from_numpy(video.frame(t)).cuda() for t in range(n_video)]
+    model = tg.GmmModel(cams, fw, fh, K)
+    n = model.n_px
+    stream = torch.cuda.current_stream()
+    h = tg._vp(stream.cuda_stream)
+
+    def update(t):
+        a = tg.gmm_args(frames[t % n_video], model, tg.gmm_params(n_mix=K, alpha=W.gmm_alpha(t)))
+        rc = tg.lib().tg_gmm_update(tg.ctypes.byref(a), h)
+        if rc != tg.OK:
+            raise tg.TgError("tg_gmm_update", rc)
+
+    for t in range(warm):
+        update(t)
+    used = torch.zeros(launches + 1, dtype=torch.int64, device="cuda")
+    used[0] = model.modes[:n].sum(dtype=torch.int64)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(launches)]
+    for i in range(launches):
+        evs[i][0].record(stream)
+        update(warm + i)
+        evs[i][1].record(stream)
+        used[i + 1] = model.modes[:n].sum(dtype=torch.int64)
+    torch.cuda.synchronize()
+    us = [e0.elapsed_time(e1) * 1e3 for e0, e1 in evs]
+    u = used.cpu().numpy()
+    nbytes = [6 * n + 20 * int(u[i] + u[i + 1]) for i in range(launches)]
+    gbs = float(np.mean(nbytes)) / float(np.mean(us)) / 1e3
+    out = {"workload": f"{cams} cameras x {fw}x{fh}, {K} components, synthetic video "
+                       f"({cfg['objects']} moving objects per camera), frames {warm}..{warm + launches - 1}",
+           "us_per_update": round(float(np.mean(us)), 2),
+           "gpx_per_s": round(n / float(np.mean(us)) / 1e3, 2),
+           "components_per_pixel": round(float(u[1:].mean()) / n, 3),
+           "foreground": round(float(model.mask[:n].float().mean()), 4),
+           "algorithmic_bytes_per_update": int(np.mean(nbytes)),
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)}}
+    # tg_mask_rois on the last mask
+    bufs = tg.MaskRoisBuffers(cams, fw, fh, 1 << 20, 1 << 22)
+    ra = tg.mask_rois_args(model.mask, bufs, 16)
+    for _ in range(2):
+        tg.lib().tg_mask_rois(tg.ctypes.byref(ra), h)
+    torch.cuda.synchronize()
+    mevs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    mevs[0].record(stream)
+    for i in range(launches):
+        rc = tg.lib().tg_mask_rois(tg.ctypes.byref(ra), h)
+        if rc != tg.OK:
+            raise tg.TgError("tg_mask_rois", rc)
+        mevs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    mus = float(np.mean([mevs[i].elapsed_time(mevs[i + 1]) * 1e3 for i in range(launches)]))
+    _, _, _, n_rois, n_comp = bufs.result()
+    out["mask_rois"] = {"us_per_call": round(mus, 2), "rois": int(n_rois),
+                        "components": int(n_comp), "min_area": 16,
+                        "gpx_per_s": round(n / mus / 1e3, 2)}
+    if with_oracle:
+        import oracle
+
+        px = fw * fh  # the oracle on camera 0 only, two frames
+        st, md = oracle.gmm_state(px, K)
+        host = [video.frame(t)[0].reshape(-1, 3) for t in range(2)]
+        t0 = time.perf_counter()
+        for t in range(2):
+            oracle.gmm_update(host[t], st, md, oracle.gmm_params(n_mix=K, alpha=W.gmm_alpha(t)))
+        el = time.perf_counter() - t0
+        out["oracle_gpx_per_s"] = round(2 * px / el / 1e9, 4)
+        out["oracle_sample"] = f"camera 0, frames 0-1 ({2 * px} pixel updates), {el:.2f} s, 1 thread"
+    del frames, model
+    return out
+
+
 def stream_ceiling(torch, read_bytes: int, write_bytes: int, launches: int = 40):
     """A plain streaming kernel (libtg_probe.so) moving the stitch launch's algorithmic
     reads and writes, writes alternating between two outputs and reads cycling through a
@@ -504,6 +586,7 @@ def main():
     result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
     result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
     result["merge"] = merge_cost(tg, W, torch, uargs, ubufs, wl.n_frames, not args.no_cpu_baseline)
+    result["gmm"] = gmm_cost(tg, W, torch, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         frames_np = frames_d.cpu().numpy()
         result["cpu_baseline"] = cpu_baseline(wl, rois, frames_np, boxes, canv, args.cpu_seconds)
