@@ -6,17 +6,21 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order), in seven launches on the caller's stream:
 //  1. clear:  zeroes the tickets and look-back words of launches 4 and 6.
-//  2. local:  one 256-thread workgroup per 32x32 tile labels the tile in LDS and writes,
-//             for each foreground pixel, the frame index of its tile-local root.
-//  3. merge:  one wave per tile joins its top-row and left-column pixels with their
-//             foreground neighbours in the tiles above and to the left (global atomics
-//             on the label array). Every 8-neighbour pair across a tile border is seen
-//             from the tile below or to the right of it.
-//  4. roots:  8192-pixel raster spans in ticket order find the pixels still labelled
+//  2. local:  one 256-thread workgroup per 16 32x32 tiles side by side (their mask
+//             words loaded together up front; a group without foreground leaves at once)
+//             labels each tile in LDS and writes, for each foreground pixel, the frame
+//             index of its tile-local root.
+//  3. merge:  one thread per 16 pixels of a tile border row or column joins each
+//             foreground pixel with its foreground neighbours in the tile above (border rows) or to
+//             the left (border columns), with global atomics on the label array. Every
+//             8-neighbour pair across a tile border is seen from the tile below or to the
+//             right of it.
+//  4. roots:  32768-pixel raster spans in ticket order (each thread's 128 mask bytes as
+//             eight 16-byte loads) find the foreground pixels still labelled
 //             with their own index (the components), number them in raster order with a
 //             decoupled look-back, initialise each component's record and mark the root
 //             with its number.
-//  5. boxes:  per tile again, the tile's local components (relabelled in LDS) fold their
+//  5. boxes:  per 16 tiles again, each tile's local components (relabelled in LDS) fold their
 //             pixels' extent and count in LDS; each local component then follows the
 //             label chain to its component number and folds its totals into the record
 //             with global atomics: one set of atomics per (tile, component).
@@ -35,9 +39,12 @@ namespace {
 
 constexpr int kTile = 32;
 constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
-constexpr int kSpan = 8192;        // pixels per workgroup of the roots pass
-constexpr int kSpanThreads = 256;  // 32 pixels per thread
+constexpr int kTilesPerGroup = 16;  // tiles side by side per workgroup of local and boxes
+constexpr int kBorderThreads = 256;
+constexpr int kSpan = 32768;       // pixels per workgroup of the roots pass
+constexpr int kSpanThreads = 256;  // 128 pixels per thread: eight 16-byte loads
 constexpr int kSpanPix = kSpan / kSpanThreads;
+constexpr int kSpanWords = kSpanPix / 32;  // foreground / root bit words per thread
 constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
 constexpr int kFilterThreads = 256;
 
@@ -128,24 +135,59 @@ __device__ __forceinline__ void g_unite(int32_t *L, int a, int b) {
   }
 }
 
-// Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
-// within the tile). Thread t holds row t / 8, columns 4 (t % 8) .. + 3; fg[k] says which
-// of them are foreground. Returns false, uniformly, when the tile has no foreground.
-__device__ __forceinline__ bool label_tile(const uint8_t *mf, int W, int H, int tx0, int ty0,
-                                           int *L, bool fg[4]) {
+// Foreground bits of this thread's 4 pixels in each of the kTilesPerGroup tiles of a
+// group (tile q at column tx0 + 32 q, row ty0): thread t holds row t / 8, columns
+// 4 (t % 8) .. + 3 of every tile. All loads are issued before any is used, from addresses
+// clamped into the frame (pixels outside it are masked off afterwards): one dword per
+// tile when every row start is dword-aligned (kWord), else four bytes.
+template <bool kWord>
+__device__ __forceinline__ void load_group_fg(const uint8_t *mf, int W, int H, int tx0, int ty0,
+                                              uint32_t fg[kTilesPerGroup]) {
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
-  bool any = false;
+  const uint8_t *row = mf + static_cast<int64_t>(min(y, H - 1)) * W;
+  uint32_t raw[kTilesPerGroup][kWord ? 1 : 4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int x = tx0 + c0 + k;
-    fg[k] = y < H && x < W && mf[static_cast<int64_t>(y) * W + x] != 0;
-    L[r * kTile + c0 + k] = fg[k] ? r * kTile + c0 + k : -1;
-    any |= fg[k];
+  for (int q = 0; q < kTilesPerGroup; ++q) {
+    const int x0 = tx0 + q * kTile + c0;
+    if (kWord) {
+      raw[q][0] = *reinterpret_cast<const uint32_t *>(row + min(x0, W - 4));
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) raw[q][kWord ? 0 : k] = row[min(x0 + k, W - 1)];
+    }
   }
-  if (!__syncthreads_or(any)) return false;
+#pragma unroll
+  for (int q = 0; q < kTilesPerGroup; ++q) {
+    const int x0 = tx0 + q * kTile + c0;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t v = kWord ? (raw[q][0] >> (8 * k)) & 0xFFu : raw[q][kWord ? 0 : k];
+      bits |= (v != 0 && x0 + k < W) ? 1u << k : 0u;
+    }
+    fg[q] = y < H ? bits : 0u;
+  }
+}
+
+// Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
+// within the tile) from this thread's foreground bits (load_group_fg). Returns false,
+// uniformly, when the tile has no foreground. Starts with a barrier, so the caller's
+// previous use of L (and of any other LDS) is over before L is rewritten.
+__device__ __forceinline__ bool label_tile(uint32_t fg, int *L) {
+  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
+  if (!__syncthreads_or(fg != 0)) return false;
+  if (__syncthreads_and(fg == 0xFu)) {  // a solid tile is one set rooted at its pixel 0
+#pragma unroll
+    for (int k = 0; k < 4; ++k) L[r * kTile + c0 + k] = 0;
+    __syncthreads();
+    return true;
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) L[r * kTile + c0 + k] = (fg >> k & 1u) ? r * kTile + c0 + k : -1;
+  __syncthreads();
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    if (!fg[k]) continue;
+    if (!(fg >> k & 1u)) continue;
     const int c = c0 + k, i = r * kTile + c;
     if (c > 0 && lds_load(&L[i - 1]) >= 0) lds_unite(L, i, i - 1);
     if (r > 0) {
@@ -165,52 +207,106 @@ __global__ void clear_kernel(uint64_t *words, int64_t n) {
   if (i < n) words[i] = 0;
 }
 
+template <bool kWord>
 __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask, int W, int H,
-                                                             int64_t frame_px,
-                                                             int32_t *label) {
+                                                             int64_t frame_px, int32_t *label) {
   __shared__ int L[kTile * kTile];
   const int64_t f = blockIdx.z;
-  const int tx0 = blockIdx.x * kTile, ty0 = blockIdx.y * kTile;
-  bool fg[4];
-  if (!label_tile(mask + f * frame_px, W, H, tx0, ty0, L, fg)) return;
+  const int ty0 = blockIdx.y * kTile;
+  const uint8_t *mf = mask + f * frame_px;
+  uint32_t fg[kTilesPerGroup];
+  load_group_fg<kWord>(mf, W, H, blockIdx.x * kTilesPerGroup * kTile, ty0, fg);
+  uint32_t any = 0;
+#pragma unroll
+  for (int q = 0; q < kTilesPerGroup; ++q) any |= fg[q];
+  if (!__syncthreads_or(any != 0)) return;
   int32_t *lf = label + f * frame_px;
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
+  for (int q = 0; q < kTilesPerGroup; ++q) {
+    const int tx0 = (blockIdx.x * kTilesPerGroup + q) * kTile;
+    if (!label_tile(fg[q], L)) continue;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (!fg[k]) continue;
-    const int root = lds_find(L, r * kTile + c0 + k);
-    lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] =
-        (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
+    for (int k = 0; k < 4; ++k) {
+      if (!(fg[q] >> k & 1u)) continue;
+      const int root = lds_find(L, r * kTile + c0 + k);
+      lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] =
+          (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
+    }
   }
 }
 
-__global__ __launch_bounds__(64) void merge_kernel(const uint8_t *mask, int W, int H,
-                                                   int64_t frame_px, int32_t *label) {
-  const int64_t f = blockIdx.z;
-  const int tx0 = blockIdx.x * kTile, ty0 = blockIdx.y * kTile, lane = threadIdx.x;
+// Thread i of frame blockIdx.y: 16 consecutive pixels of a border row (rows 32, 64, ...
+// below the first, each against the row above; one 16-byte load where the row is
+// 16-byte aligned), then 16 consecutive pixels of a border column (columns 32, 64, ...,
+// each against the column to its left).
+__global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *mask, int W, int H,
+                                                               int64_t frame_px, bool vec,
+                                                               int row_items, int n_row,
+                                                               int col_items, int n_all,
+                                                               int32_t *label) {
+  const int i = blockIdx.x * kBorderThreads + threadIdx.x;
+  if (i >= n_all) return;
+  const int64_t f = blockIdx.y;
   const uint8_t *mf = mask + f * frame_px;
   int32_t *lf = label + f * frame_px;
-  if (lane < kTile) {  // top row against the row above
-    const int x = tx0 + lane, y = ty0;
-    if (y > 0 && x < W && mf[y * W + x]) {
+  uint32_t fg = 0;
+  if (i < n_row) {  // top rows of tiles against the rows above
+    const int b = i / row_items, x0 = 16 * (i - b * row_items), y = (b + 1) * kTile;
+    const uint8_t *p = mf + y * W + x0;
+    if (vec && x0 + 16 <= W) {
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) fg |= ((v[k >> 2] >> (8 * (k & 3))) & 0xFFu) ? 1u << k : 0u;
+    } else {
+      const uint8_t *rowp = mf + y * W;
+      uint32_t v[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) v[k] = rowp[min(x0 + k, W - 1)];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && x0 + k < W) ? 1u << k : 0u;
+    }
+    // Join through the pixels' current labels (members of their sets), skipping a pair
+    // equal to the one just joined: along a border most pairs repeat.
+    int la = -1, lb = -1;
+    for (; fg != 0; fg &= fg - 1) {
+      const int x = x0 + __builtin_ctz(fg);
       for (int dx = -1; dx <= 1; ++dx) {
         const int nx = x + dx;
-        if (nx >= 0 && nx < W && mf[(y - 1) * W + nx]) g_unite(lf, y * W + x, (y - 1) * W + nx);
+        if (nx < 0 || nx >= W || !mf[(y - 1) * W + nx]) continue;
+        const int a = g_load(&lf[y * W + x]), b = g_load(&lf[(y - 1) * W + nx]);
+        if (a == la && b == lb) continue;
+        g_unite(lf, a, b);
+        la = a;
+        lb = b;
       }
     }
-  } else {  // left column against the column to the left
-    const int x = tx0, y = ty0 + lane - kTile;
-    if (x > 0 && y < H && mf[y * W + x]) {
+  } else {  // left columns of tiles against the columns to their left
+    const int j = i - n_row, b = j / col_items, y0 = 16 * (j - b * col_items);
+    const int x = (b + 1) * kTile;
+    uint32_t v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = mf[min(y0 + k, H - 1) * W + x];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && y0 + k < H) ? 1u << k : 0u;
+    int la = -1, lb = -1;
+    for (; fg != 0; fg &= fg - 1) {
+      const int y = y0 + __builtin_ctz(fg);
       for (int dy = -1; dy <= 1; ++dy) {
         const int ny = y + dy;
-        if (ny >= 0 && ny < H && mf[ny * W + x - 1]) g_unite(lf, y * W + x, ny * W + x - 1);
+        if (ny < 0 || ny >= H || !mf[ny * W + x - 1]) continue;
+        const int a = g_load(&lf[y * W + x]), b = g_load(&lf[ny * W + x - 1]);
+        if (a == la && b == lb) continue;
+        g_unite(lf, a, b);
+        la = a;
+        lb = b;
       }
     }
   }
 }
 
 __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
-    const uint8_t *mask, int64_t n_px, int64_t frame_px, int64_t n_spans, int32_t *label,
+    const uint8_t *mask, bool vec, int64_t n_px, int64_t frame_px, int64_t n_spans, int32_t *label,
     Comp *comp, int32_t max_components, uint64_t *words, uint64_t *state,
     int32_t *n_components) {
   __shared__ int s_span, s_base;
@@ -224,23 +320,38 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   const int64_t span = s_span;
   const int64_t p0 = span * kSpan + static_cast<int64_t>(tid) * kSpanPix;
 
-  // Which of this thread's 32 pixels are roots.
-  uint32_t roots = 0;
-  int64_t f0 = p0 / frame_px;
+  // Which of this thread's 128 pixels are foreground (16-byte loads when the mask is
+  // 16-byte aligned and the bytes are inside it), then which of those are roots.
+  uint32_t fgm[kSpanWords] = {};
   if (p0 < n_px) {
-    int64_t local = p0 - f0 * frame_px;
-#pragma unroll 4
-    for (int j = 0; j < kSpanPix; ++j) {
-      const int64_t P = p0 + j;
-      if (P >= n_px) break;
-      if (local == frame_px) local = 0;
-      if (mask[P] && label[P] == static_cast<int32_t>(local)) roots |= 1u << j;
-      ++local;
+    if (vec && p0 + kSpanPix <= n_px) {
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      u32x4 v[kSpanPix / 16];
+#pragma unroll
+      for (int q = 0; q < kSpanPix / 16; ++q) v[q] = *reinterpret_cast<const u32x4 *>(mask + p0 + 16 * q);
+#pragma unroll
+      for (int q = 0; q < kSpanPix / 16; ++q)
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          fgm[q >> 1] |= ((v[q][j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << (16 * (q & 1) + j) : 0u;
+    } else {
+      for (int j = 0; j < kSpanPix; ++j)
+        fgm[j >> 5] |= (p0 + j < n_px && mask[min(p0 + j, n_px - 1)]) ? 1u << (j & 31) : 0u;
     }
+  }
+  uint32_t roots[kSpanWords] = {};
+  int cnt = 0;
+#pragma unroll
+  for (int w = 0; w < kSpanWords; ++w) {
+    for (uint32_t m = fgm[w]; m != 0; m &= m - 1) {
+      const int j = 32 * w + __builtin_ctz(m);
+      const int64_t P = p0 + j;
+      if (label[P] == static_cast<int32_t>(P % frame_px)) roots[w] |= 1u << (j & 31);
+    }
+    cnt += __popc(roots[w]);
   }
 
   // Exclusive scan of the counts over the workgroup, then the look-back over spans.
-  const int cnt = __popc(roots);
   int incl = cnt;
   for (int o = 1; o < 64; o <<= 1) {
     const int v = __shfl_up(incl, o);
@@ -264,22 +375,15 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   __syncthreads();
 
   int id = s_base + before + incl - cnt;
-  if (roots) {
-    int64_t local = p0 - f0 * frame_px, f = f0;
-    for (int j = 0; j < kSpanPix; ++j) {
-      if (local == frame_px) {
-        local = 0;
-        ++f;
-      }
-      if (roots >> j & 1u) {
-        if (id < max_components) {
-          comp[id] = Comp{static_cast<int32_t>(f), static_cast<int32_t>(local), INT_MAX, INT_MAX,
-                          INT_MIN, INT_MIN, 0, 0};
-          label[p0 + j] = -(id + 1);
-        }
-        ++id;
-      }
-      ++local;
+#pragma unroll
+  for (int w = 0; w < kSpanWords; ++w) {
+    for (uint32_t m = roots[w]; m != 0; m &= m - 1, ++id) {
+      if (id >= max_components) continue;
+      const int64_t P = p0 + 32 * w + __builtin_ctz(m);
+      const int64_t f = P / frame_px;
+      comp[id] = Comp{static_cast<int32_t>(f), static_cast<int32_t>(P - f * frame_px), INT_MAX,
+                      INT_MAX, INT_MIN, INT_MIN, 0, 0};
+      label[P] = -(id + 1);
     }
   }
 }
@@ -297,6 +401,7 @@ __device__ __forceinline__ int wave_sum(int v) {
   return v;
 }
 
+template <bool kWord>
 __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask, int W, int H,
                                                              int64_t frame_px,
                                                              const int32_t *label,
@@ -305,70 +410,81 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
   __shared__ int bx0[kTile * kTile], by0[kTile * kTile], bx1[kTile * kTile],
       by1[kTile * kTile], bn[kTile * kTile];
   const int64_t f = blockIdx.z;
-  const int tx0 = blockIdx.x * kTile, ty0 = blockIdx.y * kTile;
-  bool fg[4];
-  if (!label_tile(mask + f * frame_px, W, H, tx0, ty0, L, fg)) return;
-  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
-  int root[4];
+  const int ty0 = blockIdx.y * kTile;
+  const uint8_t *mf = mask + f * frame_px;
+  uint32_t fgw[kTilesPerGroup];
+  load_group_fg<kWord>(mf, W, H, blockIdx.x * kTilesPerGroup * kTile, ty0, fgw);
+  uint32_t any = 0;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = r * kTile + c0 + k;
-    root[k] = fg[k] ? lds_find(L, i) : -1;
-    if (root[k] == i) {
-      bx0[i] = INT_MAX;
-      by0[i] = INT_MAX;
-      bx1[i] = INT_MIN;
-      by1[i] = INT_MIN;
-      bn[i] = 0;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int x = tx0 + c0 + k;
-    // When every foreground lane of the wave is in one local component, reduce across
-    // the wave first and fold once.
-    const uint64_t fgm = __ballot(fg[k]);
-    if (!fgm) continue;
-    const int lead = __shfl(root[k], __builtin_ctzll(fgm));
-    if (__ballot(fg[k] && root[k] != lead) == 0) {
-      const int mx0 = wave_min(fg[k] ? x : INT_MAX), my0 = wave_min(fg[k] ? y : INT_MAX);
-      const int mx1 = wave_max(fg[k] ? x : INT_MIN), my1 = wave_max(fg[k] ? y : INT_MIN);
-      const int n = wave_sum(fg[k] ? 1 : 0);
-      if ((threadIdx.x & 63) == 0) {
-        atomicMin(&bx0[lead], mx0);
-        atomicMin(&by0[lead], my0);
-        atomicMax(&bx1[lead], mx1);
-        atomicMax(&by1[lead], my1);
-        atomicAdd(&bn[lead], n);
-      }
-    } else if (fg[k]) {
-      atomicMin(&bx0[root[k]], x);
-      atomicMin(&by0[root[k]], y);
-      atomicMax(&bx1[root[k]], x);
-      atomicMax(&by1[root[k]], y);
-      atomicAdd(&bn[root[k]], 1);
-    }
-  }
-  __syncthreads();
+  for (int q = 0; q < kTilesPerGroup; ++q) any |= fgw[q];
+  if (!__syncthreads_or(any != 0)) return;
   const int32_t *lf = label + f * frame_px;
+  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
+  for (int q = 0; q < kTilesPerGroup; ++q) {
+    const int tx0 = (blockIdx.x * kTilesPerGroup + q) * kTile;
+    if (!label_tile(fgw[q], L)) continue;
+    bool fg[4];
+    int root[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = r * kTile + c0 + k;
-    if (root[k] != i) continue;
-    int cur = y * W + tx0 + c0 + k;
-    int v = lf[cur];
-    while (v >= 0 && v != cur) {
-      cur = v;
-      v = lf[cur];
+    for (int k = 0; k < 4; ++k) {
+      const int i = r * kTile + c0 + k;
+      fg[k] = fgw[q] >> k & 1u;
+      root[k] = fg[k] ? lds_find(L, i) : -1;
+      if (root[k] == i) {
+        bx0[i] = INT_MAX;
+        by0[i] = INT_MAX;
+        bx1[i] = INT_MIN;
+        by1[i] = INT_MIN;
+        bn[i] = 0;
+      }
     }
-    if (v >= 0) continue;  // a component past max_components: not measured
-    Comp *c = comp + (-v - 1);
-    atomicMin(&c->x0, bx0[i]);
-    atomicMin(&c->y0, by0[i]);
-    atomicMax(&c->x1, bx1[i]);
-    atomicMax(&c->y1, by1[i]);
-    atomicAdd(&c->area, bn[i]);
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int x = tx0 + c0 + k;
+      // When every foreground lane of the wave is in one local component, reduce across
+      // the wave first and fold once.
+      const uint64_t fgm = __ballot(fg[k]);
+      if (!fgm) continue;
+      const int lead = __shfl(root[k], __builtin_ctzll(fgm));
+      if (__ballot(fg[k] && root[k] != lead) == 0) {
+        const int mx0 = wave_min(fg[k] ? x : INT_MAX), my0 = wave_min(fg[k] ? y : INT_MAX);
+        const int mx1 = wave_max(fg[k] ? x : INT_MIN), my1 = wave_max(fg[k] ? y : INT_MIN);
+        const int n = wave_sum(fg[k] ? 1 : 0);
+        if ((threadIdx.x & 63) == 0) {
+          atomicMin(&bx0[lead], mx0);
+          atomicMin(&by0[lead], my0);
+          atomicMax(&bx1[lead], mx1);
+          atomicMax(&by1[lead], my1);
+          atomicAdd(&bn[lead], n);
+        }
+      } else if (fg[k]) {
+        atomicMin(&bx0[root[k]], x);
+        atomicMin(&by0[root[k]], y);
+        atomicMax(&bx1[root[k]], x);
+        atomicMax(&by1[root[k]], y);
+        atomicAdd(&bn[root[k]], 1);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = r * kTile + c0 + k;
+      if (root[k] != i) continue;
+      int cur = y * W + tx0 + c0 + k;
+      int v = lf[cur];
+      while (v >= 0 && v != cur) {
+        cur = v;
+        v = lf[cur];
+      }
+      if (v >= 0) continue;  // a component past max_components: not measured
+      Comp *c = comp + (-v - 1);
+      atomicMin(&c->x0, bx0[i]);
+      atomicMin(&c->y0, by0[i]);
+      atomicMax(&c->x1, bx1[i]);
+      atomicMax(&c->y1, by1[i]);
+      atomicAdd(&c->area, bn[i]);
+    }
   }
 }
 
@@ -482,8 +598,15 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
     return TG_E_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int W = a->width, H = a->height;
-  const dim3 tiles((W + kTile - 1) / kTile, (H + kTile - 1) / kTile,
-                   static_cast<uint32_t>(a->n_frames));
+  const int tiles_x = (W + kTile - 1) / kTile, tiles_y = (H + kTile - 1) / kTile;
+  const dim3 groups((tiles_x + kTilesPerGroup - 1) / kTilesPerGroup, tiles_y,
+                    static_cast<uint32_t>(a->n_frames));
+  // dword mask reads need every row start dword-aligned; 16-byte span reads need the
+  // mask itself 16-byte aligned
+  const uintptr_t mp = reinterpret_cast<uintptr_t>(a->mask);
+  const bool word = mp % 4 == 0 && W % 4 == 0, vec = mp % 16 == 0;
+  const int row_items = (W + 15) / 16, col_items = (H + 15) / 16;
+  const int n_row = (tiles_y - 1) * row_items, n_all = n_row + (tiles_x - 1) * col_items;
   const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
   const int64_t n_filter = (a->max_components + kFilterBlock - 1) / kFilterBlock;
 
@@ -494,14 +617,27 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   }
   hipLaunchKernelGGL(clear_kernel, dim3(static_cast<uint32_t>((L.n_words + 255) / 256)),
                      dim3(256), 0, s, L.words, L.n_words);
-  hipLaunchKernelGGL(local_kernel, tiles, dim3(kTileThreads), 0, s, a->mask, W, H, frame_px,
-                     L.label);
-  hipLaunchKernelGGL(merge_kernel, tiles, dim3(64), 0, s, a->mask, W, H, frame_px, L.label);
+  if (word)
+    hipLaunchKernelGGL(local_kernel<true>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
+                       frame_px, L.label);
+  else
+    hipLaunchKernelGGL(local_kernel<false>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
+                       frame_px, L.label);
+  if (n_all > 0)
+    hipLaunchKernelGGL(merge_kernel,
+                       dim3(static_cast<uint32_t>((n_all + kBorderThreads - 1) / kBorderThreads),
+                            static_cast<uint32_t>(a->n_frames)),
+                       dim3(kBorderThreads), 0, s, a->mask, W, H, frame_px,
+                       vec && W % 16 == 0, row_items, n_row, col_items, n_all, L.label);
   hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_spans)), dim3(kSpanThreads), 0,
-                     s, a->mask, n_px, frame_px, n_spans, L.label, L.comp, a->max_components,
-                     L.words, L.root_state, a->n_components);
-  hipLaunchKernelGGL(boxes_kernel, tiles, dim3(kTileThreads), 0, s, a->mask, W, H, frame_px,
-                     L.label, L.comp);
+                     s, a->mask, vec, n_px, frame_px, n_spans, L.label, L.comp,
+                     a->max_components, L.words, L.root_state, a->n_components);
+  if (word)
+    hipLaunchKernelGGL(boxes_kernel<true>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
+                       frame_px, L.label, L.comp);
+  else
+    hipLaunchKernelGGL(boxes_kernel<false>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
+                       frame_px, L.label, L.comp);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
                      0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,
                      a->areas, a->max_rois, L.kept_frame, L.words, L.filter_state, a->n_rois);
