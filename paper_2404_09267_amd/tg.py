@@ -390,6 +390,7 @@ def stitch_args(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w,
         if unit_order.numel() < n_units:
             raise ValueError(f"unit_order must hold {n_units} unit ids")
         a.unit_order = unit_order.data_ptr()
+    a._keep = (frames, dplan, out, unit_order)  # the struct holds raw pointers: keep their owners alive
     return a
 
 
@@ -445,6 +446,7 @@ def partition_args(boxes, frame_begin, frame_w, frame_h, zones_x, zones_y,
     a.zone_of_box = bufs.zone_of_box.data_ptr() if zone_of_box else None
     a.n_patches = bufs.n_patches.data_ptr()
     a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    a._keep = (boxes, frame_begin, bufs)  # the struct holds raw pointers: keep their owners alive
     return a
 
 
@@ -493,6 +495,7 @@ def unstitch_args(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuff
                                      bufs.n_out.data_ptr())
     a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
     a.rule = int(rule)
+    a._keep = (boxes, box_canvas, dplan, bufs)  # the struct holds raw pointers: keep their owners alive
     return a
 
 
@@ -545,6 +548,7 @@ def merge_args(dets, n_dets, scores, n_frames, iou_threshold, cross_only,
     a.keep, a.out = bufs.keep.data_ptr(), bufs.out.data_ptr()
     a.n_kept, a.n_overflow = bufs.n_kept.data_ptr(), bufs.n_overflow.data_ptr()
     a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    a._keep = (dets, n_dets, scores, bufs)  # the struct holds raw pointers: keep their owners alive
     return a
 
 
@@ -602,6 +606,7 @@ def gmm_args(frames, model: GmmModel, params: GmmParams) -> GmmArgs:
     a.n_frames, a.width, a.height = model.n_frames, model.width, model.height
     a.state, a.modes, a.mask = model.state.data_ptr(), model.modes.data_ptr(), model.mask.data_ptr()
     a.params = params
+    a._keep = (frames, model)  # the struct holds raw pointers: keep their owners alive
     return a
 
 
@@ -655,6 +660,7 @@ def mask_rois_args(mask, bufs: MaskRoisBuffers, min_area: int) -> MaskRoisArgs:
     a.n_components = bufs.counts.data_ptr() + 4
     a.max_components = bufs.max_components
     a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
+    a._keep = (mask, bufs)  # the struct holds raw pointers: keep their owners alive
     return a
 
 

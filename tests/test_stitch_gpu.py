@@ -329,3 +329,32 @@ def test_unit_order_that_is_not_a_permutation(torch):
                 np.testing.assert_array_equal(got[c, :, y], want[c, :, y])
             else:
                 assert np.all(got[c, :, y] == SENTINEL), (c, y)
+
+
+def test_argument_struct_keeps_its_tensors(torch):
+    """stitch_args returns a struct of raw device pointers; it holds the tensors they
+    point into, so a launch order passed as a temporary lives as long as the struct."""
+    import gc
+    import weakref
+
+    rng = np.random.default_rng(11)
+    rois = W.random_rois(rng, 30, 2, 90, 70, 4, 40, 40)
+    plan = tg.plan_pack(rois, 128, 96, 90, 70, 2, tg.SHELF_FFDH)
+    frames = torch.from_numpy(W.random_frames_np(2, 70, 90, 3)).cuda()
+    dplan = tg.DevicePlan(rois, plan)
+    out = torch.empty((plan.n_canvases, 3, 96, 128), dtype=torch.float16, device="cuda")
+    order = torch.from_numpy(tg.stitch_schedule(rois, plan, 0, plan.n_canvases, 128, 96)).cuda()
+    alive = weakref.ref(order)
+    a = tg.stitch_args(frames, dplan, 0, plan.n_canvases, 128, 96, W.MEAN, W.STD, W.PAD, out,
+                       unit_order=order)
+    del order
+    gc.collect()
+    assert alive() is not None
+    assert tg.lib().tg_stitch(tg.ctypes.byref(a), tg._stream_handle(None)) == tg.OK
+    torch.cuda.synchronize()
+    want = oracle.stitch(frames.cpu().numpy(), rois, oracle_plan(plan), 0, plan.n_canvases, 128,
+                         96, W.MEAN, W.STD, W.PAD)
+    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint16), want)
+    del a
+    gc.collect()
+    assert alive() is None
