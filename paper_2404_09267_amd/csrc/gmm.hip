@@ -9,7 +9,7 @@
 //
 // The kernel is a stream over HBM: per pixel it reads the sample (3 bytes), the count of
 // components in use and those components (20 bytes each), and writes them back with the
-// mask. State is planar (one plane per component field) so that a wave's 64 threads, four
+// mask. Component 0's planes are read together with the sample and the counts. State is planar (one plane per component field) so that a wave's 64 threads, four
 // pixels each, load and store 1 KB contiguous runs per plane, and planes past the
 // components a thread's pixels use are neither read nor written. All arithmetic uses
 // explicitly rounded operations, so the foreground decisions match any binary32
@@ -179,7 +179,10 @@ __global__ __launch_bounds__(kThreads) void gmm_kernel(const uint8_t *__restrict
 #pragma unroll
     for (int m = 0; m < K; ++m) {
       f32x4 f[kFields];
-      if (m < nmax) {
+      // Component 0 is loaded without waiting for the counts (every pixel past its first
+      // frame uses it; for a fresh pixel the values are ignored), so its loads travel
+      // with the sample's and the counts' instead of one round trip later.
+      if (m == 0 || m < nmax) {
 #pragma unroll
         for (int q = 0; q < kFields; ++q)
           f[q] = __builtin_nontemporal_load(
