@@ -346,42 +346,54 @@ def stream_ceiling(torch, read_bytes: int, write_bytes: int, launches: int = 40)
     reads and writes, writes alternating between two outputs and reads cycling through a
     pool of five read regions, as consecutive stitch batches do: what the memory system
     gives a kernel with no work of its own for this mix. Swept over the bytes each
-    workgroup writes; the best rate is the ceiling."""
+    workgroup writes, once with each workgroup writing one contiguous run (`sweep`; the
+    best rate is the ceiling) and once with its writes cut into three runs at the same
+    offset of three planes, as a stitch unit writes its rows' fp16 planes (`planes3`)."""
     import ctypes
 
     L = ctypes.CDLL(os.path.join(ROOT, "paper_2404_09267_amd", "libtg_probe.so"))
-    L.tg_probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
-                                  ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    L.tg_probe_stream_planes.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_void_p]
     r = read_bytes // 4096 * 4096
-    w = write_bytes // 4096 * 4096
+    w = write_bytes // 4096 * 4096 // 48 * 48
     regions = 5
     pool = torch.empty(regions * r, dtype=torch.uint8, device="cuda").fill_(1)
     outs = [torch.empty(w, dtype=torch.uint8, device="cuda") for _ in range(2)]
     stream = torch.cuda.current_stream()
     h = ctypes.c_void_p(stream.cuda_stream)
     out = {"kernel": "plain stream, libtg_probe.so", "read_bytes": r, "write_bytes": w}
-    out["sweep"] = {}
-    for chunk in (8192, 16384, 32768, 49152, 131072):
-        def launch(i):
-            rc = L.tg_probe_stream(ctypes.c_void_p(pool.data_ptr() + (i % regions) * r), r,
-                                   ctypes.c_void_p(outs[i & 1].data_ptr()), w, chunk, h)
-            if rc != 0:
-                raise RuntimeError(f"tg_probe_stream: {rc}")
-        for i in range(4):
-            launch(i)
-        torch.cuda.synchronize()
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
-        evs[0].record(stream)
-        for i in range(launches):
-            launch(i)
-            evs[i + 1].record(stream)
-        torch.cuda.synchronize()
-        us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
-        out["sweep"][f"{chunk // 1024}k"] = {"us": round(us, 2), "gbs": round((r + w) / us / 1e3, 1)}
-    del pool, outs
+
+    def sweep(planes):
+        res = {}
+        for chunk in (8192, 16384, 32768, 49152, 131072):
+            def launch(i):
+                rc = L.tg_probe_stream_planes(
+                    ctypes.c_void_p(pool.data_ptr() + (i % regions) * r), r,
+                    ctypes.c_void_p(outs[i & 1].data_ptr()), w, chunk, planes, h)
+                if rc != 0:
+                    raise RuntimeError(f"tg_probe_stream_planes: {rc}")
+            for i in range(4):
+                launch(i)
+            torch.cuda.synchronize()
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+            evs[0].record(stream)
+            for i in range(launches):
+                launch(i)
+                evs[i + 1].record(stream)
+            torch.cuda.synchronize()
+            us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
+            res[f"{chunk // 1024}k"] = {"us": round(us, 2), "gbs": round((r + w) / us / 1e3, 1)}
+        return res
+
+    out["sweep"] = sweep(1)
     best = max(out["sweep"], key=lambda k: out["sweep"][k]["gbs"])
     out["best_chunk"] = best
     out["gbs"] = out["sweep"][best]["gbs"]
+    p3 = sweep(3)
+    b3 = max(p3, key=lambda k: p3[k]["gbs"])
+    out["planes3"] = {"sweep": p3, "best_chunk": b3, "gbs": p3[b3]["gbs"]}
+    del pool, outs
     return out
 
 
@@ -581,6 +593,7 @@ def main():
     write_bytes = int(np.mean([c * wl.canvas * wl.canvas * 6 for _, c in batches]))
     ceil = stream_ceiling(torch, int(avg_bytes) - write_bytes, write_bytes)
     ceil["stitch_frac"] = round(achieved / ceil["gbs"], 4)
+    ceil["planes3"]["stitch_frac"] = round(achieved / ceil["planes3"]["gbs"], 4)
     result["ceiling"] = ceil
     result["unstitch"] = unstitch_cost(tg, torch, uargs, n_boxes)
     result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)

@@ -23,6 +23,13 @@ extern "C" {
 int tg_probe_stream(const void *src, int64_t read_bytes, void *dst, int64_t write_bytes,
                     int32_t chunk, void *stream);
 
+/* The same with the written bytes cut into `planes` equal planes (1..4; write_bytes a
+ * multiple of 16 * planes) and each workgroup writing its chunk as `planes` equal runs at
+ * the same offset in every plane, as a stitch work unit writes the three fp16 planes of
+ * its rows. planes == 1 is tg_probe_stream. Same arguments and returns otherwise. */
+int tg_probe_stream_planes(const void *src, int64_t read_bytes, void *dst, int64_t write_bytes,
+                           int32_t chunk, int32_t planes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

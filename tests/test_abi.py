@@ -255,7 +255,7 @@ def test_probe_library_exports_its_header():
     text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "tg_probe.h")).read(),
                   flags=re.S)
     names = sorted(set(re.findall(r"\b(tg_\w+)\s*\(", text)))
-    assert names == ["tg_probe_stream"]
+    assert names == ["tg_probe_stream", "tg_probe_stream_planes"]
     L = ctypes.CDLL(os.path.join(ROOT, "paper_2404_09267_amd", "libtg_probe.so"))
     f = L.tg_probe_stream
     f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
@@ -266,3 +266,9 @@ def test_probe_library_exports_its_header():
     assert f(ok, 4100, ok, 4096, 4096, None) == -1            # size not a multiple of 16
     assert f(ok, 4096, ok, 4096, 1000, None) == -1            # chunk not whole pages
     assert f(ctypes.c_void_p(4104), 4096, ok, 4096, 4096, None) == -1  # misaligned
+    g = L.tg_probe_stream_planes
+    g.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+    assert g(ok, 4096, ok, 4800, 4096, 0, None) == -1        # no planes
+    assert g(ok, 4096, ok, 4800, 4096, 5, None) == -1        # too many planes
+    assert g(ok, 4096, ok, 4816, 4096, 3, None) == -1        # planes of whole 16-byte words
