@@ -15,8 +15,8 @@
 //             the left (border columns), with global atomics on the label array. Every
 //             8-neighbour pair across a tile border is seen from the tile below or to the
 //             right of it.
-//  4. roots:  32768-pixel raster spans in ticket order (each thread's 128 mask bytes as
-//             eight 16-byte loads) find the foreground pixels still labelled
+//  4. roots:  65536-pixel raster spans in ticket order (each thread's 256 mask bytes as
+//             sixteen 16-byte loads) find the foreground pixels still labelled
 //             with their own index (the components), number them in raster order with a
 //             decoupled look-back, initialise each component's record and mark the root
 //             with its number.
@@ -41,8 +41,8 @@ constexpr int kTile = 32;
 constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
 constexpr int kTilesPerGroup = 16;  // tiles side by side per workgroup of local and boxes
 constexpr int kBorderThreads = 256;
-constexpr int kSpan = 32768;       // pixels per workgroup of the roots pass
-constexpr int kSpanThreads = 256;  // 128 pixels per thread: eight 16-byte loads
+constexpr int kSpan = 65536;       // pixels per workgroup of the roots pass
+constexpr int kSpanThreads = 256;  // 256 pixels per thread: sixteen 16-byte loads
 constexpr int kSpanPix = kSpan / kSpanThreads;
 constexpr int kSpanWords = kSpanPix / 32;  // foreground / root bit words per thread
 constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
@@ -89,9 +89,18 @@ Layout layout(void *base, int64_t n_px, int32_t max_components) {
 __device__ __forceinline__ int lds_load(int *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
+// Root of i's set, halving the path on the way: every link points to a smaller index of
+// the same set, so relinking i to its grandparent with an atomic min keeps the sets and
+// their roots and never undoes a concurrent link.
 __device__ __forceinline__ int lds_find(int *L, int i) {
-  for (int p = lds_load(&L[i]); p != i; p = lds_load(&L[i])) i = p;
-  return i;
+  for (;;) {
+    const int p = lds_load(&L[i]);
+    if (p == i) return i;
+    const int g = lds_load(&L[p]);
+    if (g == p) return p;
+    atomicMin(&L[i], g);
+    i = g;
+  }
 }
 // Joins the sets of a and b: the larger root is linked under the smaller with an atomic
 // min; if that root was relinked meanwhile, retry from what it now points to.
@@ -114,9 +123,15 @@ __device__ __forceinline__ void lds_unite(int *L, int a, int b) {
 __device__ __forceinline__ int g_load(const int32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ int g_find(int32_t *L, int i) {
-  for (int p = g_load(&L[i]); p != i; p = g_load(&L[i])) i = p;
-  return i;
+__device__ __forceinline__ int g_find(int32_t *L, int i) {  // as lds_find, in global memory
+  for (;;) {
+    const int p = g_load(&L[i]);
+    if (p == i) return i;
+    const int g = g_load(&L[p]);
+    if (g == p) return p;
+    __hip_atomic_fetch_min(&L[i], g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    i = g;
+  }
 }
 __device__ __forceinline__ void g_unite(int32_t *L, int a, int b) {
   for (;;) {
@@ -320,7 +335,7 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   const int64_t span = s_span;
   const int64_t p0 = span * kSpan + static_cast<int64_t>(tid) * kSpanPix;
 
-  // Which of this thread's 128 pixels are foreground (16-byte loads when the mask is
+  // Which of this thread's 256 pixels are foreground (16-byte loads when the mask is
   // 16-byte aligned and the bytes are inside it), then which of those are roots.
   uint32_t fgm[kSpanWords] = {};
   if (p0 < n_px) {
@@ -339,14 +354,35 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
         fgm[j >> 5] |= (p0 + j < n_px && mask[min(p0 + j, n_px - 1)]) ? 1u << (j & 31) : 0u;
     }
   }
+  // A foreground pixel is a root when its label is its own frame index. The 32 labels of a
+  // word with any foreground are read as eight 16-byte loads issued together (one round
+  // trip per word, not one per pixel); a word that would leave the label array, or frames
+  // of under 32 pixels, go pixel by pixel.
   uint32_t roots[kSpanWords] = {};
   int cnt = 0;
 #pragma unroll
   for (int w = 0; w < kSpanWords; ++w) {
-    for (uint32_t m = fgm[w]; m != 0; m &= m - 1) {
-      const int j = 32 * w + __builtin_ctz(m);
-      const int64_t P = p0 + j;
-      if (label[P] == static_cast<int32_t>(P % frame_px)) roots[w] |= 1u << (j & 31);
+    if (fgm[w] == 0) continue;
+    const int64_t P0 = p0 + 32 * w;
+    if (P0 + 32 <= n_px && frame_px >= 32) {
+      typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+      i32x4 lv[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) lv[q] = *reinterpret_cast<const i32x4 *>(label + P0 + 4 * q);
+      int64_t local = P0 % frame_px;
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        if (local == frame_px) local = 0;
+        if ((fgm[w] >> j & 1u) && lv[j >> 2][j & 3] == static_cast<int32_t>(local))
+          roots[w] |= 1u << j;
+        ++local;
+      }
+    } else {
+      for (uint32_t m = fgm[w]; m != 0; m &= m - 1) {
+        const int j = __builtin_ctz(m);
+        const int64_t P = P0 + j;
+        if (label[P] == static_cast<int32_t>(P % frame_px)) roots[w] |= 1u << j;
+      }
     }
     cnt += __popc(roots[w]);
   }
@@ -495,14 +531,18 @@ __global__ __launch_bounds__(kFilterThreads) void filter_kernel(
   __shared__ int s_blk, s_base;
   __shared__ int s_wave[kFilterThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The grid is sized for max_components; only the first max(1, ceil(n / kFilterBlock))
+  // workgroups take a ticket, so the ticket counter sees no more atomics than there are
+  // blocks of components (at least one workgroup runs, to write n_rois when n == 0).
+  const int n = min(*n_components, max_components);
+  const int need = n > 0 ? (n + kFilterBlock - 1) / kFilterBlock : 1;
+  if (static_cast<int>(blockIdx.x) >= need) return;
   if (tid == 0)
     s_blk = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words + 1), 1u,
                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
   __syncthreads();
-  const int blk = s_blk;
-  const int n = min(*n_components, max_components);
+  const int blk = s_blk;  // < need: exactly `need` workgroups take tickets
   const int start = blk * kFilterBlock;
-  if (start >= n && !(n == 0 && blk == 0)) return;  // uniform: later tickets lie further on
 
   constexpr int kPer = kFilterBlock / kFilterThreads;
   bool keep[kPer];
