@@ -250,6 +250,47 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask
   }
 }
 
+// Joins the foreground pixels of a 16-pixel run along a tile border (bits of `fg`) with
+// their foreground neighbours across it. Along the border the run covers coordinates
+// start .. start + 15 of [0, lim); pixel k is frame index own0 + k ostep, and the 18
+// pixels across the border at coordinates start - 1 .. start + 16 are nb0 + k' nstep.
+// Neighbour bytes and all labels are read first (addresses clamped into the frame), then
+// each pixel joins neighbours k, k + 1, k + 2 through their current labels (members of
+// their sets), skipping a pair equal to the one just joined: along a border most repeat.
+__device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint32_t fg, int own0,
+                                            int ostep, int nb0, int nstep, int start, int lim) {
+  if (fg == 0) return;
+  uint32_t m[18];
+  int32_t ln[18], lo[16];
+#pragma unroll
+  for (int k = 0; k < 18; ++k) {
+    const int c = min(max(start - 1 + k, 0), lim - 1);
+    const int idx = nb0 + (c - (start - 1)) * nstep;
+    m[k] = mf[idx];
+    ln[k] = g_load(&lf[idx]);
+  }
+#pragma unroll
+  for (int k = 0; k < 16; ++k) lo[k] = g_load(&lf[own0 + (min(start + k, lim - 1) - start) * ostep]);
+  uint32_t nb = 0;
+#pragma unroll
+  for (int k = 0; k < 18; ++k)
+    nb |= (m[k] != 0 && start - 1 + k >= 0 && start - 1 + k < lim) ? 1u << k : 0u;
+  int pa = -1, pb = -1;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    if (!(fg >> k & 1u)) continue;
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+      if (!(nb >> (k + d) & 1u)) continue;
+      const int a = lo[k], b = ln[k + d];
+      if (a == pa && b == pb) continue;
+      g_unite(lf, a, b);
+      pa = a;
+      pb = b;
+    }
+  }
+}
+
 // Thread i of frame blockIdx.y: 16 consecutive pixels of a border row (rows 32, 64, ...
 // below the first, each against the row above; one 16-byte load where the row is
 // 16-byte aligned), then 16 consecutive pixels of a border column (columns 32, 64, ...,
@@ -281,21 +322,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *ma
 #pragma unroll
       for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && x0 + k < W) ? 1u << k : 0u;
     }
-    // Join through the pixels' current labels (members of their sets), skipping a pair
-    // equal to the one just joined: along a border most pairs repeat.
-    int la = -1, lb = -1;
-    for (; fg != 0; fg &= fg - 1) {
-      const int x = x0 + __builtin_ctz(fg);
-      for (int dx = -1; dx <= 1; ++dx) {
-        const int nx = x + dx;
-        if (nx < 0 || nx >= W || !mf[(y - 1) * W + nx]) continue;
-        const int a = g_load(&lf[y * W + x]), b = g_load(&lf[(y - 1) * W + nx]);
-        if (a == la && b == lb) continue;
-        g_unite(lf, a, b);
-        la = a;
-        lb = b;
-      }
-    }
+    join_border(mf, lf, fg, y * W + x0, 1, (y - 1) * W + x0 - 1, 1, x0, W);
   } else {  // left columns of tiles against the columns to their left
     const int j = i - n_row, b = j / col_items, y0 = 16 * (j - b * col_items);
     const int x = (b + 1) * kTile;
@@ -304,19 +331,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *ma
     for (int k = 0; k < 16; ++k) v[k] = mf[min(y0 + k, H - 1) * W + x];
 #pragma unroll
     for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && y0 + k < H) ? 1u << k : 0u;
-    int la = -1, lb = -1;
-    for (; fg != 0; fg &= fg - 1) {
-      const int y = y0 + __builtin_ctz(fg);
-      for (int dy = -1; dy <= 1; ++dy) {
-        const int ny = y + dy;
-        if (ny < 0 || ny >= H || !mf[ny * W + x - 1]) continue;
-        const int a = g_load(&lf[y * W + x]), b = g_load(&lf[ny * W + x - 1]);
-        if (a == la && b == lb) continue;
-        g_unite(lf, a, b);
-        la = a;
-        lb = b;
-      }
-    }
+    join_border(mf, lf, fg, y0 * W + x, W, (y0 - 1) * W + x - 1, W, y0, H);
   }
 }
 
