@@ -235,3 +235,31 @@ def test_roi_source_end_to_end_full_size(torch):
     torch.cuda.synchronize()
     _, want_patches = opart.partition(want_rows.tolist(), want_fb.tolist(), w, h, 4, 4)
     np.testing.assert_array_equal(pb.patches_numpy(), np.array(want_patches, np.int32).reshape(-1, 5))
+
+
+def test_mask_rois_unaligned_mask_pointer(torch):
+    """A mask that starts one byte into its buffer: every pass takes its byte-wise reads
+    (the dword, 16-byte and span loads need aligned rows); several 65,536-pixel spans and
+    rows whose width is a multiple of 16, so only the pointer differs from the fast paths."""
+    rng = np.random.default_rng(21)
+    F, H, Wd = 3, 200, 160
+    mask = np.zeros((F, H, Wd), np.uint8)
+    for f in range(F):
+        for _ in range(25):
+            h, w = (int(v) for v in rng.integers(2, 70, 2))
+            y, x = int(rng.integers(0, H - h)), int(rng.integers(0, Wd - w))
+            mask[f, y:y + h, x:x + w] = 1
+    mask |= (rng.random(mask.shape) < 0.02).astype(np.uint8)
+    buf = torch.zeros(mask.size + 16, dtype=torch.uint8, device="cuda")
+    buf[1:1 + mask.size] = torch.from_numpy(mask.reshape(-1)).cuda()
+    view = buf[1:1 + mask.size]
+    assert view.data_ptr() % 4 == 1
+    say("mask_rois unaligned", mask.shape)
+    bufs = tg.MaskRoisBuffers(F, Wd, H, 1 << 16, 1 << 16)
+    tg.mask_rois(view, bufs, 2)
+    rows, areas, fb, n_rois, n_comp = bufs.result()
+    want_rows, want_areas, want_fb = oracle.mask_rois(mask, 2)
+    np.testing.assert_array_equal(rows, want_rows)
+    np.testing.assert_array_equal(areas, want_areas)
+    np.testing.assert_array_equal(fb, want_fb)
+    assert n_rois == len(want_rows) and n_comp == len(oracle.mask_rois(mask, 1)[0])
