@@ -506,7 +506,7 @@ size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t hei
  * and the order are this library's reading). RoIs are listed frame by frame, each
  * frame's in raster order of the component's first pixel, ready for tg_partition.
  * Enqueued on `stream`; allocates nothing. Returns TG_E_INVAL (null pointer,
- * non-positive sizes, more than 65535 frames or tile rows, width * height >= 2^31,
+ * non-positive sizes, more than 65535 frames or tile rows, width * height >= 2^30,
  * max_components < 1, max_rois < 0), TG_E_WORKSPACE, TG_E_HIP.
  */
 int tg_mask_rois(const tg_mask_rois_args *args, void *stream);

@@ -16,14 +16,13 @@
 //             8-neighbour pair across a tile border is seen from the tile below or to the
 //             right of it.
 //  4. roots:  65536-pixel raster spans in ticket order (each thread's 256 mask bytes as
-//             sixteen 16-byte loads) find the foreground pixels still labelled
-//             with their own index (the components), number them in raster order with a
-//             decoupled look-back, initialise each component's record and mark the root
-//             with its number.
-//  5. boxes:  per 16 tiles again, each tile's local components (relabelled in LDS) fold their
-//             pixels' extent and count in LDS; each local component then follows the
-//             label chain to its component number and folds its totals into the record
-//             with global atomics: one set of atomics per (tile, component).
+//             sixteen 16-byte loads) find the tile-local roots still their own parent
+//             (the components), number them in raster order with a decoupled look-back,
+//             initialise each component's record and mark the root with its number.
+//  5. boxes:  per 16 tiles again, each tile's local components, read off the labels the
+//             local pass left, fold their pixels' extent and count in LDS; each local
+//             component then follows the union-find to its component number and folds its
+//             totals into the record with global atomics: one set per (tile, component).
 //  6. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows.
 //  7. begin:  frame_begin by binary search over the kept rows' frames.
@@ -41,6 +40,13 @@ constexpr int kTile = 32;
 constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
 constexpr int kTilesPerGroup = 16;  // tiles side by side per workgroup of local and boxes
 constexpr int kBorderThreads = 256;
+// Labels: a foreground pixel's word holds its tile-local root (a frame index) once the
+// local pass is done, and never changes afterwards unless the pixel is a tile-local root.
+// A tile-local root's word holds kRootFlag | its parent in the union-find over roots
+// (itself at first), and becomes -(component + 1) once it is numbered. Frames have fewer
+// than 2^30 pixels, so the flag bit is free.
+constexpr int32_t kRootFlag = 1 << 30;
+constexpr int32_t kIndex = kRootFlag - 1;
 constexpr int kSpan = 65536;       // pixels per workgroup of the roots pass
 constexpr int kSpanThreads = 256;  // 256 pixels per thread: sixteen 16-byte loads
 constexpr int kSpanPix = kSpan / kSpanThreads;
@@ -123,13 +129,14 @@ __device__ __forceinline__ void lds_unite(int *L, int a, int b) {
 __device__ __forceinline__ int g_load(const int32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ int g_find(int32_t *L, int i) {  // as lds_find, in global memory
+// As lds_find, over the flagged words of tile-local roots in global memory.
+__device__ __forceinline__ int g_find(int32_t *L, int i) {
   for (;;) {
-    const int p = g_load(&L[i]);
+    const int p = g_load(&L[i]) & kIndex;
     if (p == i) return i;
-    const int g = g_load(&L[p]);
+    const int g = g_load(&L[p]) & kIndex;
     if (g == p) return p;
-    __hip_atomic_fetch_min(&L[i], g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_min(&L[i], g | kRootFlag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     i = g;
   }
 }
@@ -143,8 +150,8 @@ __device__ __forceinline__ void g_unite(int32_t *L, int a, int b) {
       a = b;
       b = t;
     }
-    const int old =
-        __hip_atomic_fetch_min(&L[b], a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int old = __hip_atomic_fetch_min(&L[b], a | kRootFlag, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT) & kIndex;
     if (old == b) return;
     b = old;
   }
@@ -243,9 +250,9 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (!(fg[q] >> k & 1u)) continue;
-      const int root = lds_find(L, r * kTile + c0 + k);
-      lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] =
-          (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
+      const int i = r * kTile + c0 + k, root = lds_find(L, i);
+      const int gr = (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
+      lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] = root == i ? gr | kRootFlag : gr;
     }
   }
 }
@@ -267,10 +274,11 @@ __device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint
     const int c = min(max(start - 1 + k, 0), lim - 1);
     const int idx = nb0 + (c - (start - 1)) * nstep;
     m[k] = mf[idx];
-    ln[k] = g_load(&lf[idx]);
+    ln[k] = g_load(&lf[idx]) & kIndex;
   }
 #pragma unroll
-  for (int k = 0; k < 16; ++k) lo[k] = g_load(&lf[own0 + (min(start + k, lim - 1) - start) * ostep]);
+  for (int k = 0; k < 16; ++k)
+    lo[k] = g_load(&lf[own0 + (min(start + k, lim - 1) - start) * ostep]) & kIndex;
   uint32_t nb = 0;
 #pragma unroll
   for (int k = 0; k < 18; ++k)
@@ -369,7 +377,8 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
         fgm[j >> 5] |= (p0 + j < n_px && mask[min(p0 + j, n_px - 1)]) ? 1u << (j & 31) : 0u;
     }
   }
-  // A foreground pixel is a root when its label is its own frame index. The 32 labels of a
+  // A foreground pixel is a root when its label is its own frame index, flagged (a
+  // tile-local root still its own parent). The 32 labels of a
   // word with any foreground are read as eight 16-byte loads issued together (one round
   // trip per word, not one per pixel); a word that would leave the label array, or frames
   // of under 32 pixels, go pixel by pixel.
@@ -388,7 +397,7 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
 #pragma unroll
       for (int j = 0; j < 32; ++j) {
         if (local == frame_px) local = 0;
-        if ((fgm[w] >> j & 1u) && lv[j >> 2][j & 3] == static_cast<int32_t>(local))
+        if ((fgm[w] >> j & 1u) && lv[j >> 2][j & 3] == (static_cast<int32_t>(local) | kRootFlag))
           roots[w] |= 1u << j;
         ++local;
       }
@@ -396,7 +405,7 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
       for (uint32_t m = fgm[w]; m != 0; m &= m - 1) {
         const int j = __builtin_ctz(m);
         const int64_t P = P0 + j;
-        if (label[P] == static_cast<int32_t>(P % frame_px)) roots[w] |= 1u << j;
+        if (label[P] == (static_cast<int32_t>(P % frame_px) | kRootFlag)) roots[w] |= 1u << j;
       }
     }
     cnt += __popc(roots[w]);
@@ -457,7 +466,6 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
                                                              int64_t frame_px,
                                                              const int32_t *label,
                                                              Comp *comp) {
-  __shared__ int L[kTile * kTile];
   __shared__ int bx0[kTile * kTile], by0[kTile * kTile], bx1[kTile * kTile],
       by1[kTile * kTile], bn[kTile * kTile];
   const int64_t f = blockIdx.z;
@@ -471,16 +479,40 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
   if (!__syncthreads_or(any != 0)) return;
   const int32_t *lf = label + f * frame_px;
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
+  const int32_t *row = lf + static_cast<int64_t>(min(y, H - 1)) * W;
   for (int q = 0; q < kTilesPerGroup; ++q) {
     const int tx0 = (blockIdx.x * kTilesPerGroup + q) * kTile;
-    if (!label_tile(fgw[q], L)) continue;
+    // (also the barrier between this tile's use of the LDS sums and the previous one's)
+    if (!__syncthreads_or(fgw[q] != 0)) continue;
+    // The tile-local components come from the labels the local pass left: a foreground
+    // pixel's word is its local root, unless the pixel is a local root itself (flagged or
+    // already numbered).
+    int32_t lv[4];
+    if (kWord) {
+      typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+      const i32x4 v = *reinterpret_cast<const i32x4 *>(row + min(tx0 + c0, W - 4));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) lv[k] = v[k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) lv[k] = row[min(tx0 + c0 + k, W - 1)];
+    }
     bool fg[4];
     int root[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int i = r * kTile + c0 + k;
       fg[k] = fgw[q] >> k & 1u;
-      root[k] = fg[k] ? lds_find(L, i) : -1;
+      root[k] = -1;
+      if (fg[k]) {
+        const int v = lv[k];
+        if (v < 0 || (v & kRootFlag)) {
+          root[k] = i;
+        } else {
+          const int vy = v / W;
+          root[k] = (vy - ty0) * kTile + (v - vy * W - tx0);
+        }
+      }
       if (root[k] == i) {
         bx0[i] = INT_MAX;
         by0[i] = INT_MAX;
@@ -522,10 +554,13 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
     for (int k = 0; k < 4; ++k) {
       const int i = r * kTile + c0 + k;
       if (root[k] != i) continue;
+      // up the union-find over local roots to the numbered root
       int cur = y * W + tx0 + c0 + k;
-      int v = lf[cur];
-      while (v >= 0 && v != cur) {
-        cur = v;
+      int v = lv[k];
+      while (v >= 0) {
+        const int nx = v & kIndex;
+        if (nx == cur) break;
+        cur = nx;
         v = lf[cur];
       }
       if (v >= 0) continue;  // a component past max_components: not measured
@@ -627,7 +662,7 @@ __global__ void empty_kernel(int32_t *n_rois, int32_t *n_components, int32_t *fr
 bool sizes_ok(int32_t n_frames, int32_t width, int32_t height, int32_t max_components) {
   if (n_frames < 0 || n_frames > 65535 || width < 1 || height < 1 || max_components < 1)
     return false;
-  if (int64_t(width) * height >= (int64_t(1) << 31)) return false;
+  if (int64_t(width) * height >= (int64_t(1) << 30)) return false;  // the label flag bit
   if ((int64_t(height) + kTile - 1) / kTile > 65535) return false;
   return true;
 }
