@@ -223,6 +223,8 @@ def test_gmm_and_mask_rois_validation_without_gpu():
     assert L.tg_mask_rois_workspace_bytes(1, 8, 8, 0) == 0
     assert L.tg_mask_rois_workspace_bytes(70000, 8, 8, 4) == 0
     assert L.tg_mask_rois_workspace_bytes(1, 1 << 16, 1 << 15, 4) == 0
+    assert L.tg_mask_rois_workspace_bytes(1, 1 << 15, 1 << 15, 4) == 0  # 2^30 pixels: no flag bit
+    assert L.tg_mask_rois_workspace_bytes(1, 1 << 15, (1 << 15) - 1, 4) > 0
     ws = L.tg_mask_rois_workspace_bytes(2, 100, 50, 1000)
     assert ws >= 4 * 2 * 100 * 50 + 32 * 1000 + 4 * 1000 and ws % 256 == 0
     m = tg.MaskRoisArgs()
