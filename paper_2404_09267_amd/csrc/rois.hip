@@ -6,7 +6,7 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order), in seven launches on the caller's stream:
 //  1. clear:  zeroes the tickets and look-back words of launches 4 and 6.
-//  2. local:  one 256-thread workgroup per 16 32x32 tiles side by side (their mask
+//  2. local:  one 256-thread workgroup per four 32x32 tiles side by side (their mask
 //             words loaded together up front; a group without foreground leaves at once)
 //             labels each tile in LDS and writes, for each foreground pixel, the frame
 //             index of its tile-local root.
@@ -19,7 +19,7 @@
 //             sixteen 16-byte loads) find the tile-local roots still their own parent
 //             (the components), number them in raster order with a decoupled look-back,
 //             initialise each component's record and mark the root with its number.
-//  5. boxes:  per 16 tiles again, each tile's local components, read off the labels the
+//  5. boxes:  per four tiles again, each tile's local components, read off the labels the
 //             local pass left, fold their pixels' extent and count in LDS; each local
 //             component then follows the union-find to its component number and folds its
 //             totals into the record with global atomics: one set per (tile, component).
@@ -38,7 +38,7 @@ namespace {
 
 constexpr int kTile = 32;
 constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
-constexpr int kTilesPerGroup = 16;  // tiles side by side per workgroup of local and boxes
+constexpr int kTilesPerGroup = 4;  // tiles side by side per workgroup of local and boxes
 constexpr int kBorderThreads = 256;
 // Labels: a foreground pixel's word holds its tile-local root (a frame index) once the
 // local pass is done, and never changes afterwards unless the pixel is a tile-local root.
