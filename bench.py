@@ -2,8 +2,8 @@
 """Throughput of the patch-stitching path on one MI355X.
 
 One step = one pass of the whole path over one batch of synthetic input:
-  tg_plan_pack and tg_stitch_schedule (host C++) -> plan and unit orders uploaded
-  to HBM -> tg_stitch once per batch of canvases -> tg_unstitch of every detector box.
+  tg_plan_pack (host C++) -> plan uploaded to HBM -> tg_stitch once per batch of
+  canvases -> tg_unstitch of every detector box.
 Frames, the RoI table and the boxes are resident in HBM before timing starts. The
 host plan of step s+1 overlaps the GPU work of step s (double-buffered pinned
 staging), as a serving loop would run it.
@@ -44,9 +44,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="cam20_4k")
     ap.add_argument("--policy", type=int, default=0, help="0 shelf FFDH, 1 shelf arrival, 2 guillotine")
-    ap.add_argument("--unit-order", choices=["heavy", "natural"], default="heavy",
-                    help="tg_stitch launch order: heaviest units first (tg_stitch_schedule) "
-                         "or canvas order")
+    ap.add_argument("--unit-order", choices=["natural", "xcd"], default="natural",
+                    help="tg_stitch launch order: units in address order (the default), or "
+                         "each of the 8 XCDs sweeping its own contiguous eighth of the batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum wall time of the oracle's CPU sample")
@@ -79,6 +79,16 @@ def calib_copy(mb: int, steps: int):
     us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(steps)) * 1e3 / steps
     print(json.dumps({"calib_copy_bytes": n, "launches": steps + 2, "avg_copy_us": round(us, 2),
                       "read_plus_write_gbs": round(2 * n / us / 1e3, 1)}), flush=True)
+
+
+def xcd_order(n: int) -> np.ndarray:
+    """A launch order of n stitch units in which XCD x (the workgroups b with b % 8 == x,
+    dealt round-robin by the dispatcher) runs one contiguous block of units in address
+    order, instead of every eighth unit of the whole batch."""
+    slots = [(n - x + 7) // 8 for x in range(8)]
+    start = np.concatenate([[0], np.cumsum(slots)])
+    b = np.arange(n)
+    return (start[b % 8] + b // 8).astype(np.int32)
 
 
 def stitch_bytes(rois, plan, first, count, canvas) -> int:
@@ -459,12 +469,8 @@ def main():
     ubufs = tg.UnstitchBuffers(n_boxes)
     batches = [tg.batch_range(J, wl.batch_cap, k) for k in range(tg.batch_count(J, wl.batch_cap))]
 
-    # device plan arrays and per-batch unit orders, refreshed every step from
-    # double-buffered pinned staging
-    scheduled = args.unit_order == "heavy"
-    n_units = [tg.stitch_units(wl.canvas, wl.canvas, c) if scheduled else 0 for _, c in batches]
-    unit_off = np.concatenate([[0], np.cumsum(n_units)]).astype(np.int64) + 5 * n_rois + 1
-    words = int(unit_off[-1])
+    # device plan arrays, refreshed every step from double-buffered pinned staging
+    words = 5 * n_rois + 1
     staging = [torch.empty(words, dtype=torch.int32, pin_memory=True) for _ in range(2)]
     staging_np = [s.numpy() for s in staging]
     plan_d = torch.zeros(words, dtype=torch.int32, device=dev)
@@ -475,11 +481,12 @@ def main():
     J_buf = np.zeros(1, np.int32)
     bad_buf = np.zeros(1, np.int32)
     params = tg.PackParams(wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, args.policy)
+    unit_orders = [torch.from_numpy(xcd_order(tg.stitch_units(wl.canvas, wl.canvas, c))).to(dev)
+                   if args.unit_order == "xcd" else None for _, c in batches]
     # argument blocks are built once: no pointer changes between steps
     stitch_args = [tg.stitch_args(frames_d, dplan, first, count, wl.canvas, wl.canvas,
                                   W.MEAN, W.STD, W.PAD, out[first:first + count],
-                                  unit_order=plan_d[unit_off[k]:unit_off[k + 1]]
-                                  if scheduled else None)
+                                  unit_order=unit_orders[k])
                    for k, (first, count) in enumerate(batches)]
     uargs = tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
     stitch_events = []
@@ -498,14 +505,6 @@ def main():
                                    J_buf.ctypes.data, bad_buf.ctypes.data)
         if rc != tg.OK or J_buf[0] != J:
             raise tg.TgError("tg_plan_pack", rc)
-        if scheduled:
-            for k, (first, count) in enumerate(batches):
-                rc = tg.lib().tg_stitch_schedule(
-                    rois.ctypes.data, place.ctypes.data, order.ctypes.data, cbeg.ctypes.data,
-                    n_rois, J, first, count, wl.canvas, wl.canvas,
-                    st[unit_off[k]:].ctypes.data)
-                if rc != tg.OK:
-                    raise tg.TgError("tg_stitch_schedule", rc)
         plan_d.copy_(staging[buf], non_blocking=True)
         # One timing event before each tg_stitch launch and one after the last: launch k
         # runs between events k and k + 1. The first also marks the staging upload as done.
@@ -530,11 +529,6 @@ def main():
     # sanity: the plan the steps recompute equals the one the buffers were sized for
     chk = plan_d.cpu().numpy()
     assert np.array_equal(chk[: 3 * n_rois].reshape(n_rois, 3), plan0.place)
-    for k, (first, count) in enumerate(batches):
-        if scheduled:
-            assert np.array_equal(chk[unit_off[k]:unit_off[k + 1]],
-                                  tg.stitch_schedule(rois, plan0, first, count, wl.canvas,
-                                                     wl.canvas))
     timing["on"] = True
     torch.cuda.synchronize()
     t0 = time.perf_counter()

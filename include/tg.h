@@ -262,11 +262,11 @@ typedef struct {
    * canvas_first + c. Every element is written exactly once. */
   uint16_t *out;
   /* Optional launch order of the work units, device, int32
-   * [tg_stitch_units(canvas_w, canvas_h, canvas_count)]: a permutation of the unit ids,
-   * normally from tg_stitch_schedule for the same plan and canvas range. NULL runs the
-   * units in id order. The order changes only speed, never the output -- provided it
-   * is a permutation: an id missing from it leaves that unit's canvas region unwritten,
-   * a repeated id writes it twice (same values), ids outside the range are ignored. */
+   * [tg_stitch_units(canvas_w, canvas_h, canvas_count)]: workgroup b runs unit
+   * unit_order[b]. NULL runs the units in id order, which is address order and the
+   * fastest. The order changes only speed, never the output -- provided it is a
+   * permutation: an id missing from it leaves that unit's pixels unwritten, a repeated
+   * id writes them twice (same values), ids outside the range are ignored. */
   const int32_t *unit_order;
 } tg_stitch_args;
 
@@ -299,34 +299,16 @@ int tg_stitch(const tg_stitch_args *args, void *stream);
 int32_t tg_stitch_norm_uses_table(const float mean[3], const float std[3]);
 
 /*
- * Work units of one tg_stitch launch (host only). A canvas is cut into tiles of at most
- * 1280 columns and each tile into bands of rows; one unit = one band of one tile of one
- * canvas, run by one workgroup. Unit k is canvas canvas_first + k / (bands * tiles),
- * band (k / tiles) % bands, tile k % tiles.
+ * Work units of one tg_stitch launch (host only). Each canvas plane is cut, in raster
+ * order, into runs of 2048 pixels (the last run of a canvas may be shorter); one unit =
+ * one run of one canvas, written in all three planes by one workgroup. Unit k is run
+ * k % runs of canvas canvas_first + k / runs, with runs = ceil(canvas_w * canvas_h / 2048),
+ * i.e. canvas pixels [2048 r, min(2048 (r + 1), canvas_w * canvas_h)).
  * Returns the number of units for canvas_count canvases of canvas_w x canvas_h (0 when
- * canvas_count == 0), or TG_E_INVAL for non-positive sizes or a negative count.
+ * canvas_count == 0), or TG_E_INVAL for non-positive sizes, a negative count, or more
+ * than 2^31 - 1 units.
  */
 int32_t tg_stitch_units(int32_t canvas_w, int32_t canvas_h, int32_t canvas_count);
-
-/*
- * A launch order for tg_stitch's units (host only): heaviest first, weight = canvas
- * pixels of the unit that patches cover (ties keep unit order). Run last, the lightest
- * units fill the tail of the launch, which otherwise waits on a few heavy ones.
- *
- * In: the plan as tg_plan_pack wrote it (host arrays; n_rois RoIs, n_canvases
- * canvases), the canvas range and canvas size of the tg_stitch call.
- * Out: unit_order[tg_stitch_units(canvas_w, canvas_h, canvas_count)] (host), a
- * permutation of the unit ids; upload it and pass it as tg_stitch_args.unit_order.
- * Plan entries that tg_stitch would skip (ids out of range, a place on another canvas,
- * rectangles outside the canvas) add no weight.
- * Returns TG_E_INVAL for null pointers or bad sizes, TG_E_RANGE when the canvas range
- * leaves [0, n_canvases), TG_E_INTERNAL on host allocation failure; canvas_count == 0
- * writes nothing and returns TG_OK.
- */
-int tg_stitch_schedule(const tg_roi *rois, const tg_place *place, const int32_t *order,
-                       const int32_t *canvas_begin, int32_t n_rois, int32_t n_canvases,
-                       int32_t canvas_first, int32_t canvas_count, int32_t canvas_w,
-                       int32_t canvas_h, int32_t *unit_order);
 
 typedef struct {
   const tg_box *boxes;        /* device [n_boxes] */

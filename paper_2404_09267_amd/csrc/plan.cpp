@@ -139,94 +139,4 @@ extern "C" int32_t tg_stitch_units(int32_t canvas_w, int32_t canvas_h, int32_t c
   return g.n_units;
 }
 
-extern "C" int tg_stitch_schedule(const tg_roi *rois, const tg_place *place,
-                                  const int32_t *order, const int32_t *canvas_begin,
-                                  int32_t n_rois, int32_t n_canvases, int32_t canvas_first,
-                                  int32_t canvas_count, int32_t canvas_w, int32_t canvas_h,
-                                  int32_t *unit_order) {
-  if (n_rois < 0 || n_canvases < 0 || canvas_first < 0 || canvas_count < 0 || canvas_w < 1 ||
-      canvas_h < 1)
-    return TG_E_INVAL;
-  if (int64_t(canvas_first) + canvas_count > n_canvases) return TG_E_RANGE;
-  if (canvas_count == 0) return TG_OK;
-  if (!canvas_begin || !unit_order || (n_rois > 0 && (!rois || !place || !order)))
-    return TG_E_INVAL;
-  tg_detail::StitchGeometry g;
-  if (!tg_detail::stitch_geometry(canvas_w, canvas_h, canvas_count, &g)) return TG_E_INVAL;
-  try {
-    const int64_t band_rows = int64_t(g.band_steps) * tg_detail::kStitchStepRows;
-    const int64_t tile_w = tg_detail::kStitchTileW;
-    const int64_t per_canvas = int64_t(g.bands_y) * g.tiles_x;
-    // weight: pixels of a patch's first and last band, added directly; full[]: a
-    // difference array over bands (per tile) for the full bands in between.
-    std::vector<int64_t> weight(static_cast<size_t>(g.n_units), 0);
-    std::vector<int64_t> full(static_cast<size_t>(per_canvas + g.tiles_x), 0);
-    for (int32_t c = 0; c < canvas_count; ++c) {
-      std::fill(full.begin(), full.end(), 0);
-      int64_t *wc = weight.data() + static_cast<size_t>(int64_t(c) * per_canvas);
-      const int32_t j = canvas_first + c;
-      const int64_t lo = std::clamp<int64_t>(canvas_begin[j], 0, n_rois);
-      const int64_t hi = std::clamp<int64_t>(canvas_begin[j + 1], lo, n_rois);
-      for (int64_t k = lo; k < hi; ++k) {
-        const int32_t id = order[k];
-        if (id < 0 || id >= n_rois) continue;
-        const tg_roi &r = rois[id];
-        const tg_place &pl = place[id];
-        if (pl.canvas != j || r.w < 1 || r.h < 1 || pl.x < 0 || pl.y < 0 ||
-            int64_t(pl.x) + r.w > canvas_w || int64_t(pl.y) + r.h > canvas_h)
-          continue;
-        const int64_t y0 = pl.y, y1 = int64_t(pl.y) + r.h;
-        const int64_t b0 = y0 / band_rows, b1 = (y1 - 1) / band_rows;
-        for (int64_t tx = pl.x / tile_w; tx * tile_w < int64_t(pl.x) + r.w; ++tx) {
-          const int64_t cols = std::min<int64_t>(pl.x + r.w, (tx + 1) * tile_w) -
-                               std::max<int64_t>(pl.x, tx * tile_w);
-          if (b0 == b1) {
-            wc[b0 * g.tiles_x + tx] += cols * (y1 - y0);
-            continue;
-          }
-          wc[b0 * g.tiles_x + tx] += cols * ((b0 + 1) * band_rows - y0);
-          wc[b1 * g.tiles_x + tx] += cols * (y1 - b1 * band_rows);
-          full[(b0 + 1) * g.tiles_x + tx] += cols * band_rows;
-          full[b1 * g.tiles_x + tx] -= cols * band_rows;
-        }
-      }
-      for (int32_t tx = 0; tx < g.tiles_x; ++tx) {
-        int64_t run = 0;
-        for (int64_t b = 0; b < g.bands_y; ++b) {
-          run += full[b * g.tiles_x + tx];
-          wc[b * g.tiles_x + tx] += run;
-        }
-      }
-    }
-    // Heaviest first, ties in unit order: a stable counting sort on key (max - weight).
-    // A unit's weight is at most its area, below 2^22 (band rows <= 3072, tile columns <=
-    // 1280); keys below 2^16 take one pass over max + 1 buckets, larger ones an LSD radix
-    // sort of 11 bits per pass.
-    int64_t wmax = 0;
-    for (int64_t v : weight) wmax = std::max(wmax, v);
-    const size_t n = static_cast<size_t>(g.n_units);
-    if (wmax < (int64_t(1) << 16)) {
-      std::vector<int32_t> count(static_cast<size_t>(wmax) + 2, 0);
-      for (size_t u = 0; u < n; ++u) ++count[static_cast<size_t>(wmax - weight[u]) + 1];
-      for (int64_t b = 0; b < wmax; ++b) count[b + 1] += count[b];
-      for (size_t u = 0; u < n; ++u)
-        unit_order[count[static_cast<size_t>(wmax - weight[u])]++] = static_cast<int32_t>(u);
-      return TG_OK;
-    }
-    std::vector<int32_t> ids(n), tmp(n);
-    std::iota(ids.begin(), ids.end(), 0);
-    for (int shift = 0; (wmax >> shift) > 0; shift += 11) {
-      size_t count[2049] = {};
-      for (int32_t u : ids) ++count[((wmax - weight[static_cast<size_t>(u)]) >> shift & 2047) + 1];
-      for (int b = 0; b < 2048; ++b) count[b + 1] += count[b];
-      for (int32_t u : ids) tmp[count[(wmax - weight[static_cast<size_t>(u)]) >> shift & 2047]++] = u;
-      ids.swap(tmp);
-    }
-    std::copy(ids.begin(), ids.end(), unit_order);
-    return TG_OK;
-  } catch (...) {
-    return TG_E_INTERNAL;
-  }
-}
-
-extern "C" int32_t tg_abi_version(void) { return 5; }
+extern "C" int32_t tg_abi_version(void) { return 6; }

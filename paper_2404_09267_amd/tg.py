@@ -97,7 +97,7 @@ GMM_MAX_MIX = 5
 EXPORTS = ["tg_gmm_plane_stride", "tg_gmm_state_bytes", "tg_gmm_update",
            "tg_mask_rois_workspace_bytes", "tg_mask_rois", "tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
            "tg_batch_range", "tg_slo_replay", "tg_stitch",
-           "tg_stitch_units", "tg_stitch_schedule", "tg_stitch_norm_uses_table",
+           "tg_stitch_units", "tg_stitch_norm_uses_table",
            "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_merge_workspace_bytes", "tg_merge",
            "tg_strerror", "tg_abi_version"]
 
@@ -140,9 +140,6 @@ def lib() -> ctypes.CDLL:
         L.tg_stitch_norm_uses_table.restype = _i32
         L.tg_stitch_units.argtypes = [_i32, _i32, _i32]
         L.tg_stitch_units.restype = _i32
-        L.tg_stitch_schedule.argtypes = [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32,
-                                         _vp]
-        L.tg_stitch_schedule.restype = ctypes.c_int
         L.tg_unstitch_workspace_bytes.argtypes = [_i32]
         L.tg_unstitch_workspace_bytes.restype = ctypes.c_size_t
         L.tg_unstitch.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
@@ -338,26 +335,6 @@ def stitch_units(canvas_w: int, canvas_h: int, canvas_count: int) -> int:
     return n
 
 
-def stitch_schedule(rois: np.ndarray, plan: Plan, canvas_first: int, canvas_count: int,
-                    canvas_w: int, canvas_h: int, out: np.ndarray | None = None) -> np.ndarray:
-    """Host: heaviest-first launch order of the units of one tg_stitch call (int32)."""
-    r = np.ascontiguousarray(rois, dtype=np.int32).reshape(-1, 5)
-    place = np.ascontiguousarray(plan.place, dtype=np.int32)
-    order = np.ascontiguousarray(plan.order, dtype=np.int32)
-    cbeg = np.ascontiguousarray(plan.canvas_begin, dtype=np.int32)
-    n_units = stitch_units(canvas_w, canvas_h, canvas_count)
-    if out is None:
-        out = np.empty(n_units, dtype=np.int32)
-    if out.dtype != np.int32 or not out.flags.c_contiguous or out.size < n_units:
-        raise ValueError(f"unit order buffer must be contiguous int32 with >= {n_units} entries")
-    rc = lib().tg_stitch_schedule(_np_ptr(r), _np_ptr(place), _np_ptr(order), _np_ptr(cbeg),
-                                  r.shape[0], plan.n_canvases, canvas_first, canvas_count,
-                                  canvas_w, canvas_h, _np_ptr(out))
-    if rc != OK:
-        raise TgError("tg_stitch_schedule", rc)
-    return out[:n_units]
-
-
 def stitch_args(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w, canvas_h,
                 mean, std, pad, out, unit_order=None) -> StitchArgs:
     import torch
@@ -397,7 +374,7 @@ def stitch_args(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w,
 def stitch(frames, dplan: DevicePlan, canvas_first, canvas_count, canvas_w, canvas_h,
            mean, std, pad, out, stream=None, unit_order=None) -> None:
     """Enqueue tg_stitch for canvases [canvas_first, +canvas_count) into `out`
-    (`unit_order`: optional device int32 launch order from stitch_schedule)."""
+    (`unit_order`: optional device int32 launch order of the units)."""
     a = stitch_args(frames, dplan, canvas_first, canvas_count, canvas_w, canvas_h,
                     mean, std, pad, out, unit_order)
     rc = lib().tg_stitch(ctypes.byref(a), _stream_handle(stream))

@@ -1,32 +1,36 @@
-"""tg_stitch's unit geometry restated from its definition (test infrastructure): tiles of
-at most 1280 columns, bands of whole 3-row steps, about 6144 units per launch, at most
-1024 steps per band."""
+"""tg_stitch's unit geometry restated from its definition (test infrastructure): each
+canvas plane cut in raster order into runs of 2048 pixels, one unit per run."""
 import math
 
-TILE_W, STEP_ROWS, UNIT_TARGET, MAX_STEPS = 1280, 3, 6144, 1024
+RUN = 2048
 
 
 def geometry(cw, ch, count):
-    """(tiles across, rows per band, bands down, units) of a launch over `count`
-    canvases of cw x ch."""
-    tiles = math.ceil(cw / TILE_W)
-    steps = math.ceil(ch / STEP_ROWS)
-    band_steps = min(max(math.ceil(steps * tiles * count / UNIT_TARGET), 1), MAX_STEPS)
-    bands = math.ceil(steps / band_steps)
-    return tiles, band_steps * STEP_ROWS, bands, bands * tiles * count
+    """(runs per canvas, units) of a launch over `count` canvases of cw x ch."""
+    runs = math.ceil(cw * ch / RUN)
+    return runs, runs * count
+
+
+def unit_pixels(cw, ch, count, u):
+    """Canvas (local index) and the raster pixel range [p0, p1) of unit u."""
+    runs, _ = geometry(cw, ch, count)
+    c, r = divmod(u, runs)
+    return c, r * RUN, min((r + 1) * RUN, cw * ch)
 
 
 def records_per_unit(rois, plan, first, count, cw, ch):
-    """Patches of each unit of a launch: those whose placed rectangle meets the unit's
-    band of rows and tile of columns."""
-    tiles, band_rows, bands, n_units = geometry(cw, ch, count)
+    """Patches of each unit of a launch: those with at least one pixel in the unit's run."""
+    runs, n_units = geometry(cw, ch, count)
     rec = [0] * n_units
     for c in range(count):
         j = first + c
         for i in plan.order[plan.canvas_begin[j]:plan.canvas_begin[j + 1]]:
             _, x, y = (int(v) for v in plan.place[i])
             w, h = int(rois[i, 3]), int(rois[i, 4])
-            for b in range(y // band_rows, (y + h - 1) // band_rows + 1):
-                for t in range(x // TILE_W, (x + w - 1) // TILE_W + 1):
-                    rec[(c * bands + b) * tiles + t] += 1
+            hit = set()
+            for yy in range(y, y + h):
+                a, b = yy * cw + x, yy * cw + x + w - 1
+                hit.update(range(a // RUN, b // RUN + 1))
+            for r in hit:
+                rec[c * runs + r] += 1
     return rec

@@ -6,7 +6,7 @@ import pytest
 import oracle
 from gpu_helpers import (SENTINEL, assert_stitch_parity, coverage, oracle_plan, run_stitch,
                          say)
-from stitch_geometry import geometry, records_per_unit
+from stitch_geometry import records_per_unit, unit_pixels
 from paper_2404_09267_amd import tg
 from paper_2404_09267_amd import workload as W
 
@@ -56,23 +56,23 @@ def test_odd_frame_widths_and_mean_std(torch):
               std=(0.01, 1000.0, 3.5), pad=(255, 0, 7))
 
 
-def test_many_patches_per_band_take_the_slow_path(torch):
-    """More than 192 patches meeting one unit (the fast path's list size) and exactly 192:
-    tiny RoIs, including 1 x 1."""
+def test_many_patches_per_run_take_further_lists(torch):
+    """More than 128 patches meeting one run (the size of one list; the rest take further
+    lists) and exactly 128 and 129: tiny RoIs, including 1 x 1."""
     rng = np.random.default_rng(5)
-    # expect: the exact maximum of patches per unit, or ">" (over 192), or "<=" (192 or fewer)
+    # expect: the exact maximum of patches per unit, or ">" (over 128), or "<=" (128 or fewer)
     for cw, ch, n, lo, hi, pol, expect in [
-            (256, 3, 193, 1, 1, 1, 193), (256, 3, 192, 1, 1, 1, 192),
+            (256, 3, 129, 1, 1, 1, 129), (256, 3, 128, 1, 1, 1, 128),
             (256, 32, 8192, 1, 1, 1, ">"), (256, 32, 3000, 1, 4, 2, ">"),
-            (64, 64, 1500, 1, 3, 0, "<="), (300, 64, 600, 1, 2, 1, ">"),
-            (1300, 6, 900, 1, 2, 0, ">")]:
+            (64, 64, 200, 2, 6, 0, "<="), (300, 64, 600, 1, 2, 1, ">"),
+            (1300, 6, 900, 1, 2, 0, ">"), (3000, 5, 700, 1, 3, 2, ">")]:
         say("dense", cw, ch, n, lo, hi, pol)
         plan, rois = _case(torch, rng, 2, 50, 60, cw, ch, n, lo, hi, hi, pol, with_rois=True)
         most = max(records_per_unit(rois, plan, 0, plan.n_canvases, cw, ch))
         if expect == ">":
-            assert most > 192
+            assert most > 128
         elif expect == "<=":
-            assert most <= 192
+            assert most <= 128
         else:
             assert most == expect
 
@@ -198,16 +198,16 @@ def test_deterministic(torch):
     np.testing.assert_array_equal(a, b)
 
 
-@pytest.mark.parametrize("name,policy,scheduled", [("cam1_1080p", 0, True), ("cam5_4k", 0, True),
-                                                   ("cam20_4k", 0, True), ("cam20_4k", 0, False),
-                                                   ("cam20_4k", 2, True),
-                                                   ("small_roi_8cam", 0, True),
-                                                   ("small_roi_8cam", 1, False)])
-def test_workload_full_parity(torch, name, policy, scheduled):
-    """Whole workloads, batch by batch as the bench launches them (with the host's
-    heaviest-first unit order, or units in id order), against the oracle."""
+@pytest.mark.parametrize("name,policy,order", [("cam1_1080p", 0, None), ("cam5_4k", 0, None),
+                                               ("cam20_4k", 0, None), ("cam20_4k", 0, "reverse"),
+                                               ("cam20_4k", 2, None),
+                                               ("small_roi_8cam", 0, None),
+                                               ("small_roi_8cam", 1, "reverse")])
+def test_workload_full_parity(torch, name, policy, order):
+    """Whole workloads, batch by batch as the bench launches them (units in address
+    order, or in reverse through the unit-order argument), against the oracle."""
     wl = W.WORKLOADS[name]
-    say("workload", name, "policy", policy, "scheduled", scheduled)
+    say("workload", name, "policy", policy, "order", order)
     rois = W.make_rois(wl)
     frames_d = W.make_frames(wl, "cuda")
     plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, policy)
@@ -217,9 +217,9 @@ def test_workload_full_parity(torch, name, policy, scheduled):
         first, count = tg.batch_range(plan.n_canvases, wl.batch_cap, k)
         say("  batch", k, first, count)
         unit_order = None
-        if scheduled:
-            unit_order = torch.from_numpy(
-                tg.stitch_schedule(rois, plan, first, count, wl.canvas, wl.canvas)).cuda()
+        if order == "reverse":
+            n_units = tg.stitch_units(wl.canvas, wl.canvas, count)
+            unit_order = torch.arange(n_units - 1, -1, -1, dtype=torch.int32, device="cuda")
         got = run_stitch(frames_d, rois, plan, first, count, wl.canvas, wl.canvas, dplan=dplan,
                          unit_order=unit_order)
         want = oracle.stitch(frames, rois, oracle_plan(plan), first, count, wl.canvas,
@@ -317,18 +317,15 @@ def test_unit_order_that_is_not_a_permutation(torch):
     torch.cuda.synchronize()
     got = out.cpu().numpy().view(np.uint16)
     assert np.all(buf[count * 3 * ch * cw:].cpu().numpy().view(np.uint16) == SENTINEL)
-    tiles, band_rows, bands, _ = geometry(cw, ch, count)
-    assert tiles == 1
-    written = np.zeros((count, ch), bool)
+    written = np.zeros((count, ch * cw), bool)
     for u in (0, n_units - 1):
-        c, b = divmod(u, bands)
-        written[c, b * band_rows:(b + 1) * band_rows] = True
+        c, p0, p1 = unit_pixels(cw, ch, count, u)
+        written[c, p0:p1] = True
+    flat = got.reshape(count, 3, ch * cw)
+    want_flat = want.reshape(count, 3, ch * cw)
     for c in range(count):
-        for y in range(ch):
-            if written[c, y]:
-                np.testing.assert_array_equal(got[c, :, y], want[c, :, y])
-            else:
-                assert np.all(got[c, :, y] == SENTINEL), (c, y)
+        np.testing.assert_array_equal(flat[c][:, written[c]], want_flat[c][:, written[c]])
+        assert np.all(flat[c][:, ~written[c]] == SENTINEL), c
 
 
 def test_argument_struct_keeps_its_tensors(torch):
@@ -343,7 +340,8 @@ def test_argument_struct_keeps_its_tensors(torch):
     frames = torch.from_numpy(W.random_frames_np(2, 70, 90, 3)).cuda()
     dplan = tg.DevicePlan(rois, plan)
     out = torch.empty((plan.n_canvases, 3, 96, 128), dtype=torch.float16, device="cuda")
-    order = torch.from_numpy(tg.stitch_schedule(rois, plan, 0, plan.n_canvases, 128, 96)).cuda()
+    n_units = tg.stitch_units(128, 96, plan.n_canvases)
+    order = torch.arange(n_units - 1, -1, -1, dtype=torch.int32, device="cuda")
     alive = weakref.ref(order)
     a = tg.stitch_args(frames, dplan, 0, plan.n_canvases, 128, 96, W.MEAN, W.STD, W.PAD, out,
                        unit_order=order)
