@@ -356,6 +356,24 @@ size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
  */
 int tg_unstitch(const tg_unstitch_args *args, void *stream);
 
+/* Largest n_boxes tg_unstitch_noalloc accepts. */
+#define TG_UNSTITCH_NOALLOC_MAX_BOXES (1 << 24)
+
+/*
+ * tg_unstitch for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same operation and
+ * results as tg_unstitch, but a->workspace and a->workspace_bytes are ignored. Instead the
+ * call uses a scratch array the library holds in device memory, one per GPU: 131 KB that
+ * each GPU the library runs on keeps until the process ends. The first call on a device
+ * looks the array up (hipGetSymbolAddress); no call allocates or frees memory. The kernels
+ * clear what they need themselves, so the array's contents from the previous call do not
+ * matter -- but every call on one GPU shares it: calls that may overlap on one GPU (two
+ * streams, two host threads) race and must be serialised by the caller.
+ * Returns what tg_unstitch returns, except: TG_E_WORKSPACE when n_boxes >
+ * TG_UNSTITCH_NOALLOC_MAX_BOXES; TG_E_HIP when the array cannot be looked up.
+ */
+int tg_unstitch_noalloc(const tg_unstitch_args *args, void *stream);
+
 /* ---- Per-frame merge of detections after unstitch (Sec. III-A patches, Sec. V-D) ---- */
 
 typedef struct {

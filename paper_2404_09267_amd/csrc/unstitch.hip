@@ -20,6 +20,7 @@
 //     box index -- a stable compaction whose output does not depend on scheduling.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 
 #include "lookback.h"
@@ -221,30 +222,45 @@ __global__ void zero_count_kernel(int32_t *n_out) { *n_out = 0; }
 
 int emit_blocks(int32_t n) { return (n + kEmitBoxes - 1) / kEmitBoxes; }
 
-}  // namespace
+// Workspace of the allocation-free entry point: the ticket word and one look-back word
+// per emit workgroup for up to TG_UNSTITCH_NOALLOC_MAX_BOXES boxes (131 KB). Each GPU the
+// library runs on holds its own copy until the process ends; host code reaches it only
+// through the address hipGetSymbolAddress returns for the current device.
+constexpr int kScratchWords = 1 + (TG_UNSTITCH_NOALLOC_MAX_BOXES + kEmitBoxes - 1) / kEmitBoxes;
+__device__ __align__(256) uint64_t scratch[kScratchWords];
 
-extern "C" size_t tg_unstitch_workspace_bytes(int32_t n_boxes) {
-  if (n_boxes <= 0) return 0;
-  return sizeof(uint64_t) * (1 + static_cast<size_t>(emit_blocks(n_boxes)));
+// Device address of `scratch` on the current device, looked up once per device id (null
+// when the lookup fails).
+void *scratch_address() {
+  static std::atomic<void *> cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  void *p = cached[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+  cached[dev].store(p, std::memory_order_release);
+  return p;
 }
 
-extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
+// Argument checks shared by both entry points (the workspace aside).
+int check_args(const tg_unstitch_args *a) {
   if (!a || a->n_boxes < 0 || a->n_rois < 0 || a->n_canvases < 0) return TG_E_INVAL;
   if (a->rule != 0 && a->rule != 1) return TG_E_INVAL;
-  hipStream_t s = static_cast<hipStream_t>(stream);
   if (!a->n_out) return TG_E_INVAL;
+  if (a->n_boxes == 0) return TG_OK;
+  if (!a->boxes || !a->box_canvas || !a->roi_of_box || !a->dets) return TG_E_INVAL;
+  if (a->n_canvases > 0 && !a->canvas_begin) return TG_E_INVAL;
+  if (a->n_rois > 0 && (!a->rois || !a->place || !a->order)) return TG_E_INVAL;
+  return TG_OK;
+}
+
+// Enqueues both launches with `ws` (device, 8-byte aligned, tg_unstitch_workspace_bytes
+// bytes) as the ticket and look-back words; the assign launch clears them first.
+int launch(const tg_unstitch_args *a, void *ws, hipStream_t s) {
   if (a->n_boxes == 0) {
     hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(1), 0, s, a->n_out);
     return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
   }
-  if (!a->boxes || !a->box_canvas || !a->roi_of_box || !a->dets) return TG_E_INVAL;
-  if (a->n_canvases > 0 && !a->canvas_begin) return TG_E_INVAL;
-  if (a->n_rois > 0 && (!a->rois || !a->place || !a->order)) return TG_E_INVAL;
-  const size_t need = tg_unstitch_workspace_bytes(a->n_boxes);
-  if (!a->workspace || a->workspace_bytes < need ||
-      reinterpret_cast<uintptr_t>(a->workspace) % 8 != 0)
-    return TG_E_WORKSPACE;
-
   UnstitchParams P;
   P.boxes = a->boxes;
   P.box_canvas = a->box_canvas;
@@ -260,8 +276,8 @@ extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
   P.roi_of_box = a->roi_of_box;
   P.dets = a->dets;
   P.n_out = a->n_out;
-  P.ticket = static_cast<uint32_t *>(a->workspace);
-  P.state = static_cast<uint64_t *>(a->workspace) + 1;
+  P.ticket = static_cast<uint32_t *>(ws);
+  P.state = static_cast<uint64_t *>(ws) + 1;
   P.n_state_words = 1 + emit_blocks(a->n_boxes);
 
   // Lanes per box: about the mean number of patches per canvas, so one ballot round
@@ -284,4 +300,32 @@ extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
   hipLaunchKernelGGL(emit_kernel, dim3(static_cast<uint32_t>(emit_blocks(a->n_boxes))),
                      dim3(kThreads), 0, s, P);
   return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
+}
+
+}  // namespace
+
+extern "C" size_t tg_unstitch_workspace_bytes(int32_t n_boxes) {
+  if (n_boxes <= 0) return 0;
+  return sizeof(uint64_t) * (1 + static_cast<size_t>(emit_blocks(n_boxes)));
+}
+
+extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
+  const int rc = check_args(a);
+  if (rc != TG_OK) return rc;
+  if (a->n_boxes > 0) {
+    const size_t need = tg_unstitch_workspace_bytes(a->n_boxes);
+    if (!a->workspace || a->workspace_bytes < need ||
+        reinterpret_cast<uintptr_t>(a->workspace) % 8 != 0)
+      return TG_E_WORKSPACE;
+  }
+  return launch(a, a->workspace, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int tg_unstitch_noalloc(const tg_unstitch_args *a, void *stream) {
+  const int rc = check_args(a);
+  if (rc != TG_OK) return rc;
+  if (a->n_boxes > TG_UNSTITCH_NOALLOC_MAX_BOXES) return TG_E_WORKSPACE;
+  void *ws = a->n_boxes > 0 ? scratch_address() : nullptr;
+  if (a->n_boxes > 0 && !ws) return TG_E_HIP;
+  return launch(a, ws, static_cast<hipStream_t>(stream));
 }

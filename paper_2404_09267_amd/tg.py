@@ -98,7 +98,8 @@ EXPORTS = ["tg_gmm_plane_stride", "tg_gmm_state_bytes", "tg_gmm_update",
            "tg_mask_rois_workspace_bytes", "tg_mask_rois", "tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
            "tg_batch_range", "tg_slo_replay", "tg_stitch",
            "tg_stitch_units", "tg_stitch_norm_uses_table",
-           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_merge_workspace_bytes", "tg_merge",
+           "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_unstitch_noalloc",
+           "tg_merge_workspace_bytes", "tg_merge",
            "tg_strerror", "tg_abi_version"]
 
 _lib = None
@@ -144,6 +145,8 @@ def lib() -> ctypes.CDLL:
         L.tg_unstitch_workspace_bytes.restype = ctypes.c_size_t
         L.tg_unstitch.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
         L.tg_unstitch.restype = ctypes.c_int
+        L.tg_unstitch_noalloc.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
+        L.tg_unstitch_noalloc.restype = ctypes.c_int
         L.tg_merge_workspace_bytes.argtypes = [_i32, _i32]
         L.tg_merge_workspace_bytes.restype = ctypes.c_size_t
         L.tg_merge.argtypes = [ctypes.POINTER(MergeArgs), _vp]
@@ -487,6 +490,15 @@ def unstitch(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuffers,
 
 def unstitch_raw(args: UnstitchArgs, stream=None) -> int:
     return int(lib().tg_unstitch(ctypes.byref(args), _stream_handle(stream)))
+
+
+UNSTITCH_NOALLOC_MAX_BOXES = 1 << 24
+
+
+def unstitch_noalloc_raw(args: UnstitchArgs, stream=None) -> int:
+    """tg_unstitch_noalloc: tg_unstitch on the library's own device scratch (the args'
+    workspace fields are ignored); calls that may overlap on one GPU must be serialised."""
+    return int(lib().tg_unstitch_noalloc(ctypes.byref(args), _stream_handle(stream)))
 
 
 class MergeBuffers:

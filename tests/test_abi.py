@@ -274,3 +274,26 @@ def test_probe_library_exports_its_header():
     assert g(ok, 4096, ok, 4800, 4096, 0, None) == -1        # no planes
     assert g(ok, 4096, ok, 4800, 4096, 5, None) == -1        # too many planes
     assert g(ok, 4096, ok, 4816, 4096, 3, None) == -1        # planes of whole 16-byte words
+
+
+def test_unstitch_noalloc_validation_without_gpu():
+    """The allocation-free entry point checks its arguments like tg_unstitch and refuses
+    more boxes than its device scratch holds, before anything is enqueued."""
+    L = tg.lib()
+    a = tg.UnstitchArgs()
+    a.n_boxes = -1
+    a.n_out = 0x1000
+    assert int(L.tg_unstitch_noalloc(ctypes.byref(a), None)) == tg.E_INVAL
+    a.n_boxes = 10
+    a.n_out = 0x1000
+    a.boxes = a.box_canvas = a.roi_of_box = a.dets = 0x2000
+    a.rois = a.place = a.order = a.canvas_begin = 0x3000
+    a.n_rois, a.n_canvases = 3, 1
+    a.rule = 2
+    assert int(L.tg_unstitch_noalloc(ctypes.byref(a), None)) == tg.E_INVAL
+    a.rule = 0
+    a.n_boxes = tg.UNSTITCH_NOALLOC_MAX_BOXES + 1
+    assert int(L.tg_unstitch_noalloc(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.n_boxes = 10
+    a.dets = None
+    assert int(L.tg_unstitch_noalloc(ctypes.byref(a), None)) == tg.E_INVAL
