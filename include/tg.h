@@ -73,7 +73,10 @@ enum tg_status {
   TG_E_RANGE = -4,         /* canvas range outside [0, n_canvases) */
   TG_E_WORKSPACE = -5,     /* workspace missing or smaller than required */
   TG_E_HIP = -6,           /* the HIP runtime refused a launch */
-  TG_E_INTERNAL = -7       /* host allocation failure or other internal error */
+  TG_E_INTERNAL = -7       /* host allocation failure or other internal error; also written
+                              to a device count output when a device pass could not
+                              complete (a grid-wide prefix whose predecessor never
+                              published, a broken union-find link) */
 };
 
 enum tg_policy {
@@ -169,6 +172,7 @@ size_t tg_partition_workspace_bytes(int32_t n_frames);
  * another frame id are skipped (zone -1). Enqueued on `stream`; the library allocates
  * nothing. Returns TG_E_INVAL (null pointer, negative count, bad sizes, more than 1024
  * zones), TG_E_WORKSPACE, TG_E_HIP. With n_frames == 0 only *n_patches = 0 is written.
+ * *n_patches = TG_E_INTERNAL reports a device-side failure of the compaction.
  */
 int tg_partition(const tg_partition_args *args, void *stream);
 
@@ -353,6 +357,7 @@ size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
  * Returns TG_E_INVAL on null pointers (unless n_boxes == 0, which only writes
  * *n_out = 0) or n_boxes < 0, TG_E_WORKSPACE when the workspace is too small,
  * TG_E_HIP on launch failure, TG_E_INVAL for a rule other than 0 or 1.
+ * *n_out = TG_E_INTERNAL reports a device-side failure of the compaction.
  */
 int tg_unstitch(const tg_unstitch_args *args, void *stream);
 
@@ -414,6 +419,7 @@ size_t tg_merge_workspace_bytes(int32_t n_max, int32_t n_frames);
  * count to *n_kept. Enqueued on `stream`; the library allocates nothing.
  * Returns TG_E_INVAL (null pointer, negative size, NaN threshold), TG_E_WORKSPACE,
  * TG_E_HIP. With n_max == 0 only *n_kept = *n_overflow = 0 is written.
+ * *n_kept = TG_E_INTERNAL reports a device-side failure of the compaction.
  */
 int tg_merge(const tg_merge_args *args, void *stream);
 
@@ -508,6 +514,10 @@ size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t hei
  * Enqueued on `stream`; allocates nothing. Returns TG_E_INVAL (null pointer,
  * non-positive sizes, more than 65535 frames or tile rows, width * height >= 2^30,
  * max_components < 1, max_rois < 0), TG_E_WORKSPACE, TG_E_HIP.
+ * *n_rois = *n_components = TG_E_INTERNAL (no RoIs, frame_begin all 0) reports a
+ * device-side failure: a union-find link that did not point to a smaller pixel index, or
+ * a compaction that could not complete. Neither happens on a correct run; each loop that
+ * could otherwise spin ends instead.
  */
 int tg_mask_rois(const tg_mask_rois_args *args, void *stream);
 

@@ -14,7 +14,8 @@ import subprocess
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboracle.so")
+# TG_LIBORACLE names another build of the oracle (the host-sanitizer build, say).
+LIB_PATH = os.environ.get("TG_LIBORACLE") or os.path.join(HERE, "liboracle.so")
 SOURCES = [os.path.join(HERE, "tg_oracle.c"), os.path.join(HERE, "gmm_oracle.c")]
 
 SHELF_FFDH, SHELF_ARRIVAL, GUILLOTINE_BSSF = 0, 1, 2
@@ -26,14 +27,18 @@ DET_DTYPE = np.dtype([("box", "<i4"), ("roi", "<i4"), ("frame", "<i4"),
                       ("x1", "<f4"), ("y1", "<f4"), ("x2", "<f4"), ("y2", "<f4")])
 
 
-def build(force: bool = True) -> str:
-    """Compile liboracle.so with gcc (always, when ``force``)."""
-    if force or not os.path.exists(LIB_PATH):
-        cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC",
-               "-shared", "-Wall", "-Wextra", "-o", LIB_PATH + ".tmp", *SOURCES, "-lm"]
+def build(force: bool = True, path: str | None = None, sanitize: bool = False) -> str:
+    """Compile liboracle.so with gcc (always, when ``force``); with ``sanitize`` under
+    ASan + UBSan (every undefined-behaviour report fatal) into ``path``."""
+    path = path or LIB_PATH
+    if force or not os.path.exists(path):
+        san = (["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+                "-fno-omit-frame-pointer", "-g"] if sanitize else [])
+        cmd = ["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC", *san,
+               "-shared", "-Wall", "-Wextra", "-o", path + ".tmp", *SOURCES, "-lm"]
         subprocess.run(cmd, check=True)
-        os.replace(LIB_PATH + ".tmp", LIB_PATH)
-    return LIB_PATH
+        os.replace(path + ".tmp", path)
+    return path
 
 
 _lib = None

@@ -1,9 +1,15 @@
 """Build libtg.so in-tree: the host planner with g++, the kernels with hipcc for gfx950.
 
-    python -m paper_2404_09267_amd.build
+    python -m paper_2404_09267_amd.build              # the library the binding loads
+    python -m paper_2404_09267_amd.build --sanitize   # host code under ASan + UBSan
 
 Objects go to _build/ at the repository root; the shared library lands next to this
-file, where the ctypes binding looks for it.
+file, where the ctypes binding looks for it. With --sanitize the host-only sources
+(planner, invoker, normalisation constants) are compiled with
+-fsanitize=address,undefined (every undefined-behaviour report fatal) into
+_build/sanitize/libtg.so; the HIP sources are built as usual (no GPU code is ever
+instrumented). Load that library with GCC's ASan runtime preloaded
+(tests/sanitize_host.py does).
 """
 from __future__ import annotations
 
@@ -35,6 +41,9 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLU
 # the command-line switch reaches them.
 EXACT_FP32 = {"unstitch.hip", "merge.hip", "gmm.hip"}
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-I", INCLUDE, "-Wall", "-Wextra"]
+SANITIZE_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+                  "-fno-omit-frame-pointer", "-g"]
+SANITIZE_LIB = os.path.join(BUILD, "sanitize", "libtg.so")
 
 
 def hipcc() -> str:
@@ -49,21 +58,32 @@ def _run(cmd):
     subprocess.run(cmd, check=True)
 
 
-def build(verbose_isa: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose_isa: bool = False, sanitize: bool = False) -> str:
+    out_dir = os.path.join(BUILD, "sanitize") if sanitize else BUILD
+    os.makedirs(out_dir, exist_ok=True)
     objs = []
     for src in HOST_SOURCES:
-        obj = os.path.join(BUILD, src + ".o")
-        _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        obj = os.path.join(out_dir, src + ".o")
+        _run(["g++", *HOST_FLAGS, *(SANITIZE_FLAGS if sanitize else []), "-c",
+              os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     cc = hipcc()
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
-        extra = ["-save-temps=obj"] if verbose_isa else []
-        if src in EXACT_FP32:
-            extra.append("-ffp-contract=off")
-        _run([cc, *HIP_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj])
+        if not sanitize or not os.path.exists(obj):
+            extra = ["-save-temps=obj"] if verbose_isa else []
+            if src in EXACT_FP32:
+                extra.append("-ffp-contract=off")
+            _run([cc, *HIP_FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
+    if sanitize:
+        # the GCC sanitizer runtimes the host objects were built against
+        rt = [subprocess.run(["gcc", f"-print-file-name={n}"], check=True, capture_output=True,
+                             text=True).stdout.strip() for n in ("libasan.so", "libubsan.so")]
+        tmp = SANITIZE_LIB + ".tmp"
+        _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs, *rt])
+        os.replace(tmp, SANITIZE_LIB)
+        return SANITIZE_LIB
     tmp = LIB + ".tmp"
     _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)
@@ -79,4 +99,4 @@ def build(verbose_isa: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    build(verbose_isa="--isa" in sys.argv)
+    build(verbose_isa="--isa" in sys.argv, sanitize="--sanitize" in sys.argv)

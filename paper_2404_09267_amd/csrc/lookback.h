@@ -1,4 +1,6 @@
-// Single-pass decoupled look-back over workgroups (stable compaction across a grid).
+// Single-pass decoupled look-back over workgroups (stable compaction across a grid): the
+// published method of Merrill and Garland (single-pass prefix scan with decoupled
+// look-back, 2016), here in a wave-wide form.
 //
 // Workgroup k (in ticket order, so every workgroup it waits on has already started)
 // publishes its own count as an "aggregate", finds the total of all earlier workgroups by
@@ -9,9 +11,11 @@
 //
 // The reading is done by a whole wave: lane l looks at workgroup k - 1 - l, a ballot
 // finds the nearest inclusive word, and the wave adds the counts up to it, or steps back
-// 64 workgroups at a time. Waits are bounded (kLookbackSpin tries); a word still unset
-// after that is taken as inclusive 0, which keeps the kernel finite but only happens if a
-// workgroup never ran.
+// 64 workgroups at a time. Waits are bounded (kLookbackSpin tries, far more than any
+// running workgroup needs to publish). A word still unset after that -- a predecessor that
+// never ran -- ends the wait: the prefix is then wrong, so the workgroup reports failure
+// and publishes its inclusive word with an error bit, which every later workgroup whose
+// prefix passes through it inherits; the caller turns it into an error count.
 #ifndef TG_LOOKBACK_H
 #define TG_LOOKBACK_H
 
@@ -23,6 +27,7 @@ namespace tg_detail {
 
 constexpr uint64_t kLookAggregate = uint64_t(1) << 32;
 constexpr uint64_t kLookInclusive = uint64_t(2) << 32;
+constexpr uint64_t kLookError = uint64_t(4) << 32;  // with kLookInclusive: prefix is wrong
 constexpr uint32_t kLookbackSpin = 1u << 22;
 
 __device__ __forceinline__ uint64_t look_load(const uint64_t *p) {
@@ -34,29 +39,36 @@ __device__ __forceinline__ void look_store(uint64_t *p, uint64_t v) {
 
 // Called by all 64 lanes of one wave of workgroup k (k = its ticket) with the
 // workgroup's own count; returns (in every lane) the total count of workgroups 0..k-1
-// and publishes this workgroup's inclusive total.
-__device__ __forceinline__ int lookback_prefix(uint64_t *state, int k, int count) {
+// and publishes this workgroup's inclusive total. *failed (every lane) is true when the
+// prefix could not be established (see the header comment).
+__device__ __forceinline__ int lookback_prefix(uint64_t *state, int k, int count,
+                                               bool *failed) {
   const int lane = threadIdx.x & 63;
+  *failed = false;
   if (k == 0) {
     if (lane == 0) look_store(&state[0], kLookInclusive | uint32_t(count));
     return 0;
   }
   if (lane == 0) look_store(&state[k], kLookAggregate | uint32_t(count));
   int prefix = 0;
+  bool err = false;
   for (int j = k - 1; j >= 0; j -= 64) {
     const int idx = j - lane;
     uint64_t s = idx >= 0 ? look_load(&state[idx]) : kLookInclusive;
     for (uint32_t spin = 0; __ballot((s >> 32) == 0) != 0 && spin < kLookbackSpin; ++spin)
       if ((s >> 32) == 0) s = look_load(&state[idx]);
-    if ((s >> 32) == 0) s = kLookInclusive;  // timed out: see the header comment
-    const uint64_t inc = __ballot((s >> 32) == (kLookInclusive >> 32));
+    if ((s >> 32) == 0) s = kLookInclusive | kLookError;  // timed out: count unknown
+    const uint64_t inc = __ballot((s & kLookInclusive) != 0);
     const int stop = inc ? __builtin_ctzll(inc) : 63;  // nearest inclusive lane, or all
     int v = lane <= stop ? static_cast<int>(static_cast<uint32_t>(s)) : 0;
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     prefix += v;
+    err = err || __ballot(lane <= stop && (s & kLookError) != 0) != 0;
     if (inc) break;
   }
-  if (lane == 0) look_store(&state[k], kLookInclusive | uint32_t(prefix + count));
+  if (lane == 0)
+    look_store(&state[k], kLookInclusive | (err ? kLookError : 0) | uint32_t(prefix + count));
+  *failed = err;
   return prefix;
 }
 

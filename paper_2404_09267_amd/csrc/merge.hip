@@ -349,10 +349,11 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const MergeParams P) 
     total += s_wave[w];
   }
   if (wave == 0) {
-    const int prefix = tg_detail::lookback_prefix(P.state, blk, total);
+    bool failed;
+    const int prefix = tg_detail::lookback_prefix(P.state, blk, total, &failed);
     if (lane == 0) {
       s_prefix = prefix;
-      if (blk == static_cast<int>(gridDim.x) - 1) *P.n_kept = prefix + total;
+      if (blk == static_cast<int>(gridDim.x) - 1) *P.n_kept = failed ? TG_E_INTERNAL : prefix + total;
     }
   }
   __syncthreads();

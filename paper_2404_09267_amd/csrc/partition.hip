@@ -114,10 +114,11 @@ __global__ __launch_bounds__(kThreads) void zone_kernel(const PartitionParams P)
     __syncthreads();
   }
   if (wave == 0) {
-    const int prefix = tg_detail::lookback_prefix(P.state, f, total);
+    bool failed;
+    const int prefix = tg_detail::lookback_prefix(P.state, f, total, &failed);
     if (lane == 0) {
       s_prefix = prefix;
-      if (f == P.n_frames - 1) *P.n_patches = prefix + total;
+      if (f == P.n_frames - 1) *P.n_patches = failed ? TG_E_INTERNAL : prefix + total;
     }
   }
   __syncthreads();

@@ -26,6 +26,9 @@
 //  6. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows.
 //  7. begin:  frame_begin by binary search over the kept rows' frames.
+// Every union-find walk checks the invariant it relies on (unionfind.h); a walk that meets a
+// link that does not point to a smaller index ends, sets the workspace's status word, and
+// the call reports *n_rois = *n_components = TG_E_INTERNAL instead of RoIs.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -33,6 +36,7 @@
 
 #include "lookback.h"
 #include "tg.h"
+#include "unionfind.h"
 
 namespace {
 
@@ -60,7 +64,7 @@ struct Comp {
 static_assert(sizeof(Comp) == 32, "component record is 32 bytes");
 
 struct Layout {
-  uint64_t *words;  // [0]: roots ticket, [1]: filter ticket, then the look-back words
+  uint64_t *words;  // [0]: roots ticket, [1]: filter ticket, [2]: status, then look-back words
   uint64_t *root_state, *filter_state;
   Comp *comp;
   int32_t *kept_frame;
@@ -75,14 +79,14 @@ Layout layout(void *base, int64_t n_px, int32_t max_components) {
   Layout L;
   const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
-  L.n_words = 2 + n_spans + n_filter;
+  L.n_words = 3 + n_spans + n_filter;
   const size_t o_comp = round_up(8 * static_cast<size_t>(L.n_words), 256);
   const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
   const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
   L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
   char *b = static_cast<char *>(base);
   L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
-  L.root_state = b ? L.words + 2 : nullptr;
+  L.root_state = b ? L.words + 3 : nullptr;
   L.filter_state = b ? L.root_state + n_spans : nullptr;
   L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
   L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
@@ -95,66 +99,31 @@ Layout layout(void *base, int64_t n_px, int32_t max_components) {
 __device__ __forceinline__ int lds_load(int *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
-// Root of i's set, halving the path on the way: every link points to a smaller index of
-// the same set, so relinking i to its grandparent with an atomic min keeps the sets and
-// their roots and never undoes a concurrent link.
-__device__ __forceinline__ int lds_find(int *L, int i) {
-  for (;;) {
-    const int p = lds_load(&L[i]);
-    if (p == i) return i;
-    const int g = lds_load(&L[p]);
-    if (g == p) return p;
-    atomicMin(&L[i], g);
-    i = g;
-  }
-}
-// Joins the sets of a and b: the larger root is linked under the smaller with an atomic
-// min; if that root was relinked meanwhile, retry from what it now points to.
-__device__ __forceinline__ void lds_unite(int *L, int a, int b) {
-  for (;;) {
-    a = lds_find(L, a);
-    b = lds_find(L, b);
-    if (a == b) return;
-    if (a > b) {
-      const int t = a;
-      a = b;
-      b = t;
-    }
-    const int old = atomicMin(&L[b], a);
-    if (old == b) return;
-    b = old;
-  }
-}
-
 __device__ __forceinline__ int g_load(const int32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// As lds_find, over the flagged words of tile-local roots in global memory.
-__device__ __forceinline__ int g_find(int32_t *L, int i) {
-  for (;;) {
-    const int p = g_load(&L[i]) & kIndex;
-    if (p == i) return i;
-    const int g = g_load(&L[p]) & kIndex;
-    if (g == p) return p;
-    __hip_atomic_fetch_min(&L[i], g | kRootFlag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    i = g;
+
+// Union-find over a tile's labels in LDS (unionfind.h).
+struct LdsLabels {
+  int *L;
+  __device__ int parent(int i) const { return lds_load(&L[i]); }
+  __device__ int link(int i, int p) { return atomicMin(&L[i], p); }
+};
+
+// Union-find over the flagged words of tile-local roots in global memory.
+struct RootLabels {
+  int32_t *L;
+  __device__ int parent(int i) const { return g_load(&L[i]) & kIndex; }
+  __device__ int link(int i, int p) {
+    return __hip_atomic_fetch_min(&L[i], p | kRootFlag, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT) & kIndex;
   }
-}
-__device__ __forceinline__ void g_unite(int32_t *L, int a, int b) {
-  for (;;) {
-    a = g_find(L, a);
-    b = g_find(L, b);
-    if (a == b) return;
-    if (a > b) {
-      const int t = a;
-      a = b;
-      b = t;
-    }
-    const int old = __hip_atomic_fetch_min(&L[b], a | kRootFlag, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT) & kIndex;
-    if (old == b) return;
-    b = old;
-  }
+};
+
+// Records in the workspace's status word that a union-find walk met a link that breaks
+// the invariant (tg_mask_rois then reports TG_E_INTERNAL instead of RoIs).
+__device__ __forceinline__ void fail(uint32_t *status) {
+  __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Foreground bits of this thread's 4 pixels in each of the kTilesPerGroup tiles of a
@@ -195,7 +164,7 @@ __device__ __forceinline__ void load_group_fg(const uint8_t *mf, int W, int H, i
 // within the tile) from this thread's foreground bits (load_group_fg). Returns false,
 // uniformly, when the tile has no foreground. Starts with a barrier, so the caller's
 // previous use of L (and of any other LDS) is over before L is rewritten.
-__device__ __forceinline__ bool label_tile(uint32_t fg, int *L) {
+__device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *status) {
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
   if (!__syncthreads_or(fg != 0)) return false;
   if (__syncthreads_and(fg == 0xFu)) {  // a solid tile is one set rooted at its pixel 0
@@ -211,12 +180,17 @@ __device__ __forceinline__ bool label_tile(uint32_t fg, int *L) {
   for (int k = 0; k < 4; ++k) {
     if (!(fg >> k & 1u)) continue;
     const int c = c0 + k, i = r * kTile + c;
-    if (c > 0 && lds_load(&L[i - 1]) >= 0) lds_unite(L, i, i - 1);
+    LdsLabels m{L};
+    bool ok = true;
+    if (c > 0 && lds_load(&L[i - 1]) >= 0) ok &= tg_detail::uf_unite(m, i, i - 1);
     if (r > 0) {
-      if (c > 0 && lds_load(&L[i - kTile - 1]) >= 0) lds_unite(L, i, i - kTile - 1);
-      if (lds_load(&L[i - kTile]) >= 0) lds_unite(L, i, i - kTile);
-      if (c + 1 < kTile && lds_load(&L[i - kTile + 1]) >= 0) lds_unite(L, i, i - kTile + 1);
+      if (c > 0 && lds_load(&L[i - kTile - 1]) >= 0)
+        ok &= tg_detail::uf_unite(m, i, i - kTile - 1);
+      if (lds_load(&L[i - kTile]) >= 0) ok &= tg_detail::uf_unite(m, i, i - kTile);
+      if (c + 1 < kTile && lds_load(&L[i - kTile + 1]) >= 0)
+        ok &= tg_detail::uf_unite(m, i, i - kTile + 1);
     }
+    if (!ok) fail(status);
   }
   __syncthreads();
   return true;
@@ -231,7 +205,8 @@ __global__ void clear_kernel(uint64_t *words, int64_t n) {
 
 template <bool kWord>
 __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask, int W, int H,
-                                                             int64_t frame_px, int32_t *label) {
+                                                             int64_t frame_px, int32_t *label,
+                                                             uint32_t *status) {
   __shared__ int L[kTile * kTile];
   const int64_t f = blockIdx.z;
   const int ty0 = blockIdx.y * kTile;
@@ -246,11 +221,17 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
   for (int q = 0; q < kTilesPerGroup; ++q) {
     const int tx0 = (blockIdx.x * kTilesPerGroup + q) * kTile;
-    if (!label_tile(fg[q], L)) continue;
+    if (!label_tile(fg[q], L, status)) continue;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (!(fg[q] >> k & 1u)) continue;
-      const int i = r * kTile + c0 + k, root = lds_find(L, i);
+      const int i = r * kTile + c0 + k;
+      LdsLabels m{L};
+      int root = tg_detail::uf_find(m, i);
+      if (root < 0) {
+        fail(status);
+        root = i;
+      }
       const int gr = (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
       lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] = root == i ? gr | kRootFlag : gr;
     }
@@ -265,7 +246,8 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask
 // each pixel joins neighbours k, k + 1, k + 2 through their current labels (members of
 // their sets), skipping a pair equal to the one just joined: along a border most repeat.
 __device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint32_t fg, int own0,
-                                            int ostep, int nb0, int nstep, int start, int lim) {
+                                            int ostep, int nb0, int nstep, int start, int lim,
+                                            uint32_t *status) {
   if (fg == 0) return;
   uint32_t m[18];
   int32_t ln[18], lo[16];
@@ -292,7 +274,8 @@ __device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint
       if (!(nb >> (k + d) & 1u)) continue;
       const int a = lo[k], b = ln[k + d];
       if (a == pa && b == pb) continue;
-      g_unite(lf, a, b);
+      RootLabels m{lf};
+      if (!tg_detail::uf_unite(m, a, b)) fail(status);
       pa = a;
       pb = b;
     }
@@ -307,7 +290,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *ma
                                                                int64_t frame_px, bool vec,
                                                                int row_items, int n_row,
                                                                int col_items, int n_all,
-                                                               int32_t *label) {
+                                                               int32_t *label, uint32_t *status) {
   const int i = blockIdx.x * kBorderThreads + threadIdx.x;
   if (i >= n_all) return;
   const int64_t f = blockIdx.y;
@@ -330,7 +313,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *ma
 #pragma unroll
       for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && x0 + k < W) ? 1u << k : 0u;
     }
-    join_border(mf, lf, fg, y * W + x0, 1, (y - 1) * W + x0 - 1, 1, x0, W);
+    join_border(mf, lf, fg, y * W + x0, 1, (y - 1) * W + x0 - 1, 1, x0, W, status);
   } else {  // left columns of tiles against the columns to their left
     const int j = i - n_row, b = j / col_items, y0 = 16 * (j - b * col_items);
     const int x = (b + 1) * kTile;
@@ -339,7 +322,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *ma
     for (int k = 0; k < 16; ++k) v[k] = mf[min(y0 + k, H - 1) * W + x];
 #pragma unroll
     for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && y0 + k < H) ? 1u << k : 0u;
-    join_border(mf, lf, fg, y0 * W + x, W, (y0 - 1) * W + x - 1, W, y0, H);
+    join_border(mf, lf, fg, y0 * W + x, W, (y0 - 1) * W + x - 1, W, y0, H, status);
   }
 }
 
@@ -426,10 +409,11 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
     total += s_wave[w];
   }
   if (wave == 0) {
-    const int prefix = tg_detail::lookback_prefix(state, static_cast<int>(span), total);
+    bool failed;
+    const int prefix = tg_detail::lookback_prefix(state, static_cast<int>(span), total, &failed);
     if (lane == 0) {
       s_base = prefix;
-      if (span == n_spans - 1) *n_components = prefix + total;
+      if (span == n_spans - 1) *n_components = failed ? TG_E_INTERNAL : prefix + total;
     }
   }
   __syncthreads();
@@ -465,7 +449,7 @@ template <bool kWord>
 __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask, int W, int H,
                                                              int64_t frame_px,
                                                              const int32_t *label,
-                                                             Comp *comp) {
+                                                             Comp *comp, uint32_t *status) {
   __shared__ int bx0[kTile * kTile], by0[kTile * kTile], bx1[kTile * kTile],
       by1[kTile * kTile], bn[kTile * kTile];
   const int64_t f = blockIdx.z;
@@ -554,16 +538,21 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
     for (int k = 0; k < 4; ++k) {
       const int i = r * kTile + c0 + k;
       if (root[k] != i) continue;
-      // up the union-find over local roots to the numbered root
+      // up the union-find over local roots to the numbered root; every link points to a
+      // smaller index (unionfind.h), so the walk ends -- a link that does not is reported
       int cur = y * W + tx0 + c0 + k;
       int v = lv[k];
       while (v >= 0) {
         const int nx = v & kIndex;
         if (nx == cur) break;
+        if (nx > cur) {
+          fail(status);
+          break;
+        }
         cur = nx;
         v = lf[cur];
       }
-      if (v >= 0) continue;  // a component past max_components: not measured
+      if (v >= 0) continue;  // a component past max_components (or a broken link): not measured
       Comp *c = comp + (-v - 1);
       atomicMin(&c->x0, bx0[i]);
       atomicMin(&c->y0, by0[i]);
@@ -575,12 +564,23 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
 }
 
 __global__ __launch_bounds__(kFilterThreads) void filter_kernel(
-    const Comp *comp, const int32_t *n_components, int32_t max_components, int32_t min_area,
+    const Comp *comp, int32_t *n_components, int32_t max_components, int32_t min_area,
     tg_roi *rois, int32_t *areas, int32_t max_rois, int32_t *kept_frame, uint64_t *words,
     uint64_t *state, int32_t *n_rois) {
   __shared__ int s_blk, s_base;
   __shared__ int s_wave[kFilterThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // A failure of an earlier pass (a union-find link that broke the invariant, or a
+  // look-back that could not complete) makes the call report TG_E_INTERNAL, no RoIs.
+  const uint32_t status = __hip_atomic_load(reinterpret_cast<const uint32_t *>(words + 2),
+                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (status != 0 || *n_components < 0) {
+    if (blockIdx.x == 0 && tid == 0) {
+      *n_rois = TG_E_INTERNAL;
+      *n_components = TG_E_INTERNAL;
+    }
+    return;
+  }
   // The grid is sized for max_components; only the first max(1, ceil(n / kFilterBlock))
   // workgroups take a ticket, so the ticket counter sees no more atomics than there are
   // blocks of components (at least one workgroup runs, to write n_rois when n == 0).
@@ -617,10 +617,12 @@ __global__ __launch_bounds__(kFilterThreads) void filter_kernel(
     total += s_wave[w];
   }
   if (wave == 0) {
-    const int prefix = tg_detail::lookback_prefix(state, blk, total);
+    bool failed;
+    const int prefix = tg_detail::lookback_prefix(state, blk, total, &failed);
     if (lane == 0) {
       s_base = prefix;
-      if ((start < n && n <= start + kFilterBlock) || n == 0) *n_rois = prefix + total;
+      if ((start < n && n <= start + kFilterBlock) || n == 0)
+        *n_rois = failed ? TG_E_INTERNAL : prefix + total;
     }
   }
   __syncthreads();
@@ -705,29 +707,30 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
                        a->frame_begin);
     return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
   }
+  uint32_t *status = reinterpret_cast<uint32_t *>(L.words + 2);
   hipLaunchKernelGGL(clear_kernel, dim3(static_cast<uint32_t>((L.n_words + 255) / 256)),
                      dim3(256), 0, s, L.words, L.n_words);
   if (word)
     hipLaunchKernelGGL(local_kernel<true>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label);
+                       frame_px, L.label, status);
   else
     hipLaunchKernelGGL(local_kernel<false>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label);
+                       frame_px, L.label, status);
   if (n_all > 0)
     hipLaunchKernelGGL(merge_kernel,
                        dim3(static_cast<uint32_t>((n_all + kBorderThreads - 1) / kBorderThreads),
                             static_cast<uint32_t>(a->n_frames)),
                        dim3(kBorderThreads), 0, s, a->mask, W, H, frame_px,
-                       vec && W % 16 == 0, row_items, n_row, col_items, n_all, L.label);
+                       vec && W % 16 == 0, row_items, n_row, col_items, n_all, L.label, status);
   hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_spans)), dim3(kSpanThreads), 0,
                      s, a->mask, vec, n_px, frame_px, n_spans, L.label, L.comp,
                      a->max_components, L.words, L.root_state, a->n_components);
   if (word)
     hipLaunchKernelGGL(boxes_kernel<true>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label, L.comp);
+                       frame_px, L.label, L.comp, status);
   else
     hipLaunchKernelGGL(boxes_kernel<false>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label, L.comp);
+                       frame_px, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
                      0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,
                      a->areas, a->max_rois, L.kept_frame, L.words, L.filter_state, a->n_rois);

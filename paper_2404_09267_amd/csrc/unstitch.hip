@@ -205,10 +205,11 @@ __global__ __launch_bounds__(kThreads) void emit_kernel(const UnstitchParams P) 
     total += s_wave[w];
   }
   if (wave == 0) {
-    const int prefix = tg_detail::lookback_prefix(P.state, blk, total);
+    bool failed;
+    const int prefix = tg_detail::lookback_prefix(P.state, blk, total, &failed);
     if (lane == 0) {
       s_prefix = prefix;
-      if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = prefix + total;
+      if (blk == static_cast<int>(gridDim.x) - 1) *P.n_out = failed ? TG_E_INTERNAL : prefix + total;
     }
   }
   __syncthreads();

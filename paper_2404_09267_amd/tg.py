@@ -12,7 +12,9 @@ from dataclasses import dataclass
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtg.so")
+# TG_LIBTG names another build of the same library (the host-sanitizer build, say).
+LIB_PATH = os.environ.get("TG_LIBTG") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                      "libtg.so")
 
 SHELF_FFDH, SHELF_ARRIVAL, GUILLOTINE_BSSF = 0, 1, 2
 OK = 0
@@ -113,6 +115,15 @@ class TgError(RuntimeError):
         super().__init__(msg)
         self.code = code
         self.bad_index = bad_index
+
+
+def _device_count(call: str, value) -> int:
+    """A count a kernel wrote: negative values are status codes (TG_E_INTERNAL when a
+    device pass could not complete), raised as TgError."""
+    n = int(value)
+    if n < 0:
+        raise TgError(call, n)
+    return n
 
 
 def lib() -> ctypes.CDLL:
@@ -408,7 +419,7 @@ class PartitionBuffers:
         self.workspace_bytes = ws
 
     def patches_numpy(self) -> np.ndarray:
-        n = int(self.n_patches.item())
+        n = _device_count("tg_partition", self.n_patches.item())
         return self.patches[:n].cpu().numpy()
 
 
@@ -454,7 +465,7 @@ class UnstitchBuffers:
         self.workspace_bytes = ws
 
     def dets_numpy(self) -> np.ndarray:
-        n = int(self.n_out.item())
+        n = _device_count("tg_unstitch", self.n_out.item())
         return self.dets[:n].cpu().numpy().view(DET_DTYPE).reshape(-1)
 
 
@@ -517,7 +528,7 @@ class MergeBuffers:
         self.workspace_bytes = ws
 
     def kept_numpy(self) -> np.ndarray:
-        n = int(self.n_kept.item())
+        n = _device_count("tg_merge", self.n_kept.item())
         return self.out[:n].cpu().numpy().view(DET_DTYPE).reshape(-1)
 
 
@@ -629,6 +640,7 @@ class MaskRoisBuffers:
     def result(self):
         """(rois int32 [n][5], areas int32 [n], frame_begin, n_rois, n_components)."""
         n_rois, n_comp = (int(v) for v in self.counts.cpu().tolist())
+        _device_count("tg_mask_rois", n_rois)
         n = min(n_rois, self.max_rois)
         return (self.rois[:n].cpu().numpy(), self.areas[:n].cpu().numpy(),
                 self.frame_begin.cpu().numpy(), n_rois, n_comp)

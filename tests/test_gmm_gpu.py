@@ -171,6 +171,89 @@ def test_mask_rois_structured(torch):
     _assert_rois(torch, m, 10)
 
 
+def _labels_after(torch, bufs, n_px):
+    """The label array and the status word that a tg_mask_rois call left in its
+    workspace. The labels are the workspace's last region, 256-byte aligned and padded to
+    256 bytes, so they start round_up(4 n_px, 256) bytes before its end; the status word
+    is the workspace's third 8-byte word."""
+    ws = bufs.workspace.cpu().numpy()
+    lab_bytes = (4 * n_px + 255) // 256 * 256
+    start = bufs.workspace_bytes - lab_bytes
+    labels = ws[start:start + 4 * n_px].view(np.int32)
+    status = int(ws[16:20].view(np.uint32)[0])
+    return labels, status
+
+
+def test_mask_rois_labels_keep_the_union_find_invariant(torch):
+    """After a call, the labels read back from the workspace satisfy, checked on the CPU
+    against scipy's 8-connected labelling: a foreground pixel holds either its tile-local
+    root (a pixel at or before it in the same 32x32 tile, itself a root) or, at a root, a
+    flagged link to a smaller index, or the negated component number; links stay in the
+    pixel's component; each component is numbered once, at its first pixel in raster
+    order, in raster order over the frames; following the links from any foreground
+    pixel ends at its component's number. The status word is clear."""
+    from scipy import ndimage
+
+    rng = np.random.default_rng(21)
+    F, H, Wd = 3, 197, 261
+    mask = (rng.random((F, H, Wd)) < 0.5).astype(np.uint8)
+    mask[1, 40:120, 30:200] = 1                     # one blob over many tiles
+    mask[2, ::2, ::2] = 1                           # isolated pixels next to noise
+    say("mask_rois labels", mask.shape)
+    n_px = F * H * Wd
+    bufs = tg.MaskRoisBuffers(F, Wd, H, n_px // 2 + 1, n_px // 2 + 1)
+    tg.mask_rois(torch.from_numpy(mask).cuda(), bufs, 1)
+    torch.cuda.synchronize()
+    _, _, _, n_rois, n_comp = bufs.result()
+    labels, status = _labels_after(torch, bufs, n_px)
+    assert status == 0
+    labels = labels.reshape(F, H * Wd).astype(np.int64)
+    flag, index = 1 << 30, (1 << 30) - 1
+    offset = 0
+    for f in range(F):
+        lab = labels[f]
+        comp, n = ndimage.label(mask[f], structure=np.ones((3, 3), np.int32))
+        comp = comp.reshape(-1)
+        idx = np.flatnonzero(mask[f].reshape(-1))
+        v = lab[idx]
+        numbered = v < 0
+        flagged = (v >= 0) & ((v & flag) != 0)
+        plain = (v >= 0) & ((v & flag) == 0)
+        is_root = lambda q: (lab[q] < 0) | ((lab[q] & flag) != 0)  # noqa: E731
+
+        t, i = v[plain], idx[plain]          # tile-local root of a non-root pixel
+        assert np.all((0 <= t) & (t < i))
+        assert np.array_equal((t // Wd) // 32, (i // Wd) // 32)
+        assert np.array_equal((t % Wd) // 32, (i % Wd) // 32)
+        assert np.all(is_root(t)) and np.array_equal(comp[t], comp[i])
+
+        p, i = v[flagged] & index, idx[flagged]  # tile-local root: link to a smaller one
+        assert np.all(p <= i)
+        own = p == i                        # still its own parent: must have been numbered
+        assert not own.any()
+        assert np.all(is_root(p)) and np.array_equal(comp[p], comp[i])
+
+        first = np.full(n + 1, np.iinfo(np.int64).max)
+        np.minimum.at(first, comp[idx], idx)
+        roots = idx[numbered]
+        assert np.array_equal(roots, np.sort(first[1:]))
+        ids = -v[numbered] - 1
+        assert np.array_equal(ids, np.arange(offset, offset + len(roots)))
+        id_of_comp = np.empty(n + 1, np.int64)
+        id_of_comp[comp[roots]] = ids
+
+        cur = v.copy()
+        for _ in range(len(idx) + 2):  # each link strictly lowers the index: bounded
+            live = cur >= 0
+            if not live.any():
+                break
+            cur[live] = lab[cur[live] & index]
+        assert np.all(cur < 0)
+        assert np.array_equal(-cur - 1, id_of_comp[comp[idx]])
+        offset += len(roots)
+    assert offset == n_comp and n_rois == n_comp
+
+
 def test_mask_rois_caps(torch):
     rng = np.random.default_rng(5)
     mask = (rng.random((2, 50, 70)) < 0.3).astype(np.uint8)
