@@ -393,10 +393,8 @@ typedef struct {
   int32_t *keep;            /* device out [n_max]: 1 kept, 0 dropped, for the first *n_dets */
   tg_det *out;              /* device out [n_max]: kept detections in input order */
   int32_t *n_kept;          /* device out, one int32 */
-  int32_t *n_overflow;      /* device out, one int32: frames with more than 2048 detections,
-                               left unmerged (all kept) */
   void *workspace;          /* device scratch, >= tg_merge_workspace_bytes(n_max, n_frames),
-                               8-byte aligned */
+                               16-byte aligned */
   size_t workspace_bytes;
 } tg_merge_args;
 
@@ -416,9 +414,12 @@ size_t tg_merge_workspace_bytes(int32_t n_max, int32_t n_frames);
  * area = max(0, x2 - x1) * max(0, y2 - y1), union = (area_a + area_b) - inter,
  * suppressed when inter > iou_threshold * union. Detections whose frame is outside
  * [0, n_frames) are dropped. Kept detections are written to out in input order and their
- * count to *n_kept. Enqueued on `stream`; the library allocates nothing.
+ * count to *n_kept. Every frame is merged, whatever its number of detections (frames of up
+ * to 1024 are ranked and walked in on-chip memory, larger ones in the workspace). The
+ * coordinates are not expected to be NaN (tg_unstitch never keeps such a box); if one is,
+ * min and max ignore the NaN operand. Enqueued on `stream`; the library allocates nothing.
  * Returns TG_E_INVAL (null pointer, negative size, NaN threshold), TG_E_WORKSPACE,
- * TG_E_HIP. With n_max == 0 only *n_kept = *n_overflow = 0 is written.
+ * TG_E_HIP. With n_max == 0 only *n_kept = 0 is written.
  * *n_kept = TG_E_INTERNAL reports a device-side failure of the compaction.
  */
 int tg_merge(const tg_merge_args *args, void *stream);

@@ -67,7 +67,7 @@ class MergeArgs(ctypes.Structure):
     _fields_ = [("dets", _vp), ("n_dets", _vp), ("n_max", _i32), ("scores", _vp),
                 ("n_scores", _i32), ("n_frames", _i32), ("iou_threshold", _f32),
                 ("cross_only", _i32), ("keep", _vp), ("out", _vp), ("n_kept", _vp),
-                ("n_overflow", _vp), ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace", _vp), ("workspace_bytes", ctypes.c_size_t)]
 
 
 class SloParams(ctypes.Structure):
@@ -522,7 +522,6 @@ class MergeBuffers:
         self.keep = torch.empty(max(n_max, 1), dtype=torch.int32, device=device)
         self.out = torch.empty((max(n_max, 1), DET_WORDS), dtype=torch.int32, device=device)
         self.n_kept = torch.empty(1, dtype=torch.int32, device=device)
-        self.n_overflow = torch.empty(1, dtype=torch.int32, device=device)
         ws = int(lib().tg_merge_workspace_bytes(n_max, n_frames))
         self.workspace = torch.empty(max(ws, 8), dtype=torch.uint8, device=device)
         self.workspace_bytes = ws
@@ -546,7 +545,7 @@ def merge_args(dets, n_dets, scores, n_frames, iou_threshold, cross_only,
     a.scores, a.n_scores = scores.data_ptr(), scores.numel()
     a.n_frames, a.iou_threshold, a.cross_only = n_frames, float(iou_threshold), int(bool(cross_only))
     a.keep, a.out = bufs.keep.data_ptr(), bufs.out.data_ptr()
-    a.n_kept, a.n_overflow = bufs.n_kept.data_ptr(), bufs.n_overflow.data_ptr()
+    a.n_kept = bufs.n_kept.data_ptr()
     a.workspace, a.workspace_bytes = bufs.workspace.data_ptr(), bufs.workspace_bytes
     a._keep = (dets, n_dets, scores, bufs)  # the struct holds raw pointers: keep their owners alive
     return a

@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version():
-    assert tg.lib().tg_abi_version() == 6
+    assert tg.lib().tg_abi_version() == 7
 
 
 def test_strerror():

@@ -52,6 +52,39 @@ def test_overlap_test_is_exact_on_small_integers():
         assert got == want, (a, b, thr)
 
 
+def test_vectorised_overlap_equals_scalar():
+    """suppressed_by_any (the merge's test against a whole kept list) equals any() of the
+    scalar suppresses over the same rows, on boxes mixing ordinary corners with NaN,
+    infinities, signed zeros, empty and inverted boxes and huge values, for thresholds of
+    both signs and with and without the patch mask."""
+    from oracle import merge
+
+    rng = np.random.default_rng(21)
+    special = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0, 1e38, -1e38, 3.0, 3.0000002],
+                       np.float32)
+
+    def boxes(k):
+        x = rng.uniform(-50, 150, (k, 4)).astype(np.float32)
+        x[:, 2:] = x[:, :2] + rng.uniform(-5, 60, (k, 2)).astype(np.float32)
+        odd = rng.random((k, 4)) < 0.08
+        x[odd] = rng.choice(special, odd.sum())
+        return x
+
+    for trial in range(400):
+        K = int(rng.integers(0, 12))
+        kept = boxes(K)
+        b = boxes(1)[0]
+        thr = float(rng.choice([0.5, 0.0, -0.0, -0.5, 1.0, 0.1, 2.0]))
+        roi = rng.integers(0, 3, K)
+        rb = int(rng.integers(0, 3))
+        bt = tuple(np.float32(v) for v in b)
+        rows = [tuple(np.float32(v) for v in r) for r in kept]
+        want_all = any(merge.suppresses(r, bt, thr) for r in rows)
+        want_cross = any(merge.suppresses(r, bt, thr) for r, q in zip(rows, roi) if q != rb)
+        assert merge.suppressed_by_any(kept, b, thr) == want_all, (kept, b, thr)
+        assert merge.suppressed_by_any(kept, b, thr, roi, rb) == want_cross, (kept, b, thr)
+
+
 def other_greedy(dets, scores, n_frames, thr, cross_only):
     """The same greedy, written as 'take the best remaining, drop what it overlaps'."""
     from oracle.merge import suppresses
@@ -117,7 +150,7 @@ def test_merge_argument_checks():
     L = tg.lib()
     a = tg.MergeArgs()
     a.dets, a.n_dets, a.scores, a.keep, a.out = 0x1000, 0x2000, 0x3000, 0x4000, 0x5000
-    a.n_kept, a.n_overflow, a.workspace = 0x6000, 0x7000, 0x8000
+    a.n_kept, a.workspace = 0x6000, 0x8000
     a.n_max, a.n_scores, a.n_frames, a.iou_threshold, a.cross_only = 100, 100, 4, 0.5, 1
     a.workspace_bytes = L.tg_merge_workspace_bytes(100, 4)
 
@@ -137,5 +170,13 @@ def test_merge_argument_checks():
     assert call(scores=None) == tg.E_INVAL
     assert call(workspace=None) == tg.E_WORKSPACE
     assert call(workspace_bytes=a.workspace_bytes - 1) == tg.E_WORKSPACE
+    assert call(workspace=0x8008) == tg.E_WORKSPACE  # not 16-byte aligned
     assert L.tg_merge_workspace_bytes(0, 4) == 0
-    assert L.tg_merge_workspace_bytes(1024, 3) == 8 * 2 + 4 * (3 + 3 + 4) + 4 * 1024
+    # ticket + one look-back word (16), counts, cursors, starts (3 + 3 + 4 int32), grouped
+    # ids (4 n); then, 16-byte aligned, the large-frame scratch: keys and their detections
+    # (2 n each, 12 bytes), ranked boxes (16 n), patch ids and cell ranges (4 n each), the
+    # per-cell lists of kept boxes and patch ids (4 n entries, 20 bytes), the kept list (20 n)
+    n = 1024
+    small = 8 * 2 + 4 * (3 + 3 + 4) + 4 * n
+    assert L.tg_merge_workspace_bytes(n, 3) == (small + 15) // 16 * 16 + 24 * n + 16 * n + \
+        4 * n + 4 * n + 4 * 20 * n + 20 * n

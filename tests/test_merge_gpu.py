@@ -34,27 +34,25 @@ def run_gpu(torch, dets, scores, n_frames, thr, cross_only, n_max=None):
              torch.from_numpy(np.ascontiguousarray(scores, np.float32)).cuda(), n_frames, thr,
              cross_only, bufs)
     torch.cuda.synchronize()
-    return (bufs.keep[:n].cpu().numpy(), bufs.kept_numpy(), int(bufs.n_kept.item()),
-            int(bufs.n_overflow.item()))
+    return bufs.keep[:n].cpu().numpy(), bufs.kept_numpy(), int(bufs.n_kept.item())
 
 
 def check(torch, dets, scores, n_frames, thr, cross_only, **kw):
     from oracle import merge
 
     say("merge", len(dets), n_frames, thr, cross_only)
-    keep, kept, n_kept, over = run_gpu(torch, dets, scores, n_frames, thr, cross_only, **kw)
+    keep, kept, n_kept = run_gpu(torch, dets, scores, n_frames, thr, cross_only, **kw)
     want_keep, want_kept = merge.merge(dets, scores, n_frames, thr, cross_only)
     np.testing.assert_array_equal(keep, want_keep.astype(np.int32))
     assert n_kept == len(want_kept)
     np.testing.assert_array_equal(kept.view(np.int32), want_kept.view(np.int32))
-    assert over == 0
     return keep
 
 
 @pytest.mark.parametrize("cross_only,key", [(True, "keep_cross_only"), (False, "keep_all_pairs")])
 def test_golden(torch, cross_only, key):
     g, dets, scores = golden_inputs()
-    keep, _, _, _ = run_gpu(torch, dets, scores, g["n_frames"], g["threshold"], cross_only)
+    keep, _, _ = run_gpu(torch, dets, scores, g["n_frames"], g["threshold"], cross_only)
     assert keep.tolist() == g[key]
 
 
@@ -66,11 +64,14 @@ def test_random(torch, cross_only, thr):
     check(torch, dets, scores, 40, thr, cross_only)
 
 
-def test_after_unstitch_on_device(torch):
-    """tg_unstitch's device outputs feed tg_merge directly (no host copy in between)."""
+@pytest.mark.parametrize("name", ["cam20_4k", "small_roi_8cam"])
+def test_after_unstitch_on_device(torch, name):
+    """tg_unstitch's device outputs feed tg_merge directly (no host copy in between); on
+    small_roi_8cam every frame holds several thousand detections (the workspace path)."""
     from oracle import merge
 
-    wl = W.WORKLOADS["cam20_4k"]
+    say("unstitch -> merge", name)
+    wl = W.WORKLOADS[name]
     rois = W.make_rois(wl)
     plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
     boxes, canv = W.make_boxes(wl, plan.n_canvases)
@@ -89,20 +90,37 @@ def test_after_unstitch_on_device(torch):
 
 
 def test_large_frames(torch):
+    """Frames on both sides of the on-chip limit (1024 detections) and far past it: 1024,
+    1025, 2048, 2049, 5000 and 20000 detections in one frame next to a small frame, in
+    crowded and sparse layouts, with and without cross_only."""
     rng = np.random.default_rng(9)
-    # exactly 2048 detections in frame 0, 300 in frame 1: merged
-    dets, scores = random_dets(rng, 2348, 2, 10, span=600.0)
-    dets["frame"] = np.r_[np.zeros(2048, np.int32), np.ones(300, np.int32)]
-    check(torch, dets, scores, 2, 0.5, True)
-    # 2049 in frame 0: left unmerged (all kept), frame 1 still merged
-    dets, scores = random_dets(rng, 2349, 2, 10, span=600.0)
-    dets["frame"] = np.r_[np.zeros(2049, np.int32), np.ones(300, np.int32)]
-    keep, kept, n_kept, over = run_gpu(torch, dets, scores, 2, 0.5, True)
-    assert over == 1 and keep[:2049].all()
-    from oracle import merge
+    for big, span, thr, cross in [(1024, 400.0, 0.5, True), (1025, 400.0, 0.5, True),
+                                  (1025, 100.0, 0.3, False), (2048, 600.0, 0.5, True),
+                                  (2049, 600.0, 0.5, True),
+                                  (2049, 150.0, 0.3, False), (5000, 1500.0, 0.5, True),
+                                  (5000, 300.0, 0.4, False), (20000, 3000.0, 0.5, True)]:
+        dets, scores = random_dets(rng, big + 300, 2, 10, span=span)
+        dets["frame"] = np.r_[np.zeros(big, np.int32), np.ones(300, np.int32)]
+        check(torch, dets, scores, 2, thr, cross)
 
-    want, _ = merge.merge(dets[2049:], scores, 2, 0.5, True)
-    np.testing.assert_array_equal(keep[2049:], want.astype(np.int32))
+
+def test_large_frames_special_boxes(torch):
+    """A 3000-detection frame with the cases the cell index treats apart: boxes with
+    infinite corners, inverted boxes, boxes wider than the frame, duplicates of one box,
+    and a negative threshold (every pair suppresses)."""
+    rng = np.random.default_rng(19)
+    dets, scores = random_dets(rng, 3000, 1, 12, span=800.0)
+    k = rng.permutation(3000)
+    dets["x2"][k[:40]] = np.inf
+    dets["y1"][k[40:80]] = -np.inf
+    dets["x1"][k[80:120]], dets["x2"][k[80:120]] = dets["x2"][k[80:120]], dets["x1"][k[80:120]]
+    dets["x1"][k[120:160]], dets["x2"][k[120:160]] = -50.0, 2000.0
+    for c in ("x1", "y1", "x2", "y2"):
+        dets[c][k[160:400]] = dets[c][k[160]]
+    check(torch, dets, scores, 1, 0.5, True)
+    check(torch, dets, scores, 1, 0.5, False)
+    check(torch, dets, scores, 1, -0.5, False)
+    check(torch, dets, scores, 1, 0.0, True)
 
 
 def test_frames_around_the_matrix_limit(torch):
@@ -128,11 +146,11 @@ def test_partial_count_and_empty(torch):
     # only the first 600 entries are valid (device count), capacity 800
     from oracle import merge
 
-    keep, kept, n_kept, _ = run_gpu(torch, dets[:600], scores, 5, 0.5, True, n_max=800)
+    keep, kept, n_kept = run_gpu(torch, dets[:600], scores, 5, 0.5, True, n_max=800)
     want_keep, want_kept = merge.merge(dets[:600], scores, 5, 0.5, True)
     np.testing.assert_array_equal(keep, want_keep.astype(np.int32))
     assert n_kept == len(want_kept)
-    _, _, n_kept, over = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=64)
-    assert n_kept == 0 and over == 0
-    _, _, n_kept, over = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=0)
-    assert n_kept == 0 and over == 0
+    _, _, n_kept = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=64)
+    assert n_kept == 0
+    _, _, n_kept = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=0)
+    assert n_kept == 0
