@@ -29,7 +29,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 METRIC = "stitched canvas Mpixel/s and achieved HBM GB/s (% of peak), 20-cam 4K"
 STITCH_SRC = os.path.join(ROOT, "paper_2404_09267_amd", "csrc", "stitch.hip")
-COUNTERS = os.path.join(ROOT, "profiles", "stitch_cam20_4k_counters.json")
+def counters_path(workload: str) -> str:
+    """Calibrated rocprofv3 traffic of tg_stitch on a workload, with the hash of the
+    kernel source they were taken on (profiles/stitch_<workload>_counters.json)."""
+    return os.path.join(ROOT, "profiles", f"stitch_{workload}_counters.json")
 
 
 def source_hash(path=STITCH_SRC) -> str:
@@ -48,6 +51,10 @@ def parse():
                     help="tg_stitch launch order: units in address order (the default), or "
                          "each of the 8 XCDs sweeping its own contiguous eighth of the batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-aux", action="store_true",
+                    help="only the path's own legs (stitch roofline, unstitch, merge, CPU "
+                         "baseline): skip the streaming ceiling, invoker, partition and "
+                         "background-model legs, which do not depend on --workload")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum wall time of the oracle's CPU sample")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -100,19 +107,37 @@ def stitch_bytes(rois, plan, first, count, canvas) -> int:
     return int(count) * canvas * canvas * 6 + 3 * px + 36 * (hi - lo)
 
 
-def cpu_baseline(wl, rois, frames_np, boxes, canv, min_seconds: float):
+def sample_frames(frames_d, rois, plan, sample_canvases):
+    """The frames the first canvases read, copied to the host, and the RoI table with
+    those RoIs' frame ids renumbered into that copy (other RoIs point at frame 0, which
+    the sample's stitch does not read for them): the oracle's stitch of the sample needs
+    no host copy of the whole window."""
+    lo, hi = 0, int(plan.canvas_begin[sample_canvases])
+    ids = plan.order[lo:hi]
+    used = np.unique(rois[ids, 0])
+    remap = np.zeros(int(rois[:, 0].max()) + 1, np.int32)
+    remap[used] = np.arange(len(used), dtype=np.int32)
+    r2 = rois.copy()
+    r2[:, 0] = 0
+    r2[ids, 0] = remap[rois[ids, 0]]
+    idx = __import__("torch").from_numpy(used.astype(np.int64)).to(frames_d.device)
+    return frames_d.index_select(0, idx).cpu().numpy(), r2
+
+
+def cpu_baseline(wl, rois, frames_d, boxes, canv, plan, min_seconds: float):
     """The oracle, untuned, on a bounded sample of the same workload: the full plan,
     the first canvases' stitch and those canvases' boxes, repeated until at least
     `min_seconds` of wall time have passed."""
     import oracle
 
-    sample_canvases = 4
+    sample_canvases = min(4, plan.n_canvases)
+    frames_np, srois = sample_frames(frames_d, rois, plan, sample_canvases)
     t0 = time.perf_counter()
     reps = 0
     while True:
         rc, _, oplan = oracle.pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h,
                                    wl.n_frames, 0)
-        oracle.stitch(frames_np, rois, oplan, 0, sample_canvases, wl.canvas, wl.canvas,
+        oracle.stitch(frames_np, srois, oplan, 0, sample_canvases, wl.canvas, wl.canvas,
                       _W.MEAN, _W.STD, _W.PAD)
         sel = canv < sample_canvases
         oracle.unstitch(boxes[sel], canv[sel], rois, oplan, 1)
@@ -128,7 +153,7 @@ def cpu_baseline(wl, rois, frames_np, boxes, canv, min_seconds: float):
     while True:
         rc, _, oplan = oracle.pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h,
                                    wl.n_frames, 0)
-        oracle.stitch(frames_np, rois, oplan, 0, sample_canvases, wl.canvas, wl.canvas,
+        oracle.stitch(frames_np, srois, oplan, 0, sample_canvases, wl.canvas, wl.canvas,
                       _W.MEAN, _W.STD, _W.PAD)
         oracle.unstitch(boxes[sel], canv[sel], rois, oplan, 1)
         reps1 += 1
@@ -230,9 +255,10 @@ def partition_cost(tg, W, torch, with_oracle: bool, launches: int = 50):
     return out
 
 
-def merge_cost(tg, W, torch, uargs, ubufs, n_frames, with_oracle: bool, launches: int = 50):
-    """tg_merge on the bench's own tg_unstitch output (cam20_4k, 10,000 boxes, seeded
-    detector scores, IoU 0.5 across patches), timed with HIP events; the oracle beside."""
+def merge_cost(tg, W, torch, uargs, ubufs, name, n_frames, with_oracle: bool,
+               launches: int = 50):
+    """tg_merge on the bench's own tg_unstitch output (seeded detector scores, IoU 0.5
+    across patches), timed with HIP events; the oracle beside."""
     stream = torch.cuda.current_stream()
     h = tg._vp(stream.cuda_stream)
     rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
@@ -256,9 +282,11 @@ def merge_cost(tg, W, torch, uargs, ubufs, n_frames, with_oracle: bool, launches
     torch.cuda.synchronize()
     us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
     n_dets = int(ubufs.n_out.item())
-    out = {"input": f"tg_unstitch output of cam20_4k ({n_dets} detections, {n_frames} frames), "
-                    "IoU 0.5 across patches", "kept": int(mb.n_kept.item()),
-           "us_per_call": round(us, 2), "bound": "latency: 6 small launches"}
+    per_frame = np.bincount(ubufs.dets_numpy()["frame"], minlength=n_frames)
+    out = {"input": f"tg_unstitch output of {name} ({n_dets} detections, {n_frames} frames, "
+                    f"up to {int(per_frame.max())} per frame), IoU 0.5 across patches",
+           "kept": int(mb.n_kept.item()), "us_per_call": round(us, 2),
+           "bound": "latency: 6 launches, one workgroup per frame"}
     if with_oracle:
         from oracle import merge
 
@@ -490,6 +518,8 @@ def main():
                    for k, (first, count) in enumerate(batches)]
     uargs = tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
     stitch_events = []
+    unstitch_events = []
+    plan_s = []
     timing = {"on": False}
 
     def step(s: int):
@@ -500,9 +530,12 @@ def main():
         place = st[: 3 * n_rois].reshape(n_rois, 3)
         order = st[3 * n_rois: 4 * n_rois]
         cbeg = st[4 * n_rois: 5 * n_rois + 1]
+        tp = time.perf_counter()
         rc = tg.lib().tg_plan_pack(rois.ctypes.data, n_rois, tg.ctypes.byref(params),
                                    place.ctypes.data, order.ctypes.data, cbeg.ctypes.data,
                                    J_buf.ctypes.data, bad_buf.ctypes.data)
+        if timing["on"]:
+            plan_s.append(time.perf_counter() - tp)
         if rc != tg.OK or J_buf[0] != J:
             raise tg.TgError("tg_plan_pack", rc)
         plan_d.copy_(staging[buf], non_blocking=True)
@@ -522,6 +555,10 @@ def main():
         rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
         if rc != tg.OK:
             raise tg.TgError("tg_unstitch", rc)
+        if timing["on"]:
+            ue = torch.cuda.Event(enable_timing=True)
+            ue.record(stream)
+            unstitch_events.append((evs[-1], ue))
 
     for s in range(args.warmup):
         step(s)
@@ -554,8 +591,8 @@ def main():
     avg_bytes = tot_bytes / n_launch
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
     traffic = None
-    if os.path.exists(COUNTERS):
-        with open(COUNTERS) as f:
+    if os.path.exists(counters_path(wl.name)):
+        with open(counters_path(wl.name)) as f:
             cnt = json.load(f)
         if cnt.get("stitch_source_sha256_16") == source_hash() and \
                 cnt.get("workload") == wl.name:
@@ -583,20 +620,32 @@ def main():
         "roofline": roofline,
         "stitch_gbs": round(achieved, 1),
         "stitch_pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
+        # per step, over the timed steps: the host plan (overlapped with the previous
+        # step's GPU work), the GPU time of all of the step's stitch launches, and of its
+        # tg_unstitch
+        "step_parts": {
+            "plan_ms": round(1e3 * float(np.mean(plan_s)), 4),
+            "stitch_ms": round(tot_ms / args.steps, 4),
+            "unstitch_ms": round(float(np.mean([a.elapsed_time(b) for a, b in unstitch_events])), 4),
+            "stitch_launches": len(batches)},
     }
-    write_bytes = int(np.mean([c * wl.canvas * wl.canvas * 6 for _, c in batches]))
-    ceil = stream_ceiling(torch, int(avg_bytes) - write_bytes, write_bytes)
-    ceil["stitch_frac"] = round(achieved / ceil["gbs"], 4)
-    ceil["planes3"]["stitch_frac"] = round(achieved / ceil["planes3"]["gbs"], 4)
-    result["ceiling"] = ceil
+    if not args.no_aux:
+        write_bytes = int(np.mean([c * wl.canvas * wl.canvas * 6 for _, c in batches]))
+        ceil = stream_ceiling(torch, int(avg_bytes) - write_bytes, write_bytes)
+        ceil["stitch_frac"] = round(achieved / ceil["gbs"], 4)
+        ceil["planes3"]["stitch_frac"] = round(achieved / ceil["planes3"]["gbs"], 4)
+        result["ceiling"] = ceil
     result["unstitch"] = unstitch_cost(tg, torch, uargs, n_boxes)
-    result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
-    result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
-    result["merge"] = merge_cost(tg, W, torch, uargs, ubufs, wl.n_frames, not args.no_cpu_baseline)
-    result["gmm"] = gmm_cost(tg, W, torch, not args.no_cpu_baseline)
+    if not args.no_aux:
+        result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
+        result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
+    result["merge"] = merge_cost(tg, W, torch, uargs, ubufs, wl.name, wl.n_frames,
+                                 not args.no_cpu_baseline)
+    if not args.no_aux:
+        result["gmm"] = gmm_cost(tg, W, torch, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
-        frames_np = frames_d.cpu().numpy()
-        result["cpu_baseline"] = cpu_baseline(wl, rois, frames_np, boxes, canv, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(wl, rois, frames_d, boxes, canv, plan0,
+                                              args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 

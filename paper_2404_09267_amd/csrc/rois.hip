@@ -4,7 +4,10 @@
 //
 // Connected components by union-find with atomic-min linking (a root always points to
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
-// order), in seven launches on the caller's stream:
+// order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
+// 2018), tile-local first and merged along tile borders as in the block-based labelling of
+// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in seven launches on the
+// caller's stream:
 //  1. clear:  zeroes the tickets and look-back words of launches 4 and 6.
 //  2. local:  one 256-thread workgroup per four 32x32 tiles side by side (their mask
 //             words loaded together up front; a group without foreground leaves at once)

@@ -57,8 +57,8 @@ def test_odd_frame_widths_and_mean_std(torch):
 
 
 def test_many_patches_per_run_take_further_lists(torch):
-    """More than 128 patches meeting one run (the size of one list; the rest take further
-    lists) and exactly 128 and 129: tiny RoIs, including 1 x 1."""
+    """Runs met by more patches than one list holds (the rest take further lists): up to
+    8192 tiny RoIs on a small canvas, including 1 x 1, and exactly 128 and 129."""
     rng = np.random.default_rng(5)
     # expect: the exact maximum of patches per unit, or ">" (over 128), or "<=" (128 or fewer)
     for cw, ch, n, lo, hi, pol, expect in [
