@@ -6,34 +6,38 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
 // 2018), tile-local first and merged along tile borders as in the block-based labelling of
-// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in seven launches on the
-// caller's stream:
-//  1. clear:  zeroes the tickets and look-back words of launches 4 and 6.
-//  2. local:  one 256-thread workgroup per four 32x32 tiles side by side (their mask
-//             words loaded together up front; a group without foreground leaves at once)
-//             labels each tile in LDS and writes, for each foreground pixel, the frame
-//             index of its tile-local root.
-//  3. merge:  one thread per 16 pixels of a tile border row or column joins each
-//             foreground pixel with its foreground neighbours in the tile above (border rows) or to
-//             the left (border columns), with global atomics on the label array. Every
-//             8-neighbour pair across a tile border is seen from the tile below or to the
-//             right of it.
-//  4. roots:  65536-pixel raster spans in ticket order (each thread's 256 mask bytes as
-//             sixteen 16-byte loads) find the tile-local roots still their own parent
+// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in eight launches on
+// the caller's stream. Foreground masks are sparse, so only one pass reads every mask
+// byte; the others visit the 32x32 tiles that hold foreground.
+//  1. clear:  zeroes the tickets, counters, look-back words and the tile bitmap.
+//  2. scan:   one 256-thread workgroup per 16 tiles side by side streams the mask (16-byte
+//             loads where it can), sets a bit per tile with foreground and appends those
+//             tiles to a list.
+//  3. local:  a fixed grid walks the list: each tile is labelled in LDS and every
+//             foreground pixel gets the frame index of its tile-local root.
+//  4. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
+//             column in two halves) join each foreground pixel with its foreground
+//             neighbours across the border, with global atomics on the label array; an
+//             item whose neighbouring tiles are all empty is skipped. Every 8-neighbour
+//             pair across a tile border is seen from the tile below or to the right of it.
+//  5. roots:  65536-pixel raster spans in ticket order (each thread's 256 mask bytes as
+//             sixteen 16-byte loads, skipping 32-pixel words of empty tiles when rows are
+//             a multiple of 32 pixels) find the tile-local roots still their own parent
 //             (the components), number them in raster order with a decoupled look-back,
 //             initialise each component's record and mark the root with its number.
-//  5. boxes:  per four tiles again, each tile's local components, read off the labels the
-//             local pass left, fold their pixels' extent and count in LDS; each local
-//             component then follows the union-find to its component number and folds its
-//             totals into the record with global atomics: one set per (tile, component).
-//  6. filter: components of at least min_area pixels, compacted in number order with a
+//  6. boxes:  the grid walks the list again: each tile's local components, read off the
+//             labels the local pass left, fold their pixels' extent and count in LDS; each
+//             local component then follows the union-find to its component number and
+//             folds its totals into the record with global atomics.
+//  7. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows.
-//  7. begin:  frame_begin by binary search over the kept rows' frames.
+//  8. begin:  frame_begin by binary search over the kept rows' frames.
 // Every union-find walk checks the invariant it relies on (unionfind.h); a walk that meets a
 // link that does not point to a smaller index ends, sets the workspace's status word, and
 // the call reports *n_rois = *n_components = TG_E_INTERNAL instead of RoIs.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cstdint>
 
@@ -45,7 +49,9 @@ namespace {
 
 constexpr int kTile = 32;
 constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
-constexpr int kTilesPerGroup = 4;  // tiles side by side per workgroup of local and boxes
+constexpr int kScanTiles = 16;     // tiles side by side per workgroup of the scan pass
+constexpr int kScanThreads = 256;  // 8 threads per row of 16 tiles, 64 pixels each
+constexpr int kListGroups = 2048;  // workgroups walking the list of non-empty tiles
 constexpr int kBorderThreads = 256;
 // Labels: a foreground pixel's word holds its tile-local root (a frame index) once the
 // local pass is done, and never changes afterwards unless the pixel is a tile-local root.
@@ -66,9 +72,21 @@ struct Comp {
 };
 static_assert(sizeof(Comp) == 32, "component record is 32 bytes");
 
+// Tiles of all frames, numbered frame by frame, tile rows top to bottom, tiles left to
+// right: tile (f, ty, tx) is (f * tiles_y + ty) * tiles_x + tx.
+struct Tiles {
+  int tiles_x, tiles_y;
+  int64_t n;
+};
+
 struct Layout {
-  uint64_t *words;  // [0]: roots ticket, [1]: filter ticket, [2]: status, then look-back words
+  // [0]: roots ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed, then
+  // the look-back words of the roots and filter passes, then the tile bitmap (bit t of
+  // 32-bit word t / 32: tile t holds foreground); all cleared by the first launch
+  uint64_t *words;
   uint64_t *root_state, *filter_state;
+  uint32_t *tile_bits;
+  int32_t *tile_list;  // ids of the non-empty tiles, in no particular order
   Comp *comp;
   int32_t *kept_frame;
   int32_t *label;
@@ -78,19 +96,23 @@ struct Layout {
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-Layout layout(void *base, int64_t n_px, int32_t max_components) {
+Layout layout(void *base, int64_t n_px, int64_t n_tiles, int32_t max_components) {
   Layout L;
   const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
-  L.n_words = 3 + n_spans + n_filter;
-  const size_t o_comp = round_up(8 * static_cast<size_t>(L.n_words), 256);
+  const int64_t bit_words64 = (n_tiles + 63) / 64;
+  L.n_words = 4 + n_spans + n_filter + bit_words64;
+  const size_t o_list = round_up(8 * static_cast<size_t>(L.n_words), 256);
+  const size_t o_comp = round_up(o_list + 4 * static_cast<size_t>(n_tiles), 256);
   const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
   const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
   L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
   char *b = static_cast<char *>(base);
   L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
-  L.root_state = b ? L.words + 3 : nullptr;
+  L.root_state = b ? L.words + 4 : nullptr;
   L.filter_state = b ? L.root_state + n_spans : nullptr;
+  L.tile_bits = b ? reinterpret_cast<uint32_t *>(L.filter_state + n_filter) : nullptr;
+  L.tile_list = b ? reinterpret_cast<int32_t *>(b + o_list) : nullptr;
   L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
   L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
   L.label = b ? reinterpret_cast<int32_t *>(b + o_label) : nullptr;
@@ -129,45 +151,65 @@ __device__ __forceinline__ void fail(uint32_t *status) {
   __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Foreground bits of this thread's 4 pixels in each of the kTilesPerGroup tiles of a
-// group (tile q at column tx0 + 32 q, row ty0): thread t holds row t / 8, columns
-// 4 (t % 8) .. + 3 of every tile. All loads are issued before any is used, from addresses
-// clamped into the frame (pixels outside it are masked off afterwards): one dword per
-// tile when every row start is dword-aligned (kWord), else four bytes.
+// Foreground bits of this thread's 4 pixels of the tile at column tx0, row ty0: thread t
+// holds row t / 8, columns 4 (t % 8) .. + 3, read from addresses clamped into the frame
+// (pixels outside it are masked off): one dword when every row start is dword-aligned
+// (kWord), else four bytes.
 template <bool kWord>
-__device__ __forceinline__ void load_group_fg(const uint8_t *mf, int W, int H, int tx0, int ty0,
-                                              uint32_t fg[kTilesPerGroup]) {
+__device__ __forceinline__ uint32_t load_tile_fg(const uint8_t *mf, int W, int H, int tx0,
+                                                 int ty0) {
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
   const uint8_t *row = mf + static_cast<int64_t>(min(y, H - 1)) * W;
-  uint32_t raw[kTilesPerGroup][kWord ? 1 : 4];
+  const int x0 = tx0 + c0;
+  uint32_t raw[4];
+  if (kWord) {
+    raw[0] = *reinterpret_cast<const uint32_t *>(row + min(x0, W - 4));
+  } else {
 #pragma unroll
-  for (int q = 0; q < kTilesPerGroup; ++q) {
-    const int x0 = tx0 + q * kTile + c0;
-    if (kWord) {
-      raw[q][0] = *reinterpret_cast<const uint32_t *>(row + min(x0, W - 4));
-    } else {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) raw[q][kWord ? 0 : k] = row[min(x0 + k, W - 1)];
-    }
+    for (int k = 0; k < 4; ++k) raw[k] = row[min(x0 + k, W - 1)];
   }
+  uint32_t bits = 0;
 #pragma unroll
-  for (int q = 0; q < kTilesPerGroup; ++q) {
-    const int x0 = tx0 + q * kTile + c0;
-    uint32_t bits = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t v = kWord ? (raw[q][0] >> (8 * k)) & 0xFFu : raw[q][kWord ? 0 : k];
-      bits |= (v != 0 && x0 + k < W) ? 1u << k : 0u;
-    }
-    fg[q] = y < H ? bits : 0u;
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t v = kWord ? (raw[0] >> (8 * k)) & 0xFFu : raw[k];
+    bits |= (v != 0 && x0 + k < W) ? 1u << k : 0u;
   }
+  return y < H ? bits : 0u;
+}
+
+__device__ __forceinline__ bool tile_set(const uint32_t *bits, int t) {
+  return (bits[t >> 5] >> (t & 31)) & 1u;
+}
+
+// Frame, tile row and tile column of tile id t.
+struct TileAt {
+  int f, ty, tx;
+};
+__device__ __forceinline__ TileAt tile_at(const Tiles &T, int t) {
+  const int ft = t / T.tiles_x;
+  TileAt a;
+  a.tx = t - ft * T.tiles_x;
+  a.f = ft / T.tiles_y;
+  a.ty = ft - a.f * T.tiles_y;
+  return a;
 }
 
 // Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
-// within the tile) from this thread's foreground bits (load_group_fg). Returns false,
-// uniformly, when the tile has no foreground. Starts with a barrier, so the caller's
-// previous use of L (and of any other LDS) is over before L is rewritten.
-__device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *status) {
+// within the tile; rows: 32 words of scratch) from this thread's foreground bits
+// (load_tile_fg). Returns false, uniformly, when the tile has no foreground. Starts with a
+// barrier, so the caller's previous use of L (and of any other LDS) is over before L is
+// rewritten.
+//
+// A pixel starts linked to the first pixel of its horizontal run among the thread's four,
+// so runs inside a thread cost no union. Each pixel p then joins the neighbours that a
+// raster-scan decision tree for 8-connectivity requires -- with a the upper-left, b the
+// upper, c the upper-right and d the left neighbour: b alone when b is foreground (a and c
+// touch b, and d touches b diagonally, through their own joins); otherwise d (when it lies
+// in another thread) and c; otherwise a and c -- and skips b when the previous pixel of its
+// run has already joined a, which touches b. That reaches the same sets as joining every
+// foreground neighbour, with about one union per run instead of four per pixel.
+__device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *rows,
+                                           uint32_t *status) {
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
   if (!__syncthreads_or(fg != 0)) return false;
   if (__syncthreads_and(fg == 0xFu)) {  // a solid tile is one set rooted at its pixel 0
@@ -176,25 +218,41 @@ __device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *status
     __syncthreads();
     return true;
   }
+  // this row's foreground as one word (the 8 threads of a row are 8 consecutive lanes)
+  uint32_t row = fg << c0;
+  row |= __shfl_xor(row, 1);
+  row |= __shfl_xor(row, 2);
+  row |= __shfl_xor(row, 4);
+  if ((t & 7) == 0) rows[r] = row;
+  int start = -1;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) L[r * kTile + c0 + k] = (fg >> k & 1u) ? r * kTile + c0 + k : -1;
+  for (int k = 0; k < 4; ++k) {
+    const int i = r * kTile + c0 + k;
+    start = (fg >> k & 1u) ? (start >= 0 ? start : i) : -1;
+    L[i] = start;
+  }
   __syncthreads();
+  const uint32_t up = r > 0 ? rows[r - 1] : 0u;
+  LdsLabels m{L};
+  bool ok = true;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     if (!(fg >> k & 1u)) continue;
     const int c = c0 + k, i = r * kTile + c;
-    LdsLabels m{L};
-    bool ok = true;
-    if (c > 0 && lds_load(&L[i - 1]) >= 0) ok &= tg_detail::uf_unite(m, i, i - 1);
-    if (r > 0) {
-      if (c > 0 && lds_load(&L[i - kTile - 1]) >= 0)
-        ok &= tg_detail::uf_unite(m, i, i - kTile - 1);
-      if (lds_load(&L[i - kTile]) >= 0) ok &= tg_detail::uf_unite(m, i, i - kTile);
-      if (c + 1 < kTile && lds_load(&L[i - kTile + 1]) >= 0)
-        ok &= tg_detail::uf_unite(m, i, i - kTile + 1);
+    const bool a = c > 0 && (up >> (c - 1) & 1u), b = up >> c & 1u;
+    const bool cc = c + 1 < kTile && (up >> (c + 1) & 1u);
+    const bool d = c > 0 && (row >> (c - 1) & 1u);
+    if (b) {
+      if (!(k > 0 && d && a)) ok &= tg_detail::uf_unite(m, i, i - kTile);
+    } else if (d) {
+      if (k == 0) ok &= tg_detail::uf_unite(m, i, i - 1);
+      if (cc) ok &= tg_detail::uf_unite(m, i, i - kTile + 1);
+    } else {
+      if (a) ok &= tg_detail::uf_unite(m, i, i - kTile - 1);
+      if (cc) ok &= tg_detail::uf_unite(m, i, i - kTile + 1);
     }
-    if (!ok) fail(status);
   }
+  if (!ok) fail(status);
   __syncthreads();
   return true;
 }
@@ -206,28 +264,104 @@ __global__ void clear_kernel(uint64_t *words, int64_t n) {
   if (i < n) words[i] = 0;
 }
 
+// Which tiles hold foreground: one workgroup per 16 tiles side by side (a 512 x 32 block
+// of one frame), thread t reading row t / 8 of the block, pixels 64 (t % 8) .. + 63 (the
+// row segments of two tiles) with 16-byte loads (kMode 2: mask 16-byte aligned and rows a
+// multiple of 16 bytes), dwords (kMode 1) or bytes (kMode 0), all issued before any is
+// used. A block with foreground sets its tiles' bits and appends their ids to the list.
+template <int kMode>
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask, int W, int H,
+                                                            int64_t frame_px, Tiles T,
+                                                            uint32_t *tile_bits,
+                                                            int32_t *tile_list,
+                                                            uint32_t *n_list) {
+  __shared__ uint32_t s_bits;
+  const int t = threadIdx.x, r = t >> 3, q = t & 7;
+  const int64_t f = blockIdx.z;
+  const int tx0 = blockIdx.x * kScanTiles, ty = blockIdx.y;
+  const int y = ty * kTile + r, x = tx0 * kTile + 64 * q;
+  if (t == 0) s_bits = 0;
+  bool nz0 = false, nz1 = false;  // pixels x .. x + 31, x + 32 .. x + 63 of row y
+  if (y < H && x < W) {
+    const uint8_t *row = mask + f * frame_px + static_cast<int64_t>(y) * W;
+    if (kMode == 2) {  // rows a multiple of 16 bytes: a chunk is wholly inside or outside
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      u32x4 v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        v[i] = x + 16 * i < W ? *reinterpret_cast<const u32x4 *>(row + x + 16 * i) : u32x4{0, 0, 0, 0};
+      const u32x4 a = v[0] | v[1], b = v[2] | v[3];
+      nz0 = (a.x | a.y | a.z | a.w) != 0;
+      nz1 = (b.x | b.y | b.z | b.w) != 0;
+    } else if (kMode == 1) {  // rows a multiple of 4 bytes
+      uint32_t v[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        v[i] = x + 4 * i < W ? *reinterpret_cast<const uint32_t *>(row + x + 4 * i) : 0u;
+      uint32_t a = 0, b = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        a |= v[i];
+        b |= v[i + 8];
+      }
+      nz0 = a != 0;
+      nz1 = b != 0;
+    } else {
+      uint32_t a = 0, b = 0;
+#pragma unroll 8
+      for (int i = 0; i < 32; ++i) {
+        a |= x + i < W ? row[x + i] : 0u;
+        b |= x + 32 + i < W ? row[x + 32 + i] : 0u;
+      }
+      nz0 = a != 0;
+      nz1 = b != 0;
+    }
+  }
+  // lane l of a wave is row l / 8, tile pair l % 8: a tile holds foreground when any of
+  // the wave's rows does
+  const uint64_t b0 = __ballot(nz0), b1 = __ballot(nz1);
+  if ((t & 63) == 0) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      m |= ((b0 >> k) & 0x0101010101010101ull) ? 1u << (2 * k) : 0u;
+      m |= ((b1 >> k) & 0x0101010101010101ull) ? 1u << (2 * k + 1) : 0u;
+    }
+    if (m) atomicOr(&s_bits, m);
+  }
+  __syncthreads();
+  const uint32_t m = s_bits;
+  if (m == 0 || t != 0) return;
+  const int id0 = static_cast<int>((f * T.tiles_y + ty) * T.tiles_x + tx0);
+  const int sh = id0 & 31;
+  atomicOr(&tile_bits[id0 >> 5], m << sh);
+  if (sh > 16 && (m >> (32 - sh)) != 0)  // only words that hold existing tiles
+    atomicOr(&tile_bits[(id0 >> 5) + 1], m >> (32 - sh));
+  int at = static_cast<int>(atomicAdd(n_list, static_cast<uint32_t>(__popc(m))));
+  for (uint32_t k = m; k != 0; k &= k - 1) tile_list[at++] = id0 + __builtin_ctz(k);
+}
+
+// Labels the listed tiles, a grid of kListGroups workgroups walking the list: for each
+// foreground pixel, the frame index of its tile-local root (flagged on the roots).
 template <bool kWord>
 __global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask, int W, int H,
-                                                             int64_t frame_px, int32_t *label,
-                                                             uint32_t *status) {
+                                                             int64_t frame_px, Tiles T,
+                                                             const int32_t *tile_list,
+                                                             const uint32_t *n_list,
+                                                             int32_t *label, uint32_t *status) {
   __shared__ int L[kTile * kTile];
-  const int64_t f = blockIdx.z;
-  const int ty0 = blockIdx.y * kTile;
-  const uint8_t *mf = mask + f * frame_px;
-  uint32_t fg[kTilesPerGroup];
-  load_group_fg<kWord>(mf, W, H, blockIdx.x * kTilesPerGroup * kTile, ty0, fg);
-  uint32_t any = 0;
-#pragma unroll
-  for (int q = 0; q < kTilesPerGroup; ++q) any |= fg[q];
-  if (!__syncthreads_or(any != 0)) return;
-  int32_t *lf = label + f * frame_px;
+  __shared__ uint32_t rows[kTile];
+  const int n = static_cast<int>(*n_list);
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
-  for (int q = 0; q < kTilesPerGroup; ++q) {
-    const int tx0 = (blockIdx.x * kTilesPerGroup + q) * kTile;
-    if (!label_tile(fg[q], L, status)) continue;
+  for (int it = blockIdx.x; it < n; it += gridDim.x) {
+    const TileAt a = tile_at(T, tile_list[it]);
+    const int tx0 = a.tx * kTile, ty0 = a.ty * kTile;
+    const uint32_t fg = load_tile_fg<kWord>(mask + a.f * frame_px, W, H, tx0, ty0);
+    if (!label_tile(fg, L, rows, status)) continue;  // (a listed tile always holds foreground)
+    int32_t *lf = label + a.f * frame_px;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      if (!(fg[q] >> k & 1u)) continue;
+      if (!(fg >> k & 1u)) continue;
       const int i = r * kTile + c0 + k;
       LdsLabels m{L};
       int root = tg_detail::uf_find(m, i);
@@ -285,54 +419,70 @@ __device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint
   }
 }
 
-// Thread i of frame blockIdx.y: 16 consecutive pixels of a border row (rows 32, 64, ...
-// below the first, each against the row above; one 16-byte load where the row is
-// 16-byte aligned), then 16 consecutive pixels of a border column (columns 32, 64, ...,
-// each against the column to its left).
+// Four items per listed tile, walked by a grid of kListGroups workgroups: its top row in
+// two halves of 16 pixels against the row above (one 16-byte load where the row is
+// 16-byte aligned), then its left column in two halves against the column to its left.
+// Every 8-neighbour pair across a tile border is seen from the tile below or to the right
+// of it, and needs foreground on both sides: an item runs only when its own tile is listed
+// and one of the three tiles holding its neighbours is non-empty.
 __global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *mask, int W, int H,
-                                                               int64_t frame_px, bool vec,
-                                                               int row_items, int n_row,
-                                                               int col_items, int n_all,
+                                                               int64_t frame_px, Tiles T,
+                                                               const uint32_t *tile_bits,
+                                                               const int32_t *tile_list,
+                                                               const uint32_t *n_list, bool vec,
                                                                int32_t *label, uint32_t *status) {
-  const int i = blockIdx.x * kBorderThreads + threadIdx.x;
-  if (i >= n_all) return;
-  const int64_t f = blockIdx.y;
-  const uint8_t *mf = mask + f * frame_px;
-  int32_t *lf = label + f * frame_px;
-  uint32_t fg = 0;
-  if (i < n_row) {  // top rows of tiles against the rows above
-    const int b = i / row_items, x0 = 16 * (i - b * row_items), y = (b + 1) * kTile;
-    const uint8_t *p = mf + y * W + x0;
-    if (vec && x0 + 16 <= W) {
-      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-      const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+  const int n4 = 4 * static_cast<int>(*n_list);
+  for (int i = blockIdx.x * kBorderThreads + threadIdx.x; i < n4;
+       i += gridDim.x * kBorderThreads) {
+    const int id = tile_list[i >> 2], k = i & 3;
+    const TileAt a = tile_at(T, id);
+    const uint8_t *mf = mask + a.f * frame_px;
+    int32_t *lf = label + a.f * frame_px;
+    uint32_t fg = 0;
+    if (k < 2) {  // top row of the tile against the row above
+      if (a.ty == 0) continue;
+      const int x0 = a.tx * kTile + 16 * k, y = a.ty * kTile;
+      const int up = id - T.tiles_x;
+      if (x0 >= W || !(tile_set(tile_bits, up) || (a.tx > 0 && tile_set(tile_bits, up - 1)) ||
+                       (a.tx + 1 < T.tiles_x && tile_set(tile_bits, up + 1))))
+        continue;
+      const uint8_t *p = mf + y * W + x0;
+      if (vec && x0 + 16 <= W) {
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) fg |= ((v[k >> 2] >> (8 * (k & 3))) & 0xFFu) ? 1u << k : 0u;
-    } else {
-      const uint8_t *rowp = mf + y * W;
+        for (int j = 0; j < 16; ++j) fg |= ((v[j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << j : 0u;
+      } else {
+        const uint8_t *rowp = mf + y * W;
+        uint32_t v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = rowp[min(x0 + j, W - 1)];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) fg |= (v[j] != 0 && x0 + j < W) ? 1u << j : 0u;
+      }
+      join_border(mf, lf, fg, y * W + x0, 1, (y - 1) * W + x0 - 1, 1, x0, W, status);
+    } else {  // left column of the tile against the column to its left
+      if (a.tx == 0) continue;
+      const int y0 = a.ty * kTile + 16 * (k - 2), x = a.tx * kTile;
+      const int left = id - 1;
+      if (y0 >= H ||
+          !(tile_set(tile_bits, left) || (a.ty > 0 && tile_set(tile_bits, left - T.tiles_x)) ||
+            (a.ty + 1 < T.tiles_y && tile_set(tile_bits, left + T.tiles_x))))
+        continue;
       uint32_t v[16];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) v[k] = rowp[min(x0 + k, W - 1)];
+      for (int j = 0; j < 16; ++j) v[j] = mf[min(y0 + j, H - 1) * W + x];
 #pragma unroll
-      for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && x0 + k < W) ? 1u << k : 0u;
+      for (int j = 0; j < 16; ++j) fg |= (v[j] != 0 && y0 + j < H) ? 1u << j : 0u;
+      join_border(mf, lf, fg, y0 * W + x, W, (y0 - 1) * W + x - 1, W, y0, H, status);
     }
-    join_border(mf, lf, fg, y * W + x0, 1, (y - 1) * W + x0 - 1, 1, x0, W, status);
-  } else {  // left columns of tiles against the columns to their left
-    const int j = i - n_row, b = j / col_items, y0 = 16 * (j - b * col_items);
-    const int x = (b + 1) * kTile;
-    uint32_t v[16];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = mf[min(y0 + k, H - 1) * W + x];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) fg |= (v[k] != 0 && y0 + k < H) ? 1u << k : 0u;
-    join_border(mf, lf, fg, y0 * W + x, W, (y0 - 1) * W + x - 1, W, y0, H, status);
   }
 }
 
 __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
-    const uint8_t *mask, bool vec, int64_t n_px, int64_t frame_px, int64_t n_spans, int32_t *label,
-    Comp *comp, int32_t max_components, uint64_t *words, uint64_t *state,
-    int32_t *n_components) {
+    const uint8_t *mask, bool vec, int64_t n_px, int64_t frame_px, int64_t n_spans, int W,
+    Tiles T, const uint32_t *tile_bits, bool skip, int32_t *label, Comp *comp,
+    int32_t max_components, uint64_t *words, uint64_t *state, int32_t *n_components) {
   __shared__ int s_span, s_base;
   __shared__ int s_wave[kSpanThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -344,15 +494,35 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   const int64_t span = s_span;
   const int64_t p0 = span * kSpan + static_cast<int64_t>(tid) * kSpanPix;
 
+  // Which of this thread's eight 32-pixel words can hold foreground: with rows a multiple
+  // of 32 pixels (`skip`) every word lies in one tile, and only words of non-empty tiles
+  // are read; otherwise all are.
+  uint32_t need = 0xFFu;
+  if (skip && p0 < n_px) {
+    need = 0;
+    int64_t f = p0 / frame_px, loc = p0 - f * frame_px;
+    for (int w = 0; w < kSpanWords && p0 + 32 * w < n_px; ++w) {
+      const int l = static_cast<int>(loc), y = l / W, x = l - y * W;
+      if (tile_set(tile_bits, static_cast<int>((f * T.tiles_y + (y >> 5)) * T.tiles_x + (x >> 5))))
+        need |= 1u << w;
+      loc += 32;
+      if (loc >= frame_px) {
+        loc -= frame_px;
+        ++f;
+      }
+    }
+  }
   // Which of this thread's 256 pixels are foreground (16-byte loads when the mask is
   // 16-byte aligned and the bytes are inside it), then which of those are roots.
   uint32_t fgm[kSpanWords] = {};
-  if (p0 < n_px) {
+  if (p0 < n_px && need != 0) {
     if (vec && p0 + kSpanPix <= n_px) {
       typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
       u32x4 v[kSpanPix / 16];
 #pragma unroll
-      for (int q = 0; q < kSpanPix / 16; ++q) v[q] = *reinterpret_cast<const u32x4 *>(mask + p0 + 16 * q);
+      for (int q = 0; q < kSpanPix / 16; ++q)
+        v[q] = (need >> (q >> 1)) & 1u ? *reinterpret_cast<const u32x4 *>(mask + p0 + 16 * q)
+                                       : u32x4{0, 0, 0, 0};
 #pragma unroll
       for (int q = 0; q < kSpanPix / 16; ++q)
 #pragma unroll
@@ -360,7 +530,8 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
           fgm[q >> 1] |= ((v[q][j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << (16 * (q & 1) + j) : 0u;
     } else {
       for (int j = 0; j < kSpanPix; ++j)
-        fgm[j >> 5] |= (p0 + j < n_px && mask[min(p0 + j, n_px - 1)]) ? 1u << (j & 31) : 0u;
+        fgm[j >> 5] |= ((need >> (j >> 5)) & 1u && p0 + j < n_px && mask[min(p0 + j, n_px - 1)])
+                           ? 1u << (j & 31) : 0u;
     }
   }
   // A foreground pixel is a root when its label is its own frame index, flagged (a
@@ -448,29 +619,27 @@ __device__ __forceinline__ int wave_sum(int v) {
   return v;
 }
 
+// Folds the listed tiles' pixels into their components' records, a grid of kListGroups
+// workgroups walking the list.
 template <bool kWord>
 __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask, int W, int H,
-                                                             int64_t frame_px,
+                                                             int64_t frame_px, Tiles T,
+                                                             const int32_t *tile_list,
+                                                             const uint32_t *n_list,
                                                              const int32_t *label,
                                                              Comp *comp, uint32_t *status) {
   __shared__ int bx0[kTile * kTile], by0[kTile * kTile], bx1[kTile * kTile],
       by1[kTile * kTile], bn[kTile * kTile];
-  const int64_t f = blockIdx.z;
-  const int ty0 = blockIdx.y * kTile;
-  const uint8_t *mf = mask + f * frame_px;
-  uint32_t fgw[kTilesPerGroup];
-  load_group_fg<kWord>(mf, W, H, blockIdx.x * kTilesPerGroup * kTile, ty0, fgw);
-  uint32_t any = 0;
-#pragma unroll
-  for (int q = 0; q < kTilesPerGroup; ++q) any |= fgw[q];
-  if (!__syncthreads_or(any != 0)) return;
-  const int32_t *lf = label + f * frame_px;
-  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
-  const int32_t *row = lf + static_cast<int64_t>(min(y, H - 1)) * W;
-  for (int q = 0; q < kTilesPerGroup; ++q) {
-    const int tx0 = (blockIdx.x * kTilesPerGroup + q) * kTile;
+  const int n_tiles = static_cast<int>(*n_list);
+  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
+  for (int it = blockIdx.x; it < n_tiles; it += gridDim.x) {
+    const TileAt a = tile_at(T, tile_list[it]);
+    const int tx0 = a.tx * kTile, ty0 = a.ty * kTile, y = ty0 + r;
+    const uint32_t fgw = load_tile_fg<kWord>(mask + a.f * frame_px, W, H, tx0, ty0);
+    const int32_t *lf = label + a.f * frame_px;
+    const int32_t *row = lf + static_cast<int64_t>(min(y, H - 1)) * W;
     // (also the barrier between this tile's use of the LDS sums and the previous one's)
-    if (!__syncthreads_or(fgw[q] != 0)) continue;
+    if (!__syncthreads_or(fgw != 0)) continue;
     // The tile-local components come from the labels the local pass left: a foreground
     // pixel's word is its local root, unless the pixel is a local root itself (flagged or
     // already numbered).
@@ -489,7 +658,7 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int i = r * kTile + c0 + k;
-      fg[k] = fgw[q] >> k & 1u;
+      fg[k] = fgw >> k & 1u;
       root[k] = -1;
       if (fg[k]) {
         const int v = lv[k];
@@ -664,11 +833,21 @@ __global__ void empty_kernel(int32_t *n_rois, int32_t *n_components, int32_t *fr
   frame_begin[0] = 0;
 }
 
+Tiles tiles_of(int32_t n_frames, int32_t width, int32_t height) {
+  Tiles T;
+  T.tiles_x = (width + kTile - 1) / kTile;
+  T.tiles_y = (height + kTile - 1) / kTile;
+  T.n = int64_t(n_frames) * T.tiles_x * T.tiles_y;
+  return T;
+}
+
 bool sizes_ok(int32_t n_frames, int32_t width, int32_t height, int32_t max_components) {
   if (n_frames < 0 || n_frames > 65535 || width < 1 || height < 1 || max_components < 1)
     return false;
   if (int64_t(width) * height >= (int64_t(1) << 30)) return false;  // the label flag bit
   if ((int64_t(height) + kTile - 1) / kTile > 65535) return false;
+  const Tiles T = tiles_of(n_frames, width, height);
+  if (T.n >= (int64_t(1) << 31)) return false;  // tile ids are int32
   return true;
 }
 
@@ -677,7 +856,8 @@ bool sizes_ok(int32_t n_frames, int32_t width, int32_t height, int32_t max_compo
 extern "C" size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t height,
                                                int32_t max_components) {
   if (!sizes_ok(n_frames, width, height, max_components)) return 0;
-  return layout(nullptr, int64_t(n_frames) * width * height, max_components).bytes;
+  return layout(nullptr, int64_t(n_frames) * width * height,
+                tiles_of(n_frames, width, height).n, max_components).bytes;
 }
 
 extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
@@ -687,21 +867,22 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   if (a->n_frames > 0 && !a->mask) return TG_E_INVAL;
   if (a->max_rois > 0 && !a->rois) return TG_E_INVAL;
   const int64_t frame_px = int64_t(a->width) * a->height, n_px = a->n_frames * frame_px;
-  const Layout L = layout(a->workspace, n_px, a->max_components);
+  const Tiles T = tiles_of(a->n_frames, a->width, a->height);
+  const Layout L = layout(a->workspace, n_px, T.n, a->max_components);
   if (!a->workspace || a->workspace_bytes < L.bytes ||
       reinterpret_cast<uintptr_t>(a->workspace) % 16 != 0)
     return TG_E_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int W = a->width, H = a->height;
-  const int tiles_x = (W + kTile - 1) / kTile, tiles_y = (H + kTile - 1) / kTile;
-  const dim3 groups((tiles_x + kTilesPerGroup - 1) / kTilesPerGroup, tiles_y,
-                    static_cast<uint32_t>(a->n_frames));
-  // dword mask reads need every row start dword-aligned; 16-byte span reads need the
-  // mask itself 16-byte aligned
+  const dim3 scan_groups(static_cast<uint32_t>((T.tiles_x + kScanTiles - 1) / kScanTiles),
+                         static_cast<uint32_t>(T.tiles_y), static_cast<uint32_t>(a->n_frames));
+  const dim3 list_groups(static_cast<uint32_t>(std::min<int64_t>(T.n, kListGroups)));
+  const dim3 border_groups(static_cast<uint32_t>(
+      std::min<int64_t>((4 * T.n + kBorderThreads - 1) / kBorderThreads, kListGroups)));
+  // dword mask reads need every row start dword-aligned; 16-byte reads need the mask
+  // itself 16-byte aligned (and, for whole rows, rows a multiple of 16 bytes)
   const uintptr_t mp = reinterpret_cast<uintptr_t>(a->mask);
   const bool word = mp % 4 == 0 && W % 4 == 0, vec = mp % 16 == 0;
-  const int row_items = (W + 15) / 16, col_items = (H + 15) / 16;
-  const int n_row = (tiles_y - 1) * row_items, n_all = n_row + (tiles_x - 1) * col_items;
   const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
   const int64_t n_filter = (a->max_components + kFilterBlock - 1) / kFilterBlock;
 
@@ -713,27 +894,35 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   uint32_t *status = reinterpret_cast<uint32_t *>(L.words + 2);
   hipLaunchKernelGGL(clear_kernel, dim3(static_cast<uint32_t>((L.n_words + 255) / 256)),
                      dim3(256), 0, s, L.words, L.n_words);
-  if (word)
-    hipLaunchKernelGGL(local_kernel<true>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label, status);
+  uint32_t *n_list = reinterpret_cast<uint32_t *>(L.words + 3);
+  if (vec && W % 16 == 0)
+    hipLaunchKernelGGL(scan_kernel<2>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
+                       frame_px, T, L.tile_bits, L.tile_list, n_list);
+  else if (word)
+    hipLaunchKernelGGL(scan_kernel<1>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
+                       frame_px, T, L.tile_bits, L.tile_list, n_list);
   else
-    hipLaunchKernelGGL(local_kernel<false>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label, status);
-  if (n_all > 0)
-    hipLaunchKernelGGL(merge_kernel,
-                       dim3(static_cast<uint32_t>((n_all + kBorderThreads - 1) / kBorderThreads),
-                            static_cast<uint32_t>(a->n_frames)),
-                       dim3(kBorderThreads), 0, s, a->mask, W, H, frame_px,
-                       vec && W % 16 == 0, row_items, n_row, col_items, n_all, L.label, status);
+    hipLaunchKernelGGL(scan_kernel<0>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
+                       frame_px, T, L.tile_bits, L.tile_list, n_list);
+  if (word)
+    hipLaunchKernelGGL(local_kernel<true>, list_groups, dim3(kTileThreads), 0, s, a->mask, W, H,
+                       frame_px, T, L.tile_list, n_list, L.label, status);
+  else
+    hipLaunchKernelGGL(local_kernel<false>, list_groups, dim3(kTileThreads), 0, s, a->mask, W,
+                       H, frame_px, T, L.tile_list, n_list, L.label, status);
+  hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, a->mask, W, H,
+                     frame_px, T, L.tile_bits, L.tile_list, n_list, vec && W % 16 == 0, L.label,
+                     status);
   hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_spans)), dim3(kSpanThreads), 0,
-                     s, a->mask, vec, n_px, frame_px, n_spans, L.label, L.comp,
-                     a->max_components, L.words, L.root_state, a->n_components);
+                     s, a->mask, vec, n_px, frame_px, n_spans, W, T, L.tile_bits, W % 32 == 0,
+                     L.label, L.comp, a->max_components, L.words, L.root_state,
+                     a->n_components);
   if (word)
-    hipLaunchKernelGGL(boxes_kernel<true>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label, L.comp, status);
+    hipLaunchKernelGGL(boxes_kernel<true>, list_groups, dim3(kTileThreads), 0, s, a->mask, W, H,
+                       frame_px, T, L.tile_list, n_list, L.label, L.comp, status);
   else
-    hipLaunchKernelGGL(boxes_kernel<false>, groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, L.label, L.comp, status);
+    hipLaunchKernelGGL(boxes_kernel<false>, list_groups, dim3(kTileThreads), 0, s, a->mask, W,
+                       H, frame_px, T, L.tile_list, n_list, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
                      0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,
                      a->areas, a->max_rois, L.kept_frame, L.words, L.filter_state, a->n_rois);
