@@ -51,7 +51,7 @@ constexpr int kTile = 32;
 constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
 constexpr int kScanTiles = 16;     // tiles side by side per workgroup of the scan pass
 constexpr int kScanThreads = 256;  // 8 threads per row of 16 tiles, 64 pixels each
-constexpr int kListGroups = 2048;  // workgroups walking the list of non-empty tiles
+constexpr int kListGroups = 2048;  // list-walking grid when the occupancy query fails
 constexpr int kBorderThreads = 256;
 // Labels: a foreground pixel's word holds its tile-local root (a frame index) once the
 // local pass is done, and never changes afterwards unless the pixel is a tile-local root.
@@ -80,13 +80,25 @@ struct Tiles {
 };
 
 struct Layout {
-  // [0]: roots ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed, then
-  // the look-back words of the roots and filter passes, then the tile bitmap (bit t of
-  // 32-bit word t / 32: tile t holds foreground); all cleared by the first launch
+  // [0]: roots ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed,
+  // [4]: unused, then the look-back words of the roots and filter
+  // passes, then the tile bitmap (bit t of 32-bit word t / 32: tile t holds foreground);
+  // all cleared by the first launch
   uint64_t *words;
   uint64_t *root_state, *filter_state;
   uint32_t *tile_bits;
   int32_t *tile_list;  // ids of the non-empty tiles, in no particular order
+  // Record of the tile at list slot s: fg[32 s + r], row r's foreground as a 32-bit mask;
+  // roots[32 s + r], row r's tile-local roots; border[128 s + e], the tile-local root (a
+  // frame index) of border pixel e: row 0 (e < 32), row 31, column 0, column 31 (e - 96).
+  uint32_t *rec_fg, *rec_roots;
+  int32_t *rec_border;
+  int32_t *tile_slot;  // list slot of each non-empty tile
+  // One entry per tile-local component, at most 256 per tile (8-connected, 32x32):
+  // entries[256 s + j], j < n_ent[s]: local root << 26 | x0 << 21 | x1 << 16 | y1 << 11 |
+  // pixel count, the box in tile coordinates (its top row is the root's).
+  uint64_t *entries;
+  int32_t *n_ent;
   Comp *comp;
   int32_t *kept_frame;
   int32_t *label;
@@ -101,18 +113,31 @@ Layout layout(void *base, int64_t n_px, int64_t n_tiles, int32_t max_components)
   const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
   const int64_t bit_words64 = (n_tiles + 63) / 64;
-  L.n_words = 4 + n_spans + n_filter + bit_words64;
+  L.n_words = 5 + n_spans + n_filter + bit_words64;
+  const size_t nt = static_cast<size_t>(n_tiles);
   const size_t o_list = round_up(8 * static_cast<size_t>(L.n_words), 256);
-  const size_t o_comp = round_up(o_list + 4 * static_cast<size_t>(n_tiles), 256);
+  const size_t o_slot = round_up(o_list + 4 * nt, 256);
+  const size_t o_fg = round_up(o_slot + 4 * nt, 256);
+  const size_t o_roots = round_up(o_fg + 128 * nt, 256);
+  const size_t o_border = round_up(o_roots + 128 * nt, 256);
+  const size_t o_entries = round_up(o_border + 512 * nt, 256);
+  const size_t o_nent = round_up(o_entries + 8 * 256 * nt, 256);
+  const size_t o_comp = round_up(o_nent + 4 * nt, 256);
   const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
   const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
   L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
   char *b = static_cast<char *>(base);
   L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
-  L.root_state = b ? L.words + 4 : nullptr;
+  L.root_state = b ? L.words + 5 : nullptr;
   L.filter_state = b ? L.root_state + n_spans : nullptr;
   L.tile_bits = b ? reinterpret_cast<uint32_t *>(L.filter_state + n_filter) : nullptr;
   L.tile_list = b ? reinterpret_cast<int32_t *>(b + o_list) : nullptr;
+  L.tile_slot = b ? reinterpret_cast<int32_t *>(b + o_slot) : nullptr;
+  L.rec_fg = b ? reinterpret_cast<uint32_t *>(b + o_fg) : nullptr;
+  L.rec_roots = b ? reinterpret_cast<uint32_t *>(b + o_roots) : nullptr;
+  L.rec_border = b ? reinterpret_cast<int32_t *>(b + o_border) : nullptr;
+  L.entries = b ? reinterpret_cast<uint64_t *>(b + o_entries) : nullptr;
+  L.n_ent = b ? reinterpret_cast<int32_t *>(b + o_nent) : nullptr;
   L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
   L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
   L.label = b ? reinterpret_cast<int32_t *>(b + o_label) : nullptr;
@@ -151,30 +176,25 @@ __device__ __forceinline__ void fail(uint32_t *status) {
   __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Foreground bits of this thread's 4 pixels of the tile at column tx0, row ty0: thread t
-// holds row t / 8, columns 4 (t % 8) .. + 3, read from addresses clamped into the frame
-// (pixels outside it are masked off): one dword when every row start is dword-aligned
-// (kWord), else four bytes.
-template <bool kWord>
-__device__ __forceinline__ uint32_t load_tile_fg(const uint8_t *mf, int W, int H, int tx0,
-                                                 int ty0) {
-  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4, y = ty0 + r;
-  const uint8_t *row = mf + static_cast<int64_t>(min(y, H - 1)) * W;
-  const int x0 = tx0 + c0;
-  uint32_t raw[4];
-  if (kWord) {
-    raw[0] = *reinterpret_cast<const uint32_t *>(row + min(x0, W - 4));
-  } else {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) raw[k] = row[min(x0 + k, W - 1)];
-  }
-  uint32_t bits = 0;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint32_t v = kWord ? (raw[0] >> (8 * k)) & 0xFFu : raw[k];
-    bits |= (v != 0 && x0 + k < W) ? 1u << k : 0u;
-  }
-  return y < H ? bits : 0u;
+__device__ __forceinline__ int wave_min(int v) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_max(int v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ int wave_sum(int v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Workgroup barrier that orders LDS only: no wait for the workgroup's outstanding global
+// stores, which a plain __syncthreads() would drain first.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 __device__ __forceinline__ bool tile_set(const uint32_t *bits, int t) {
@@ -195,8 +215,8 @@ __device__ __forceinline__ TileAt tile_at(const Tiles &T, int t) {
 }
 
 // Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
-// within the tile; rows: 32 words of scratch) from this thread's foreground bits
-// (load_tile_fg). Returns false, uniformly, when the tile has no foreground. Starts with a
+// within the tile; rows: 32 words of scratch) from this thread's foreground bits (its 4
+// pixels of row t / 8, columns 4 (t % 8) .. + 3). Returns false, uniformly, when the tile has no foreground. Starts with a
 // barrier, so the caller's previous use of L (and of any other LDS) is over before L is
 // rewritten.
 //
@@ -211,13 +231,28 @@ __device__ __forceinline__ TileAt tile_at(const Tiles &T, int t) {
 __device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *rows,
                                            uint32_t *status) {
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
-  if (!__syncthreads_or(fg != 0)) return false;
-  if (__syncthreads_and(fg == 0xFu)) {  // a solid tile is one set rooted at its pixel 0
+  // rows[0] counts the waves with foreground, rows[1] the waves with every pixel set
+  lds_barrier();  // the caller's previous use of L and rows is over
+  if (t == 0) {
+    rows[0] = 0;
+    rows[1] = 0;
+  }
+  lds_barrier();
+  const uint64_t any = __ballot(fg != 0), all = __ballot(fg == 0xFu);
+  if ((t & 63) == 0) {
+    if (any) atomicAdd(&rows[0], 1u);
+    if (all == ~uint64_t(0)) atomicAdd(&rows[1], 1u);
+  }
+  lds_barrier();
+  const uint32_t n_any = rows[0], n_all = rows[1];
+  if (n_any == 0) return false;
+  if (n_all == kTileThreads / 64) {  // a solid tile is one set rooted at its pixel 0
 #pragma unroll
     for (int k = 0; k < 4; ++k) L[r * kTile + c0 + k] = 0;
-    __syncthreads();
+    lds_barrier();
     return true;
   }
+  lds_barrier();  // every wave has read the counts before rows is rewritten
   // this row's foreground as one word (the 8 threads of a row are 8 consecutive lanes)
   uint32_t row = fg << c0;
   row |= __shfl_xor(row, 1);
@@ -231,7 +266,7 @@ __device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *rows,
     start = (fg >> k & 1u) ? (start >= 0 ? start : i) : -1;
     L[i] = start;
   }
-  __syncthreads();
+  lds_barrier();
   const uint32_t up = r > 0 ? rows[r - 1] : 0u;
   LdsLabels m{L};
   bool ok = true;
@@ -253,7 +288,7 @@ __device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *rows,
     }
   }
   if (!ok) fail(status);
-  __syncthreads();
+  lds_barrier();
   return true;
 }
 
@@ -268,20 +303,23 @@ __global__ void clear_kernel(uint64_t *words, int64_t n) {
 // of one frame), thread t reading row t / 8 of the block, pixels 64 (t % 8) .. + 63 (the
 // row segments of two tiles) with 16-byte loads (kMode 2: mask 16-byte aligned and rows a
 // multiple of 16 bytes), dwords (kMode 1) or bytes (kMode 0), all issued before any is
-// used. A block with foreground sets its tiles' bits and appends their ids to the list.
+// used. A block with foreground sets its tiles' bits, appends them to the list (a tile's
+// list position is its record slot) and writes each listed tile's 32 row masks.
 template <int kMode>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask, int W, int H,
                                                             int64_t frame_px, Tiles T,
                                                             uint32_t *tile_bits,
                                                             int32_t *tile_list,
+                                                            int32_t *tile_slot, uint32_t *rec_fg,
                                                             uint32_t *n_list) {
   __shared__ uint32_t s_bits;
+  __shared__ int s_base;
   const int t = threadIdx.x, r = t >> 3, q = t & 7;
   const int64_t f = blockIdx.z;
   const int tx0 = blockIdx.x * kScanTiles, ty = blockIdx.y;
   const int y = ty * kTile + r, x = tx0 * kTile + 64 * q;
   if (t == 0) s_bits = 0;
-  bool nz0 = false, nz1 = false;  // pixels x .. x + 31, x + 32 .. x + 63 of row y
+  uint32_t m0 = 0, m1 = 0;  // row y: foreground of pixels x + c and x + 32 + c as bit c
   if (y < H && x < W) {
     const uint8_t *row = mask + f * frame_px + static_cast<int64_t>(y) * W;
     if (kMode == 2) {  // rows a multiple of 16 bytes: a chunk is wholly inside or outside
@@ -290,36 +328,42 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         v[i] = x + 16 * i < W ? *reinterpret_cast<const u32x4 *>(row + x + 16 * i) : u32x4{0, 0, 0, 0};
-      const u32x4 a = v[0] | v[1], b = v[2] | v[3];
-      nz0 = (a.x | a.y | a.z | a.w) != 0;
-      nz1 = (b.x | b.y | b.z | b.w) != 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const uint32_t bit = ((v[i][j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << (16 * (i & 1) + j) : 0u;
+          if (i < 2)
+            m0 |= bit;
+          else
+            m1 |= bit;
+        }
     } else if (kMode == 1) {  // rows a multiple of 4 bytes
       uint32_t v[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         v[i] = x + 4 * i < W ? *reinterpret_cast<const uint32_t *>(row + x + 4 * i) : 0u;
-      uint32_t a = 0, b = 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        a |= v[i];
-        b |= v[i + 8];
-      }
-      nz0 = a != 0;
-      nz1 = b != 0;
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t bit = ((v[i] >> (8 * k)) & 0xFFu) ? 1u << (4 * (i & 7) + k) : 0u;
+          if (i < 8)
+            m0 |= bit;
+          else
+            m1 |= bit;
+        }
     } else {
-      uint32_t a = 0, b = 0;
 #pragma unroll 8
       for (int i = 0; i < 32; ++i) {
-        a |= x + i < W ? row[x + i] : 0u;
-        b |= x + 32 + i < W ? row[x + 32 + i] : 0u;
+        m0 |= (x + i < W && row[x + i]) ? 1u << i : 0u;
+        m1 |= (x + 32 + i < W && row[x + 32 + i]) ? 1u << i : 0u;
       }
-      nz0 = a != 0;
-      nz1 = b != 0;
     }
   }
   // lane l of a wave is row l / 8, tile pair l % 8: a tile holds foreground when any of
   // the wave's rows does
-  const uint64_t b0 = __ballot(nz0), b1 = __ballot(nz1);
+  const uint64_t b0 = __ballot(m0 != 0), b1 = __ballot(m1 != 0);
   if ((t & 63) == 0) {
     uint32_t m = 0;
 #pragma unroll
@@ -331,78 +375,166 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
   }
   __syncthreads();
   const uint32_t m = s_bits;
-  if (m == 0 || t != 0) return;
+  if (m == 0) return;  // uniform
   const int id0 = static_cast<int>((f * T.tiles_y + ty) * T.tiles_x + tx0);
-  const int sh = id0 & 31;
-  atomicOr(&tile_bits[id0 >> 5], m << sh);
-  if (sh > 16 && (m >> (32 - sh)) != 0)  // only words that hold existing tiles
-    atomicOr(&tile_bits[(id0 >> 5) + 1], m >> (32 - sh));
-  int at = static_cast<int>(atomicAdd(n_list, static_cast<uint32_t>(__popc(m))));
-  for (uint32_t k = m; k != 0; k &= k - 1) tile_list[at++] = id0 + __builtin_ctz(k);
+  if (t == 0) {
+    const int sh = id0 & 31;
+    atomicOr(&tile_bits[id0 >> 5], m << sh);
+    if (sh > 16 && (m >> (32 - sh)) != 0)  // only words that hold existing tiles
+      atomicOr(&tile_bits[(id0 >> 5) + 1], m >> (32 - sh));
+    s_base = static_cast<int>(atomicAdd(n_list, static_cast<uint32_t>(__popc(m))));
+  }
+  __syncthreads();
+  const int base = s_base;
+  if (t < kScanTiles && (m >> t & 1u)) {
+    const int slot = base + __popc(m & ((1u << t) - 1u));
+    tile_list[slot] = id0 + t;
+    tile_slot[id0 + t] = slot;
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int j = 2 * q + h;
+    if (m >> j & 1u)
+      rec_fg[32 * (base + __popc(m & ((1u << j) - 1u))) + r] = h ? m1 : m0;
+  }
 }
 
 // Labels the listed tiles, a grid of kListGroups workgroups walking the list: for each
 // foreground pixel, the frame index of its tile-local root (flagged on the roots).
-template <bool kWord>
-__global__ __launch_bounds__(kTileThreads) void local_kernel(const uint8_t *mask, int W, int H,
-                                                             int64_t frame_px, Tiles T,
+__global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t frame_px, Tiles T,
                                                              const int32_t *tile_list,
                                                              const uint32_t *n_list,
-                                                             int32_t *label, uint32_t *status) {
+                                                             const uint32_t *rec_fg,
+                                                             uint32_t *rec_roots,
+                                                             int32_t *rec_border, uint64_t *entries,
+                                                             int32_t *n_ent, int32_t *label,
+                                                             uint32_t *status) {
   __shared__ int L[kTile * kTile];
   __shared__ uint32_t rows[kTile];
+  __shared__ int s_wave[kTileThreads / 64];
+  __shared__ int sx0[kTile * kTile], sx1[kTile * kTile], sy1[kTile * kTile], sn[kTile * kTile];
   const int n = static_cast<int>(*n_list);
-  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
+  const int t = threadIdx.x, lane = t & 63, r = t >> 3, c0 = (t & 7) * 4;
   for (int it = blockIdx.x; it < n; it += gridDim.x) {
     const TileAt a = tile_at(T, tile_list[it]);
     const int tx0 = a.tx * kTile, ty0 = a.ty * kTile;
-    const uint32_t fg = load_tile_fg<kWord>(mask + a.f * frame_px, W, H, tx0, ty0);
+    const uint32_t fg = (rec_fg[32 * it + r] >> c0) & 0xFu;
+    // (starts with a barrier: the previous tile's use of the LDS arrays is over)
     if (!label_tile(fg, L, rows, status)) continue;  // (a listed tile always holds foreground)
     int32_t *lf = label + a.f * frame_px;
+    int32_t *border = rec_border + 128 * static_cast<int64_t>(it);
+    uint32_t rb = 0;  // this thread's local roots, as bits of its row
+    int root[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
+      root[k] = -1;
       if (!(fg >> k & 1u)) continue;
-      const int i = r * kTile + c0 + k;
+      const int c = c0 + k, i = r * kTile + c;
       LdsLabels m{L};
-      int root = tg_detail::uf_find(m, i);
-      if (root < 0) {
+      int rt = tg_detail::uf_find(m, i);
+      if (rt < 0) {
         fail(status);
-        root = i;
+        rt = i;
       }
-      const int gr = (ty0 + (root >> 5)) * W + tx0 + (root & (kTile - 1));
-      lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c0 + k] = root == i ? gr | kRootFlag : gr;
+      root[k] = rt;
+      const int gr = (ty0 + (rt >> 5)) * W + tx0 + (rt & (kTile - 1));
+      lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c] = rt == i ? gr | kRootFlag : gr;
+      rb |= rt == i ? 1u << c : 0u;
+      if (r == 0) border[c] = gr;
+      if (r == kTile - 1) border[32 + c] = gr;
+      if (c == 0) border[64 + r] = gr;
+      if (c == kTile - 1) border[96 + r] = gr;
+      if (rt == i) {
+        sx0[i] = kTile;
+        sx1[i] = -1;
+        sy1[i] = -1;
+        sn[i] = 0;
+      }
+    }
+    rb |= __shfl_xor(rb, 1);
+    rb |= __shfl_xor(rb, 2);
+    rb |= __shfl_xor(rb, 4);
+    if ((t & 7) == 0) rec_roots[32 * it + r] = rb;
+    lds_barrier();
+    // Each local component's box (tile coordinates) and pixel count, folded in LDS: a
+    // thread folds each run of its pixels with one root once; when every foreground pixel
+    // of the wave has one root, the wave reduces first and folds once.
+    {
+      const uint32_t fgb = fg;
+      const int lead0 = fgb ? root[__builtin_ctz(fgb)] : -1;
+      bool one = true;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) one &= root[k] < 0 || root[k] == lead0;
+      const uint64_t any = __ballot(fgb != 0);
+      const int lead = any ? __shfl(lead0, __builtin_ctzll(any)) : -1;
+      if (any && __ballot(fgb != 0 && !(one && lead0 == lead)) == 0) {
+        const int mx0 = wave_min(fgb ? c0 + __builtin_ctz(fgb) : INT_MAX);
+        const int mx1 = wave_max(fgb ? c0 + 31 - __builtin_clz(fgb) : INT_MIN);
+        const int my1 = wave_max(fgb ? r : INT_MIN), cnt = wave_sum(__popc(fgb));
+        if (lane == 0) {
+          atomicMin(&sx0[lead], mx0);
+          atomicMax(&sx1[lead], mx1);
+          atomicMax(&sy1[lead], my1);
+          atomicAdd(&sn[lead], cnt);
+        }
+      } else {
+        int k = 0;
+        while (k < 4) {
+          if (root[k] < 0) {
+            ++k;
+            continue;
+          }
+          int e = k + 1;  // pixels k .. e - 1 share root[k]
+          while (e < 4 && root[e] == root[k]) ++e;
+          const int rt = root[k];
+          atomicMin(&sx0[rt], c0 + k);
+          atomicMax(&sx1[rt], c0 + e - 1);
+          atomicMax(&sy1[rt], r);
+          atomicAdd(&sn[rt], e - k);
+          k = e;
+        }
+      }
+    }
+    lds_barrier();
+    // one entry per local component, in the tile's own 256 entries
+    int mine = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) mine += root[k] == r * kTile + c0 + k;
+    int incl = mine;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    if (lane == 63) s_wave[t >> 6] = incl;
+    lds_barrier();
+    int at = incl - mine, total = 0;
+#pragma unroll
+    for (int w = 0; w < kTileThreads / 64; ++w) {
+      if (w < (t >> 6)) at += s_wave[w];
+      total += s_wave[w];
+    }
+    if (t == 0) n_ent[it] = total;
+    uint64_t *ent = entries + 256 * static_cast<int64_t>(it);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = r * kTile + c0 + k;
+      if (root[k] != i) continue;
+      ent[at++] = static_cast<uint64_t>(i) << 26 | static_cast<uint64_t>(sx0[i]) << 21 |
+                  static_cast<uint64_t>(sx1[i]) << 16 | static_cast<uint64_t>(sy1[i]) << 11 |
+                  static_cast<uint64_t>(sn[i]);
     }
   }
 }
 
-// Joins the foreground pixels of a 16-pixel run along a tile border (bits of `fg`) with
-// their foreground neighbours across it. Along the border the run covers coordinates
-// start .. start + 15 of [0, lim); pixel k is frame index own0 + k ostep, and the 18
-// pixels across the border at coordinates start - 1 .. start + 16 are nb0 + k' nstep.
-// Neighbour bytes and all labels are read first (addresses clamped into the frame), then
-// each pixel joins neighbours k, k + 1, k + 2 through their current labels (members of
-// their sets), skipping a pair equal to the one just joined: along a border most repeat.
-__device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint32_t fg, int own0,
-                                            int ostep, int nb0, int nstep, int start, int lim,
-                                            uint32_t *status) {
-  if (fg == 0) return;
-  uint32_t m[18];
-  int32_t ln[18], lo[16];
-#pragma unroll
-  for (int k = 0; k < 18; ++k) {
-    const int c = min(max(start - 1 + k, 0), lim - 1);
-    const int idx = nb0 + (c - (start - 1)) * nstep;
-    m[k] = mf[idx];
-    ln[k] = g_load(&lf[idx]) & kIndex;
-  }
-#pragma unroll
-  for (int k = 0; k < 16; ++k)
-    lo[k] = g_load(&lf[own0 + (min(start + k, lim - 1) - start) * ostep]) & kIndex;
-  uint32_t nb = 0;
-#pragma unroll
-  for (int k = 0; k < 18; ++k)
-    nb |= (m[k] != 0 && start - 1 + k >= 0 && start - 1 + k < lim) ? 1u << k : 0u;
+// Joins the foreground pixels of a 16-pixel run along a tile border (bits of fg, their
+// tile-local roots lo) with their foreground neighbours across it: the 18 pixels at
+// offsets -1 .. 16 along the border (bits of nb, tile-local roots ln). Pixel k meets
+// neighbours k, k + 1, k + 2; a pair equal to the one just joined is skipped (along a
+// border most repeat).
+__device__ __forceinline__ void join_pairs(int32_t *lf, uint32_t fg, const int32_t lo[16],
+                                           uint32_t nb, const int32_t ln[18], uint32_t *status) {
   int pa = -1, pb = -1;
+  RootLabels m{lf};
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     if (!(fg >> k & 1u)) continue;
@@ -411,7 +543,6 @@ __device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint
       if (!(nb >> (k + d) & 1u)) continue;
       const int a = lo[k], b = ln[k + d];
       if (a == pa && b == pb) continue;
-      RootLabels m{lf};
       if (!tg_detail::uf_unite(m, a, b)) fail(status);
       pa = a;
       pb = b;
@@ -420,69 +551,103 @@ __device__ __forceinline__ void join_border(const uint8_t *mf, int32_t *lf, uint
 }
 
 // Four items per listed tile, walked by a grid of kListGroups workgroups: its top row in
-// two halves of 16 pixels against the row above (one 16-byte load where the row is
-// 16-byte aligned), then its left column in two halves against the column to its left.
-// Every 8-neighbour pair across a tile border is seen from the tile below or to the right
-// of it, and needs foreground on both sides: an item runs only when its own tile is listed
-// and one of the three tiles holding its neighbours is non-empty.
-__global__ __launch_bounds__(kBorderThreads) void merge_kernel(const uint8_t *mask, int W, int H,
-                                                               int64_t frame_px, Tiles T,
-                                                               const uint32_t *tile_bits,
-                                                               const int32_t *tile_list,
-                                                               const uint32_t *n_list, bool vec,
-                                                               int32_t *label, uint32_t *status) {
+// two halves of 16 pixels against the row above, then its left column in two halves
+// against the column to its left. Every 8-neighbour pair across a tile border is seen
+// from the tile below or to the right of it. Foreground bits and tile-local roots come
+// from the tiles' records (the tile itself and the up to three tiles holding the
+// neighbours); an item whose neighbouring tiles are all empty is skipped.
+__global__ __launch_bounds__(kBorderThreads) void merge_kernel(
+    int64_t frame_px, Tiles T, const uint32_t *tile_bits, const int32_t *tile_slot,
+    const int32_t *tile_list, const uint32_t *n_list, const uint32_t *rec_fg,
+    const int32_t *rec_border, int32_t *label, uint32_t *status) {
   const int n4 = 4 * static_cast<int>(*n_list);
   for (int i = blockIdx.x * kBorderThreads + threadIdx.x; i < n4;
        i += gridDim.x * kBorderThreads) {
-    const int id = tile_list[i >> 2], k = i & 3;
+    const int s = i >> 2, k = i & 3, id = tile_list[s];
     const TileAt a = tile_at(T, id);
-    const uint8_t *mf = mask + a.f * frame_px;
-    int32_t *lf = label + a.f * frame_px;
-    uint32_t fg = 0;
-    if (k < 2) {  // top row of the tile against the row above
+    const uint32_t *fs = rec_fg + 32 * static_cast<int64_t>(s);
+    const int32_t *bs = rec_border + 128 * static_cast<int64_t>(s);
+    uint32_t fg = 0, nb = 0;
+    int32_t lo[16], ln[18];
+#pragma unroll
+    for (int j = 0; j < 18; ++j) ln[j] = 0;
+    if (k < 2) {  // top row, pixels 16 h .. 16 h + 15, against row 31 of the tiles above
+      const int h = k, up = id - T.tiles_x;
       if (a.ty == 0) continue;
-      const int x0 = a.tx * kTile + 16 * k, y = a.ty * kTile;
-      const int up = id - T.tiles_x;
-      if (x0 >= W || !(tile_set(tile_bits, up) || (a.tx > 0 && tile_set(tile_bits, up - 1)) ||
-                       (a.tx + 1 < T.tiles_x && tile_set(tile_bits, up + 1))))
-        continue;
-      const uint8_t *p = mf + y * W + x0;
-      if (vec && x0 + 16 <= W) {
-        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-        const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+      const bool u = tile_set(tile_bits, up);
+      const bool ul = h == 0 && a.tx > 0 && tile_set(tile_bits, up - 1);
+      const bool ur = h == 1 && a.tx + 1 < T.tiles_x && tile_set(tile_bits, up + 1);
+      if (!(u || ul || ur)) continue;
+      fg = (fs[0] >> (16 * h)) & 0xFFFFu;
+      if (fg == 0) continue;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) fg |= ((v[j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << j : 0u;
-      } else {
-        const uint8_t *rowp = mf + y * W;
-        uint32_t v[16];
+      for (int j = 0; j < 16; ++j) lo[j] = bs[16 * h + j];
+      if (u) {  // neighbour j is column 16 h - 1 + j of the tile above
+        const int64_t su = tile_slot[up];
+        const uint32_t row = rec_fg[32 * su + 31];
+        const int32_t *b = rec_border + 128 * su + 32;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) v[j] = rowp[min(x0 + j, W - 1)];
-#pragma unroll
-        for (int j = 0; j < 16; ++j) fg |= (v[j] != 0 && x0 + j < W) ? 1u << j : 0u;
+        for (int j = 0; j < 18; ++j) {
+          const int c = 16 * h - 1 + j;
+          if (c < 0 || c >= kTile) continue;
+          nb |= (row >> c & 1u) << j;
+          ln[j] = b[c];
+        }
       }
-      join_border(mf, lf, fg, y * W + x0, 1, (y - 1) * W + x0 - 1, 1, x0, W, status);
-    } else {  // left column of the tile against the column to its left
+      if (ul) {  // column 31 of the tile above and to the left
+        const int64_t sl = tile_slot[up - 1];
+        nb |= rec_fg[32 * sl + 31] >> 31;
+        ln[0] = rec_border[128 * sl + 32 + 31];
+      }
+      if (ur) {  // column 0 of the tile above and to the right
+        const int64_t sr = tile_slot[up + 1];
+        nb |= (rec_fg[32 * sr + 31] & 1u) << 17;
+        ln[17] = rec_border[128 * sr + 32];
+      }
+    } else {  // left column, rows 16 h .. 16 h + 15, against column 31 of the tiles left
+      const int h = k - 2, left = id - 1;
       if (a.tx == 0) continue;
-      const int y0 = a.ty * kTile + 16 * (k - 2), x = a.tx * kTile;
-      const int left = id - 1;
-      if (y0 >= H ||
-          !(tile_set(tile_bits, left) || (a.ty > 0 && tile_set(tile_bits, left - T.tiles_x)) ||
-            (a.ty + 1 < T.tiles_y && tile_set(tile_bits, left + T.tiles_x))))
-        continue;
-      uint32_t v[16];
+      const bool l = tile_set(tile_bits, left);
+      const bool lu = h == 0 && a.ty > 0 && tile_set(tile_bits, left - T.tiles_x);
+      const bool ld = h == 1 && a.ty + 1 < T.tiles_y && tile_set(tile_bits, left + T.tiles_x);
+      if (!(l || lu || ld)) continue;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) v[j] = mf[min(y0 + j, H - 1) * W + x];
+      for (int j = 0; j < 16; ++j) fg |= (fs[16 * h + j] & 1u) << j;
+      if (fg == 0) continue;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) fg |= (v[j] != 0 && y0 + j < H) ? 1u << j : 0u;
-      join_border(mf, lf, fg, y0 * W + x, W, (y0 - 1) * W + x - 1, W, y0, H, status);
+      for (int j = 0; j < 16; ++j) lo[j] = bs[64 + 16 * h + j];
+      if (l) {  // neighbour j is row 16 h - 1 + j of the tile to the left
+        const int64_t sl = tile_slot[left];
+        const uint32_t *f = rec_fg + 32 * sl;
+        const int32_t *b = rec_border + 128 * sl + 96;
+#pragma unroll
+        for (int j = 0; j < 18; ++j) {
+          const int rr = 16 * h - 1 + j;
+          if (rr < 0 || rr >= kTile) continue;
+          nb |= (f[rr] >> 31) << j;
+          ln[j] = b[rr];
+        }
+      }
+      if (lu) {  // row 31 of the tile to the left and above
+        const int64_t su = tile_slot[left - T.tiles_x];
+        nb |= rec_fg[32 * su + 31] >> 31;
+        ln[0] = rec_border[128 * su + 96 + 31];
+      }
+      if (ld) {  // row 0 of the tile to the left and below
+        const int64_t sd = tile_slot[left + T.tiles_x];
+        nb |= (rec_fg[32 * sd] >> 31) << 17;
+        ln[17] = rec_border[128 * sd + 96];
+      }
     }
+    join_pairs(label + a.f * frame_px, fg, lo, nb, ln, status);
   }
 }
 
 __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
     const uint8_t *mask, bool vec, int64_t n_px, int64_t frame_px, int64_t n_spans, int W,
-    Tiles T, const uint32_t *tile_bits, bool skip, int32_t *label, Comp *comp,
-    int32_t max_components, uint64_t *words, uint64_t *state, int32_t *n_components) {
+    Tiles T, const uint32_t *tile_bits, const int32_t *tile_slot, const uint32_t *rec_roots,
+    bool aligned, int32_t *label, Comp *comp, int32_t max_components, uint64_t *words,
+    uint64_t *state, int32_t *n_components) {
   __shared__ int s_span, s_base;
   __shared__ int s_wave[kSpanThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -494,35 +659,48 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   const int64_t span = s_span;
   const int64_t p0 = span * kSpan + static_cast<int64_t>(tid) * kSpanPix;
 
-  // Which of this thread's eight 32-pixel words can hold foreground: with rows a multiple
-  // of 32 pixels (`skip`) every word lies in one tile, and only words of non-empty tiles
-  // are read; otherwise all are.
-  uint32_t need = 0xFFu;
-  if (skip && p0 < n_px) {
-    need = 0;
+  // The components are the tile-local roots still their own parent (label = own frame
+  // index, flagged). With rows a multiple of 32 pixels (`aligned`) each of this thread's
+  // eight 32-pixel words is one row of one tile: its candidates are that row of the tile's
+  // local roots (its record; none for an empty tile), and only their labels are read.
+  // Otherwise the thread reads its 256 mask bytes (16-byte loads when the mask is
+  // 16-byte aligned and the bytes are inside it) and tests every foreground pixel.
+  uint32_t roots[kSpanWords] = {};
+  int cnt = 0;
+  if (aligned && p0 < n_px) {
+    uint32_t cand[kSpanWords] = {};
     int64_t f = p0 / frame_px, loc = p0 - f * frame_px;
-    for (int w = 0; w < kSpanWords && p0 + 32 * w < n_px; ++w) {
-      const int l = static_cast<int>(loc), y = l / W, x = l - y * W;
-      if (tile_set(tile_bits, static_cast<int>((f * T.tiles_y + (y >> 5)) * T.tiles_x + (x >> 5))))
-        need |= 1u << w;
+    int lw[kSpanWords];  // frame index of each word's first pixel
+#pragma unroll
+    for (int w = 0; w < kSpanWords; ++w) {
+      lw[w] = static_cast<int>(loc);
+      if (p0 + 32 * w < n_px) {
+        const int l = static_cast<int>(loc), y = l / W, x = l - y * W;
+        const int tile = static_cast<int>((f * T.tiles_y + (y >> 5)) * T.tiles_x + (x >> 5));
+        if (tile_set(tile_bits, tile)) cand[w] = rec_roots[32 * static_cast<int64_t>(tile_slot[tile]) + (y & 31)];
+      }
       loc += 32;
       if (loc >= frame_px) {
         loc -= frame_px;
         ++f;
       }
     }
-  }
-  // Which of this thread's 256 pixels are foreground (16-byte loads when the mask is
-  // 16-byte aligned and the bytes are inside it), then which of those are roots.
-  uint32_t fgm[kSpanWords] = {};
-  if (p0 < n_px && need != 0) {
+#pragma unroll
+    for (int w = 0; w < kSpanWords; ++w) {
+      for (uint32_t m = cand[w]; m != 0; m &= m - 1) {
+        const int j = __builtin_ctz(m);
+        if (label[p0 + 32 * w + j] == ((lw[w] + j) | kRootFlag)) roots[w] |= 1u << j;
+      }
+      cnt += __popc(roots[w]);
+    }
+  } else if (p0 < n_px) {
+    uint32_t fgm[kSpanWords] = {};
     if (vec && p0 + kSpanPix <= n_px) {
       typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
       u32x4 v[kSpanPix / 16];
 #pragma unroll
       for (int q = 0; q < kSpanPix / 16; ++q)
-        v[q] = (need >> (q >> 1)) & 1u ? *reinterpret_cast<const u32x4 *>(mask + p0 + 16 * q)
-                                       : u32x4{0, 0, 0, 0};
+        v[q] = *reinterpret_cast<const u32x4 *>(mask + p0 + 16 * q);
 #pragma unroll
       for (int q = 0; q < kSpanPix / 16; ++q)
 #pragma unroll
@@ -530,42 +708,17 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
           fgm[q >> 1] |= ((v[q][j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << (16 * (q & 1) + j) : 0u;
     } else {
       for (int j = 0; j < kSpanPix; ++j)
-        fgm[j >> 5] |= ((need >> (j >> 5)) & 1u && p0 + j < n_px && mask[min(p0 + j, n_px - 1)])
-                           ? 1u << (j & 31) : 0u;
+        fgm[j >> 5] |= (p0 + j < n_px && mask[min(p0 + j, n_px - 1)]) ? 1u << (j & 31) : 0u;
     }
-  }
-  // A foreground pixel is a root when its label is its own frame index, flagged (a
-  // tile-local root still its own parent). The 32 labels of a
-  // word with any foreground are read as eight 16-byte loads issued together (one round
-  // trip per word, not one per pixel); a word that would leave the label array, or frames
-  // of under 32 pixels, go pixel by pixel.
-  uint32_t roots[kSpanWords] = {};
-  int cnt = 0;
-#pragma unroll
-  for (int w = 0; w < kSpanWords; ++w) {
-    if (fgm[w] == 0) continue;
-    const int64_t P0 = p0 + 32 * w;
-    if (P0 + 32 <= n_px && frame_px >= 32) {
-      typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-      i32x4 lv[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) lv[q] = *reinterpret_cast<const i32x4 *>(label + P0 + 4 * q);
-      int64_t local = P0 % frame_px;
-#pragma unroll
-      for (int j = 0; j < 32; ++j) {
-        if (local == frame_px) local = 0;
-        if ((fgm[w] >> j & 1u) && lv[j >> 2][j & 3] == (static_cast<int32_t>(local) | kRootFlag))
-          roots[w] |= 1u << j;
-        ++local;
-      }
-    } else {
+    for (int w = 0; w < kSpanWords; ++w) {
+      const int64_t P0 = p0 + 32 * w;
       for (uint32_t m = fgm[w]; m != 0; m &= m - 1) {
         const int j = __builtin_ctz(m);
         const int64_t P = P0 + j;
         if (label[P] == (static_cast<int32_t>(P % frame_px) | kRootFlag)) roots[w] |= 1u << j;
       }
+      cnt += __popc(roots[w]);
     }
-    cnt += __popc(roots[w]);
   }
 
   // Exclusive scan of the counts over the workgroup, then the look-back over spans.
@@ -606,132 +759,50 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   }
 }
 
-__device__ __forceinline__ int wave_min(int v) {
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_max(int v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_sum(int v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
 
-// Folds the listed tiles' pixels into their components' records, a grid of kListGroups
-// workgroups walking the list.
-template <bool kWord>
-__global__ __launch_bounds__(kTileThreads) void boxes_kernel(const uint8_t *mask, int W, int H,
-                                                             int64_t frame_px, Tiles T,
+// Folds each tile-local component (its entry) into its component's record: up the
+// union-find from its local root to the numbered root, then one set of global atomics.
+// A grid of resident workgroups walks the listed tiles' entry slots.
+__global__ __launch_bounds__(kTileThreads) void boxes_kernel(int W, int64_t frame_px, Tiles T,
                                                              const int32_t *tile_list,
                                                              const uint32_t *n_list,
-                                                             const int32_t *label,
-                                                             Comp *comp, uint32_t *status) {
-  __shared__ int bx0[kTile * kTile], by0[kTile * kTile], bx1[kTile * kTile],
-      by1[kTile * kTile], bn[kTile * kTile];
-  const int n_tiles = static_cast<int>(*n_list);
-  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
-  for (int it = blockIdx.x; it < n_tiles; it += gridDim.x) {
-    const TileAt a = tile_at(T, tile_list[it]);
-    const int tx0 = a.tx * kTile, ty0 = a.ty * kTile, y = ty0 + r;
-    const uint32_t fgw = load_tile_fg<kWord>(mask + a.f * frame_px, W, H, tx0, ty0);
+                                                             const uint64_t *entries,
+                                                             const int32_t *n_ent,
+                                                             const int32_t *label, Comp *comp,
+                                                             uint32_t *status) {
+  const int64_t n = 256 * static_cast<int64_t>(*n_list);
+  for (int64_t e = blockIdx.x * kTileThreads + threadIdx.x; e < n;
+       e += static_cast<int64_t>(gridDim.x) * kTileThreads) {
+    const int slot = static_cast<int>(e >> 8);
+    if ((e & 255) >= n_ent[slot]) continue;
+    const uint64_t v64 = entries[e];
+    const int i = static_cast<int>(v64 >> 26) & 1023;
+    const int ex0 = static_cast<int>(v64 >> 21) & 31, ex1 = static_cast<int>(v64 >> 16) & 31;
+    const int ey1 = static_cast<int>(v64 >> 11) & 31, cnt = static_cast<int>(v64 & 2047);
+    const TileAt a = tile_at(T, tile_list[slot]);
+    const int x0 = a.tx * kTile, y0 = a.ty * kTile;
     const int32_t *lf = label + a.f * frame_px;
-    const int32_t *row = lf + static_cast<int64_t>(min(y, H - 1)) * W;
-    // (also the barrier between this tile's use of the LDS sums and the previous one's)
-    if (!__syncthreads_or(fgw != 0)) continue;
-    // The tile-local components come from the labels the local pass left: a foreground
-    // pixel's word is its local root, unless the pixel is a local root itself (flagged or
-    // already numbered).
-    int32_t lv[4];
-    if (kWord) {
-      typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-      const i32x4 v = *reinterpret_cast<const i32x4 *>(row + min(tx0 + c0, W - 4));
-#pragma unroll
-      for (int k = 0; k < 4; ++k) lv[k] = v[k];
-    } else {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) lv[k] = row[min(tx0 + c0 + k, W - 1)];
-    }
-    bool fg[4];
-    int root[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = r * kTile + c0 + k;
-      fg[k] = fgw >> k & 1u;
-      root[k] = -1;
-      if (fg[k]) {
-        const int v = lv[k];
-        if (v < 0 || (v & kRootFlag)) {
-          root[k] = i;
-        } else {
-          const int vy = v / W;
-          root[k] = (vy - ty0) * kTile + (v - vy * W - tx0);
-        }
+    // up the union-find over local roots to the numbered root; every link points to a
+    // smaller index (unionfind.h), so the walk ends -- a link that does not is reported
+    int cur = (y0 + (i >> 5)) * W + x0 + (i & 31);
+    int v = lf[cur];
+    while (v >= 0) {
+      const int nx = v & kIndex;
+      if (nx == cur) break;
+      if (nx > cur) {
+        fail(status);
+        break;
       }
-      if (root[k] == i) {
-        bx0[i] = INT_MAX;
-        by0[i] = INT_MAX;
-        bx1[i] = INT_MIN;
-        by1[i] = INT_MIN;
-        bn[i] = 0;
-      }
+      cur = nx;
+      v = lf[cur];
     }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int x = tx0 + c0 + k;
-      // When every foreground lane of the wave is in one local component, reduce across
-      // the wave first and fold once.
-      const uint64_t fgm = __ballot(fg[k]);
-      if (!fgm) continue;
-      const int lead = __shfl(root[k], __builtin_ctzll(fgm));
-      if (__ballot(fg[k] && root[k] != lead) == 0) {
-        const int mx0 = wave_min(fg[k] ? x : INT_MAX), my0 = wave_min(fg[k] ? y : INT_MAX);
-        const int mx1 = wave_max(fg[k] ? x : INT_MIN), my1 = wave_max(fg[k] ? y : INT_MIN);
-        const int n = wave_sum(fg[k] ? 1 : 0);
-        if ((threadIdx.x & 63) == 0) {
-          atomicMin(&bx0[lead], mx0);
-          atomicMin(&by0[lead], my0);
-          atomicMax(&bx1[lead], mx1);
-          atomicMax(&by1[lead], my1);
-          atomicAdd(&bn[lead], n);
-        }
-      } else if (fg[k]) {
-        atomicMin(&bx0[root[k]], x);
-        atomicMin(&by0[root[k]], y);
-        atomicMax(&bx1[root[k]], x);
-        atomicMax(&by1[root[k]], y);
-        atomicAdd(&bn[root[k]], 1);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = r * kTile + c0 + k;
-      if (root[k] != i) continue;
-      // up the union-find over local roots to the numbered root; every link points to a
-      // smaller index (unionfind.h), so the walk ends -- a link that does not is reported
-      int cur = y * W + tx0 + c0 + k;
-      int v = lv[k];
-      while (v >= 0) {
-        const int nx = v & kIndex;
-        if (nx == cur) break;
-        if (nx > cur) {
-          fail(status);
-          break;
-        }
-        cur = nx;
-        v = lf[cur];
-      }
-      if (v >= 0) continue;  // a component past max_components (or a broken link): not measured
-      Comp *c = comp + (-v - 1);
-      atomicMin(&c->x0, bx0[i]);
-      atomicMin(&c->y0, by0[i]);
-      atomicMax(&c->x1, bx1[i]);
-      atomicMax(&c->y1, by1[i]);
-      atomicAdd(&c->area, bn[i]);
-    }
+    if (v >= 0) continue;  // a component past max_components (or a broken link): not measured
+    Comp *c = comp + (-v - 1);
+    atomicMin(&c->x0, x0 + ex0);
+    atomicMin(&c->y0, y0 + (i >> 5));
+    atomicMax(&c->x1, x0 + ex1);
+    atomicMax(&c->y1, y0 + ey1);
+    atomicAdd(&c->area, cnt);
   }
 }
 
@@ -833,6 +904,18 @@ __global__ void empty_kernel(int32_t *n_rois, int32_t *n_components, int32_t *fr
   frame_begin[0] = 0;
 }
 
+// Workgroups of `kernel` (`threads` each) resident on the current device at once, at
+// least 1: the grid of a pass that walks a list, so that no workgroup waits for a slot
+// while others walk their share.
+int resident_groups(const void *kernel, int threads) {
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
+    return kListGroups;
+  return std::max(1, cus * per);
+}
+
 Tiles tiles_of(int32_t n_frames, int32_t width, int32_t height) {
   Tiles T;
   T.tiles_x = (width + kTile - 1) / kTile;
@@ -847,7 +930,7 @@ bool sizes_ok(int32_t n_frames, int32_t width, int32_t height, int32_t max_compo
   if (int64_t(width) * height >= (int64_t(1) << 30)) return false;  // the label flag bit
   if ((int64_t(height) + kTile - 1) / kTile > 65535) return false;
   const Tiles T = tiles_of(n_frames, width, height);
-  if (T.n >= (int64_t(1) << 31)) return false;  // tile ids are int32
+  if (T.n >= (int64_t(1) << 28)) return false;  // tile slots fit 28 bits of an entry
   return true;
 }
 
@@ -876,9 +959,14 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   const int W = a->width, H = a->height;
   const dim3 scan_groups(static_cast<uint32_t>((T.tiles_x + kScanTiles - 1) / kScanTiles),
                          static_cast<uint32_t>(T.tiles_y), static_cast<uint32_t>(a->n_frames));
-  const dim3 list_groups(static_cast<uint32_t>(std::min<int64_t>(T.n, kListGroups)));
-  const dim3 border_groups(static_cast<uint32_t>(
-      std::min<int64_t>((4 * T.n + kBorderThreads - 1) / kBorderThreads, kListGroups)));
+  const dim3 local_groups(static_cast<uint32_t>(
+      std::min<int64_t>(T.n, resident_groups(reinterpret_cast<const void *>(local_kernel), kTileThreads))));
+  const dim3 border_groups(static_cast<uint32_t>(std::min<int64_t>(
+      (4 * T.n + kBorderThreads - 1) / kBorderThreads,
+      resident_groups(reinterpret_cast<const void *>(merge_kernel), kBorderThreads))));
+  const dim3 entry_groups(static_cast<uint32_t>(std::min<int64_t>(
+      (256 * T.n + kTileThreads - 1) / kTileThreads,
+      resident_groups(reinterpret_cast<const void *>(boxes_kernel), kTileThreads))));
   // dword mask reads need every row start dword-aligned; 16-byte reads need the mask
   // itself 16-byte aligned (and, for whole rows, rows a multiple of 16 bytes)
   const uintptr_t mp = reinterpret_cast<uintptr_t>(a->mask);
@@ -897,32 +985,25 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   uint32_t *n_list = reinterpret_cast<uint32_t *>(L.words + 3);
   if (vec && W % 16 == 0)
     hipLaunchKernelGGL(scan_kernel<2>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.tile_list, n_list);
+                       frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
   else if (word)
     hipLaunchKernelGGL(scan_kernel<1>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.tile_list, n_list);
+                       frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
   else
     hipLaunchKernelGGL(scan_kernel<0>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.tile_list, n_list);
-  if (word)
-    hipLaunchKernelGGL(local_kernel<true>, list_groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_list, n_list, L.label, status);
-  else
-    hipLaunchKernelGGL(local_kernel<false>, list_groups, dim3(kTileThreads), 0, s, a->mask, W,
-                       H, frame_px, T, L.tile_list, n_list, L.label, status);
-  hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, a->mask, W, H,
-                     frame_px, T, L.tile_bits, L.tile_list, n_list, vec && W % 16 == 0, L.label,
-                     status);
+                       frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
+  hipLaunchKernelGGL(local_kernel, local_groups, dim3(kTileThreads), 0, s, W, frame_px, T,
+                     L.tile_list, n_list, L.rec_fg, L.rec_roots, L.rec_border, L.entries,
+                     L.n_ent, L.label, status);
+  hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, frame_px, T,
+                     L.tile_bits, L.tile_slot, L.tile_list, n_list, L.rec_fg, L.rec_border,
+                     L.label, status);
   hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_spans)), dim3(kSpanThreads), 0,
-                     s, a->mask, vec, n_px, frame_px, n_spans, W, T, L.tile_bits, W % 32 == 0,
-                     L.label, L.comp, a->max_components, L.words, L.root_state,
-                     a->n_components);
-  if (word)
-    hipLaunchKernelGGL(boxes_kernel<true>, list_groups, dim3(kTileThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_list, n_list, L.label, L.comp, status);
-  else
-    hipLaunchKernelGGL(boxes_kernel<false>, list_groups, dim3(kTileThreads), 0, s, a->mask, W,
-                       H, frame_px, T, L.tile_list, n_list, L.label, L.comp, status);
+                     s, a->mask, vec, n_px, frame_px, n_spans, W, T, L.tile_bits, L.tile_slot,
+                     L.rec_roots, W % 32 == 0, L.label, L.comp, a->max_components, L.words,
+                     L.root_state, a->n_components);
+  hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kTileThreads), 0, s, W, frame_px, T,
+                     L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
                      0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,
                      a->areas, a->max_rois, L.kept_frame, L.words, L.filter_state, a->n_rois);
