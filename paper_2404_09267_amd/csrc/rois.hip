@@ -60,10 +60,7 @@ constexpr int kBorderThreads = 256;
 // than 2^30 pixels, so the flag bit is free.
 constexpr int32_t kRootFlag = 1 << 30;
 constexpr int32_t kIndex = kRootFlag - 1;
-constexpr int kSpan = 65536;       // pixels per workgroup of the roots pass
-constexpr int kSpanThreads = 256;  // 256 pixels per thread: sixteen 16-byte loads
-constexpr int kSpanPix = kSpan / kSpanThreads;
-constexpr int kSpanWords = kSpanPix / 32;  // foreground / root bit words per thread
+constexpr int kBandThreads = 256;  // numbering pass: 8 threads per row of a 32-row band
 constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
 constexpr int kFilterThreads = 256;
 
@@ -108,9 +105,10 @@ struct Layout {
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-Layout layout(void *base, int64_t n_px, int64_t n_tiles, int32_t max_components) {
+Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
+              int32_t max_components) {
   Layout L;
-  const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
+  const int64_t n_spans = n_bands;  // look-back words of the numbering pass
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
   const int64_t bit_words64 = (n_tiles + 63) / 64;
   L.n_words = 5 + n_spans + n_filter + bit_words64;
@@ -216,9 +214,8 @@ __device__ __forceinline__ TileAt tile_at(const Tiles &T, int t) {
 
 // Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
 // within the tile; rows: 32 words of scratch) from this thread's foreground bits (its 4
-// pixels of row t / 8, columns 4 (t % 8) .. + 3). Returns false, uniformly, when the tile has no foreground. Starts with a
-// barrier, so the caller's previous use of L (and of any other LDS) is over before L is
-// rewritten.
+// pixels of row t / 8, columns 4 (t % 8) .. + 3). Starts with a barrier, so the caller's
+// previous use of L (and of any other LDS) is over before L is rewritten.
 //
 // A pixel starts linked to the first pixel of its horizontal run among the thread's four,
 // so runs inside a thread cost no union. Each pixel p then joins the neighbours that a
@@ -228,31 +225,10 @@ __device__ __forceinline__ TileAt tile_at(const Tiles &T, int t) {
 // in another thread) and c; otherwise a and c -- and skips b when the previous pixel of its
 // run has already joined a, which touches b. That reaches the same sets as joining every
 // foreground neighbour, with about one union per run instead of four per pixel.
-__device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *rows,
+__device__ __forceinline__ void label_tile(uint32_t fg, int *L, uint32_t *rows,
                                            uint32_t *status) {
   const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
-  // rows[0] counts the waves with foreground, rows[1] the waves with every pixel set
   lds_barrier();  // the caller's previous use of L and rows is over
-  if (t == 0) {
-    rows[0] = 0;
-    rows[1] = 0;
-  }
-  lds_barrier();
-  const uint64_t any = __ballot(fg != 0), all = __ballot(fg == 0xFu);
-  if ((t & 63) == 0) {
-    if (any) atomicAdd(&rows[0], 1u);
-    if (all == ~uint64_t(0)) atomicAdd(&rows[1], 1u);
-  }
-  lds_barrier();
-  const uint32_t n_any = rows[0], n_all = rows[1];
-  if (n_any == 0) return false;
-  if (n_all == kTileThreads / 64) {  // a solid tile is one set rooted at its pixel 0
-#pragma unroll
-    for (int k = 0; k < 4; ++k) L[r * kTile + c0 + k] = 0;
-    lds_barrier();
-    return true;
-  }
-  lds_barrier();  // every wave has read the counts before rows is rewritten
   // this row's foreground as one word (the 8 threads of a row are 8 consecutive lanes)
   uint32_t row = fg << c0;
   row |= __shfl_xor(row, 1);
@@ -289,7 +265,6 @@ __device__ __forceinline__ bool label_tile(uint32_t fg, int *L, uint32_t *rows,
   }
   if (!ok) fail(status);
   lds_barrier();
-  return true;
 }
 
 // ---- kernels ------------------------------------------------------------------------
@@ -415,12 +390,23 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t fram
   __shared__ int sx0[kTile * kTile], sx1[kTile * kTile], sy1[kTile * kTile], sn[kTile * kTile];
   const int n = static_cast<int>(*n_list);
   const int t = threadIdx.x, lane = t & 63, r = t >> 3, c0 = (t & 7) * 4;
+  // each tile's list entry and row mask are loaded one tile ahead
+  int next_id = 0;
+  uint32_t next_row = 0;
+  if (static_cast<int>(blockIdx.x) < n) {
+    next_id = tile_list[blockIdx.x];
+    next_row = rec_fg[32 * static_cast<int64_t>(blockIdx.x) + r];
+  }
   for (int it = blockIdx.x; it < n; it += gridDim.x) {
-    const TileAt a = tile_at(T, tile_list[it]);
+    const TileAt a = tile_at(T, next_id);
+    const uint32_t fg = (next_row >> c0) & 0xFu;
+    if (it + static_cast<int>(gridDim.x) < n) {
+      next_id = tile_list[it + gridDim.x];
+      next_row = rec_fg[32 * static_cast<int64_t>(it + gridDim.x) + r];
+    }
     const int tx0 = a.tx * kTile, ty0 = a.ty * kTile;
-    const uint32_t fg = (rec_fg[32 * it + r] >> c0) & 0xFu;
     // (starts with a barrier: the previous tile's use of the LDS arrays is over)
-    if (!label_tile(fg, L, rows, status)) continue;  // (a listed tile always holds foreground)
+    label_tile(fg, L, rows, status);
     int32_t *lf = label + a.f * frame_px;
     int32_t *border = rec_border + 128 * static_cast<int64_t>(it);
     uint32_t rb = 0;  // this thread's local roots, as bits of its row
@@ -495,7 +481,6 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t fram
         }
       }
     }
-    lds_barrier();
     // one entry per local component, in the tile's own 256 entries
     int mine = 0;
 #pragma unroll
@@ -506,7 +491,7 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t fram
       if (lane >= o) incl += v;
     }
     if (lane == 63) s_wave[t >> 6] = incl;
-    lds_barrier();
+    lds_barrier();  // the folds and the wave counts are complete
     int at = incl - mine, total = 0;
 #pragma unroll
     for (int w = 0; w < kTileThreads / 64; ++w) {
@@ -643,85 +628,70 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
   }
 }
 
-__global__ __launch_bounds__(kSpanThreads) void roots_kernel(
-    const uint8_t *mask, bool vec, int64_t n_px, int64_t frame_px, int64_t n_spans, int W,
-    Tiles T, const uint32_t *tile_bits, const int32_t *tile_slot, const uint32_t *rec_roots,
-    bool aligned, int32_t *label, Comp *comp, int32_t max_components, uint64_t *words,
-    uint64_t *state, int32_t *n_components) {
-  __shared__ int s_span, s_base;
-  __shared__ int s_wave[kSpanThreads / 64];
+// Numbers the components in raster order: one workgroup per band of 32 rows of a frame
+// (a tile row), in ticket order, bands in raster order. Thread t takes row t / 8 of the
+// band and the t % 8-th eighth of its tiles, left to right, so thread order is raster
+// order within the band. Its candidates are the recorded tile-local roots of that row of
+// its listed tiles; a candidate is a component when it is still its own parent (label =
+// own frame index, flagged). A block-wide scan and a decoupled look-back over bands give
+// each component its number; the thread then walks its tiles again (the same loads, now
+// in cache) to initialise the records and mark the roots.
+__device__ __forceinline__ int band_roots(int W, const uint32_t *tile_bits,
+                                          const int32_t *tile_slot, const uint32_t *rec_roots,
+                                          int32_t *lf, int base, int y, int tx_lo, int tx_hi,
+                                          int rr, Comp *comp, int f, int id,
+                                          int32_t max_components, bool assign) {
+  int cnt = 0;
+  int wi = -1;
+  uint32_t wv = 0;
+  for (int tx = tx_lo; tx < tx_hi; ++tx) {
+    const int tile = base + tx;
+    if ((tile >> 5) != wi) {  // the bitmap word holding this tile
+      wi = tile >> 5;
+      wv = tile_bits[wi];
+    }
+    if (!(wv >> (tile & 31) & 1u)) continue;
+    const uint32_t cand = rec_roots[32 * static_cast<int64_t>(tile_slot[tile]) + rr];
+    for (uint32_t m = cand; m != 0; m &= m - 1) {
+      const int P = y * W + tx * kTile + __builtin_ctz(m);
+      if (lf[P] != (P | kRootFlag)) continue;
+      if (assign && id < max_components) {
+        comp[id] = Comp{f, P, INT_MAX, INT_MAX, INT_MIN, INT_MIN, 0, 0};
+        lf[P] = -(id + 1);
+      }
+      ++cnt;
+      ++id;
+    }
+  }
+  return cnt;
+}
+
+__global__ __launch_bounds__(kBandThreads) void roots_kernel(
+    int W, int H, int64_t frame_px, Tiles T, const uint32_t *tile_bits,
+    const int32_t *tile_slot, const uint32_t *rec_roots, int32_t *label, Comp *comp,
+    int32_t max_components, uint64_t *words, uint64_t *state, int32_t n_bands,
+    int32_t *n_components) {
+  __shared__ int s_band, s_base;
+  __shared__ int s_wave[kBandThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0)
-    s_span = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words), 1u,
+    s_band = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words), 1u,
                                                      __ATOMIC_RELAXED,
                                                      __HIP_MEMORY_SCOPE_AGENT));
   __syncthreads();
-  const int64_t span = s_span;
-  const int64_t p0 = span * kSpan + static_cast<int64_t>(tid) * kSpanPix;
+  const int band = s_band;
+  const int f = band / T.tiles_y, ty = band - f * T.tiles_y;
+  const int rr = tid >> 3, q = tid & 7, y = ty * kTile + rr;
+  const int chunk = (T.tiles_x + 7) / 8;
+  const int tx_lo = min(q * chunk, T.tiles_x), tx_hi = min(tx_lo + chunk, T.tiles_x);
+  const int base = (f * T.tiles_y + ty) * T.tiles_x;
+  int32_t *lf = label + static_cast<int64_t>(f) * frame_px;
+  const bool rows_in = y < H;
+  const int cnt = rows_in ? band_roots(W, tile_bits, tile_slot, rec_roots, lf, base, y, tx_lo,
+                                       tx_hi, rr, comp, f, 0, max_components, false)
+                          : 0;
 
-  // The components are the tile-local roots still their own parent (label = own frame
-  // index, flagged). With rows a multiple of 32 pixels (`aligned`) each of this thread's
-  // eight 32-pixel words is one row of one tile: its candidates are that row of the tile's
-  // local roots (its record; none for an empty tile), and only their labels are read.
-  // Otherwise the thread reads its 256 mask bytes (16-byte loads when the mask is
-  // 16-byte aligned and the bytes are inside it) and tests every foreground pixel.
-  uint32_t roots[kSpanWords] = {};
-  int cnt = 0;
-  if (aligned && p0 < n_px) {
-    uint32_t cand[kSpanWords] = {};
-    int64_t f = p0 / frame_px, loc = p0 - f * frame_px;
-    int lw[kSpanWords];  // frame index of each word's first pixel
-#pragma unroll
-    for (int w = 0; w < kSpanWords; ++w) {
-      lw[w] = static_cast<int>(loc);
-      if (p0 + 32 * w < n_px) {
-        const int l = static_cast<int>(loc), y = l / W, x = l - y * W;
-        const int tile = static_cast<int>((f * T.tiles_y + (y >> 5)) * T.tiles_x + (x >> 5));
-        if (tile_set(tile_bits, tile)) cand[w] = rec_roots[32 * static_cast<int64_t>(tile_slot[tile]) + (y & 31)];
-      }
-      loc += 32;
-      if (loc >= frame_px) {
-        loc -= frame_px;
-        ++f;
-      }
-    }
-#pragma unroll
-    for (int w = 0; w < kSpanWords; ++w) {
-      for (uint32_t m = cand[w]; m != 0; m &= m - 1) {
-        const int j = __builtin_ctz(m);
-        if (label[p0 + 32 * w + j] == ((lw[w] + j) | kRootFlag)) roots[w] |= 1u << j;
-      }
-      cnt += __popc(roots[w]);
-    }
-  } else if (p0 < n_px) {
-    uint32_t fgm[kSpanWords] = {};
-    if (vec && p0 + kSpanPix <= n_px) {
-      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-      u32x4 v[kSpanPix / 16];
-#pragma unroll
-      for (int q = 0; q < kSpanPix / 16; ++q)
-        v[q] = *reinterpret_cast<const u32x4 *>(mask + p0 + 16 * q);
-#pragma unroll
-      for (int q = 0; q < kSpanPix / 16; ++q)
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          fgm[q >> 1] |= ((v[q][j >> 2] >> (8 * (j & 3))) & 0xFFu) ? 1u << (16 * (q & 1) + j) : 0u;
-    } else {
-      for (int j = 0; j < kSpanPix; ++j)
-        fgm[j >> 5] |= (p0 + j < n_px && mask[min(p0 + j, n_px - 1)]) ? 1u << (j & 31) : 0u;
-    }
-    for (int w = 0; w < kSpanWords; ++w) {
-      const int64_t P0 = p0 + 32 * w;
-      for (uint32_t m = fgm[w]; m != 0; m &= m - 1) {
-        const int j = __builtin_ctz(m);
-        const int64_t P = P0 + j;
-        if (label[P] == (static_cast<int32_t>(P % frame_px) | kRootFlag)) roots[w] |= 1u << j;
-      }
-      cnt += __popc(roots[w]);
-    }
-  }
-
-  // Exclusive scan of the counts over the workgroup, then the look-back over spans.
+  // Exclusive scan of the counts over the workgroup, then the look-back over bands.
   int incl = cnt;
   for (int o = 1; o < 64; o <<= 1) {
     const int v = __shfl_up(incl, o);
@@ -731,34 +701,23 @@ __global__ __launch_bounds__(kSpanThreads) void roots_kernel(
   __syncthreads();
   int before = 0, total = 0;
 #pragma unroll
-  for (int w = 0; w < kSpanThreads / 64; ++w) {
+  for (int w = 0; w < kBandThreads / 64; ++w) {
     if (w < wave) before += s_wave[w];
     total += s_wave[w];
   }
   if (wave == 0) {
     bool failed;
-    const int prefix = tg_detail::lookback_prefix(state, static_cast<int>(span), total, &failed);
+    const int prefix = tg_detail::lookback_prefix(state, band, total, &failed);
     if (lane == 0) {
       s_base = prefix;
-      if (span == n_spans - 1) *n_components = failed ? TG_E_INTERNAL : prefix + total;
+      if (band == n_bands - 1) *n_components = failed ? TG_E_INTERNAL : prefix + total;
     }
   }
   __syncthreads();
-
-  int id = s_base + before + incl - cnt;
-#pragma unroll
-  for (int w = 0; w < kSpanWords; ++w) {
-    for (uint32_t m = roots[w]; m != 0; m &= m - 1, ++id) {
-      if (id >= max_components) continue;
-      const int64_t P = p0 + 32 * w + __builtin_ctz(m);
-      const int64_t f = P / frame_px;
-      comp[id] = Comp{static_cast<int32_t>(f), static_cast<int32_t>(P - f * frame_px), INT_MAX,
-                      INT_MAX, INT_MIN, INT_MIN, 0, 0};
-      label[P] = -(id + 1);
-    }
-  }
+  if (cnt > 0)
+    band_roots(W, tile_bits, tile_slot, rec_roots, lf, base, y, tx_lo, tx_hi, rr, comp, f,
+               s_base + before + incl - cnt, max_components, true);
 }
-
 
 // Folds each tile-local component (its entry) into its component's record: up the
 // union-find from its local root to the numbered root, then one set of global atomics.
@@ -939,8 +898,10 @@ bool sizes_ok(int32_t n_frames, int32_t width, int32_t height, int32_t max_compo
 extern "C" size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t height,
                                                int32_t max_components) {
   if (!sizes_ok(n_frames, width, height, max_components)) return 0;
-  return layout(nullptr, int64_t(n_frames) * width * height,
-                tiles_of(n_frames, width, height).n, max_components).bytes;
+  const Tiles T = tiles_of(n_frames, width, height);
+  return layout(nullptr, int64_t(n_frames) * width * height, int64_t(n_frames) * T.tiles_y, T.n,
+                max_components)
+      .bytes;
 }
 
 extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
@@ -951,7 +912,8 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   if (a->max_rois > 0 && !a->rois) return TG_E_INVAL;
   const int64_t frame_px = int64_t(a->width) * a->height, n_px = a->n_frames * frame_px;
   const Tiles T = tiles_of(a->n_frames, a->width, a->height);
-  const Layout L = layout(a->workspace, n_px, T.n, a->max_components);
+  const int64_t n_bands = int64_t(a->n_frames) * T.tiles_y;
+  const Layout L = layout(a->workspace, n_px, n_bands, T.n, a->max_components);
   if (!a->workspace || a->workspace_bytes < L.bytes ||
       reinterpret_cast<uintptr_t>(a->workspace) % 16 != 0)
     return TG_E_WORKSPACE;
@@ -971,7 +933,6 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   // itself 16-byte aligned (and, for whole rows, rows a multiple of 16 bytes)
   const uintptr_t mp = reinterpret_cast<uintptr_t>(a->mask);
   const bool word = mp % 4 == 0 && W % 4 == 0, vec = mp % 16 == 0;
-  const int64_t n_spans = (n_px + kSpan - 1) / kSpan;
   const int64_t n_filter = (a->max_components + kFilterBlock - 1) / kFilterBlock;
 
   if (n_px == 0) {  // no frames: no components, no rows
@@ -998,10 +959,10 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, frame_px, T,
                      L.tile_bits, L.tile_slot, L.tile_list, n_list, L.rec_fg, L.rec_border,
                      L.label, status);
-  hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_spans)), dim3(kSpanThreads), 0,
-                     s, a->mask, vec, n_px, frame_px, n_spans, W, T, L.tile_bits, L.tile_slot,
-                     L.rec_roots, W % 32 == 0, L.label, L.comp, a->max_components, L.words,
-                     L.root_state, a->n_components);
+  hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_bands)), dim3(kBandThreads), 0,
+                     s, W, H, frame_px, T, L.tile_bits, L.tile_slot, L.rec_roots, L.label,
+                     L.comp, a->max_components, L.words, L.root_state,
+                     static_cast<int32_t>(n_bands), a->n_components);
   hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kTileThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
