@@ -7,28 +7,33 @@
 // order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
 // 2018), tile-local first and merged along tile borders as in the block-based labelling of
 // S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in eight launches on
-// the caller's stream. Foreground masks are sparse, so only one pass reads every mask
-// byte; the others visit the 32x32 tiles that hold foreground.
+// the caller's stream. Foreground masks are sparse, so only the scan reads the mask; the
+// other passes visit the 32x32 tiles that hold foreground, through compact per-tile
+// records (row masks, local-root masks, the tile-local roots of the border pixels).
 //  1. clear:  zeroes the tickets, counters, look-back words and the tile bitmap.
 //  2. scan:   one 256-thread workgroup per 16 tiles side by side streams the mask (16-byte
-//             loads where it can), sets a bit per tile with foreground and appends those
-//             tiles to a list.
-//  3. local:  a fixed grid walks the list: each tile is labelled in LDS and every
-//             foreground pixel gets the frame index of its tile-local root.
+//             loads where it can), sets a bit per tile with foreground, appends those
+//             tiles to a list (a tile's list position is its record slot) and writes
+//             their 32 row masks.
+//  3. local:  a grid of resident workgroups walks the list: each tile is labelled in LDS
+//             (one union per run and neighbouring run), every foreground pixel gets the
+//             frame index of its tile-local root, the tile's local roots and border roots
+//             go to its record, and each local component's box and pixel count, folded in
+//             LDS, to one of the tile's 256 entry slots.
 //  4. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
 //             column in two halves) join each foreground pixel with its foreground
-//             neighbours across the border, with global atomics on the label array; an
-//             item whose neighbouring tiles are all empty is skipped. Every 8-neighbour
-//             pair across a tile border is seen from the tile below or to the right of it.
-//  5. roots:  65536-pixel raster spans in ticket order (each thread's 256 mask bytes as
-//             sixteen 16-byte loads, skipping 32-pixel words of empty tiles when rows are
-//             a multiple of 32 pixels) find the tile-local roots still their own parent
-//             (the components), number them in raster order with a decoupled look-back,
-//             initialise each component's record and mark the root with its number.
-//  6. boxes:  the grid walks the list again: each tile's local components, read off the
-//             labels the local pass left, fold their pixels' extent and count in LDS; each
-//             local component then follows the union-find to its component number and
-//             folds its totals into the record with global atomics.
+//             neighbours across the border, reading the records of the tile and of the
+//             tiles around it, with global atomics on the label array; an item whose
+//             neighbouring tiles are all empty is skipped. Every 8-neighbour pair across a
+//             tile border is seen from the tile below or to the right of it.
+//  5. roots:  one workgroup per band of 32 rows (a tile row of a frame), in ticket order,
+//             thread order being raster order over the band's listed tiles, tests the
+//             recorded local roots (still their own parent: a component), numbers them in
+//             raster order with a decoupled look-back over bands, initialises each
+//             component's record and marks the root with its number.
+//  6. boxes:  each local component (its entry) follows the union-find from its root to
+//             its component's number and folds its box and count into the record with
+//             one set of global atomics.
 //  7. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows.
 //  8. begin:  frame_begin by binary search over the kept rows' frames.
