@@ -513,8 +513,9 @@ size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, int32_t hei
  * and the order are this library's reading). RoIs are listed frame by frame, each
  * frame's in raster order of the component's first pixel, ready for tg_partition.
  * Enqueued on `stream`; allocates nothing. Returns TG_E_INVAL (null pointer,
- * non-positive sizes, more than 65535 frames or tile rows, width * height >= 2^30,
- * max_components < 1, max_rois < 0), TG_E_WORKSPACE, TG_E_HIP.
+ * non-positive sizes, more than 65535 frames or tile rows, width * height >= 2^30, 2^28 or
+ * more 32x32 tiles over all frames, max_components < 1, max_rois < 0), TG_E_WORKSPACE,
+ * TG_E_HIP. The workspace holds 4 bytes per pixel plus about 2.8 KB per 32x32 tile.
  * *n_rois = *n_components = TG_E_INTERNAL (no RoIs, frame_begin all 0) reports a
  * device-side failure: a union-find link that did not point to a smaller pixel index, or
  * a compaction that could not complete. Neither happens on a correct run; each loop that

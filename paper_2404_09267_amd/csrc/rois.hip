@@ -379,8 +379,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
   }
 }
 
-// Labels the listed tiles, a grid of kListGroups workgroups walking the list: for each
-// foreground pixel, the frame index of its tile-local root (flagged on the roots).
+// Labels the listed tiles, a grid of resident workgroups walking the list (each tile's
+// list entry and row mask loaded one tile ahead): for each foreground pixel, the frame
+// index of its tile-local root (flagged on the roots) in the label array; the tile's
+// local-root row masks and border roots in its record; one entry per local component
+// (its box in tile coordinates and its pixel count, folded in LDS) in the tile's slots.
 __global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t frame_px, Tiles T,
                                                              const int32_t *tile_list,
                                                              const uint32_t *n_list,
@@ -540,7 +543,7 @@ __device__ __forceinline__ void join_pairs(int32_t *lf, uint32_t fg, const int32
   }
 }
 
-// Four items per listed tile, walked by a grid of kListGroups workgroups: its top row in
+// Four items per listed tile, walked by a grid of resident workgroups: its top row in
 // two halves of 16 pixels against the row above, then its left column in two halves
 // against the column to its left. Every 8-neighbour pair across a tile border is seen
 // from the tile below or to the right of it. Foreground bits and tile-local roots come

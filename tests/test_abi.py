@@ -225,8 +225,17 @@ def test_gmm_and_mask_rois_validation_without_gpu():
     assert L.tg_mask_rois_workspace_bytes(1, 1 << 16, 1 << 15, 4) == 0
     assert L.tg_mask_rois_workspace_bytes(1, 1 << 15, 1 << 15, 4) == 0  # 2^30 pixels: no flag bit
     assert L.tg_mask_rois_workspace_bytes(1, 1 << 15, (1 << 15) - 1, 4) > 0
+    # tile slots are 28-bit: 65535 frames of 64 x 64 tiles fit (268,431,360 < 2^28), of
+    # 64 x 65 tiles do not
+    assert L.tg_mask_rois_workspace_bytes(65535, 2048, 2048, 4) > 0
+    assert L.tg_mask_rois_workspace_bytes(65535, 2048, 2080, 4) == 0
     ws = L.tg_mask_rois_workspace_bytes(2, 100, 50, 1000)
-    assert ws >= 4 * 2 * 100 * 50 + 32 * 1000 + 4 * 1000 and ws % 256 == 0
+    # labels, component records and kept frames, and per 32 x 32 tile (2 frames x 4 x 2
+    # tiles) its list entry, slot, records (row masks, root masks, border roots) and
+    # entry slots
+    tiles = 2 * 4 * 2
+    assert ws >= 4 * 2 * 100 * 50 + 32 * 1000 + 4 * 1000 + tiles * (4 + 4 + 128 + 128 + 512 + 2048)
+    assert ws % 256 == 0
     m = tg.MaskRoisArgs()
     m.mask = m.rois = m.areas = m.frame_begin = m.n_rois = m.n_components = 0x1000
     m.n_frames, m.width, m.height, m.min_area, m.max_rois, m.max_components = 2, 100, 50, 1, 10, 1000
