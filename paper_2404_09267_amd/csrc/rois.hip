@@ -15,11 +15,12 @@
 //             loads where it can), sets a bit per tile with foreground, appends those
 //             tiles to a list (a tile's list position is its record slot) and writes
 //             their 32 row masks.
-//  3. local:  a grid of resident workgroups walks the list: each tile is labelled in LDS
-//             (one union per run and neighbouring run), every foreground pixel gets the
-//             frame index of its tile-local root, the tile's local roots and border roots
-//             go to its record, and each local component's box and pixel count, folded in
-//             LDS, to one of the tile's 256 entry slots.
+//  3. local:  one wave per listed tile, a grid of resident one-wave workgroups walking
+//             the list: union-find in LDS over the tile's row runs (one union per pair
+//             of touching runs); each tile-local root's label word gets its own frame
+//             index, the tile's local roots and border roots go to its record, and each
+//             local component's box and pixel count, folded in LDS, to one of the tile's
+//             256 entry slots. No other label word is written or read.
 //  4. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
 //             column in two halves) join each foreground pixel with its foreground
 //             neighbours across the border, reading the records of the tile and of the
@@ -53,16 +54,14 @@
 namespace {
 
 constexpr int kTile = 32;
-constexpr int kTileThreads = 256;  // 8 threads per tile row, 4 pixels each
+constexpr int kEntryThreads = 256;  // boxes pass: one thread per entry slot
 constexpr int kScanTiles = 16;     // tiles side by side per workgroup of the scan pass
 constexpr int kScanThreads = 256;  // 8 threads per row of 16 tiles, 64 pixels each
 constexpr int kListGroups = 2048;  // list-walking grid when the occupancy query fails
 constexpr int kBorderThreads = 256;
-// Labels: a foreground pixel's word holds its tile-local root (a frame index) once the
-// local pass is done, and never changes afterwards unless the pixel is a tile-local root.
-// A tile-local root's word holds kRootFlag | its parent in the union-find over roots
-// (itself at first), and becomes -(component + 1) once it is numbered. Frames have fewer
-// than 2^30 pixels, so the flag bit is free.
+// Labels: only the words of tile-local roots are used. Such a word holds kRootFlag | its
+// parent in the union-find over roots (itself at first), and becomes -(component + 1)
+// once it is numbered. Frames have fewer than 2^30 pixels, so the flag bit is free.
 constexpr int32_t kRootFlag = 1 << 30;
 constexpr int32_t kIndex = kRootFlag - 1;
 constexpr int kBandThreads = 256;  // numbering pass: 8 threads per row of a 32-row band
@@ -179,19 +178,6 @@ __device__ __forceinline__ void fail(uint32_t *status) {
   __hip_atomic_fetch_or(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ int wave_min(int v) {
-  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_max(int v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ int wave_sum(int v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
 // Workgroup barrier that orders LDS only: no wait for the workgroup's outstanding global
 // stores, which a plain __syncthreads() would drain first.
 __device__ __forceinline__ void lds_barrier() {
@@ -217,59 +203,38 @@ __device__ __forceinline__ TileAt tile_at(const Tiles &T, int t) {
   return a;
 }
 
-// Labels one 32x32 tile in LDS (L: 1024 ints, -1 for background, else a parent index
-// within the tile; rows: 32 words of scratch) from this thread's foreground bits (its 4
-// pixels of row t / 8, columns 4 (t % 8) .. + 3). Starts with a barrier, so the caller's
-// previous use of L (and of any other LDS) is over before L is rewritten.
-//
-// A pixel starts linked to the first pixel of its horizontal run among the thread's four,
-// so runs inside a thread cost no union. Each pixel p then joins the neighbours that a
-// raster-scan decision tree for 8-connectivity requires -- with a the upper-left, b the
-// upper, c the upper-right and d the left neighbour: b alone when b is foreground (a and c
-// touch b, and d touches b diagonally, through their own joins); otherwise d (when it lies
-// in another thread) and c; otherwise a and c -- and skips b when the previous pixel of its
-// run has already joined a, which touches b. That reaches the same sets as joining every
-// foreground neighbour, with about one union per run instead of four per pixel.
-__device__ __forceinline__ void label_tile(uint32_t fg, int *L, uint32_t *rows,
-                                           uint32_t *status) {
-  const int t = threadIdx.x, r = t >> 3, c0 = (t & 7) * 4;
-  lds_barrier();  // the caller's previous use of L and rows is over
-  // this row's foreground as one word (the 8 threads of a row are 8 consecutive lanes)
-  uint32_t row = fg << c0;
-  row |= __shfl_xor(row, 1);
-  row |= __shfl_xor(row, 2);
-  row |= __shfl_xor(row, 4);
-  if ((t & 7) == 0) rows[r] = row;
-  int start = -1;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = r * kTile + c0 + k;
-    start = (fg >> k & 1u) ? (start >= 0 ? start : i) : -1;
-    L[i] = start;
-  }
-  lds_barrier();
-  const uint32_t up = r > 0 ? rows[r - 1] : 0u;
-  LdsLabels m{L};
-  bool ok = true;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (!(fg >> k & 1u)) continue;
-    const int c = c0 + k, i = r * kTile + c;
-    const bool a = c > 0 && (up >> (c - 1) & 1u), b = up >> c & 1u;
-    const bool cc = c + 1 < kTile && (up >> (c + 1) & 1u);
-    const bool d = c > 0 && (row >> (c - 1) & 1u);
-    if (b) {
-      if (!(k > 0 && d && a)) ok &= tg_detail::uf_unite(m, i, i - kTile);
-    } else if (d) {
-      if (k == 0) ok &= tg_detail::uf_unite(m, i, i - 1);
-      if (cc) ok &= tg_detail::uf_unite(m, i, i - kTile + 1);
-    } else {
-      if (a) ok &= tg_detail::uf_unite(m, i, i - kTile - 1);
-      if (cc) ok &= tg_detail::uf_unite(m, i, i - kTile + 1);
-    }
-  }
-  if (!ok) fail(status);
-  lds_barrier();
+// Run-based labelling of one 32x32 tile by one wave. A row's foreground is a 32-bit
+// word; its runs (maximal horizontal segments) are the union-find nodes, run j of row r
+// being node 16 r + j (a row holds at most 16 runs), so node order is raster order of the
+// runs' first pixels and every set ends rooted at the run holding its first pixel. A run
+// of row r touches, 8-connected, the runs of row r - 1 that meet columns s - 1 .. e + 1
+// of its span s .. e: consecutive runs of that row, from the one holding the lowest
+// foreground column of the window to the one holding the highest.
+constexpr int kLocalThreads = 64;  // one wave per tile: lane l on row l % 32
+constexpr int kRunNodes = kTile * 16;
+
+struct RunTile {
+  int L[kRunNodes];                    // union-find links over the runs
+  unsigned long long span[kRunNodes];  // per root: row bits << 32 | column bits
+  int count[kRunNodes];                // per root: pixels
+  uint8_t col[kRunNodes];              // first column of each run
+};
+
+// Ordinal of the run of row word `starts` (its runs' first columns as bits) that holds
+// column c, c being foreground.
+__device__ __forceinline__ int run_ordinal(uint32_t starts, int c) {
+  return __popc(starts & (0xFFFFFFFFu >> (31 - c))) - 1;
+}
+
+// Last column of the run that starts at column s of a row whose runs end at the bits of
+// `ends`.
+__device__ __forceinline__ int run_end(uint32_t ends, int s) {
+  return __builtin_ctz(ends & (0xFFFFFFFFu << s));
+}
+
+// Columns lo .. hi as bits (0 <= lo <= hi <= 31).
+__device__ __forceinline__ uint32_t col_span(int lo, int hi) {
+  return (0xFFFFFFFFu >> (31 - hi)) & (0xFFFFFFFFu << lo);
 }
 
 // ---- kernels ------------------------------------------------------------------------
@@ -379,26 +344,26 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
   }
 }
 
-// Labels the listed tiles, a grid of resident workgroups walking the list (each tile's
-// list entry and row mask loaded one tile ahead): for each foreground pixel, the frame
-// index of its tile-local root (flagged on the roots) in the label array; the tile's
-// local-root row masks and border roots in its record; one entry per local component
-// (its box in tile coordinates and its pixel count, folded in LDS) in the tile's slots.
-__global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t frame_px, Tiles T,
-                                                             const int32_t *tile_list,
-                                                             const uint32_t *n_list,
-                                                             const uint32_t *rec_fg,
-                                                             uint32_t *rec_roots,
-                                                             int32_t *rec_border, uint64_t *entries,
-                                                             int32_t *n_ent, int32_t *label,
-                                                             uint32_t *status) {
-  __shared__ int L[kTile * kTile];
-  __shared__ uint32_t rows[kTile];
-  __shared__ int s_wave[kTileThreads / 64];
-  __shared__ int sx0[kTile * kTile], sx1[kTile * kTile], sy1[kTile * kTile], sn[kTile * kTile];
+// Labels the listed tiles, one wave per tile, a grid of resident one-wave workgroups
+// walking the list (each tile's list entry and row mask loaded one tile ahead). Lane l
+// holds row l % 32; the row's runs are shared between the two halves of the wave by the
+// parity of their ordinal. Per tile: union-find over the runs in LDS (one union per pair
+// of touching runs of adjacent rows), each run resolved to its root, and the root's rows,
+// columns and pixel count folded in LDS. Written: the frame index of each tile-local root
+// (flagged) in the label array -- the only label words any later pass reads --, the
+// tile's local-root row masks and border roots in its record, and one entry per local
+// component (its box in tile coordinates and its pixel count) in the tile's slots.
+__global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t frame_px, Tiles T,
+                                                              const int32_t *tile_list,
+                                                              const uint32_t *n_list,
+                                                              const uint32_t *rec_fg,
+                                                              uint32_t *rec_roots,
+                                                              int32_t *rec_border,
+                                                              uint64_t *entries, int32_t *n_ent,
+                                                              int32_t *label, uint32_t *status) {
+  __shared__ RunTile S;
   const int n = static_cast<int>(*n_list);
-  const int t = threadIdx.x, lane = t & 63, r = t >> 3, c0 = (t & 7) * 4;
-  // each tile's list entry and row mask are loaded one tile ahead
+  const int lane = threadIdx.x, r = lane & 31, half = lane >> 5;
   int next_id = 0;
   uint32_t next_row = 0;
   if (static_cast<int>(blockIdx.x) < n) {
@@ -407,114 +372,104 @@ __global__ __launch_bounds__(kTileThreads) void local_kernel(int W, int64_t fram
   }
   for (int it = blockIdx.x; it < n; it += gridDim.x) {
     const TileAt a = tile_at(T, next_id);
-    const uint32_t fg = (next_row >> c0) & 0xFu;
+    const uint32_t w = next_row;
     if (it + static_cast<int>(gridDim.x) < n) {
       next_id = tile_list[it + gridDim.x];
       next_row = rec_fg[32 * static_cast<int64_t>(it + gridDim.x) + r];
     }
     const int tx0 = a.tx * kTile, ty0 = a.ty * kTile;
-    // (starts with a barrier: the previous tile's use of the LDS arrays is over)
-    label_tile(fg, L, rows, status);
     int32_t *lf = label + a.f * frame_px;
-    int32_t *border = rec_border + 128 * static_cast<int64_t>(it);
-    uint32_t rb = 0;  // this thread's local roots, as bits of its row
-    int root[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      root[k] = -1;
-      if (!(fg >> k & 1u)) continue;
-      const int c = c0 + k, i = r * kTile + c;
-      LdsLabels m{L};
-      int rt = tg_detail::uf_find(m, i);
-      if (rt < 0) {
-        fail(status);
-        rt = i;
-      }
-      root[k] = rt;
-      const int gr = (ty0 + (rt >> 5)) * W + tx0 + (rt & (kTile - 1));
-      lf[static_cast<int64_t>(ty0 + r) * W + tx0 + c] = rt == i ? gr | kRootFlag : gr;
-      rb |= rt == i ? 1u << c : 0u;
-      if (r == 0) border[c] = gr;
-      if (r == kTile - 1) border[32 + c] = gr;
-      if (c == 0) border[64 + r] = gr;
-      if (c == kTile - 1) border[96 + r] = gr;
-      if (rt == i) {
-        sx0[i] = kTile;
-        sx1[i] = -1;
-        sy1[i] = -1;
-        sn[i] = 0;
-      }
+    const uint32_t up = __shfl(w, (lane + 63) & 63);  // row r - 1 (used for r > 0)
+    const uint32_t st = w & ~(w << 1), en = w & ~(w >> 1), ust = up & ~(up << 1);
+    // the runs of even ordinal go to half 0, odd to half 1: bit s of the prefix parity
+    // of st is set when the run starting at s has an even ordinal
+    uint32_t par = st;
+    par ^= par << 1;
+    par ^= par << 2;
+    par ^= par << 4;
+    par ^= par << 8;
+    par ^= par << 16;
+    const uint32_t mine = half ? st & ~par : st & par;
+    lds_barrier();  // the previous tile's reads of S are over
+    for (uint32_t m = mine; m; m &= m - 1) {
+      const int s = __builtin_ctz(m), node = 16 * r + run_ordinal(st, s);
+      S.L[node] = node;
+      S.span[node] = 0;
+      S.count[node] = 0;
+      S.col[node] = static_cast<uint8_t>(s);
     }
-    rb |= __shfl_xor(rb, 1);
-    rb |= __shfl_xor(rb, 2);
-    rb |= __shfl_xor(rb, 4);
-    if ((t & 7) == 0) rec_roots[32 * it + r] = rb;
     lds_barrier();
-    // Each local component's box (tile coordinates) and pixel count, folded in LDS: a
-    // thread folds each run of its pixels with one root once; when every foreground pixel
-    // of the wave has one root, the wave reduces first and folds once.
-    {
-      const uint32_t fgb = fg;
-      const int lead0 = fgb ? root[__builtin_ctz(fgb)] : -1;
-      bool one = true;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) one &= root[k] < 0 || root[k] == lead0;
-      const uint64_t any = __ballot(fgb != 0);
-      const int lead = any ? __shfl(lead0, __builtin_ctzll(any)) : -1;
-      if (any && __ballot(fgb != 0 && !(one && lead0 == lead)) == 0) {
-        const int mx0 = wave_min(fgb ? c0 + __builtin_ctz(fgb) : INT_MAX);
-        const int mx1 = wave_max(fgb ? c0 + 31 - __builtin_clz(fgb) : INT_MIN);
-        const int my1 = wave_max(fgb ? r : INT_MIN), cnt = wave_sum(__popc(fgb));
-        if (lane == 0) {
-          atomicMin(&sx0[lead], mx0);
-          atomicMax(&sx1[lead], mx1);
-          atomicMax(&sy1[lead], my1);
-          atomicAdd(&sn[lead], cnt);
-        }
-      } else {
-        int k = 0;
-        while (k < 4) {
-          if (root[k] < 0) {
-            ++k;
-            continue;
-          }
-          int e = k + 1;  // pixels k .. e - 1 share root[k]
-          while (e < 4 && root[e] == root[k]) ++e;
-          const int rt = root[k];
-          atomicMin(&sx0[rt], c0 + k);
-          atomicMax(&sx1[rt], c0 + e - 1);
-          atomicMax(&sy1[rt], r);
-          atomicAdd(&sn[rt], e - k);
-          k = e;
-        }
+    LdsLabels lab{S.L};
+    bool ok = true;
+    if (r > 0) {
+      for (uint32_t m = mine; m; m &= m - 1) {
+        const int s = __builtin_ctz(m), e = run_end(en, s);
+        const uint32_t x = up & col_span(s > 0 ? s - 1 : 0, e < kTile - 1 ? e + 1 : kTile - 1);
+        if (!x) continue;
+        const int node = 16 * r + run_ordinal(st, s);
+        const int kb = run_ordinal(ust, __builtin_ctz(x)), ke = run_ordinal(ust, 31 - __builtin_clz(x));
+        for (int k = kb; k <= ke; ++k) ok &= tg_detail::uf_unite(lab, node, 16 * (r - 1) + k);
       }
     }
-    // one entry per local component, in the tile's own 256 entries
-    int mine = 0;
+    if (!ok) fail(status);
+    lds_barrier();  // every union is in
+    // each run to its root (left in L, so that after the barrier L maps a run to its root),
+    // folded into the root's rows, columns and count; the roots written to the label array
+    uint32_t roots = 0;
+    for (uint32_t m = mine; m; m &= m - 1) {
+      const int s = __builtin_ctz(m), e = run_end(en, s), node = 16 * r + run_ordinal(st, s);
+      int R = tg_detail::uf_find(lab, node);
+      if (R < 0) {
+        fail(status);
+        R = node;
+      }
+      if (R != node) lab.link(node, R);
+      atomicOr(&S.span[R], static_cast<unsigned long long>(1u << r) << 32 | col_span(s, e));
+      atomicAdd(&S.count[R], e - s + 1);
+      if (R == node) {
+        roots |= 1u << s;
+        const int P = (ty0 + r) * W + tx0 + s;
+        lf[P] = P | kRootFlag;
+      }
+    }
+    roots |= __shfl_xor(roots, 32);
+    if (half == 0) rec_roots[32 * static_cast<int64_t>(it) + r] = roots;
+    lds_barrier();  // L resolved, the folds complete
+    // border roots: lane l takes entry l (row 0 / row 31, column l % 32), then entry 64 + l
+    // (column 0 / column 31, row l % 32); background entries are -1
+    int32_t *border = rec_border + 128 * static_cast<int64_t>(it);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) mine += root[k] == r * kTile + c0 + k;
-    int incl = mine;
-    for (int o = 1; o < 64; o <<= 1) {
+    for (int pass = 0; pass < 2; ++pass) {
+      const int row = pass ? r : (half ? kTile - 1 : 0), c = pass ? (half ? kTile - 1 : 0) : r;
+      const uint32_t rw = pass ? w : __shfl(w, half ? kTile - 1 : 0);
+      int32_t v = -1;
+      if (rw >> c & 1u) {
+        const int R = S.L[16 * row + run_ordinal(rw & ~(rw << 1), c)];
+        v = (ty0 + (R >> 4)) * W + tx0 + S.col[R];
+      }
+      border[64 * pass + lane] = v;
+    }
+    // one entry per local component, in the tile's own 256 entries, in row order
+    const int mine_roots = half ? 0 : __popc(roots);
+    int incl = mine_roots;
+    for (int o = 1; o < 32; o <<= 1) {
       const int v = __shfl_up(incl, o);
-      if (lane >= o) incl += v;
+      if (r >= o) incl += v;
     }
-    if (lane == 63) s_wave[t >> 6] = incl;
-    lds_barrier();  // the folds and the wave counts are complete
-    int at = incl - mine, total = 0;
-#pragma unroll
-    for (int w = 0; w < kTileThreads / 64; ++w) {
-      if (w < (t >> 6)) at += s_wave[w];
-      total += s_wave[w];
-    }
-    if (t == 0) n_ent[it] = total;
-    uint64_t *ent = entries + 256 * static_cast<int64_t>(it);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = r * kTile + c0 + k;
-      if (root[k] != i) continue;
-      ent[at++] = static_cast<uint64_t>(i) << 26 | static_cast<uint64_t>(sx0[i]) << 21 |
-                  static_cast<uint64_t>(sx1[i]) << 16 | static_cast<uint64_t>(sy1[i]) << 11 |
-                  static_cast<uint64_t>(sn[i]);
+    const int total = __shfl(incl, kTile - 1);
+    if (lane == 0) n_ent[it] = total;
+    uint64_t *ent = entries + 256 * static_cast<int64_t>(it) + (incl - mine_roots);
+    if (half == 0) {
+      for (uint32_t m = roots; m; m &= m - 1) {
+        const int s = __builtin_ctz(m), node = 16 * r + run_ordinal(st, s);
+        const unsigned long long sp = S.span[node];
+        const uint32_t cols = static_cast<uint32_t>(sp), rows = static_cast<uint32_t>(sp >> 32);
+        *ent++ = static_cast<uint64_t>(r * kTile + s) << 26 |
+                 static_cast<uint64_t>(__builtin_ctz(cols)) << 21 |
+                 static_cast<uint64_t>(31 - __builtin_clz(cols)) << 16 |
+                 static_cast<uint64_t>(31 - __builtin_clz(rows)) << 11 |
+                 static_cast<uint64_t>(S.count[node]);
+      }
     }
   }
 }
@@ -730,7 +685,7 @@ __global__ __launch_bounds__(kBandThreads) void roots_kernel(
 // Folds each tile-local component (its entry) into its component's record: up the
 // union-find from its local root to the numbered root, then one set of global atomics.
 // A grid of resident workgroups walks the listed tiles' entry slots.
-__global__ __launch_bounds__(kTileThreads) void boxes_kernel(int W, int64_t frame_px, Tiles T,
+__global__ __launch_bounds__(kEntryThreads) void boxes_kernel(int W, int64_t frame_px, Tiles T,
                                                              const int32_t *tile_list,
                                                              const uint32_t *n_list,
                                                              const uint64_t *entries,
@@ -738,8 +693,8 @@ __global__ __launch_bounds__(kTileThreads) void boxes_kernel(int W, int64_t fram
                                                              const int32_t *label, Comp *comp,
                                                              uint32_t *status) {
   const int64_t n = 256 * static_cast<int64_t>(*n_list);
-  for (int64_t e = blockIdx.x * kTileThreads + threadIdx.x; e < n;
-       e += static_cast<int64_t>(gridDim.x) * kTileThreads) {
+  for (int64_t e = blockIdx.x * kEntryThreads + threadIdx.x; e < n;
+       e += static_cast<int64_t>(gridDim.x) * kEntryThreads) {
     const int slot = static_cast<int>(e >> 8);
     if ((e & 255) >= n_ent[slot]) continue;
     const uint64_t v64 = entries[e];
@@ -929,14 +884,14 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   const int W = a->width, H = a->height;
   const dim3 scan_groups(static_cast<uint32_t>((T.tiles_x + kScanTiles - 1) / kScanTiles),
                          static_cast<uint32_t>(T.tiles_y), static_cast<uint32_t>(a->n_frames));
-  const dim3 local_groups(static_cast<uint32_t>(
-      std::min<int64_t>(T.n, resident_groups(reinterpret_cast<const void *>(local_kernel), kTileThreads))));
+  const dim3 local_groups(static_cast<uint32_t>(std::min<int64_t>(
+      T.n, resident_groups(reinterpret_cast<const void *>(local_kernel), kLocalThreads))));
   const dim3 border_groups(static_cast<uint32_t>(std::min<int64_t>(
       (4 * T.n + kBorderThreads - 1) / kBorderThreads,
       resident_groups(reinterpret_cast<const void *>(merge_kernel), kBorderThreads))));
   const dim3 entry_groups(static_cast<uint32_t>(std::min<int64_t>(
-      (256 * T.n + kTileThreads - 1) / kTileThreads,
-      resident_groups(reinterpret_cast<const void *>(boxes_kernel), kTileThreads))));
+      (256 * T.n + kEntryThreads - 1) / kEntryThreads,
+      resident_groups(reinterpret_cast<const void *>(boxes_kernel), kEntryThreads))));
   // dword mask reads need every row start dword-aligned; 16-byte reads need the mask
   // itself 16-byte aligned (and, for whole rows, rows a multiple of 16 bytes)
   const uintptr_t mp = reinterpret_cast<uintptr_t>(a->mask);
@@ -961,7 +916,7 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   else
     hipLaunchKernelGGL(scan_kernel<0>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
                        frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
-  hipLaunchKernelGGL(local_kernel, local_groups, dim3(kTileThreads), 0, s, W, frame_px, T,
+  hipLaunchKernelGGL(local_kernel, local_groups, dim3(kLocalThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.rec_fg, L.rec_roots, L.rec_border, L.entries,
                      L.n_ent, L.label, status);
   hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, frame_px, T,
@@ -971,7 +926,7 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
                      s, W, H, frame_px, T, L.tile_bits, L.tile_slot, L.rec_roots, L.label,
                      L.comp, a->max_components, L.words, L.root_state,
                      static_cast<int32_t>(n_bands), a->n_components);
-  hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kTileThreads), 0, s, W, frame_px, T,
+  hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kEntryThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
                      0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,

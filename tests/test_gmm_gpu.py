@@ -184,14 +184,32 @@ def _labels_after(torch, bufs, n_px):
     return labels, status
 
 
+def _tile_local_roots(mask2d):
+    """Frame indices of the tile-local roots of one frame: per 32x32 tile, the first pixel
+    (raster order) of each of the tile's own 8-connected components."""
+    from scipy import ndimage
+
+    H, Wd = mask2d.shape
+    out = []
+    for y0 in range(0, H, 32):
+        for x0 in range(0, Wd, 32):
+            sub = mask2d[y0:y0 + 32, x0:x0 + 32]
+            lab, n = ndimage.label(sub, structure=np.ones((3, 3), np.int32))
+            for k in range(1, n + 1):
+                ys, xs = np.nonzero(lab == k)
+                out.append((y0 + ys[0]) * Wd + x0 + xs[0])
+    return np.sort(np.array(out, np.int64))
+
+
 def test_mask_rois_labels_keep_the_union_find_invariant(torch):
-    """After a call, the labels read back from the workspace satisfy, checked on the CPU
-    against scipy's 8-connected labelling: a foreground pixel holds either its tile-local
-    root (a pixel at or before it in the same 32x32 tile, itself a root) or, at a root, a
-    flagged link to a smaller index, or the negated component number; links stay in the
-    pixel's component; each component is numbered once, at its first pixel in raster
-    order, in raster order over the frames; following the links from any foreground
-    pixel ends at its component's number. The status word is clear."""
+    """After a call, the label words of the tile-local roots (per 32x32 tile, the first
+    pixel of each of the tile's own 8-connected components; no other label word is read
+    by the labelling), read back from the workspace, satisfy, checked on the CPU against
+    scipy's 8-connected labelling: each holds a flagged link to a smaller tile-local root
+    of the same component, or the negated component number; each component is numbered
+    once, at its first pixel in raster order, in raster order over the frames; following
+    the links from any tile-local root ends at its component's number. The status word is
+    clear."""
     from scipy import ndimage
 
     rng = np.random.default_rng(21)
@@ -214,24 +232,17 @@ def test_mask_rois_labels_keep_the_union_find_invariant(torch):
         lab = labels[f]
         comp, n = ndimage.label(mask[f], structure=np.ones((3, 3), np.int32))
         comp = comp.reshape(-1)
-        idx = np.flatnonzero(mask[f].reshape(-1))
+        idx = _tile_local_roots(mask[f])
+        is_local_root = np.zeros(H * Wd, bool)
+        is_local_root[idx] = True
         v = lab[idx]
         numbered = v < 0
         flagged = (v >= 0) & ((v & flag) != 0)
-        plain = (v >= 0) & ((v & flag) == 0)
-        is_root = lambda q: (lab[q] < 0) | ((lab[q] & flag) != 0)  # noqa: E731
+        assert np.all(numbered | flagged)
 
-        t, i = v[plain], idx[plain]          # tile-local root of a non-root pixel
-        assert np.all((0 <= t) & (t < i))
-        assert np.array_equal((t // Wd) // 32, (i // Wd) // 32)
-        assert np.array_equal((t % Wd) // 32, (i % Wd) // 32)
-        assert np.all(is_root(t)) and np.array_equal(comp[t], comp[i])
-
-        p, i = v[flagged] & index, idx[flagged]  # tile-local root: link to a smaller one
-        assert np.all(p <= i)
-        own = p == i                        # still its own parent: must have been numbered
-        assert not own.any()
-        assert np.all(is_root(p)) and np.array_equal(comp[p], comp[i])
+        p, i = v[flagged] & index, idx[flagged]  # link to a smaller tile-local root
+        assert np.all(p < i)
+        assert np.all(is_local_root[p]) and np.array_equal(comp[p], comp[i])
 
         first = np.full(n + 1, np.iinfo(np.int64).max)
         np.minimum.at(first, comp[idx], idx)
