@@ -6,38 +6,40 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
 // 2018), tile-local first and merged along tile borders as in the block-based labelling of
-// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in eight launches on
+// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in eleven launches on
 // the caller's stream. Foreground masks are sparse, so only the scan reads the mask; the
-// other passes visit the 32x32 tiles that hold foreground, through compact per-tile
-// records (row masks, local-root masks, the tile-local roots of the border pixels).
+// other passes visit the 32x32 tiles that hold foreground, through per-tile records
+// (row masks, local-root masks, the tile-local roots of the border pixels) indexed by
+// tile id. Same-address global atomics serialize across the chip, so no pass counts or
+// takes tickets on one word per workgroup of a large grid.
 //  1. clear:  zeroes the tickets, counters, look-back words and the tile bitmap.
 //  2. scan:   one 256-thread workgroup per 16 tiles side by side streams the mask (16-byte
-//             loads where it can), sets a bit per tile with foreground, appends those
-//             tiles to a list (a tile's list position is its record slot) and writes
-//             their 32 row masks.
-//  3. local:  one wave per listed tile, a grid of resident one-wave workgroups walking
+//             loads where it can), sets a bit per tile with foreground and writes those
+//             tiles' 32 row masks.
+//  3. list:   compacts the bitmap into the list of non-empty tiles (increasing ids), a
+//             few large workgroups with a decoupled look-back.
+//  4. local:  one wave per listed tile, a grid of resident one-wave workgroups walking
 //             the list: union-find in LDS over the tile's row runs (one union per pair
 //             of touching runs); each tile-local root's label word gets its own frame
 //             index, the tile's local roots and border roots go to its record, and each
 //             local component's box and pixel count, folded in LDS, to one of the tile's
 //             256 entry slots. No other label word is written or read.
-//  4. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
+//  5. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
 //             column in two halves) join each foreground pixel with its foreground
 //             neighbours across the border, reading the records of the tile and of the
 //             tiles around it, with global atomics on the label array; an item whose
 //             neighbouring tiles are all empty is skipped. Every 8-neighbour pair across a
 //             tile border is seen from the tile below or to the right of it.
-//  5. roots:  one workgroup per band of 32 rows (a tile row of a frame), in ticket order,
-//             thread order being raster order over the band's listed tiles, tests the
-//             recorded local roots (still their own parent: a component), numbers them in
-//             raster order with a decoupled look-back over bands, initialises each
-//             component's record and marks the root with its number.
-//  6. boxes:  each local component (its entry) follows the union-find from its root to
+//  6-8. count, scan, assign: per band of 32 rows (a tile row of a frame), the recorded
+//             local roots that are still their own parent (the components) are counted
+//             in raster order; one workgroup scans the bands' counts; per band, each
+//             component's record is initialised and its root marked with its number.
+//  9. boxes:  each local component (its entry) follows the union-find from its root to
 //             its component's number and folds its box and count into the record with
 //             one set of global atomics.
-//  7. filter: components of at least min_area pixels, compacted in number order with a
+// 10. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows.
-//  8. begin:  frame_begin by binary search over the kept rows' frames.
+// 11. begin:  frame_begin by binary search over the kept rows' frames.
 // Every union-find walk checks the invariant it relies on (unionfind.h); a walk that meets a
 // link that does not point to a smaller index ends, sets the workspace's status word, and
 // the call reports *n_rois = *n_components = TG_E_INTERNAL instead of RoIs.
@@ -58,13 +60,18 @@ constexpr int kEntryThreads = 256;  // boxes pass: one thread per entry slot
 constexpr int kScanTiles = 16;     // tiles side by side per workgroup of the scan pass
 constexpr int kScanThreads = 256;  // 8 threads per row of 16 tiles, 64 pixels each
 constexpr int kListGroups = 2048;  // list-walking grid when the occupancy query fails
+constexpr int kListThreads = 256;  // list pass: kListPer bitmap words per thread
+constexpr int kListPer = 4;
+constexpr int kListChunk = kListThreads * kListPer;  // bitmap words per list workgroup
 constexpr int kBorderThreads = 256;
 // Labels: only the words of tile-local roots are used. Such a word holds kRootFlag | its
 // parent in the union-find over roots (itself at first), and becomes -(component + 1)
 // once it is numbered. Frames have fewer than 2^30 pixels, so the flag bit is free.
 constexpr int32_t kRootFlag = 1 << 30;
 constexpr int32_t kIndex = kRootFlag - 1;
-constexpr int kBandThreads = 256;  // numbering pass: 8 threads per row of a 32-row band
+constexpr int kBandThreads = 256;  // numbering passes: 8 threads per row of a 32-row band
+constexpr int kBandBatch = 16;     // tiles whose loads a numbering thread issues together
+constexpr int kBandScanThreads = 1024;  // the scan over the bands' counts: one workgroup
 constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
 constexpr int kFilterThreads = 256;
 
@@ -81,25 +88,26 @@ struct Tiles {
 };
 
 struct Layout {
-  // [0]: roots ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed,
-  // [4]: unused, then the look-back words of the roots and filter
-  // passes, then the tile bitmap (bit t of 32-bit word t / 32: tile t holds foreground);
-  // all cleared by the first launch
+  // [0]: list ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed,
+  // [4]: unused, then the look-back words of the list and filter passes, then the tile
+  // bitmap (bit t of 32-bit word t / 32: tile t holds foreground); all cleared by the
+  // first launch
   uint64_t *words;
-  uint64_t *root_state, *filter_state;
+  uint64_t *list_state, *filter_state;
   uint32_t *tile_bits;
-  int32_t *tile_list;  // ids of the non-empty tiles, in no particular order
-  // Record of the tile at list slot s: fg[32 s + r], row r's foreground as a 32-bit mask;
-  // roots[32 s + r], row r's tile-local roots; border[128 s + e], the tile-local root (a
-  // frame index) of border pixel e: row 0 (e < 32), row 31, column 0, column 31 (e - 96).
+  int32_t *tile_list;  // ids of the non-empty tiles, in increasing order
+  // Record of non-empty tile t: fg[32 t + r], row r's foreground as a 32-bit mask;
+  // roots[32 t + r], row r's tile-local roots; border[128 t + e], the tile-local root (a
+  // frame index) of border pixel e -- row 0 (e < 32), row 31, column 0, column 31
+  // (e - 96) -- or -1 for background.
   uint32_t *rec_fg, *rec_roots;
   int32_t *rec_border;
-  int32_t *tile_slot;  // list slot of each non-empty tile
   // One entry per tile-local component, at most 256 per tile (8-connected, 32x32):
-  // entries[256 s + j], j < n_ent[s]: local root << 26 | x0 << 21 | x1 << 16 | y1 << 11 |
+  // entries[256 t + j], j < n_ent[t]: local root << 26 | x0 << 21 | x1 << 16 | y1 << 11 |
   // pixel count, the box in tile coordinates (its top row is the root's).
   uint64_t *entries;
   int32_t *n_ent;
+  int32_t *band_first;  // per band: its count of components, then its first one's number
   Comp *comp;
   int32_t *kept_frame;
   int32_t *label;
@@ -109,37 +117,41 @@ struct Layout {
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+int64_t list_chunks(int64_t n_tiles) {
+  return ((n_tiles + 31) / 32 + kListChunk - 1) / kListChunk;
+}
+
 Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
               int32_t max_components) {
   Layout L;
-  const int64_t n_spans = n_bands;  // look-back words of the numbering pass
+  const int64_t n_chunks = list_chunks(n_tiles);
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
   const int64_t bit_words64 = (n_tiles + 63) / 64;
-  L.n_words = 5 + n_spans + n_filter + bit_words64;
+  L.n_words = 5 + n_chunks + n_filter + bit_words64;
   const size_t nt = static_cast<size_t>(n_tiles);
   const size_t o_list = round_up(8 * static_cast<size_t>(L.n_words), 256);
-  const size_t o_slot = round_up(o_list + 4 * nt, 256);
-  const size_t o_fg = round_up(o_slot + 4 * nt, 256);
+  const size_t o_fg = round_up(o_list + 4 * nt, 256);
   const size_t o_roots = round_up(o_fg + 128 * nt, 256);
   const size_t o_border = round_up(o_roots + 128 * nt, 256);
   const size_t o_entries = round_up(o_border + 512 * nt, 256);
   const size_t o_nent = round_up(o_entries + 8 * 256 * nt, 256);
-  const size_t o_comp = round_up(o_nent + 4 * nt, 256);
+  const size_t o_band = round_up(o_nent + 4 * nt, 256);
+  const size_t o_comp = round_up(o_band + 4 * static_cast<size_t>(n_bands), 256);
   const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
   const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
   L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
   char *b = static_cast<char *>(base);
   L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
-  L.root_state = b ? L.words + 5 : nullptr;
-  L.filter_state = b ? L.root_state + n_spans : nullptr;
+  L.list_state = b ? L.words + 5 : nullptr;
+  L.filter_state = b ? L.list_state + n_chunks : nullptr;
   L.tile_bits = b ? reinterpret_cast<uint32_t *>(L.filter_state + n_filter) : nullptr;
   L.tile_list = b ? reinterpret_cast<int32_t *>(b + o_list) : nullptr;
-  L.tile_slot = b ? reinterpret_cast<int32_t *>(b + o_slot) : nullptr;
   L.rec_fg = b ? reinterpret_cast<uint32_t *>(b + o_fg) : nullptr;
   L.rec_roots = b ? reinterpret_cast<uint32_t *>(b + o_roots) : nullptr;
   L.rec_border = b ? reinterpret_cast<int32_t *>(b + o_border) : nullptr;
   L.entries = b ? reinterpret_cast<uint64_t *>(b + o_entries) : nullptr;
   L.n_ent = b ? reinterpret_cast<int32_t *>(b + o_nent) : nullptr;
+  L.band_first = b ? reinterpret_cast<int32_t *>(b + o_band) : nullptr;
   L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
   L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
   L.label = b ? reinterpret_cast<int32_t *>(b + o_label) : nullptr;
@@ -248,17 +260,15 @@ __global__ void clear_kernel(uint64_t *words, int64_t n) {
 // of one frame), thread t reading row t / 8 of the block, pixels 64 (t % 8) .. + 63 (the
 // row segments of two tiles) with 16-byte loads (kMode 2: mask 16-byte aligned and rows a
 // multiple of 16 bytes), dwords (kMode 1) or bytes (kMode 0), all issued before any is
-// used. A block with foreground sets its tiles' bits, appends them to the list (a tile's
-// list position is its record slot) and writes each listed tile's 32 row masks.
+// used. A block with foreground sets its tiles' bits and writes each such tile's 32 row
+// masks to its record. Nothing is counted here: the same-address atomics of a global
+// list counter would serialize the workgroups.
 template <int kMode>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask, int W, int H,
                                                             int64_t frame_px, Tiles T,
                                                             uint32_t *tile_bits,
-                                                            int32_t *tile_list,
-                                                            int32_t *tile_slot, uint32_t *rec_fg,
-                                                            uint32_t *n_list) {
+                                                            uint32_t *rec_fg) {
   __shared__ uint32_t s_bits;
-  __shared__ int s_base;
   const int t = threadIdx.x, r = t >> 3, q = t & 7;
   const int64_t f = blockIdx.z;
   const int tx0 = blockIdx.x * kScanTiles, ty = blockIdx.y;
@@ -327,21 +337,67 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
     atomicOr(&tile_bits[id0 >> 5], m << sh);
     if (sh > 16 && (m >> (32 - sh)) != 0)  // only words that hold existing tiles
       atomicOr(&tile_bits[(id0 >> 5) + 1], m >> (32 - sh));
-    s_base = static_cast<int>(atomicAdd(n_list, static_cast<uint32_t>(__popc(m))));
-  }
-  __syncthreads();
-  const int base = s_base;
-  if (t < kScanTiles && (m >> t & 1u)) {
-    const int slot = base + __popc(m & ((1u << t) - 1u));
-    tile_list[slot] = id0 + t;
-    tile_slot[id0 + t] = slot;
   }
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int j = 2 * q + h;
-    if (m >> j & 1u)
-      rec_fg[32 * (base + __popc(m & ((1u << j) - 1u))) + r] = h ? m1 : m0;
+    if (m >> j & 1u) rec_fg[32 * static_cast<int64_t>(id0 + j) + r] = h ? m1 : m0;
   }
+}
+
+// Lists the non-empty tiles in increasing order: workgroup c (in ticket order) takes
+// kListChunk words of the tile bitmap, kListPer per thread; a block-wide scan of their
+// counts and a decoupled look-back over the workgroups place each set bit. The last
+// workgroup writes the count (0, with the status word set, if the look-back failed).
+__global__ __launch_bounds__(kListThreads) void list_kernel(const uint32_t *tile_bits,
+                                                            int64_t n_bit_words,
+                                                            int32_t *tile_list,
+                                                            uint64_t *words, uint64_t *state,
+                                                            int32_t n_chunks, uint32_t *n_list,
+                                                            uint32_t *status) {
+  __shared__ int s_chunk;
+  __shared__ int s_wave[kListThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0)
+    s_chunk = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words), 1u,
+                                                      __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT));
+  __syncthreads();
+  const int c = s_chunk;  // < n_chunks: exactly n_chunks workgroups take tickets
+  const int64_t w0 = static_cast<int64_t>(c) * kListChunk + tid * kListPer;
+  uint32_t bits[kListPer];
+  int cnt = 0;
+#pragma unroll
+  for (int i = 0; i < kListPer; ++i) {
+    bits[i] = w0 + i < n_bit_words ? tile_bits[w0 + i] : 0u;
+    cnt += __popc(bits[i]);
+  }
+  int incl = cnt;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o);
+    if (lane >= o) incl += v;
+  }
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kListThreads / 64; ++w) {
+    if (w < wave) before += s_wave[w];
+    total += s_wave[w];
+  }
+  bool failed;
+  const int prefix = tg_detail::lookback_prefix_block<kListThreads, 1>(state, c, total, &failed);
+  if (failed) {
+    if (tid == 0) fail(status);
+  } else {
+    int at = prefix + before + incl - cnt;
+#pragma unroll
+    for (int i = 0; i < kListPer; ++i)
+      for (uint32_t m = bits[i]; m != 0; m &= m - 1)
+        tile_list[at++] = static_cast<int32_t>((w0 + i) * 32 + __builtin_ctz(m));
+  }
+  if (c == n_chunks - 1 && tid == 0)
+    *n_list = failed ? 0u : static_cast<uint32_t>(prefix + total);
 }
 
 // Labels the listed tiles, one wave per tile, a grid of resident one-wave workgroups
@@ -368,14 +424,15 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
   uint32_t next_row = 0;
   if (static_cast<int>(blockIdx.x) < n) {
     next_id = tile_list[blockIdx.x];
-    next_row = rec_fg[32 * static_cast<int64_t>(blockIdx.x) + r];
+    next_row = rec_fg[32 * static_cast<int64_t>(next_id) + r];
   }
   for (int it = blockIdx.x; it < n; it += gridDim.x) {
-    const TileAt a = tile_at(T, next_id);
+    const int id = next_id;
+    const TileAt a = tile_at(T, id);
     const uint32_t w = next_row;
     if (it + static_cast<int>(gridDim.x) < n) {
       next_id = tile_list[it + gridDim.x];
-      next_row = rec_fg[32 * static_cast<int64_t>(it + gridDim.x) + r];
+      next_row = rec_fg[32 * static_cast<int64_t>(next_id) + r];
     }
     const int tx0 = a.tx * kTile, ty0 = a.ty * kTile;
     int32_t *lf = label + a.f * frame_px;
@@ -433,11 +490,11 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
       }
     }
     roots |= __shfl_xor(roots, 32);
-    if (half == 0) rec_roots[32 * static_cast<int64_t>(it) + r] = roots;
+    if (half == 0) rec_roots[32 * static_cast<int64_t>(id) + r] = roots;
     lds_barrier();  // L resolved, the folds complete
     // border roots: lane l takes entry l (row 0 / row 31, column l % 32), then entry 64 + l
     // (column 0 / column 31, row l % 32); background entries are -1
-    int32_t *border = rec_border + 128 * static_cast<int64_t>(it);
+    int32_t *border = rec_border + 128 * static_cast<int64_t>(id);
 #pragma unroll
     for (int pass = 0; pass < 2; ++pass) {
       const int row = pass ? r : (half ? kTile - 1 : 0), c = pass ? (half ? kTile - 1 : 0) : r;
@@ -457,8 +514,8 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
       if (r >= o) incl += v;
     }
     const int total = __shfl(incl, kTile - 1);
-    if (lane == 0) n_ent[it] = total;
-    uint64_t *ent = entries + 256 * static_cast<int64_t>(it) + (incl - mine_roots);
+    if (lane == 0) n_ent[id] = total;
+    uint64_t *ent = entries + 256 * static_cast<int64_t>(id) + (incl - mine_roots);
     if (half == 0) {
       for (uint32_t m = roots; m; m &= m - 1) {
         const int s = __builtin_ctz(m), node = 16 * r + run_ordinal(st, s);
@@ -505,16 +562,16 @@ __device__ __forceinline__ void join_pairs(int32_t *lf, uint32_t fg, const int32
 // from the tiles' records (the tile itself and the up to three tiles holding the
 // neighbours); an item whose neighbouring tiles are all empty is skipped.
 __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
-    int64_t frame_px, Tiles T, const uint32_t *tile_bits, const int32_t *tile_slot,
-    const int32_t *tile_list, const uint32_t *n_list, const uint32_t *rec_fg,
-    const int32_t *rec_border, int32_t *label, uint32_t *status) {
+    int64_t frame_px, Tiles T, const uint32_t *tile_bits, const int32_t *tile_list,
+    const uint32_t *n_list, const uint32_t *rec_fg, const int32_t *rec_border, int32_t *label,
+    uint32_t *status) {
   const int n4 = 4 * static_cast<int>(*n_list);
   for (int i = blockIdx.x * kBorderThreads + threadIdx.x; i < n4;
        i += gridDim.x * kBorderThreads) {
     const int s = i >> 2, k = i & 3, id = tile_list[s];
     const TileAt a = tile_at(T, id);
-    const uint32_t *fs = rec_fg + 32 * static_cast<int64_t>(s);
-    const int32_t *bs = rec_border + 128 * static_cast<int64_t>(s);
+    const uint32_t *fs = rec_fg + 32 * static_cast<int64_t>(id);
+    const int32_t *bs = rec_border + 128 * static_cast<int64_t>(id);
     uint32_t fg = 0, nb = 0;
     int32_t lo[16], ln[18];
 #pragma unroll
@@ -531,7 +588,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 #pragma unroll
       for (int j = 0; j < 16; ++j) lo[j] = bs[16 * h + j];
       if (u) {  // neighbour j is column 16 h - 1 + j of the tile above
-        const int64_t su = tile_slot[up];
+        const int64_t su = up;
         const uint32_t row = rec_fg[32 * su + 31];
         const int32_t *b = rec_border + 128 * su + 32;
 #pragma unroll
@@ -543,12 +600,12 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
         }
       }
       if (ul) {  // column 31 of the tile above and to the left
-        const int64_t sl = tile_slot[up - 1];
+        const int64_t sl = up - 1;
         nb |= rec_fg[32 * sl + 31] >> 31;
         ln[0] = rec_border[128 * sl + 32 + 31];
       }
       if (ur) {  // column 0 of the tile above and to the right
-        const int64_t sr = tile_slot[up + 1];
+        const int64_t sr = up + 1;
         nb |= (rec_fg[32 * sr + 31] & 1u) << 17;
         ln[17] = rec_border[128 * sr + 32];
       }
@@ -565,7 +622,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 #pragma unroll
       for (int j = 0; j < 16; ++j) lo[j] = bs[64 + 16 * h + j];
       if (l) {  // neighbour j is row 16 h - 1 + j of the tile to the left
-        const int64_t sl = tile_slot[left];
+        const int64_t sl = left;
         const uint32_t *f = rec_fg + 32 * sl;
         const int32_t *b = rec_border + 128 * sl + 96;
 #pragma unroll
@@ -577,12 +634,12 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
         }
       }
       if (lu) {  // row 31 of the tile to the left and above
-        const int64_t su = tile_slot[left - T.tiles_x];
+        const int64_t su = left - T.tiles_x;
         nb |= rec_fg[32 * su + 31] >> 31;
         ln[0] = rec_border[128 * su + 96 + 31];
       }
       if (ld) {  // row 0 of the tile to the left and below
-        const int64_t sd = tile_slot[left + T.tiles_x];
+        const int64_t sd = left + T.tiles_x;
         nb |= (rec_fg[32 * sd] >> 31) << 17;
         ln[17] = rec_border[128 * sd + 96];
       }
@@ -591,117 +648,179 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
   }
 }
 
-// Numbers the components in raster order: one workgroup per band of 32 rows of a frame
-// (a tile row), in ticket order, bands in raster order. Thread t takes row t / 8 of the
-// band and the t % 8-th eighth of its tiles, left to right, so thread order is raster
-// order within the band. Its candidates are the recorded tile-local roots of that row of
-// its listed tiles; a candidate is a component when it is still its own parent (label =
-// own frame index, flagged). A block-wide scan and a decoupled look-back over bands give
-// each component its number; the thread then walks its tiles again (the same loads, now
-// in cache) to initialise the records and mark the roots.
+// Numbers the components in raster order, in three launches over the bands of 32 rows (a
+// tile row of a frame: band b is frame b / tiles_y, tile row b % tiles_y), none of whose
+// workgroups waits for another:
+//  count:  one workgroup per band. Thread t takes row t / 8 of the band and the t % 8-th
+//          eighth of its tiles, left to right, so thread order is raster order within
+//          the band. Its candidates are the recorded tile-local roots of that row of its
+//          non-empty tiles; a candidate is a component when it is still its own parent
+//          (label = own frame index, flagged). The band's count goes to band_first.
+//  scan:   one workgroup turns the counts into each band's first number and writes the
+//          number of components.
+//  assign: per band, the count again (the same loads, now in cache), a block-wide scan,
+//          then each component's record initialised and its root marked with its number.
 __device__ __forceinline__ int band_roots(int W, const uint32_t *tile_bits,
-                                          const int32_t *tile_slot, const uint32_t *rec_roots,
-                                          int32_t *lf, int base, int y, int tx_lo, int tx_hi,
-                                          int rr, Comp *comp, int f, int id,
-                                          int32_t max_components, bool assign) {
+                                          const uint32_t *rec_roots, int32_t *lf, int base,
+                                          int y, int tx_lo, int tx_hi, int rr, Comp *comp,
+                                          int f, int id, int32_t max_components, bool assign) {
   int cnt = 0;
-  int wi = -1;
-  uint32_t wv = 0;
-  for (int tx = tx_lo; tx < tx_hi; ++tx) {
-    const int tile = base + tx;
-    if ((tile >> 5) != wi) {  // the bitmap word holding this tile
-      wi = tile >> 5;
-      wv = tile_bits[wi];
+  // kBandBatch tiles at a time, each level of loads (bitmap, records, labels) issued for
+  // the whole batch before any is used
+  for (int b0 = tx_lo; b0 < tx_hi; b0 += kBandBatch) {
+    uint32_t cand[kBandBatch];
+#pragma unroll
+    for (int u = 0; u < kBandBatch; ++u) {
+      const int tile = base + b0 + u;
+      cand[u] = b0 + u < tx_hi && tile_set(tile_bits, tile)
+                    ? rec_roots[32 * static_cast<int64_t>(tile) + rr]
+                    : 0u;
     }
-    if (!(wv >> (tile & 31) & 1u)) continue;
-    const uint32_t cand = rec_roots[32 * static_cast<int64_t>(tile_slot[tile]) + rr];
-    for (uint32_t m = cand; m != 0; m &= m - 1) {
-      const int P = y * W + tx * kTile + __builtin_ctz(m);
-      if (lf[P] != (P | kRootFlag)) continue;
-      if (assign && id < max_components) {
-        comp[id] = Comp{f, P, INT_MAX, INT_MAX, INT_MIN, INT_MIN, 0, 0};
-        lf[P] = -(id + 1);
+#pragma unroll
+    for (int u = 0; u < kBandBatch; ++u) {
+      for (uint32_t m = cand[u]; m != 0; m &= m - 1) {
+        const int P = y * W + (b0 + u) * kTile + __builtin_ctz(m);
+        if (lf[P] != (P | kRootFlag)) continue;
+        if (assign && id < max_components) {
+          comp[id] = Comp{f, P, INT_MAX, y, INT_MIN, INT_MIN, 0, 0};
+          lf[P] = -(id + 1);
+        }
+        ++cnt;
+        ++id;
       }
-      ++cnt;
-      ++id;
     }
   }
   return cnt;
 }
 
-__global__ __launch_bounds__(kBandThreads) void roots_kernel(
-    int W, int H, int64_t frame_px, Tiles T, const uint32_t *tile_bits,
-    const int32_t *tile_slot, const uint32_t *rec_roots, int32_t *label, Comp *comp,
-    int32_t max_components, uint64_t *words, uint64_t *state, int32_t n_bands,
-    int32_t *n_components) {
-  __shared__ int s_band, s_base;
-  __shared__ int s_wave[kBandThreads / 64];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0)
-    s_band = static_cast<int>(__hip_atomic_fetch_add(reinterpret_cast<uint32_t *>(words), 1u,
-                                                     __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT));
-  __syncthreads();
-  const int band = s_band;
-  const int f = band / T.tiles_y, ty = band - f * T.tiles_y;
-  const int rr = tid >> 3, q = tid & 7, y = ty * kTile + rr;
-  const int chunk = (T.tiles_x + 7) / 8;
-  const int tx_lo = min(q * chunk, T.tiles_x), tx_hi = min(tx_lo + chunk, T.tiles_x);
-  const int base = (f * T.tiles_y + ty) * T.tiles_x;
-  int32_t *lf = label + static_cast<int64_t>(f) * frame_px;
-  const bool rows_in = y < H;
-  const int cnt = rows_in ? band_roots(W, tile_bits, tile_slot, rec_roots, lf, base, y, tx_lo,
-                                       tx_hi, rr, comp, f, 0, max_components, false)
-                          : 0;
+// This thread's share of a band: frame, first tile id of the band, pixel row, tile range.
+struct BandPart {
+  int f, base, y, tx_lo, tx_hi, rr;
+  bool rows_in;
+};
+__device__ __forceinline__ BandPart band_part(const Tiles &T, int H, int band) {
+  BandPart p;
+  const int tid = threadIdx.x;
+  p.f = band / T.tiles_y;
+  const int ty = band - p.f * T.tiles_y;
+  p.rr = tid >> 3;
+  p.y = ty * kTile + p.rr;
+  const int q = tid & 7, chunk = (T.tiles_x + 7) / 8;
+  p.tx_lo = min(q * chunk, T.tiles_x);
+  p.tx_hi = min(p.tx_lo + chunk, T.tiles_x);
+  p.base = (p.f * T.tiles_y + ty) * T.tiles_x;
+  p.rows_in = p.y < H;
+  return p;
+}
 
-  // Exclusive scan of the counts over the workgroup, then the look-back over bands.
-  int incl = cnt;
+// Exclusive scan of v over a workgroup of kThreads threads (s_wave: kThreads / 64 ints of
+// LDS); *total gets the sum.
+template <int kThreads>
+__device__ __forceinline__ int block_exclusive(int v, int *s_wave, int *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = v;
   for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o);
-    if (lane >= o) incl += v;
+    const int u = __shfl_up(incl, o);
+    if (lane >= o) incl += u;
   }
   if (lane == 63) s_wave[wave] = incl;
   __syncthreads();
-  int before = 0, total = 0;
+  int before = 0, sum = 0;
 #pragma unroll
-  for (int w = 0; w < kBandThreads / 64; ++w) {
+  for (int w = 0; w < kThreads / 64; ++w) {
     if (w < wave) before += s_wave[w];
-    total += s_wave[w];
+    sum += s_wave[w];
   }
-  if (wave == 0) {
-    bool failed;
-    const int prefix = tg_detail::lookback_prefix(state, band, total, &failed);
-    if (lane == 0) {
-      s_base = prefix;
-      if (band == n_bands - 1) *n_components = failed ? TG_E_INTERNAL : prefix + total;
+  *total = sum;
+  return before + incl - v;
+}
+
+__global__ __launch_bounds__(kBandThreads) void count_kernel(int W, int H, int64_t frame_px,
+                                                             Tiles T, const uint32_t *tile_bits,
+                                                             const uint32_t *rec_roots,
+                                                             int32_t *label,
+                                                             int32_t *band_first) {
+  __shared__ int s_wave[kBandThreads / 64];
+  const int band = blockIdx.x;
+  const BandPart p = band_part(T, H, band);
+  int32_t *lf = label + static_cast<int64_t>(p.f) * frame_px;
+  const int cnt = p.rows_in ? band_roots(W, tile_bits, rec_roots, lf, p.base, p.y, p.tx_lo,
+                                         p.tx_hi, p.rr, nullptr, p.f, 0, 0, false)
+                            : 0;
+  int total;
+  block_exclusive<kBandThreads>(cnt, s_wave, &total);
+  if (threadIdx.x == 0) band_first[band] = total;
+}
+
+__global__ __launch_bounds__(kBandScanThreads) void band_scan_kernel(int32_t *band_first,
+                                                                     int64_t n_bands,
+                                                                     int32_t *n_components) {
+  __shared__ int s_wave[kBandScanThreads / 64];
+  constexpr int kPer = 4;
+  int carry = 0;
+  for (int64_t b0 = 0; b0 < n_bands; b0 += kBandScanThreads * kPer) {
+    const int64_t i0 = b0 + threadIdx.x * kPer;
+    int v[kPer], cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      v[k] = i0 + k < n_bands ? band_first[i0 + k] : 0;
+      cnt += v[k];
     }
+    int total;
+    int at = carry + block_exclusive<kBandScanThreads>(cnt, s_wave, &total);
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      if (i0 + k < n_bands) band_first[i0 + k] = at;
+      at += v[k];
+    }
+    carry += total;
+    __syncthreads();  // s_wave is written again by the next step
   }
-  __syncthreads();
+  if (threadIdx.x == 0) *n_components = carry;
+}
+
+__global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int H, int64_t frame_px,
+                                                              Tiles T, const uint32_t *tile_bits,
+                                                              const uint32_t *rec_roots,
+                                                              int32_t *label,
+                                                              const int32_t *band_first,
+                                                              Comp *comp,
+                                                              int32_t max_components) {
+  __shared__ int s_wave[kBandThreads / 64];
+  const int band = blockIdx.x;
+  const BandPart p = band_part(T, H, band);
+  int32_t *lf = label + static_cast<int64_t>(p.f) * frame_px;
+  const int cnt = p.rows_in ? band_roots(W, tile_bits, rec_roots, lf, p.base, p.y, p.tx_lo,
+                                         p.tx_hi, p.rr, comp, p.f, 0, max_components, false)
+                            : 0;
+  int total;
+  const int before = block_exclusive<kBandThreads>(cnt, s_wave, &total);
   if (cnt > 0)
-    band_roots(W, tile_bits, tile_slot, rec_roots, lf, base, y, tx_lo, tx_hi, rr, comp, f,
-               s_base + before + incl - cnt, max_components, true);
+    band_roots(W, tile_bits, rec_roots, lf, p.base, p.y, p.tx_lo, p.tx_hi, p.rr, comp, p.f,
+               band_first[band] + before, max_components, true);
 }
 
 // Folds each tile-local component (its entry) into its component's record: up the
-// union-find from its local root to the numbered root, then one set of global atomics.
-// A grid of resident workgroups walks the listed tiles' entry slots.
+// union-find from its local root to the numbered root, then one set of global atomics
+// (the record's top row is its root's, set when it was numbered). A grid of resident
+// workgroups walks the listed tiles' entry slots.
 __global__ __launch_bounds__(kEntryThreads) void boxes_kernel(int W, int64_t frame_px, Tiles T,
-                                                             const int32_t *tile_list,
-                                                             const uint32_t *n_list,
-                                                             const uint64_t *entries,
-                                                             const int32_t *n_ent,
-                                                             const int32_t *label, Comp *comp,
-                                                             uint32_t *status) {
+                                                              const int32_t *tile_list,
+                                                              const uint32_t *n_list,
+                                                              const uint64_t *entries,
+                                                              const int32_t *n_ent,
+                                                              const int32_t *label, Comp *comp,
+                                                              uint32_t *status) {
   const int64_t n = 256 * static_cast<int64_t>(*n_list);
   for (int64_t e = blockIdx.x * kEntryThreads + threadIdx.x; e < n;
        e += static_cast<int64_t>(gridDim.x) * kEntryThreads) {
-    const int slot = static_cast<int>(e >> 8);
-    if ((e & 255) >= n_ent[slot]) continue;
-    const uint64_t v64 = entries[e];
+    const int id = tile_list[e >> 8], j = static_cast<int>(e & 255);
+    if (j >= n_ent[id]) continue;
+    const uint64_t v64 = entries[256 * static_cast<int64_t>(id) + j];
     const int i = static_cast<int>(v64 >> 26) & 1023;
     const int ex0 = static_cast<int>(v64 >> 21) & 31, ex1 = static_cast<int>(v64 >> 16) & 31;
     const int ey1 = static_cast<int>(v64 >> 11) & 31, cnt = static_cast<int>(v64 & 2047);
-    const TileAt a = tile_at(T, tile_list[slot]);
+    const TileAt a = tile_at(T, id);
     const int x0 = a.tx * kTile, y0 = a.ty * kTile;
     const int32_t *lf = label + a.f * frame_px;
     // up the union-find over local roots to the numbered root; every link points to a
@@ -721,7 +840,6 @@ __global__ __launch_bounds__(kEntryThreads) void boxes_kernel(int W, int64_t fra
     if (v >= 0) continue;  // a component past max_components (or a broken link): not measured
     Comp *c = comp + (-v - 1);
     atomicMin(&c->x0, x0 + ex0);
-    atomicMin(&c->y0, y0 + (i >> 5));
     atomicMax(&c->x1, x0 + ex1);
     atomicMax(&c->y1, y0 + ey1);
     atomicAdd(&c->area, cnt);
@@ -904,28 +1022,35 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
     return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
   }
   uint32_t *status = reinterpret_cast<uint32_t *>(L.words + 2);
+  uint32_t *n_list = reinterpret_cast<uint32_t *>(L.words + 3);
   hipLaunchKernelGGL(clear_kernel, dim3(static_cast<uint32_t>((L.n_words + 255) / 256)),
                      dim3(256), 0, s, L.words, L.n_words);
-  uint32_t *n_list = reinterpret_cast<uint32_t *>(L.words + 3);
   if (vec && W % 16 == 0)
     hipLaunchKernelGGL(scan_kernel<2>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
+                       frame_px, T, L.tile_bits, L.rec_fg);
   else if (word)
     hipLaunchKernelGGL(scan_kernel<1>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
+                       frame_px, T, L.tile_bits, L.rec_fg);
   else
     hipLaunchKernelGGL(scan_kernel<0>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.tile_list, L.tile_slot, L.rec_fg, n_list);
+                       frame_px, T, L.tile_bits, L.rec_fg);
+  const int64_t n_chunks = list_chunks(T.n);
+  hipLaunchKernelGGL(list_kernel, dim3(static_cast<uint32_t>(n_chunks)), dim3(kListThreads), 0,
+                     s, L.tile_bits, (T.n + 31) / 32, L.tile_list, L.words, L.list_state,
+                     static_cast<int32_t>(n_chunks), n_list, status);
   hipLaunchKernelGGL(local_kernel, local_groups, dim3(kLocalThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.rec_fg, L.rec_roots, L.rec_border, L.entries,
                      L.n_ent, L.label, status);
   hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, frame_px, T,
-                     L.tile_bits, L.tile_slot, L.tile_list, n_list, L.rec_fg, L.rec_border,
-                     L.label, status);
-  hipLaunchKernelGGL(roots_kernel, dim3(static_cast<uint32_t>(n_bands)), dim3(kBandThreads), 0,
-                     s, W, H, frame_px, T, L.tile_bits, L.tile_slot, L.rec_roots, L.label,
-                     L.comp, a->max_components, L.words, L.root_state,
-                     static_cast<int32_t>(n_bands), a->n_components);
+                     L.tile_bits, L.tile_list, n_list, L.rec_fg, L.rec_border, L.label, status);
+  const dim3 bands(static_cast<uint32_t>(n_bands));
+  hipLaunchKernelGGL(count_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
+                     L.tile_bits, L.rec_roots, L.label, L.band_first);
+  hipLaunchKernelGGL(band_scan_kernel, dim3(1), dim3(kBandScanThreads), 0, s, L.band_first,
+                     n_bands, a->n_components);
+  hipLaunchKernelGGL(assign_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
+                     L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
+                     a->max_components);
   hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kEntryThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
