@@ -6,7 +6,7 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
 // 2018), tile-local first and merged along tile borders as in the block-based labelling of
-// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in eleven launches on
+// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in ten launches on
 // the caller's stream. Foreground masks are sparse, so only the scan reads the mask; the
 // other passes visit the 32x32 tiles that hold foreground, through per-tile records
 // (row masks, local-root masks, the tile-local roots of the border pixels) indexed by
@@ -23,23 +23,25 @@
 //             of touching runs); each tile-local root's label word gets its own frame
 //             index, the tile's local roots and border roots go to its record, and each
 //             local component's box and pixel count, folded in LDS, to one of the tile's
-//             256 entry slots. No other label word is written or read.
+//             256 entry slots, and the tile's count of local roots is added to its
+//             band's. No other label word is written or read.
 //  5. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
 //             column in two halves) join each foreground pixel with its foreground
 //             neighbours across the border, reading the records of the tile and of the
 //             tiles around it, with global atomics on the label array; an item whose
 //             neighbouring tiles are all empty is skipped. Every 8-neighbour pair across a
-//             tile border is seen from the tile below or to the right of it.
-//  6-8. count, scan, assign: per band of 32 rows (a tile row of a frame), the recorded
-//             local roots that are still their own parent (the components) are counted
-//             in raster order; one workgroup scans the bands' counts; per band, each
-//             component's record is initialised and its root marked with its number.
-//  9. boxes:  each local component (its entry) follows the union-find from its root to
+//             tile border is seen from the tile below or to the right of it. A root that
+//             gets linked leaves its band's count, which then counts components.
+//  6-7. scan, assign: one workgroup scans the bands' counts; per band of 32 rows (a tile
+//             row of a frame), the recorded local roots still their own parent (the
+//             components) are numbered in raster order, each component's record is
+//             initialised and its root marked with its number.
+//  8. boxes:  each local component (its entry) follows the union-find from its root to
 //             its component's number and folds its box and count into the record with
 //             one set of global atomics.
-// 10. filter: components of at least min_area pixels, compacted in number order with a
+//  9. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows.
-// 11. begin:  frame_begin by binary search over the kept rows' frames.
+// 10. begin:  frame_begin by binary search over the kept rows' frames.
 // Every union-find walk checks the invariant it relies on (unionfind.h); a walk that meets a
 // link that does not point to a smaller index ends, sets the workspace's status word, and
 // the call reports *n_rois = *n_components = TG_E_INTERNAL instead of RoIs.
@@ -89,12 +91,15 @@ struct Tiles {
 
 struct Layout {
   // [0]: list ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed,
-  // [4]: unused, then the look-back words of the list and filter passes, then the tile
-  // bitmap (bit t of 32-bit word t / 32: tile t holds foreground); all cleared by the
-  // first launch
+  // [4]: unused, then the look-back words of the list and filter passes, the tile
+  // bitmap (bit t of 32-bit word t / 32: tile t holds foreground) and the bands' counts
+  // of components (32-bit); all cleared by the first launch
   uint64_t *words;
   uint64_t *list_state, *filter_state;
   uint32_t *tile_bits;
+  // per band: its count of components (tile-local roots added by the local pass, linked
+  // roots removed by the merge), then its first component's number
+  int32_t *band_first;
   int32_t *tile_list;  // ids of the non-empty tiles, in increasing order
   // Record of non-empty tile t: fg[32 t + r], row r's foreground as a 32-bit mask;
   // roots[32 t + r], row r's tile-local roots; border[128 t + e], the tile-local root (a
@@ -107,7 +112,6 @@ struct Layout {
   // pixel count, the box in tile coordinates (its top row is the root's).
   uint64_t *entries;
   int32_t *n_ent;
-  int32_t *band_first;  // per band: its count of components, then its first one's number
   Comp *comp;
   int32_t *kept_frame;
   int32_t *label;
@@ -127,7 +131,7 @@ Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
   const int64_t n_chunks = list_chunks(n_tiles);
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
   const int64_t bit_words64 = (n_tiles + 63) / 64;
-  L.n_words = 5 + n_chunks + n_filter + bit_words64;
+  L.n_words = 5 + n_chunks + n_filter + bit_words64 + (n_bands + 1) / 2;
   const size_t nt = static_cast<size_t>(n_tiles);
   const size_t o_list = round_up(8 * static_cast<size_t>(L.n_words), 256);
   const size_t o_fg = round_up(o_list + 4 * nt, 256);
@@ -135,8 +139,7 @@ Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
   const size_t o_border = round_up(o_roots + 128 * nt, 256);
   const size_t o_entries = round_up(o_border + 512 * nt, 256);
   const size_t o_nent = round_up(o_entries + 8 * 256 * nt, 256);
-  const size_t o_band = round_up(o_nent + 4 * nt, 256);
-  const size_t o_comp = round_up(o_band + 4 * static_cast<size_t>(n_bands), 256);
+  const size_t o_comp = round_up(o_nent + 4 * nt, 256);
   const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
   const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
   L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
@@ -145,13 +148,13 @@ Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
   L.list_state = b ? L.words + 5 : nullptr;
   L.filter_state = b ? L.list_state + n_chunks : nullptr;
   L.tile_bits = b ? reinterpret_cast<uint32_t *>(L.filter_state + n_filter) : nullptr;
+  L.band_first = b ? reinterpret_cast<int32_t *>(L.filter_state + n_filter + bit_words64) : nullptr;
   L.tile_list = b ? reinterpret_cast<int32_t *>(b + o_list) : nullptr;
   L.rec_fg = b ? reinterpret_cast<uint32_t *>(b + o_fg) : nullptr;
   L.rec_roots = b ? reinterpret_cast<uint32_t *>(b + o_roots) : nullptr;
   L.rec_border = b ? reinterpret_cast<int32_t *>(b + o_border) : nullptr;
   L.entries = b ? reinterpret_cast<uint64_t *>(b + o_entries) : nullptr;
   L.n_ent = b ? reinterpret_cast<int32_t *>(b + o_nent) : nullptr;
-  L.band_first = b ? reinterpret_cast<int32_t *>(b + o_band) : nullptr;
   L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
   L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
   L.label = b ? reinterpret_cast<int32_t *>(b + o_label) : nullptr;
@@ -174,13 +177,20 @@ struct LdsLabels {
   __device__ int link(int i, int p) { return atomicMin(&L[i], p); }
 };
 
-// Union-find over the flagged words of tile-local roots in global memory.
+// Union-find over the flagged words of tile-local roots in global memory (one frame's
+// labels, W pixels a row). Links only lower a word, so a root that is linked (to a
+// smaller index) stops being a root for good; that link is the one that removes it from
+// its band's count of components (band_count: the frame's bands).
 struct RootLabels {
   int32_t *L;
+  int32_t *band_count;
+  int W;
   __device__ int parent(int i) const { return g_load(&L[i]) & kIndex; }
   __device__ int link(int i, int p) {
-    return __hip_atomic_fetch_min(&L[i], p | kRootFlag, __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT) & kIndex;
+    const int old = __hip_atomic_fetch_min(&L[i], p | kRootFlag, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT) & kIndex;
+    if (old == i && p < i) atomicSub(&band_count[(i / W) / kTile], 1);
+    return old;
   }
 };
 
@@ -408,7 +418,8 @@ __global__ __launch_bounds__(kListThreads) void list_kernel(const uint32_t *tile
 // columns and pixel count folded in LDS. Written: the frame index of each tile-local root
 // (flagged) in the label array -- the only label words any later pass reads --, the
 // tile's local-root row masks and border roots in its record, and one entry per local
-// component (its box in tile coordinates and its pixel count) in the tile's slots.
+// component (its box in tile coordinates and its pixel count) in the tile's slots; the
+// number of local roots is added to the band's count of components.
 __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t frame_px, Tiles T,
                                                               const int32_t *tile_list,
                                                               const uint32_t *n_list,
@@ -416,7 +427,8 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
                                                               uint32_t *rec_roots,
                                                               int32_t *rec_border,
                                                               uint64_t *entries, int32_t *n_ent,
-                                                              int32_t *label, uint32_t *status) {
+                                                              int32_t *label, int32_t *band_count,
+                                                              uint32_t *status) {
   __shared__ RunTile S;
   const int n = static_cast<int>(*n_list);
   const int lane = threadIdx.x, r = lane & 31, half = lane >> 5;
@@ -514,7 +526,10 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
       if (r >= o) incl += v;
     }
     const int total = __shfl(incl, kTile - 1);
-    if (lane == 0) n_ent[id] = total;
+    if (lane == 0) {
+      n_ent[id] = total;
+      atomicAdd(&band_count[a.f * T.tiles_y + a.ty], total);
+    }
     uint64_t *ent = entries + 256 * static_cast<int64_t>(id) + (incl - mine_roots);
     if (half == 0) {
       for (uint32_t m = roots; m; m &= m - 1) {
@@ -536,10 +551,9 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
 // offsets -1 .. 16 along the border (bits of nb, tile-local roots ln). Pixel k meets
 // neighbours k, k + 1, k + 2; a pair equal to the one just joined is skipped (along a
 // border most repeat).
-__device__ __forceinline__ void join_pairs(int32_t *lf, uint32_t fg, const int32_t lo[16],
+__device__ __forceinline__ void join_pairs(RootLabels m, uint32_t fg, const int32_t lo[16],
                                            uint32_t nb, const int32_t ln[18], uint32_t *status) {
   int pa = -1, pb = -1;
-  RootLabels m{lf};
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     if (!(fg >> k & 1u)) continue;
@@ -562,9 +576,9 @@ __device__ __forceinline__ void join_pairs(int32_t *lf, uint32_t fg, const int32
 // from the tiles' records (the tile itself and the up to three tiles holding the
 // neighbours); an item whose neighbouring tiles are all empty is skipped.
 __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
-    int64_t frame_px, Tiles T, const uint32_t *tile_bits, const int32_t *tile_list,
+    int W, int64_t frame_px, Tiles T, const uint32_t *tile_bits, const int32_t *tile_list,
     const uint32_t *n_list, const uint32_t *rec_fg, const int32_t *rec_border, int32_t *label,
-    uint32_t *status) {
+    int32_t *band_count, uint32_t *status) {
   const int n4 = 4 * static_cast<int>(*n_list);
   for (int i = blockIdx.x * kBorderThreads + threadIdx.x; i < n4;
        i += gridDim.x * kBorderThreads) {
@@ -644,22 +658,24 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
         ln[17] = rec_border[128 * sd + 96];
       }
     }
-    join_pairs(label + a.f * frame_px, fg, lo, nb, ln, status);
+    join_pairs(RootLabels{label + a.f * frame_px, band_count + a.f * T.tiles_y, W}, fg, lo, nb,
+               ln, status);
   }
 }
 
-// Numbers the components in raster order, in three launches over the bands of 32 rows (a
-// tile row of a frame: band b is frame b / tiles_y, tile row b % tiles_y), none of whose
-// workgroups waits for another:
-//  count:  one workgroup per band. Thread t takes row t / 8 of the band and the t % 8-th
+// Numbers the components in raster order over the bands of 32 rows (a tile row of a
+// frame: band b is frame b / tiles_y, tile row b % tiles_y), in two launches none of
+// whose workgroups waits for another. The bands' counts of components are already known:
+// the local pass adds each tile's local roots, the merge removes each root it links.
+//  scan:   one workgroup turns the counts into each band's first number and writes the
+//          number of components.
+//  assign: one workgroup per band. Thread t takes row t / 8 of the band and the t % 8-th
 //          eighth of its tiles, left to right, so thread order is raster order within
 //          the band. Its candidates are the recorded tile-local roots of that row of its
 //          non-empty tiles; a candidate is a component when it is still its own parent
-//          (label = own frame index, flagged). The band's count goes to band_first.
-//  scan:   one workgroup turns the counts into each band's first number and writes the
-//          number of components.
-//  assign: per band, the count again (the same loads, now in cache), a block-wide scan,
-//          then each component's record initialised and its root marked with its number.
+//          (label = own frame index, flagged). A block-wide scan of the threads' counts
+//          places them; each component's record is initialised and its root marked with
+//          its number.
 __device__ __forceinline__ int band_roots(int W, const uint32_t *tile_bits,
                                           const uint32_t *rec_roots, int32_t *lf, int base,
                                           int y, int tx_lo, int tx_hi, int rr, Comp *comp,
@@ -681,7 +697,7 @@ __device__ __forceinline__ int band_roots(int W, const uint32_t *tile_bits,
       for (uint32_t m = cand[u]; m != 0; m &= m - 1) {
         const int P = y * W + (b0 + u) * kTile + __builtin_ctz(m);
         if (lf[P] != (P | kRootFlag)) continue;
-        if (assign && id < max_components) {
+        if (assign && id >= 0 && id < max_components) {
           comp[id] = Comp{f, P, INT_MAX, y, INT_MIN, INT_MIN, 0, 0};
           lf[P] = -(id + 1);
         }
@@ -735,26 +751,10 @@ __device__ __forceinline__ int block_exclusive(int v, int *s_wave, int *total) {
   return before + incl - v;
 }
 
-__global__ __launch_bounds__(kBandThreads) void count_kernel(int W, int H, int64_t frame_px,
-                                                             Tiles T, const uint32_t *tile_bits,
-                                                             const uint32_t *rec_roots,
-                                                             int32_t *label,
-                                                             int32_t *band_first) {
-  __shared__ int s_wave[kBandThreads / 64];
-  const int band = blockIdx.x;
-  const BandPart p = band_part(T, H, band);
-  int32_t *lf = label + static_cast<int64_t>(p.f) * frame_px;
-  const int cnt = p.rows_in ? band_roots(W, tile_bits, rec_roots, lf, p.base, p.y, p.tx_lo,
-                                         p.tx_hi, p.rr, nullptr, p.f, 0, 0, false)
-                            : 0;
-  int total;
-  block_exclusive<kBandThreads>(cnt, s_wave, &total);
-  if (threadIdx.x == 0) band_first[band] = total;
-}
-
 __global__ __launch_bounds__(kBandScanThreads) void band_scan_kernel(int32_t *band_first,
                                                                      int64_t n_bands,
-                                                                     int32_t *n_components) {
+                                                                     int32_t *n_components,
+                                                                     uint32_t *status) {
   __shared__ int s_wave[kBandScanThreads / 64];
   constexpr int kPer = 4;
   int carry = 0;
@@ -764,6 +764,10 @@ __global__ __launch_bounds__(kBandScanThreads) void band_scan_kernel(int32_t *ba
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
       v[k] = i0 + k < n_bands ? band_first[i0 + k] : 0;
+      if (v[k] < 0) {  // only a broken union-find could remove more roots than there were
+        fail(status);
+        v[k] = 0;
+      }
       cnt += v[k];
     }
     int total;
@@ -1040,14 +1044,13 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
                      static_cast<int32_t>(n_chunks), n_list, status);
   hipLaunchKernelGGL(local_kernel, local_groups, dim3(kLocalThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.rec_fg, L.rec_roots, L.rec_border, L.entries,
-                     L.n_ent, L.label, status);
-  hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, frame_px, T,
-                     L.tile_bits, L.tile_list, n_list, L.rec_fg, L.rec_border, L.label, status);
-  const dim3 bands(static_cast<uint32_t>(n_bands));
-  hipLaunchKernelGGL(count_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
-                     L.tile_bits, L.rec_roots, L.label, L.band_first);
+                     L.n_ent, L.label, L.band_first, status);
+  hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, W, frame_px, T,
+                     L.tile_bits, L.tile_list, n_list, L.rec_fg, L.rec_border, L.label,
+                     L.band_first, status);
   hipLaunchKernelGGL(band_scan_kernel, dim3(1), dim3(kBandScanThreads), 0, s, L.band_first,
-                     n_bands, a->n_components);
+                     n_bands, a->n_components, status);
+  const dim3 bands(static_cast<uint32_t>(n_bands));
   hipLaunchKernelGGL(assign_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
                      L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
                      a->max_components);
