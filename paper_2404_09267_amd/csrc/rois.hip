@@ -6,7 +6,7 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
 // 2018), tile-local first and merged along tile borders as in the block-based labelling of
-// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in ten launches on
+// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in nine launches on
 // the caller's stream. Foreground masks are sparse, so only the scan reads the mask; the
 // other passes visit the 32x32 tiles that hold foreground, through per-tile records
 // (row masks, local-root masks, the tile-local roots of the border pixels) indexed by
@@ -40,8 +40,8 @@
 //             its component's number and folds its box and count into the record with
 //             one set of global atomics.
 //  9. filter: components of at least min_area pixels, compacted in number order with a
-//             look-back, written as tg_roi rows.
-// 10. begin:  frame_begin by binary search over the kept rows' frames.
+//             look-back, written as tg_roi rows; each frame's first row (frame_begin) is
+//             the compacted position of the frame's first component.
 // Every union-find walk checks the invariant it relies on (unionfind.h); a walk that meets a
 // link that does not point to a smaller index ends, sets the workspace's status word, and
 // the call reports *n_rois = *n_components = TG_E_INTERNAL instead of RoIs.
@@ -113,7 +113,6 @@ struct Layout {
   uint64_t *entries;
   int32_t *n_ent;
   Comp *comp;
-  int32_t *kept_frame;
   int32_t *label;
   int64_t n_words;
   size_t bytes;
@@ -140,8 +139,7 @@ Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
   const size_t o_entries = round_up(o_border + 512 * nt, 256);
   const size_t o_nent = round_up(o_entries + 8 * 256 * nt, 256);
   const size_t o_comp = round_up(o_nent + 4 * nt, 256);
-  const size_t o_kept = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
-  const size_t o_label = round_up(o_kept + 4 * static_cast<size_t>(max_components), 256);
+  const size_t o_label = round_up(o_comp + sizeof(Comp) * static_cast<size_t>(max_components), 256);
   L.bytes = round_up(o_label + 4 * static_cast<size_t>(n_px), 256);
   char *b = static_cast<char *>(base);
   L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
@@ -156,7 +154,6 @@ Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
   L.entries = b ? reinterpret_cast<uint64_t *>(b + o_entries) : nullptr;
   L.n_ent = b ? reinterpret_cast<int32_t *>(b + o_nent) : nullptr;
   L.comp = b ? reinterpret_cast<Comp *>(b + o_comp) : nullptr;
-  L.kept_frame = b ? reinterpret_cast<int32_t *>(b + o_kept) : nullptr;
   L.label = b ? reinterpret_cast<int32_t *>(b + o_label) : nullptr;
   return L;
 }
@@ -180,17 +177,35 @@ struct LdsLabels {
 // Union-find over the flagged words of tile-local roots in global memory (one frame's
 // labels, W pixels a row). Links only lower a word, so a root that is linked (to a
 // smaller index) stops being a root for good; that link is the one that removes it from
-// its band's count of components (band_count: the frame's bands).
+// its band's count of components (band_count: the frame's bands). The removals are
+// collected for up to two bands and applied by flush(), so that no atomic on a count
+// sits between the loads of a union-find walk; a third band is applied at once.
 struct RootLabels {
   int32_t *L;
   int32_t *band_count;
   int W;
+  int band0 = -1, n0 = 0, band1 = -1, n1 = 0;
   __device__ int parent(int i) const { return g_load(&L[i]) & kIndex; }
   __device__ int link(int i, int p) {
     const int old = __hip_atomic_fetch_min(&L[i], p | kRootFlag, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT) & kIndex;
-    if (old == i && p < i) atomicSub(&band_count[(i / W) / kTile], 1);
+    if (old == i && p < i) {
+      const int band = (i / W) / kTile;
+      if (band == band0 || band0 < 0) {
+        band0 = band;
+        ++n0;
+      } else if (band == band1 || band1 < 0) {
+        band1 = band;
+        ++n1;
+      } else {
+        atomicSub(&band_count[band], 1);
+      }
+    }
     return old;
+  }
+  __device__ void flush() {
+    if (n0) atomicSub(&band_count[band0], n0);
+    if (n1) atomicSub(&band_count[band1], n1);
   }
 };
 
@@ -567,6 +582,7 @@ __device__ __forceinline__ void join_pairs(RootLabels m, uint32_t fg, const int3
       pb = b;
     }
   }
+  m.flush();
 }
 
 // Four items per listed tile, walked by a grid of resident workgroups: its top row in
@@ -658,8 +674,8 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
         ln[17] = rec_border[128 * sd + 96];
       }
     }
-    join_pairs(RootLabels{label + a.f * frame_px, band_count + a.f * T.tiles_y, W}, fg, lo, nb,
-               ln, status);
+    RootLabels roots{label + a.f * frame_px, band_count + a.f * T.tiles_y, W};
+    join_pairs(roots, fg, lo, nb, ln, status);
   }
 }
 
@@ -676,37 +692,52 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 //          (label = own frame index, flagged). A block-wide scan of the threads' counts
 //          places them; each component's record is initialised and its root marked with
 //          its number.
-__device__ __forceinline__ int band_roots(int W, const uint32_t *tile_bits,
-                                          const uint32_t *rec_roots, int32_t *lf, int base,
-                                          int y, int tx_lo, int tx_hi, int rr, Comp *comp,
-                                          int f, int id, int32_t max_components, bool assign) {
+// One batch of a thread's tiles (b0 .. b0 + kBandBatch - 1, below tx_hi) in row y (row rr
+// of the band): comps[u] gets the bits of tile b0 + u's recorded local roots in that row
+// that are still their own parent (the components). Each level of loads (bitmap,
+// records, labels) is issued for the whole batch before any is used. Returns how many.
+__device__ __forceinline__ int batch_roots(int W, const uint32_t *tile_bits,
+                                           const uint32_t *rec_roots, const int32_t *lf,
+                                           int base, int y, int b0, int tx_hi, int rr,
+                                           uint32_t comps[kBandBatch]) {
+  uint32_t cand[kBandBatch];
+#pragma unroll
+  for (int u = 0; u < kBandBatch; ++u) {
+    const int tile = base + b0 + u;
+    cand[u] = b0 + u < tx_hi && tile_set(tile_bits, tile)
+                  ? rec_roots[32 * static_cast<int64_t>(tile) + rr]
+                  : 0u;
+  }
   int cnt = 0;
-  // kBandBatch tiles at a time, each level of loads (bitmap, records, labels) issued for
-  // the whole batch before any is used
-  for (int b0 = tx_lo; b0 < tx_hi; b0 += kBandBatch) {
-    uint32_t cand[kBandBatch];
 #pragma unroll
-    for (int u = 0; u < kBandBatch; ++u) {
-      const int tile = base + b0 + u;
-      cand[u] = b0 + u < tx_hi && tile_set(tile_bits, tile)
-                    ? rec_roots[32 * static_cast<int64_t>(tile) + rr]
-                    : 0u;
+  for (int u = 0; u < kBandBatch; ++u) {
+    comps[u] = 0;
+    for (uint32_t m = cand[u]; m != 0; m &= m - 1) {
+      const int P = y * W + (b0 + u) * kTile + __builtin_ctz(m);
+      if (lf[P] == (P | kRootFlag)) comps[u] |= m & (0u - m);
     }
-#pragma unroll
-    for (int u = 0; u < kBandBatch; ++u) {
-      for (uint32_t m = cand[u]; m != 0; m &= m - 1) {
-        const int P = y * W + (b0 + u) * kTile + __builtin_ctz(m);
-        if (lf[P] != (P | kRootFlag)) continue;
-        if (assign && id >= 0 && id < max_components) {
-          comp[id] = Comp{f, P, INT_MAX, y, INT_MIN, INT_MIN, 0, 0};
-          lf[P] = -(id + 1);
-        }
-        ++cnt;
-        ++id;
-      }
-    }
+    cnt += __popc(comps[u]);
   }
   return cnt;
+}
+
+// Numbers the components of one batch (as found by batch_roots) from id on: initialises
+// each one's record (below max_components) and marks its root with its number.
+__device__ __forceinline__ int batch_assign(int W, int32_t *lf, int y, int b0,
+                                            const uint32_t comps[kBandBatch], Comp *comp,
+                                            int f, int id, int32_t max_components) {
+#pragma unroll
+  for (int u = 0; u < kBandBatch; ++u) {
+    for (uint32_t m = comps[u]; m != 0; m &= m - 1) {
+      const int P = y * W + (b0 + u) * kTile + __builtin_ctz(m);
+      if (id >= 0 && id < max_components) {
+        comp[id] = Comp{f, P, INT_MAX, y, INT_MIN, INT_MIN, 0, 0};
+        lf[P] = -(id + 1);
+      }
+      ++id;
+    }
+  }
+  return id;
 }
 
 // This thread's share of a band: frame, first tile id of the band, pixel row, tile range.
@@ -794,14 +825,25 @@ __global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int H, int6
   const int band = blockIdx.x;
   const BandPart p = band_part(T, H, band);
   int32_t *lf = label + static_cast<int64_t>(p.f) * frame_px;
-  const int cnt = p.rows_in ? band_roots(W, tile_bits, rec_roots, lf, p.base, p.y, p.tx_lo,
-                                         p.tx_hi, p.rr, comp, p.f, 0, max_components, false)
-                            : 0;
+  // a thread's tiles fit one batch for frames up to 8 * kBandBatch tiles wide: its
+  // components are then kept in registers between the count and the numbering
+  const bool one = (T.tiles_x + 7) / 8 <= kBandBatch;
+  uint32_t comps[kBandBatch];
+  int cnt = 0;
+  if (p.rows_in)
+    for (int b0 = p.tx_lo; b0 < p.tx_hi; b0 += kBandBatch)
+      cnt += batch_roots(W, tile_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
   int total;
-  const int before = block_exclusive<kBandThreads>(cnt, s_wave, &total);
-  if (cnt > 0)
-    band_roots(W, tile_bits, rec_roots, lf, p.base, p.y, p.tx_lo, p.tx_hi, p.rr, comp, p.f,
-               band_first[band] + before, max_components, true);
+  int id = band_first[band] + block_exclusive<kBandThreads>(cnt, s_wave, &total);
+  if (cnt == 0) return;
+  if (one) {
+    batch_assign(W, lf, p.y, p.tx_lo, comps, comp, p.f, id, max_components);
+    return;
+  }
+  for (int b0 = p.tx_lo; b0 < p.tx_hi; b0 += kBandBatch) {  // again, the loads now in cache
+    batch_roots(W, tile_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
+    id = batch_assign(W, lf, p.y, b0, comps, comp, p.f, id, max_components);
+  }
 }
 
 // Folds each tile-local component (its entry) into its component's record: up the
@@ -850,10 +892,17 @@ __global__ __launch_bounds__(kEntryThreads) void boxes_kernel(int W, int64_t fra
   }
 }
 
+// Components of at least min_area pixels, in number order: workgroup k (in ticket order)
+// takes kFilterBlock components, kPer per thread, places its kept ones with a block-wide
+// scan and a decoupled look-back, and writes them as rows. Components are numbered frame
+// by frame, so frame f's first row is the compacted position of the first component
+// numbered in a frame >= f: the thread holding component c writes frame_begin for the
+// frames after component c - 1's up to its own, and the last component's thread for the
+// frames after its own.
 __global__ __launch_bounds__(kFilterThreads) void filter_kernel(
     const Comp *comp, int32_t *n_components, int32_t max_components, int32_t min_area,
-    tg_roi *rois, int32_t *areas, int32_t max_rois, int32_t *kept_frame, uint64_t *words,
-    uint64_t *state, int32_t *n_rois) {
+    tg_roi *rois, int32_t *areas, int32_t max_rois, int32_t n_frames, int32_t *frame_begin,
+    uint64_t *words, uint64_t *state, int32_t *n_rois) {
   __shared__ int s_blk, s_base;
   __shared__ int s_wave[kFilterThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -862,6 +911,9 @@ __global__ __launch_bounds__(kFilterThreads) void filter_kernel(
   const uint32_t status = __hip_atomic_load(reinterpret_cast<const uint32_t *>(words + 2),
                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (status != 0 || *n_components < 0) {
+    for (int64_t f = blockIdx.x * static_cast<int64_t>(kFilterThreads) + tid; f <= n_frames;
+         f += static_cast<int64_t>(gridDim.x) * kFilterThreads)
+      frame_begin[f] = 0;
     if (blockIdx.x == 0 && tid == 0) {
       *n_rois = TG_E_INTERNAL;
       *n_components = TG_E_INTERNAL;
@@ -913,33 +965,27 @@ __global__ __launch_bounds__(kFilterThreads) void filter_kernel(
     }
   }
   __syncthreads();
+  if (n == 0) {  // no components: every frame begins at row 0
+    for (int f = tid; f <= n_frames; f += kFilterThreads) frame_begin[f] = 0;
+    return;
+  }
   int k_out = s_base + before + incl - cnt;
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
-    if (!keep[k]) continue;
-    const Comp c = comp[start + tid * kPer + k];
-    kept_frame[k_out] = c.frame;
-    if (k_out < max_rois) {
-      rois[k_out] = tg_roi{c.frame, c.x0, c.y0, c.x1 - c.x0 + 1, c.y1 - c.y0 + 1};
-      if (areas) areas[k_out] = c.area;
+    const int id = start + tid * kPer + k;
+    if (id >= n) break;
+    const Comp c = comp[id];
+    for (int f = id > 0 ? comp[id - 1].frame + 1 : 0; f <= c.frame; ++f) frame_begin[f] = k_out;
+    if (keep[k]) {
+      if (k_out < max_rois) {
+        rois[k_out] = tg_roi{c.frame, c.x0, c.y0, c.x1 - c.x0 + 1, c.y1 - c.y0 + 1};
+        if (areas) areas[k_out] = c.area;
+      }
+      ++k_out;
     }
-    ++k_out;
+    if (id == n - 1)
+      for (int f = c.frame + 1; f <= n_frames; ++f) frame_begin[f] = k_out;
   }
-}
-
-__global__ void begin_kernel(const int32_t *kept_frame, const int32_t *n_rois, int32_t n_frames,
-                             int32_t *frame_begin) {
-  const int f = blockIdx.x * blockDim.x + threadIdx.x;
-  if (f > n_frames) return;
-  int lo = 0, hi = *n_rois;  // first kept row whose frame is >= f
-  while (lo < hi) {
-    const int mid = lo + (hi - lo) / 2;
-    if (kept_frame[mid] < f)
-      lo = mid + 1;
-    else
-      hi = mid;
-  }
-  frame_begin[f] = lo;
 }
 
 __global__ void empty_kernel(int32_t *n_rois, int32_t *n_components, int32_t *frame_begin) {
@@ -1058,8 +1104,7 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
                      L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),
                      0, s, L.comp, a->n_components, a->max_components, a->min_area, a->rois,
-                     a->areas, a->max_rois, L.kept_frame, L.words, L.filter_state, a->n_rois);
-  hipLaunchKernelGGL(begin_kernel, dim3(static_cast<uint32_t>((a->n_frames + 1 + 255) / 256)),
-                     dim3(256), 0, s, L.kept_frame, a->n_rois, a->n_frames, a->frame_begin);
+                     a->areas, a->max_rois, a->n_frames, a->frame_begin, L.words,
+                     L.filter_state, a->n_rois);
   return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
 }

@@ -230,11 +230,11 @@ def test_gmm_and_mask_rois_validation_without_gpu():
     assert L.tg_mask_rois_workspace_bytes(65535, 2048, 2048, 4) > 0
     assert L.tg_mask_rois_workspace_bytes(65535, 2048, 2080, 4) == 0
     ws = L.tg_mask_rois_workspace_bytes(2, 100, 50, 1000)
-    # labels, component records and kept frames, and per 32 x 32 tile (2 frames x 4 x 2
+    # labels, component records, and per 32 x 32 tile (2 frames x 4 x 2
     # tiles) its list entry, records (row masks, root masks, border roots), entry slots
     # and entry count
     tiles = 2 * 4 * 2
-    assert ws >= 4 * 2 * 100 * 50 + 32 * 1000 + 4 * 1000 + tiles * (4 + 128 + 128 + 512 + 2048 + 4)
+    assert ws >= 4 * 2 * 100 * 50 + 32 * 1000 + tiles * (4 + 128 + 128 + 512 + 2048 + 4)
     assert ws % 256 == 0
     m = tg.MaskRoisArgs()
     m.mask = m.rois = m.areas = m.frame_begin = m.n_rois = m.n_components = 0x1000

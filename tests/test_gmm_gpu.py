@@ -184,6 +184,22 @@ def _labels_after(torch, bufs, n_px):
     return labels, status
 
 
+def test_mask_rois_empty_frames(torch):
+    """frame_begin over leading, inner and trailing frames without components, a frame
+    whose components are all below min_area, and a mask with no foreground at all."""
+    F, H, Wd = 7, 40, 70
+    m = np.zeros((F, H, Wd), np.uint8)
+    m[1, 3:9, 5:60] = 1
+    m[1, 30, 2] = 1
+    m[3, 10, 10] = 1          # one pixel: below min_area 2
+    m[4, 0:40, 33] = 1
+    m[4, 39, 0:70] = 1
+    say("mask_rois empty frames", m.shape)
+    _assert_rois(torch, m, 1)
+    _assert_rois(torch, m, 2)
+    _assert_rois(torch, np.zeros((3, 33, 65), np.uint8), 1)
+
+
 def _tile_local_roots(mask2d):
     """Frame indices of the tile-local roots of one frame: per 32x32 tile, the first pixel
     (raster order) of each of the tile's own 8-connected components."""
@@ -268,22 +284,27 @@ def test_mask_rois_labels_keep_the_union_find_invariant(torch):
 def test_mask_rois_caps(torch):
     rng = np.random.default_rng(5)
     mask = (rng.random((2, 50, 70)) < 0.3).astype(np.uint8)
-    all_rows, all_areas, _ = oracle.mask_rois(mask, 1)
+    all_rows, all_areas, all_fb = oracle.mask_rois(mask, 1)
     n = len(all_rows)
-    # fewer row slots than kept components: the first max_rois are written, all counted
+    # fewer row slots than kept components: the first max_rois are written, all counted,
+    # and frame_begin indexes the full list of kept components
     rows, areas, fb, n_rois, n_comp = _run_rois(torch, mask, 1, max_rois=n // 3)
     assert n_rois == n_comp == n
     np.testing.assert_array_equal(rows, all_rows[: n // 3])
+    np.testing.assert_array_equal(fb, all_fb)
     # fewer component records than components: those past the cap (raster order) are not
-    # measured, and the count says so
+    # measured, and the count says so; frame_begin covers the measured ones
     cap = n // 2
     rows, areas, fb, n_rois, n_comp = _run_rois(torch, mask, 1, max_components=cap)
     assert n_comp == n and n_rois == cap
     np.testing.assert_array_equal(rows, all_rows[:cap])
     np.testing.assert_array_equal(areas, all_areas[:cap])
+    frames = np.asarray(all_rows[:cap])[:, 0]
+    np.testing.assert_array_equal(fb, np.searchsorted(frames, np.arange(mask.shape[0] + 1)))
     # no row slots at all
     rows, areas, fb, n_rois, n_comp = _run_rois(torch, mask, 1, max_rois=0)
     assert n_rois == n and len(rows) == 0
+    np.testing.assert_array_equal(fb, all_fb)
 
 
 def test_mask_rois_twice_reuses_workspace(torch):
