@@ -561,36 +561,21 @@ __global__ __launch_bounds__(kLocalThreads) void local_kernel(int W, int64_t fra
   }
 }
 
-// Joins the foreground pixels of a 16-pixel run along a tile border (bits of fg, their
-// tile-local roots lo) with their foreground neighbours across it: the 18 pixels at
-// offsets -1 .. 16 along the border (bits of nb, tile-local roots ln). Pixel k meets
-// neighbours k, k + 1, k + 2; a pair equal to the one just joined is skipped (along a
-// border most repeat).
-__device__ __forceinline__ void join_pairs(RootLabels m, uint32_t fg, const int32_t lo[16],
-                                           uint32_t nb, const int32_t ln[18], uint32_t *status) {
-  int pa = -1, pb = -1;
-#pragma unroll
-  for (int k = 0; k < 16; ++k) {
-    if (!(fg >> k & 1u)) continue;
-#pragma unroll
-    for (int d = 0; d < 3; ++d) {
-      if (!(nb >> (k + d) & 1u)) continue;
-      const int a = lo[k], b = ln[k + d];
-      if (a == pa && b == pb) continue;
-      if (!tg_detail::uf_unite(m, a, b)) fail(status);
-      pa = a;
-      pb = b;
-    }
-  }
-  m.flush();
-}
-
 // Four items per listed tile, walked by a grid of resident workgroups: its top row in
 // two halves of 16 pixels against the row above, then its left column in two halves
 // against the column to its left. Every 8-neighbour pair across a tile border is seen
 // from the tile below or to the right of it. Foreground bits and tile-local roots come
 // from the tiles' records (the tile itself and the up to three tiles holding the
 // neighbours); an item whose neighbouring tiles are all empty is skipped.
+//
+// Along a border, the pixels of a run (adjacent foreground pixels of one tile) share
+// their tile-local root, so an item joins runs, not pixels: the item's 16 pixels (bits of
+// fg) meet the 18 neighbours at offsets -1 .. 16 along the border (bits of nb), pixel k
+// meeting neighbours k .. k + 2; neighbour runs also break where the neighbours change
+// tile (between offsets 0 and 1 of the first half, 16 and 17 of the second). Each pair of
+// touching runs is one union, the two roots loaded from the records only then -- a lane
+// has one or two pairs where a pixel-by-pixel walk had up to 48 positions, which a wave
+// would step through one union at a time.
 __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
     int W, int64_t frame_px, Tiles T, const uint32_t *tile_bits, const int32_t *tile_list,
     const uint32_t *n_list, const uint32_t *rec_fg, const int32_t *rec_border, int32_t *label,
@@ -598,16 +583,15 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
   const int n4 = 4 * static_cast<int>(*n_list);
   for (int i = blockIdx.x * kBorderThreads + threadIdx.x; i < n4;
        i += gridDim.x * kBorderThreads) {
-    const int s = i >> 2, k = i & 3, id = tile_list[s];
+    const int s = i >> 2, k = i & 3, h = k & 1, id = tile_list[s];
     const TileAt a = tile_at(T, id);
     const uint32_t *fs = rec_fg + 32 * static_cast<int64_t>(id);
-    const int32_t *bs = rec_border + 128 * static_cast<int64_t>(id);
     uint32_t fg = 0, nb = 0;
-    int32_t lo[16], ln[18];
-#pragma unroll
-    for (int j = 0; j < 18; ++j) ln[j] = 0;
+    // record index of the item's own border pixel 0; of neighbour offset j (main tile:
+    // main + j; the corner tiles before offset 0 / after offset 16: corner_lo, corner_hi)
+    int64_t own = 0, main = 0, corner_lo = 0, corner_hi = 0;
     if (k < 2) {  // top row, pixels 16 h .. 16 h + 15, against row 31 of the tiles above
-      const int h = k, up = id - T.tiles_x;
+      const int up = id - T.tiles_x;
       if (a.ty == 0) continue;
       const bool u = tile_set(tile_bits, up);
       const bool ul = h == 0 && a.tx > 0 && tile_set(tile_bits, up - 1);
@@ -615,32 +599,18 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
       if (!(u || ul || ur)) continue;
       fg = (fs[0] >> (16 * h)) & 0xFFFFu;
       if (fg == 0) continue;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) lo[j] = bs[16 * h + j];
+      own = 128 * static_cast<int64_t>(id) + 16 * h;
+      main = 128 * static_cast<int64_t>(up) + 32 + 16 * h - 1;  // row 31, column 16 h - 1 + j
+      corner_lo = 128 * static_cast<int64_t>(up - 1) + 32 + 31;
+      corner_hi = 128 * static_cast<int64_t>(up + 1) + 32;
       if (u) {  // neighbour j is column 16 h - 1 + j of the tile above
-        const int64_t su = up;
-        const uint32_t row = rec_fg[32 * su + 31];
-        const int32_t *b = rec_border + 128 * su + 32;
-#pragma unroll
-        for (int j = 0; j < 18; ++j) {
-          const int c = 16 * h - 1 + j;
-          if (c < 0 || c >= kTile) continue;
-          nb |= (row >> c & 1u) << j;
-          ln[j] = b[c];
-        }
+        const uint32_t row = rec_fg[32 * static_cast<int64_t>(up) + 31];
+        nb = h ? (row >> 15) & 0x1FFFFu : (row & 0x1FFFFu) << 1;
       }
-      if (ul) {  // column 31 of the tile above and to the left
-        const int64_t sl = up - 1;
-        nb |= rec_fg[32 * sl + 31] >> 31;
-        ln[0] = rec_border[128 * sl + 32 + 31];
-      }
-      if (ur) {  // column 0 of the tile above and to the right
-        const int64_t sr = up + 1;
-        nb |= (rec_fg[32 * sr + 31] & 1u) << 17;
-        ln[17] = rec_border[128 * sr + 32];
-      }
+      if (ul) nb |= rec_fg[32 * static_cast<int64_t>(up - 1) + 31] >> 31;
+      if (ur) nb |= (rec_fg[32 * static_cast<int64_t>(up + 1) + 31] & 1u) << 17;
     } else {  // left column, rows 16 h .. 16 h + 15, against column 31 of the tiles left
-      const int h = k - 2, left = id - 1;
+      const int left = id - 1;
       if (a.tx == 0) continue;
       const bool l = tile_set(tile_bits, left);
       const bool lu = h == 0 && a.ty > 0 && tile_set(tile_bits, left - T.tiles_x);
@@ -649,33 +619,43 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 #pragma unroll
       for (int j = 0; j < 16; ++j) fg |= (fs[16 * h + j] & 1u) << j;
       if (fg == 0) continue;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) lo[j] = bs[64 + 16 * h + j];
+      own = 128 * static_cast<int64_t>(id) + 64 + 16 * h;
+      main = 128 * static_cast<int64_t>(left) + 96 + 16 * h - 1;  // column 31, row 16 h - 1 + j
+      corner_lo = 128 * static_cast<int64_t>(left - T.tiles_x) + 96 + 31;
+      corner_hi = 128 * static_cast<int64_t>(left + T.tiles_x) + 96;
       if (l) {  // neighbour j is row 16 h - 1 + j of the tile to the left
-        const int64_t sl = left;
-        const uint32_t *f = rec_fg + 32 * sl;
-        const int32_t *b = rec_border + 128 * sl + 96;
+        const uint32_t *f = rec_fg + 32 * static_cast<int64_t>(left);
 #pragma unroll
         for (int j = 0; j < 18; ++j) {
           const int rr = 16 * h - 1 + j;
           if (rr < 0 || rr >= kTile) continue;
           nb |= (f[rr] >> 31) << j;
-          ln[j] = b[rr];
         }
       }
-      if (lu) {  // row 31 of the tile to the left and above
-        const int64_t su = left - T.tiles_x;
-        nb |= rec_fg[32 * su + 31] >> 31;
-        ln[0] = rec_border[128 * su + 96 + 31];
-      }
-      if (ld) {  // row 0 of the tile to the left and below
-        const int64_t sd = left + T.tiles_x;
-        nb |= (rec_fg[32 * sd] >> 31) << 17;
-        ln[17] = rec_border[128 * sd + 96];
+      if (lu) nb |= rec_fg[32 * static_cast<int64_t>(left - T.tiles_x) + 31] >> 31;
+      if (ld) nb |= (rec_fg[32 * static_cast<int64_t>(left + T.tiles_x)] >> 31) << 17;
+    }
+    // runs: own ones start at the bits of fst; neighbour ones at those of nst, which also
+    // break where the neighbours change tile
+    const uint32_t fst = fg & ~(fg << 1);
+    const uint32_t nst = (nb & ~(nb << 1)) | (nb & (h ? 1u << 17 : 1u << 1));
+    RootLabels roots{label + a.f * frame_px, band_count + a.f * T.tiles_y, W};
+    bool ok = true;
+    for (uint32_t m = fst; m != 0; m &= m - 1) {
+      const int s0 = __builtin_ctz(m), e = s0 + __builtin_ctz(~(fg >> s0)) - 1;
+      const uint32_t x = nb & col_span(s0, e + 2);  // the neighbours of pixels s0 .. e
+      if (x == 0) continue;
+      const int lo = __builtin_ctz(x), hi = 31 - __builtin_clz(x);
+      const int first = 31 - __builtin_clz(nst & (0xFFFFFFFFu >> (31 - lo)));  // run holding lo
+      const int ra = rec_border[own + s0];
+      for (uint32_t q = nst & col_span(first, hi); q != 0; q &= q - 1) {
+        const int j = __builtin_ctz(q);
+        const int64_t at = h == 0 && j == 0 ? corner_lo : h == 1 && j == 17 ? corner_hi : main + j;
+        ok &= tg_detail::uf_unite(roots, ra, rec_border[at]);
       }
     }
-    RootLabels roots{label + a.f * frame_px, band_count + a.f * T.tiles_y, W};
-    join_pairs(roots, fg, lo, nb, ln, status);
+    roots.flush();
+    if (!ok) fail(status);
   }
 }
 
