@@ -58,7 +58,7 @@
 namespace {
 
 constexpr int kTile = 32;
-constexpr int kEntryThreads = 256;  // boxes pass: one thread per entry slot
+constexpr int kEntryThreads = 256;  // boxes pass: one wave per listed tile
 constexpr int kScanTiles = 16;     // tiles side by side per workgroup of the scan pass
 constexpr int kScanThreads = 256;  // 8 threads per row of 16 tiles, 64 pixels each
 constexpr int kListGroups = 2048;  // list-walking grid when the occupancy query fails
@@ -688,13 +688,24 @@ __device__ __forceinline__ int batch_roots(int W, const uint32_t *tile_bits,
                   ? rec_roots[32 * static_cast<int64_t>(tile) + rr]
                   : 0u;
   }
+  // the label of each tile's first candidate, all loaded together; further candidates in
+  // the same row of a tile (a second local root there is rare) one by one
+  int first[kBandBatch];
+#pragma unroll
+  for (int u = 0; u < kBandBatch; ++u) {
+    const int P = y * W + (b0 + u) * kTile + __builtin_ctz(cand[u] | 0x80000000u);
+    first[u] = cand[u] ? lf[P] : 0;
+  }
   int cnt = 0;
 #pragma unroll
   for (int u = 0; u < kBandBatch; ++u) {
     comps[u] = 0;
-    for (uint32_t m = cand[u]; m != 0; m &= m - 1) {
-      const int P = y * W + (b0 + u) * kTile + __builtin_ctz(m);
-      if (lf[P] == (P | kRootFlag)) comps[u] |= m & (0u - m);
+    if (cand[u] == 0) continue;
+    const int P = y * W + (b0 + u) * kTile + __builtin_ctz(cand[u]);
+    if (first[u] == (P | kRootFlag)) comps[u] = cand[u] & (0u - cand[u]);
+    for (uint32_t m = cand[u] & (cand[u] - 1); m != 0; m &= m - 1) {
+      const int Q = y * W + (b0 + u) * kTile + __builtin_ctz(m);
+      if (lf[Q] == (Q | kRootFlag)) comps[u] |= m & (0u - m);
     }
     cnt += __popc(comps[u]);
   }
@@ -828,8 +839,9 @@ __global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int H, int6
 
 // Folds each tile-local component (its entry) into its component's record: up the
 // union-find from its local root to the numbered root, then one set of global atomics
-// (the record's top row is its root's, set when it was numbered). A grid of resident
-// workgroups walks the listed tiles' entry slots.
+// (the record's top row is its root's, set when it was numbered). One wave per listed
+// tile, the waves of a grid of resident workgroups walking the list; lane l takes the
+// tile's entries l, l + 64, ...
 __global__ __launch_bounds__(kEntryThreads) void boxes_kernel(int W, int64_t frame_px, Tiles T,
                                                               const int32_t *tile_list,
                                                               const uint32_t *n_list,
@@ -837,38 +849,41 @@ __global__ __launch_bounds__(kEntryThreads) void boxes_kernel(int W, int64_t fra
                                                               const int32_t *n_ent,
                                                               const int32_t *label, Comp *comp,
                                                               uint32_t *status) {
-  const int64_t n = 256 * static_cast<int64_t>(*n_list);
-  for (int64_t e = blockIdx.x * kEntryThreads + threadIdx.x; e < n;
-       e += static_cast<int64_t>(gridDim.x) * kEntryThreads) {
-    const int id = tile_list[e >> 8], j = static_cast<int>(e & 255);
-    if (j >= n_ent[id]) continue;
-    const uint64_t v64 = entries[256 * static_cast<int64_t>(id) + j];
-    const int i = static_cast<int>(v64 >> 26) & 1023;
-    const int ex0 = static_cast<int>(v64 >> 21) & 31, ex1 = static_cast<int>(v64 >> 16) & 31;
-    const int ey1 = static_cast<int>(v64 >> 11) & 31, cnt = static_cast<int>(v64 & 2047);
+  const int n = static_cast<int>(*n_list);
+  const int lane = threadIdx.x & 63;
+  const int waves = static_cast<int>(gridDim.x) * (kEntryThreads / 64);
+  for (int s = (blockIdx.x * kEntryThreads + threadIdx.x) >> 6; s < n; s += waves) {
+    const int id = tile_list[s];
+    const int ne = n_ent[id];
     const TileAt a = tile_at(T, id);
     const int x0 = a.tx * kTile, y0 = a.ty * kTile;
     const int32_t *lf = label + a.f * frame_px;
-    // up the union-find over local roots to the numbered root; every link points to a
-    // smaller index (unionfind.h), so the walk ends -- a link that does not is reported
-    int cur = (y0 + (i >> 5)) * W + x0 + (i & 31);
-    int v = lf[cur];
-    while (v >= 0) {
-      const int nx = v & kIndex;
-      if (nx == cur) break;
-      if (nx > cur) {
-        fail(status);
-        break;
+    for (int j = lane; j < ne; j += 64) {
+      const uint64_t v64 = entries[256 * static_cast<int64_t>(id) + j];
+      const int i = static_cast<int>(v64 >> 26) & 1023;
+      const int ex0 = static_cast<int>(v64 >> 21) & 31, ex1 = static_cast<int>(v64 >> 16) & 31;
+      const int ey1 = static_cast<int>(v64 >> 11) & 31, cnt = static_cast<int>(v64 & 2047);
+      // up the union-find over local roots to the numbered root; every link points to a
+      // smaller index (unionfind.h), so the walk ends -- a link that does not is reported
+      int cur = (y0 + (i >> 5)) * W + x0 + (i & 31);
+      int v = lf[cur];
+      while (v >= 0) {
+        const int nx = v & kIndex;
+        if (nx == cur) break;
+        if (nx > cur) {
+          fail(status);
+          break;
+        }
+        cur = nx;
+        v = lf[cur];
       }
-      cur = nx;
-      v = lf[cur];
+      if (v >= 0) continue;  // a component past max_components (or a broken link): not measured
+      Comp *c = comp + (-v - 1);
+      atomicMin(&c->x0, x0 + ex0);
+      atomicMax(&c->x1, x0 + ex1);
+      atomicMax(&c->y1, y0 + ey1);
+      atomicAdd(&c->area, cnt);
     }
-    if (v >= 0) continue;  // a component past max_components (or a broken link): not measured
-    Comp *c = comp + (-v - 1);
-    atomicMin(&c->x0, x0 + ex0);
-    atomicMax(&c->x1, x0 + ex1);
-    atomicMax(&c->y1, y0 + ey1);
-    atomicAdd(&c->area, cnt);
   }
 }
 
@@ -1038,7 +1053,7 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
       (4 * T.n + kBorderThreads - 1) / kBorderThreads,
       resident_groups(reinterpret_cast<const void *>(merge_kernel), kBorderThreads))));
   const dim3 entry_groups(static_cast<uint32_t>(std::min<int64_t>(
-      (256 * T.n + kEntryThreads - 1) / kEntryThreads,
+      (64 * T.n + kEntryThreads - 1) / kEntryThreads,
       resident_groups(reinterpret_cast<const void *>(boxes_kernel), kEntryThreads))));
   // dword mask reads need every row start dword-aligned; 16-byte reads need the mask
   // itself 16-byte aligned (and, for whole rows, rows a multiple of 16 bytes)
