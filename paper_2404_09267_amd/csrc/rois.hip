@@ -72,7 +72,9 @@ constexpr int kBorderThreads = 256;
 constexpr int32_t kRootFlag = 1 << 30;
 constexpr int32_t kIndex = kRootFlag - 1;
 constexpr int kBandThreads = 256;  // numbering passes: 8 threads per row of a 32-row band
-constexpr int kBandBatch = 16;     // tiles whose loads a numbering thread issues together
+constexpr int kBandBatch = 16;     // wide bands: tiles whose loads a thread issues together
+constexpr int kBandTiles = 256;    // widest band (in tiles) whose non-empty tiles go to LDS
+constexpr int kPairBatch = 4;      // (row, tile) pairs whose loads a thread issues together
 constexpr int kBandScanThreads = 1024;  // the scan over the bands' counts: one workgroup
 constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
 constexpr int kFilterThreads = 256;
@@ -665,13 +667,14 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 // the local pass adds each tile's local roots, the merge removes each root it links.
 //  scan:   one workgroup turns the counts into each band's first number and writes the
 //          number of components.
-//  assign: one workgroup per band. Thread t takes row t / 8 of the band and the t % 8-th
-//          eighth of its tiles, left to right, so thread order is raster order within
-//          the band. Its candidates are the recorded tile-local roots of that row of its
-//          non-empty tiles; a candidate is a component when it is still its own parent
-//          (label = own frame index, flagged). A block-wide scan of the threads' counts
-//          places them; each component's record is initialised and its root marked with
-//          its number.
+//  assign: one workgroup per band; its threads take the band's (row, tile) pairs in
+//          raster order, so that a block-wide scan of their counts places each component.
+//          A pair's candidates are the tile's recorded local roots in that row; a
+//          candidate is a component when it is still its own parent (label = own frame
+//          index, flagged). Each component's record is initialised and its root marked
+//          with its number. Bands up to kBandTiles tiles wide list their non-empty tiles
+//          in LDS and deal the pairs out (assign_kernel); wider ones give thread t row
+//          t / 8 and the t % 8-th eighth of the tiles (assign_wide_kernel).
 // One batch of a thread's tiles (b0 .. b0 + kBandBatch - 1, below tx_hi) in row y (row rr
 // of the band): comps[u] gets the bits of tile b0 + u's recorded local roots in that row
 // that are still their own parent (the components). Each level of loads (bitmap,
@@ -805,7 +808,7 @@ __global__ __launch_bounds__(kBandScanThreads) void band_scan_kernel(int32_t *ba
   if (threadIdx.x == 0) *n_components = carry;
 }
 
-__global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int H, int64_t frame_px,
+__global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(int W, int H, int64_t frame_px,
                                                               Tiles T, const uint32_t *tile_bits,
                                                               const uint32_t *rec_roots,
                                                               int32_t *label,
@@ -834,6 +837,108 @@ __global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int H, int6
   for (int b0 = p.tx_lo; b0 < p.tx_hi; b0 += kBandBatch) {  // again, the loads now in cache
     batch_roots(W, tile_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
     id = batch_assign(W, lf, p.y, b0, comps, comp, p.f, id, max_components);
+  }
+}
+
+// Numbering of one band when it is at most kBandTiles tiles wide: its non-empty tiles,
+// left to right, are listed in LDS from the bitmap, and the band's (row, listed tile)
+// pairs in raster order (row-major over the listed tiles) are dealt out in consecutive
+// runs of c = ceil(32 nl / kBandThreads) to the threads, so that thread order is raster
+// order and a thread usually has one pair. A pair's candidates are the tile's recorded
+// local roots in that row; the label loads of up to kPairBatch pairs are issued together.
+__global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int64_t frame_px, Tiles T,
+                                                              const uint32_t *tile_bits,
+                                                              const uint32_t *rec_roots,
+                                                              int32_t *label,
+                                                              const int32_t *band_first,
+                                                              Comp *comp,
+                                                              int32_t max_components) {
+  __shared__ int s_tx[kBandTiles];
+  __shared__ int s_nl;
+  __shared__ int s_wave[kBandThreads / 64];
+  const int tid = threadIdx.x, band = blockIdx.x;
+  const int f = band / T.tiles_y, ty = band - f * T.tiles_y;
+  const int base = band * T.tiles_x;  // tile id of the band's first tile
+  int32_t *lf = label + static_cast<int64_t>(f) * frame_px;
+  if (tid < 64) {  // the band's bitmap words, one per lane (tiles_x <= kBandTiles: <= 10)
+    const int w_lo = base >> 5, w_hi = (base + T.tiles_x - 1) >> 5;
+    uint32_t bits = 0;
+    if (tid <= w_hi - w_lo) {
+      bits = tile_bits[w_lo + tid];
+      if (tid == 0) bits &= 0xFFFFFFFFu << (base & 31);
+      if (tid == w_hi - w_lo) bits &= 0xFFFFFFFFu >> (31 - ((base + T.tiles_x - 1) & 31));
+    }
+    const int cnt = __popc(bits);
+    int incl = cnt;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (tid >= o) incl += v;
+    }
+    int at = incl - cnt;
+    for (uint32_t m = bits; m != 0; m &= m - 1)
+      s_tx[at++] = (w_lo + tid) * 32 + __builtin_ctz(m) - base;
+    if (tid == 63) s_nl = incl;
+  }
+  __syncthreads();
+  const int nl = s_nl, n_pairs = kTile * nl;
+  const int c = (n_pairs + kBandThreads - 1) / kBandThreads;
+  const int p0 = min(tid * c, n_pairs), p1 = min(p0 + c, n_pairs);
+  // the components among the candidates of pairs g .. g + kPairBatch - 1 (below p1)
+  auto batch = [&](int g, uint32_t comps[kPairBatch], int yx[kPairBatch]) {
+    uint32_t cand[kPairBatch];
+    int first[kPairBatch];
+#pragma unroll
+    for (int u = 0; u < kPairBatch; ++u) {
+      const int p = g + u, rr = p / max(nl, 1), j = p - rr * max(nl, 1);
+      const int tx = p < p1 ? s_tx[j] : 0;
+      yx[u] = (ty * kTile + rr) * W + tx * kTile;  // frame index of the pair's row start
+      cand[u] = p < p1 ? rec_roots[32 * static_cast<int64_t>(base + tx) + rr] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kPairBatch; ++u)
+      first[u] = cand[u] ? lf[yx[u] + __builtin_ctz(cand[u])] : 0;
+    int n = 0;
+#pragma unroll
+    for (int u = 0; u < kPairBatch; ++u) {
+      comps[u] = 0;
+      if (cand[u] == 0) continue;
+      const int P = yx[u] + __builtin_ctz(cand[u]);
+      if (first[u] == (P | kRootFlag)) comps[u] = cand[u] & (0u - cand[u]);
+      for (uint32_t m = cand[u] & (cand[u] - 1); m != 0; m &= m - 1) {
+        const int Q = yx[u] + __builtin_ctz(m);
+        if (lf[Q] == (Q | kRootFlag)) comps[u] |= m & (0u - m);
+      }
+      n += __popc(comps[u]);
+    }
+    return n;
+  };
+  auto number = [&](const uint32_t comps[kPairBatch], const int yx[kPairBatch], int id) {
+#pragma unroll
+    for (int u = 0; u < kPairBatch; ++u)
+      for (uint32_t m = comps[u]; m != 0; m &= m - 1) {
+        const int P = yx[u] + __builtin_ctz(m);
+        if (id >= 0 && id < max_components) {
+          comp[id] = Comp{f, P, INT_MAX, P / W, INT_MIN, INT_MIN, 0, 0};
+          lf[P] = -(id + 1);
+        }
+        ++id;
+      }
+    return id;
+  };
+  uint32_t comps[kPairBatch];
+  int yx[kPairBatch];
+  int cnt = 0;
+  for (int g = p0; g < p1; g += kPairBatch) cnt += batch(g, comps, yx);
+  int total;
+  int id = band_first[band] + block_exclusive<kBandThreads>(cnt, s_wave, &total);
+  if (cnt == 0) return;
+  if (p1 - p0 <= kPairBatch) {  // one batch: its components are still in registers
+    number(comps, yx, id);
+    return;
+  }
+  for (int g = p0; g < p1; g += kPairBatch) {  // again, the loads now in cache
+    batch(g, comps, yx);
+    id = number(comps, yx, id);
   }
 }
 
@@ -1092,9 +1197,14 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   hipLaunchKernelGGL(band_scan_kernel, dim3(1), dim3(kBandScanThreads), 0, s, L.band_first,
                      n_bands, a->n_components, status);
   const dim3 bands(static_cast<uint32_t>(n_bands));
-  hipLaunchKernelGGL(assign_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
-                     L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
-                     a->max_components);
+  if (T.tiles_x <= kBandTiles)
+    hipLaunchKernelGGL(assign_kernel, bands, dim3(kBandThreads), 0, s, W, frame_px, T,
+                       L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
+                       a->max_components);
+  else
+    hipLaunchKernelGGL(assign_wide_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
+                       L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
+                       a->max_components);
   hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kEntryThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),

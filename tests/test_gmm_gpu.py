@@ -200,6 +200,19 @@ def test_mask_rois_empty_frames(torch):
     _assert_rois(torch, np.zeros((3, 33, 65), np.uint8), 1)
 
 
+def test_mask_rois_wide_frames(torch):
+    """Frames more than 256 tiles (8192 pixels) wide, numbered by the per-chunk walk of
+    the band instead of the listed tiles, with a long component across most of a band
+    and noise; and a frame exactly 256 tiles wide, the widest the listed walk takes."""
+    rng = np.random.default_rng(31)
+    for shape in ((2, 40, 8300), (1, 45, 8192)):
+        m = (rng.random(shape) < 0.12).astype(np.uint8)
+        m[0, 5:30, 100:8100] = 1
+        m[-1, 0:shape[1], 4000:4100] = 1
+        say("mask_rois wide", shape)
+        _assert_rois(torch, m, 2)
+
+
 def _tile_local_roots(mask2d):
     """Frame indices of the tile-local roots of one frame: per 32x32 tile, the first pixel
     (raster order) of each of the tile's own 8-connected components."""
