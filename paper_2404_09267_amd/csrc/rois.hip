@@ -6,40 +6,42 @@
 // the smallest index of its set, so every set ends rooted at its first pixel in raster
 // order) -- the GPU union-find labelling of D. P. Playne and K. A. Hawick (IEEE TPDS 29(6),
 // 2018), tile-local first and merged along tile borders as in the block-based labelling of
-// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in nine launches on
+// S. Allegretti, F. Bolelli and C. Grana (IEEE TPDS 31(2), 2020) -- in seven launches on
 // the caller's stream. Foreground masks are sparse, so only the scan reads the mask; the
 // other passes visit the 32x32 tiles that hold foreground, through per-tile records
 // (row masks, local-root masks, the tile-local roots of the border pixels) indexed by
 // tile id. Same-address global atomics serialize across the chip, so no pass counts or
 // takes tickets on one word per workgroup of a large grid.
-//  1. clear:  zeroes the tickets, counters, look-back words and the tile bitmap.
-//  2. scan:   one 256-thread workgroup per 16 tiles side by side streams the mask (16-byte
-//             loads where it can), sets a bit per tile with foreground and writes those
-//             tiles' 32 row masks.
-//  3. list:   compacts the bitmap into the list of non-empty tiles (increasing ids), a
+//  1. scan:   one 256-thread workgroup per 16 tiles side by side streams the mask (16-byte
+//             loads where it can), stores a bit per tile (set: foreground) and writes the
+//             32 row masks of the tiles with foreground; it also zeroes the tickets,
+//             counters and look-back words of the later passes.
+//  2. list:   compacts the bitmap into the list of non-empty tiles (increasing ids), a
 //             few large workgroups with a decoupled look-back.
-//  4. local:  one wave per listed tile, a grid of resident one-wave workgroups walking
+//  3. local:  one wave per listed tile, a grid of resident one-wave workgroups walking
 //             the list: union-find in LDS over the tile's row runs (one union per pair
 //             of touching runs); each tile-local root's label word gets its own frame
 //             index, the tile's local roots and border roots go to its record, and each
 //             local component's box and pixel count, folded in LDS, to one of the tile's
 //             256 entry slots, and the tile's count of local roots is added to its
 //             band's. No other label word is written or read.
-//  5. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
+//  4. merge:  per listed tile, four 16-pixel items (its top row in two halves, its left
 //             column in two halves) join each foreground pixel with its foreground
 //             neighbours across the border, reading the records of the tile and of the
 //             tiles around it, with global atomics on the label array; an item whose
 //             neighbouring tiles are all empty is skipped. Every 8-neighbour pair across a
 //             tile border is seen from the tile below or to the right of it. A root that
 //             gets linked leaves its band's count, which then counts components.
-//  6-7. scan, assign: one workgroup scans the bands' counts; per band of 32 rows (a tile
-//             row of a frame), the recorded local roots still their own parent (the
-//             components) are numbered in raster order, each component's record is
-//             initialised and its root marked with its number.
-//  8. boxes:  each local component (its entry) follows the union-find from its root to
+//  5. assign: per band of 32 rows (a tile row of a frame), the recorded local roots still
+//             their own parent (the components) are numbered in raster order, each
+//             component's record is initialised and its root marked with its number. The
+//             band's first number is the sum of the earlier bands' counts, read by the
+//             band's workgroup (over kDirectBands bands, a one-workgroup scan launched
+//             before it puts it in place).
+//  6. boxes:  each local component (its entry) follows the union-find from its root to
 //             its component's number and folds its box and count into the record with
 //             one set of global atomics.
-//  9. filter: components of at least min_area pixels, compacted in number order with a
+//  7. filter: components of at least min_area pixels, compacted in number order with a
 //             look-back, written as tg_roi rows; each frame's first row (frame_begin) is
 //             the compacted position of the frame's first component.
 // Every union-find walk checks the invariant it relies on (unionfind.h); a walk that meets a
@@ -50,6 +52,9 @@
 #include <algorithm>
 #include <climits>
 #include <cstdint>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "lookback.h"
 #include "tg.h"
@@ -76,6 +81,7 @@ constexpr int kBandBatch = 16;     // wide bands: tiles whose loads a thread iss
 constexpr int kBandTiles = 256;    // widest band (in tiles) whose non-empty tiles go to LDS
 constexpr int kPairBatch = 4;      // (row, tile) pairs whose loads a thread issues together
 constexpr int kBandScanThreads = 1024;  // the scan over the bands' counts: one workgroup
+constexpr int kDirectBands = 4096;  // up to this many bands, numbering sums the counts itself
 constexpr int kFilterBlock = 1024;  // components per workgroup of the filter pass
 constexpr int kFilterThreads = 256;
 
@@ -85,19 +91,22 @@ struct Comp {
 static_assert(sizeof(Comp) == 32, "component record is 32 bytes");
 
 // Tiles of all frames, numbered frame by frame, tile rows top to bottom, tiles left to
-// right: tile (f, ty, tx) is (f * tiles_y + ty) * tiles_x + tx.
+// right: tile (f, ty, tx) is (f * tiles_y + ty) * tiles_x + tx; band f * tiles_y + ty is
+// that tile row. The tile bitmap gives each band wpb = ceil(tiles_x / 32) words of its
+// own: tile tx of band b is bit tx % 32 of word b * wpb + tx / 32.
 struct Tiles {
-  int tiles_x, tiles_y;
+  int tiles_x, tiles_y, wpb;
   int64_t n;
 };
 
 struct Layout {
   // [0]: list ticket, [1]: filter ticket, [2]: status, [3]: non-empty tiles listed,
-  // [4]: unused, then the look-back words of the list and filter passes, the tile
-  // bitmap (bit t of 32-bit word t / 32: tile t holds foreground) and the bands' counts
-  // of components (32-bit); all cleared by the first launch
+  // [4]: unused, then the look-back words of the list and filter passes and the bands'
+  // counts of components (32-bit); all cleared by the scan
   uint64_t *words;
   uint64_t *list_state, *filter_state;
+  // the tile bitmap (bit set: the tile holds foreground), band by band (Tiles), every
+  // word written by the scan
   uint32_t *tile_bits;
   // per band: its count of components (tile-local roots added by the local pass, linked
   // roots removed by the merge), then its first component's number
@@ -122,19 +131,17 @@ struct Layout {
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-int64_t list_chunks(int64_t n_tiles) {
-  return ((n_tiles + 31) / 32 + kListChunk - 1) / kListChunk;
-}
+int64_t list_chunks(int64_t n_bit_words) { return (n_bit_words + kListChunk - 1) / kListChunk; }
 
 Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
-              int32_t max_components) {
+              int64_t n_bit_words, int32_t max_components) {
   Layout L;
-  const int64_t n_chunks = list_chunks(n_tiles);
+  const int64_t n_chunks = list_chunks(n_bit_words);
   const int64_t n_filter = (max_components + kFilterBlock - 1) / kFilterBlock;
-  const int64_t bit_words64 = (n_tiles + 63) / 64;
-  L.n_words = 5 + n_chunks + n_filter + bit_words64 + (n_bands + 1) / 2;
+  L.n_words = 5 + n_chunks + n_filter + (n_bands + 1) / 2;
   const size_t nt = static_cast<size_t>(n_tiles);
-  const size_t o_list = round_up(8 * static_cast<size_t>(L.n_words), 256);
+  const size_t o_bits = round_up(8 * static_cast<size_t>(L.n_words), 256);
+  const size_t o_list = round_up(o_bits + 4 * static_cast<size_t>(n_bit_words), 256);
   const size_t o_fg = round_up(o_list + 4 * nt, 256);
   const size_t o_roots = round_up(o_fg + 128 * nt, 256);
   const size_t o_border = round_up(o_roots + 128 * nt, 256);
@@ -147,8 +154,8 @@ Layout layout(void *base, int64_t n_px, int64_t n_bands, int64_t n_tiles,
   L.words = b ? reinterpret_cast<uint64_t *>(b) : nullptr;
   L.list_state = b ? L.words + 5 : nullptr;
   L.filter_state = b ? L.list_state + n_chunks : nullptr;
-  L.tile_bits = b ? reinterpret_cast<uint32_t *>(L.filter_state + n_filter) : nullptr;
-  L.band_first = b ? reinterpret_cast<int32_t *>(L.filter_state + n_filter + bit_words64) : nullptr;
+  L.band_first = b ? reinterpret_cast<int32_t *>(L.filter_state + n_filter) : nullptr;
+  L.tile_bits = b ? reinterpret_cast<uint32_t *>(b + o_bits) : nullptr;
   L.tile_list = b ? reinterpret_cast<int32_t *>(b + o_list) : nullptr;
   L.rec_fg = b ? reinterpret_cast<uint32_t *>(b + o_fg) : nullptr;
   L.rec_roots = b ? reinterpret_cast<uint32_t *>(b + o_roots) : nullptr;
@@ -225,8 +232,9 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-__device__ __forceinline__ bool tile_set(const uint32_t *bits, int t) {
-  return (bits[t >> 5] >> (t & 31)) & 1u;
+// Whether tile tx of band `band` holds foreground.
+__device__ __forceinline__ bool tile_set(const uint32_t *bits, const Tiles &T, int band, int tx) {
+  return (bits[static_cast<int64_t>(band) * T.wpb + (tx >> 5)] >> (tx & 31)) & 1u;
 }
 
 // Frame, tile row and tile column of tile id t.
@@ -278,26 +286,28 @@ __device__ __forceinline__ uint32_t col_span(int lo, int hi) {
 
 // ---- kernels ------------------------------------------------------------------------
 
-__global__ void clear_kernel(uint64_t *words, int64_t n) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) words[i] = 0;
-}
-
 // Which tiles hold foreground: one workgroup per 16 tiles side by side (a 512 x 32 block
 // of one frame), thread t reading row t / 8 of the block, pixels 64 (t % 8) .. + 63 (the
 // row segments of two tiles) with 16-byte loads (kMode 2: mask 16-byte aligned and rows a
 // multiple of 16 bytes), dwords (kMode 1) or bytes (kMode 0), all issued before any is
-// used. A block with foreground sets its tiles' bits and writes each such tile's 32 row
-// masks to its record. Nothing is counted here: the same-address atomics of a global
-// list counter would serialize the workgroups.
+// used. Every block stores its 16 tiles' bits (half a bitmap word; the grid has
+// 2 wpb blocks per band, the last ones past the frame's width storing zeros) and writes
+// the 32 row masks of each tile with foreground to its record. Nothing is counted here:
+// the same-address atomics of a global list counter would serialize the workgroups. The
+// blocks also zero the n_clear counter words that the later passes use.
 template <int kMode>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask, int W, int H,
                                                             int64_t frame_px, Tiles T,
                                                             uint32_t *tile_bits,
-                                                            uint32_t *rec_fg) {
+                                                            uint32_t *rec_fg, uint64_t *words,
+                                                            int64_t n_clear) {
   __shared__ uint32_t s_bits;
   const int t = threadIdx.x, r = t >> 3, q = t & 7;
   const int64_t f = blockIdx.z;
+  const int64_t g = (static_cast<int64_t>(blockIdx.z) * gridDim.y + blockIdx.y) * gridDim.x +
+                    blockIdx.x;
+  const int64_t all = static_cast<int64_t>(gridDim.x) * gridDim.y * gridDim.z * kScanThreads;
+  for (int64_t i = g * kScanThreads + t; i < n_clear; i += all) words[i] = 0;
   const int tx0 = blockIdx.x * kScanTiles, ty = blockIdx.y;
   const int y = ty * kTile + r, x = tx0 * kTile + 64 * q;
   if (t == 0) s_bits = 0;
@@ -357,14 +367,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
   }
   __syncthreads();
   const uint32_t m = s_bits;
+  const int64_t band = f * T.tiles_y + ty;
+  if (t == 0)
+    reinterpret_cast<uint16_t *>(tile_bits)[band * 2 * T.wpb + blockIdx.x] =
+        static_cast<uint16_t>(m);
   if (m == 0) return;  // uniform
-  const int id0 = static_cast<int>((f * T.tiles_y + ty) * T.tiles_x + tx0);
-  if (t == 0) {
-    const int sh = id0 & 31;
-    atomicOr(&tile_bits[id0 >> 5], m << sh);
-    if (sh > 16 && (m >> (32 - sh)) != 0)  // only words that hold existing tiles
-      atomicOr(&tile_bits[(id0 >> 5) + 1], m >> (32 - sh));
-  }
+  const int id0 = static_cast<int>(band * T.tiles_x + tx0);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int j = 2 * q + h;
@@ -372,12 +380,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const uint8_t *mask,
   }
 }
 
-// Lists the non-empty tiles in increasing order: workgroup c (in ticket order) takes
-// kListChunk words of the tile bitmap, kListPer per thread; a block-wide scan of their
+// Lists the non-empty tiles in increasing order (bands in order, each band's tiles left to
+// right): workgroup c (in ticket order) takes kListChunk words of the tile bitmap, kListPer
+// per thread; a block-wide scan of their
 // counts and a decoupled look-back over the workgroups place each set bit. The last
 // workgroup writes the count (0, with the status word set, if the look-back failed).
 __global__ __launch_bounds__(kListThreads) void list_kernel(const uint32_t *tile_bits,
-                                                            int64_t n_bit_words,
+                                                            int64_t n_bit_words, Tiles T,
                                                             int32_t *tile_list,
                                                             uint64_t *words, uint64_t *state,
                                                             int32_t n_chunks, uint32_t *n_list,
@@ -419,9 +428,12 @@ __global__ __launch_bounds__(kListThreads) void list_kernel(const uint32_t *tile
   } else {
     int at = prefix + before + incl - cnt;
 #pragma unroll
-    for (int i = 0; i < kListPer; ++i)
+    for (int i = 0; i < kListPer; ++i) {
+      const int64_t band = (w0 + i) / T.wpb;
+      const int tx0 = static_cast<int>(w0 + i - band * T.wpb) * 32;
       for (uint32_t m = bits[i]; m != 0; m &= m - 1)
-        tile_list[at++] = static_cast<int32_t>((w0 + i) * 32 + __builtin_ctz(m));
+        tile_list[at++] = static_cast<int32_t>(band * T.tiles_x + tx0 + __builtin_ctz(m));
+    }
   }
   if (c == n_chunks - 1 && tid == 0)
     *n_list = failed ? 0u : static_cast<uint32_t>(prefix + total);
@@ -587,6 +599,7 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
        i += gridDim.x * kBorderThreads) {
     const int s = i >> 2, k = i & 3, h = k & 1, id = tile_list[s];
     const TileAt a = tile_at(T, id);
+    const int band = a.f * T.tiles_y + a.ty;
     const uint32_t *fs = rec_fg + 32 * static_cast<int64_t>(id);
     uint32_t fg = 0, nb = 0;
     // record index of the item's own border pixel 0; of neighbour offset j (main tile:
@@ -595,9 +608,9 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
     if (k < 2) {  // top row, pixels 16 h .. 16 h + 15, against row 31 of the tiles above
       const int up = id - T.tiles_x;
       if (a.ty == 0) continue;
-      const bool u = tile_set(tile_bits, up);
-      const bool ul = h == 0 && a.tx > 0 && tile_set(tile_bits, up - 1);
-      const bool ur = h == 1 && a.tx + 1 < T.tiles_x && tile_set(tile_bits, up + 1);
+      const bool u = tile_set(tile_bits, T, band - 1, a.tx);
+      const bool ul = h == 0 && a.tx > 0 && tile_set(tile_bits, T, band - 1, a.tx - 1);
+      const bool ur = h == 1 && a.tx + 1 < T.tiles_x && tile_set(tile_bits, T, band - 1, a.tx + 1);
       if (!(u || ul || ur)) continue;
       fg = (fs[0] >> (16 * h)) & 0xFFFFu;
       if (fg == 0) continue;
@@ -614,9 +627,9 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
     } else {  // left column, rows 16 h .. 16 h + 15, against column 31 of the tiles left
       const int left = id - 1;
       if (a.tx == 0) continue;
-      const bool l = tile_set(tile_bits, left);
-      const bool lu = h == 0 && a.ty > 0 && tile_set(tile_bits, left - T.tiles_x);
-      const bool ld = h == 1 && a.ty + 1 < T.tiles_y && tile_set(tile_bits, left + T.tiles_x);
+      const bool l = tile_set(tile_bits, T, band, a.tx - 1);
+      const bool lu = h == 0 && a.ty > 0 && tile_set(tile_bits, T, band - 1, a.tx - 1);
+      const bool ld = h == 1 && a.ty + 1 < T.tiles_y && tile_set(tile_bits, T, band + 1, a.tx - 1);
       if (!(l || lu || ld)) continue;
 #pragma unroll
       for (int j = 0; j < 16; ++j) fg |= (fs[16 * h + j] & 1u) << j;
@@ -662,12 +675,13 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 }
 
 // Numbers the components in raster order over the bands of 32 rows (a tile row of a
-// frame: band b is frame b / tiles_y, tile row b % tiles_y), in two launches none of
-// whose workgroups waits for another. The bands' counts of components are already known:
-// the local pass adds each tile's local roots, the merge removes each root it links.
-//  scan:   one workgroup turns the counts into each band's first number and writes the
-//          number of components.
-//  assign: one workgroup per band; its threads take the band's (row, tile) pairs in
+// frame: band b is frame b / tiles_y, tile row b % tiles_y), none of whose workgroups
+// waits for another. The bands' counts of components are already known: the local pass
+// adds each tile's local roots, the merge removes each root it links.
+//  scan:   (over kDirectBands bands only) one workgroup turns the counts into each band's
+//          first number and writes the number of components.
+//  assign: one workgroup per band, which (up to kDirectBands bands) sums the earlier
+//          bands' counts itself; its threads take the band's (row, tile) pairs in
 //          raster order, so that a block-wide scan of their counts places each component.
 //          A pair's candidates are the tile's recorded local roots in that row; a
 //          candidate is a component when it is still its own parent (label = own frame
@@ -676,18 +690,19 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 //          in LDS and deal the pairs out (assign_kernel); wider ones give thread t row
 //          t / 8 and the t % 8-th eighth of the tiles (assign_wide_kernel).
 // One batch of a thread's tiles (b0 .. b0 + kBandBatch - 1, below tx_hi) in row y (row rr
-// of the band): comps[u] gets the bits of tile b0 + u's recorded local roots in that row
+// of the band; band_bits: the band's bitmap words): comps[u] gets the bits of tile
+// b0 + u's recorded local roots in that row
 // that are still their own parent (the components). Each level of loads (bitmap,
 // records, labels) is issued for the whole batch before any is used. Returns how many.
-__device__ __forceinline__ int batch_roots(int W, const uint32_t *tile_bits,
+__device__ __forceinline__ int batch_roots(int W, const uint32_t *band_bits,
                                            const uint32_t *rec_roots, const int32_t *lf,
                                            int base, int y, int b0, int tx_hi, int rr,
                                            uint32_t comps[kBandBatch]) {
   uint32_t cand[kBandBatch];
 #pragma unroll
   for (int u = 0; u < kBandBatch; ++u) {
-    const int tile = base + b0 + u;
-    cand[u] = b0 + u < tx_hi && tile_set(tile_bits, tile)
+    const int tile = base + b0 + u, tx = b0 + u;
+    cand[u] = tx < tx_hi && ((band_bits[tx >> 5] >> (tx & 31)) & 1u)
                   ? rec_roots[32 * static_cast<int64_t>(tile) + rr]
                   : 0u;
   }
@@ -808,17 +823,42 @@ __global__ __launch_bounds__(kBandScanThreads) void band_scan_kernel(int32_t *ba
   if (threadIdx.x == 0) *n_components = carry;
 }
 
-__global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(int W, int H, int64_t frame_px,
-                                                              Tiles T, const uint32_t *tile_bits,
-                                                              const uint32_t *rec_roots,
-                                                              int32_t *label,
-                                                              const int32_t *band_first,
-                                                              Comp *comp,
-                                                              int32_t max_components) {
+// The number of the band's first component. With `direct` (at most kDirectBands bands)
+// the workgroup sums the earlier bands' counts itself -- each band checks its own count,
+// and the last one writes the number of components; otherwise the scan pass has already
+// put it in place of the band's count. Called by every thread of the workgroup.
+__device__ __forceinline__ int band_start(const int32_t *band_count, int band, int n_bands,
+                                          bool direct, int32_t *n_components,
+                                          uint32_t *status) {
+  __shared__ int s_sum[kBandThreads / 64];
+  if (!direct) return band_count[band];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int v = 0;
+  for (int b = tid; b < band; b += kBandThreads) v += max(band_count[b], 0);
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if (lane == 0) s_sum[wave] = v;
+  __syncthreads();
+  int sum = 0;
+#pragma unroll
+  for (int w = 0; w < kBandThreads / 64; ++w) sum += s_sum[w];
+  if (tid == 0) {
+    const int own = band_count[band];
+    if (own < 0) fail(status);  // only a broken union-find removes more roots than there were
+    if (band == n_bands - 1) *n_components = sum + max(own, 0);
+  }
+  return sum;
+}
+
+__global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(
+    int W, int H, int64_t frame_px, Tiles T, const uint32_t *tile_bits,
+    const uint32_t *rec_roots, int32_t *label, const int32_t *band_count, int direct,
+    int32_t n_bands, int32_t *n_components, Comp *comp, int32_t max_components,
+    uint32_t *status) {
   __shared__ int s_wave[kBandThreads / 64];
   const int band = blockIdx.x;
   const BandPart p = band_part(T, H, band);
   int32_t *lf = label + static_cast<int64_t>(p.f) * frame_px;
+  const uint32_t *band_bits = tile_bits + static_cast<int64_t>(band) * T.wpb;
   // a thread's tiles fit one batch for frames up to 8 * kBandBatch tiles wide: its
   // components are then kept in registers between the count and the numbering
   const bool one = (T.tiles_x + 7) / 8 <= kBandBatch;
@@ -826,16 +866,17 @@ __global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(int W, int H,
   int cnt = 0;
   if (p.rows_in)
     for (int b0 = p.tx_lo; b0 < p.tx_hi; b0 += kBandBatch)
-      cnt += batch_roots(W, tile_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
+      cnt += batch_roots(W, band_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
   int total;
-  int id = band_first[band] + block_exclusive<kBandThreads>(cnt, s_wave, &total);
+  const int start = band_start(band_count, band, n_bands, direct, n_components, status);
+  int id = start + block_exclusive<kBandThreads>(cnt, s_wave, &total);
   if (cnt == 0) return;
   if (one) {
     batch_assign(W, lf, p.y, p.tx_lo, comps, comp, p.f, id, max_components);
     return;
   }
   for (int b0 = p.tx_lo; b0 < p.tx_hi; b0 += kBandBatch) {  // again, the loads now in cache
-    batch_roots(W, tile_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
+    batch_roots(W, band_bits, rec_roots, lf, p.base, p.y, b0, p.tx_hi, p.rr, comps);
     id = batch_assign(W, lf, p.y, b0, comps, comp, p.f, id, max_components);
   }
 }
@@ -846,13 +887,10 @@ __global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(int W, int H,
 // runs of c = ceil(32 nl / kBandThreads) to the threads, so that thread order is raster
 // order and a thread usually has one pair. A pair's candidates are the tile's recorded
 // local roots in that row; the label loads of up to kPairBatch pairs are issued together.
-__global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int64_t frame_px, Tiles T,
-                                                              const uint32_t *tile_bits,
-                                                              const uint32_t *rec_roots,
-                                                              int32_t *label,
-                                                              const int32_t *band_first,
-                                                              Comp *comp,
-                                                              int32_t max_components) {
+__global__ __launch_bounds__(kBandThreads) void assign_kernel(
+    int W, int64_t frame_px, Tiles T, const uint32_t *tile_bits, const uint32_t *rec_roots,
+    int32_t *label, const int32_t *band_count, int direct, int32_t n_bands,
+    int32_t *n_components, Comp *comp, int32_t max_components, uint32_t *status) {
   __shared__ int s_tx[kBandTiles];
   __shared__ int s_nl;
   __shared__ int s_wave[kBandThreads / 64];
@@ -860,14 +898,8 @@ __global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int64_t fra
   const int f = band / T.tiles_y, ty = band - f * T.tiles_y;
   const int base = band * T.tiles_x;  // tile id of the band's first tile
   int32_t *lf = label + static_cast<int64_t>(f) * frame_px;
-  if (tid < 64) {  // the band's bitmap words, one per lane (tiles_x <= kBandTiles: <= 10)
-    const int w_lo = base >> 5, w_hi = (base + T.tiles_x - 1) >> 5;
-    uint32_t bits = 0;
-    if (tid <= w_hi - w_lo) {
-      bits = tile_bits[w_lo + tid];
-      if (tid == 0) bits &= 0xFFFFFFFFu << (base & 31);
-      if (tid == w_hi - w_lo) bits &= 0xFFFFFFFFu >> (31 - ((base + T.tiles_x - 1) & 31));
-    }
+  if (tid < 64) {  // the band's bitmap words, one per lane (tiles_x <= kBandTiles: <= 8)
+    const uint32_t bits = tid < T.wpb ? tile_bits[static_cast<int64_t>(band) * T.wpb + tid] : 0u;
     const int cnt = __popc(bits);
     int incl = cnt;
     for (int o = 1; o < 64; o <<= 1) {
@@ -875,8 +907,7 @@ __global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int64_t fra
       if (tid >= o) incl += v;
     }
     int at = incl - cnt;
-    for (uint32_t m = bits; m != 0; m &= m - 1)
-      s_tx[at++] = (w_lo + tid) * 32 + __builtin_ctz(m) - base;
+    for (uint32_t m = bits; m != 0; m &= m - 1) s_tx[at++] = tid * 32 + __builtin_ctz(m);
     if (tid == 63) s_nl = incl;
   }
   __syncthreads();
@@ -930,7 +961,8 @@ __global__ __launch_bounds__(kBandThreads) void assign_kernel(int W, int64_t fra
   int cnt = 0;
   for (int g = p0; g < p1; g += kPairBatch) cnt += batch(g, comps, yx);
   int total;
-  int id = band_first[band] + block_exclusive<kBandThreads>(cnt, s_wave, &total);
+  const int start = band_start(band_count, band, n_bands, direct, n_components, status);
+  int id = start + block_exclusive<kBandThreads>(cnt, s_wave, &total);
   if (cnt == 0) return;
   if (p1 - p0 <= kPairBatch) {  // one batch: its components are still in registers
     number(comps, yx, id);
@@ -1096,20 +1128,33 @@ __global__ void empty_kernel(int32_t *n_rois, int32_t *n_components, int32_t *fr
 
 // Workgroups of `kernel` (`threads` each) resident on the current device at once, at
 // least 1: the grid of a pass that walks a list, so that no workgroup waits for a slot
-// while others walk their share.
+// while others walk their share. Asked of the runtime once per device and kernel.
 int resident_groups(const void *kernel, int threads) {
-  int dev = 0, cus = 0, per = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return kListGroups;
+  static std::mutex mu;
+  static std::map<std::tuple<int, const void *, int>, int> known;
+  const auto key = std::make_tuple(dev, kernel, threads);
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = known.find(key);
+    if (it != known.end()) return it->second;
+  }
+  int cus = 0, per = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
     return kListGroups;
-  return std::max(1, cus * per);
+  const int groups = std::max(1, cus * per);
+  std::lock_guard<std::mutex> lock(mu);
+  known[key] = groups;
+  return groups;
 }
 
 Tiles tiles_of(int32_t n_frames, int32_t width, int32_t height) {
   Tiles T;
   T.tiles_x = (width + kTile - 1) / kTile;
   T.tiles_y = (height + kTile - 1) / kTile;
+  T.wpb = (T.tiles_x + 31) / 32;
   T.n = int64_t(n_frames) * T.tiles_x * T.tiles_y;
   return T;
 }
@@ -1130,7 +1175,8 @@ extern "C" size_t tg_mask_rois_workspace_bytes(int32_t n_frames, int32_t width, 
                                                int32_t max_components) {
   if (!sizes_ok(n_frames, width, height, max_components)) return 0;
   const Tiles T = tiles_of(n_frames, width, height);
-  return layout(nullptr, int64_t(n_frames) * width * height, int64_t(n_frames) * T.tiles_y, T.n,
+  const int64_t n_bands = int64_t(n_frames) * T.tiles_y;
+  return layout(nullptr, int64_t(n_frames) * width * height, n_bands, T.n, n_bands * T.wpb,
                 max_components)
       .bytes;
 }
@@ -1144,13 +1190,13 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   const int64_t frame_px = int64_t(a->width) * a->height, n_px = a->n_frames * frame_px;
   const Tiles T = tiles_of(a->n_frames, a->width, a->height);
   const int64_t n_bands = int64_t(a->n_frames) * T.tiles_y;
-  const Layout L = layout(a->workspace, n_px, n_bands, T.n, a->max_components);
+  const Layout L = layout(a->workspace, n_px, n_bands, T.n, n_bands * T.wpb, a->max_components);
   if (!a->workspace || a->workspace_bytes < L.bytes ||
       reinterpret_cast<uintptr_t>(a->workspace) % 16 != 0)
     return TG_E_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int W = a->width, H = a->height;
-  const dim3 scan_groups(static_cast<uint32_t>((T.tiles_x + kScanTiles - 1) / kScanTiles),
+  const dim3 scan_groups(static_cast<uint32_t>(2 * T.wpb),
                          static_cast<uint32_t>(T.tiles_y), static_cast<uint32_t>(a->n_frames));
   const dim3 local_groups(static_cast<uint32_t>(std::min<int64_t>(
       T.n, resident_groups(reinterpret_cast<const void *>(local_kernel), kLocalThreads))));
@@ -1173,20 +1219,18 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   }
   uint32_t *status = reinterpret_cast<uint32_t *>(L.words + 2);
   uint32_t *n_list = reinterpret_cast<uint32_t *>(L.words + 3);
-  hipLaunchKernelGGL(clear_kernel, dim3(static_cast<uint32_t>((L.n_words + 255) / 256)),
-                     dim3(256), 0, s, L.words, L.n_words);
   if (vec && W % 16 == 0)
     hipLaunchKernelGGL(scan_kernel<2>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.rec_fg);
+                       frame_px, T, L.tile_bits, L.rec_fg, L.words, L.n_words);
   else if (word)
     hipLaunchKernelGGL(scan_kernel<1>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.rec_fg);
+                       frame_px, T, L.tile_bits, L.rec_fg, L.words, L.n_words);
   else
     hipLaunchKernelGGL(scan_kernel<0>, scan_groups, dim3(kScanThreads), 0, s, a->mask, W, H,
-                       frame_px, T, L.tile_bits, L.rec_fg);
-  const int64_t n_chunks = list_chunks(T.n);
+                       frame_px, T, L.tile_bits, L.rec_fg, L.words, L.n_words);
+  const int64_t n_bit_words = n_bands * T.wpb, n_chunks = list_chunks(n_bit_words);
   hipLaunchKernelGGL(list_kernel, dim3(static_cast<uint32_t>(n_chunks)), dim3(kListThreads), 0,
-                     s, L.tile_bits, (T.n + 31) / 32, L.tile_list, L.words, L.list_state,
+                     s, L.tile_bits, n_bit_words, T, L.tile_list, L.words, L.list_state,
                      static_cast<int32_t>(n_chunks), n_list, status);
   hipLaunchKernelGGL(local_kernel, local_groups, dim3(kLocalThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.rec_fg, L.rec_roots, L.rec_border, L.entries,
@@ -1194,17 +1238,20 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   hipLaunchKernelGGL(merge_kernel, border_groups, dim3(kBorderThreads), 0, s, W, frame_px, T,
                      L.tile_bits, L.tile_list, n_list, L.rec_fg, L.rec_border, L.label,
                      L.band_first, status);
-  hipLaunchKernelGGL(band_scan_kernel, dim3(1), dim3(kBandScanThreads), 0, s, L.band_first,
-                     n_bands, a->n_components, status);
+  const int direct = n_bands <= kDirectBands;
+  if (!direct)
+    hipLaunchKernelGGL(band_scan_kernel, dim3(1), dim3(kBandScanThreads), 0, s, L.band_first,
+                       n_bands, a->n_components, status);
   const dim3 bands(static_cast<uint32_t>(n_bands));
+  const int32_t nb = static_cast<int32_t>(n_bands);
   if (T.tiles_x <= kBandTiles)
     hipLaunchKernelGGL(assign_kernel, bands, dim3(kBandThreads), 0, s, W, frame_px, T,
-                       L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
-                       a->max_components);
+                       L.tile_bits, L.rec_roots, L.label, L.band_first, direct, nb,
+                       a->n_components, L.comp, a->max_components, status);
   else
     hipLaunchKernelGGL(assign_wide_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
-                       L.tile_bits, L.rec_roots, L.label, L.band_first, L.comp,
-                       a->max_components);
+                       L.tile_bits, L.rec_roots, L.label, L.band_first, direct, nb,
+                       a->n_components, L.comp, a->max_components, status);
   hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kEntryThreads), 0, s, W, frame_px, T,
                      L.tile_list, n_list, L.entries, L.n_ent, L.label, L.comp, status);
   hipLaunchKernelGGL(filter_kernel, dim3(static_cast<uint32_t>(n_filter)), dim3(kFilterThreads),

@@ -213,6 +213,18 @@ def test_mask_rois_wide_frames(torch):
         _assert_rois(torch, m, 2)
 
 
+def test_mask_rois_many_bands(torch):
+    """More than 4096 bands of 32 rows (150 frames of 29 tile rows): the numbering takes
+    each band's first number from a scan over the bands' counts instead of summing them
+    in each band's workgroup."""
+    rng = np.random.default_rng(41)
+    m = (rng.random((150, 900, 20)) < 0.2).astype(np.uint8)
+    m[3, 100:800, 5:15] = 1
+    m[149, 0:900:3, :] = 1
+    say("mask_rois many bands", m.shape)
+    _assert_rois(torch, m, 1)
+
+
 def _tile_local_roots(mask2d):
     """Frame indices of the tile-local roots of one frame: per 32x32 tile, the first pixel
     (raster order) of each of the tile's own 8-connected components."""
