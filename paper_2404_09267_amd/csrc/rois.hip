@@ -32,7 +32,7 @@
 //             neighbouring tiles are all empty is skipped. Every 8-neighbour pair across a
 //             tile border is seen from the tile below or to the right of it. A root that
 //             gets linked leaves its band's count, which then counts components.
-//  5. assign: per band of 32 rows (a tile row of a frame), the recorded local roots still
+//  5. number: per band of 32 rows (a tile row of a frame), the recorded local roots still
 //             their own parent (the components) are numbered in raster order, each
 //             component's record is initialised and its root marked with its number. The
 //             band's first number is the sum of the earlier bands' counts, read by the
@@ -680,15 +680,15 @@ __global__ __launch_bounds__(kBorderThreads) void merge_kernel(
 // adds each tile's local roots, the merge removes each root it links.
 //  scan:   (over kDirectBands bands only) one workgroup turns the counts into each band's
 //          first number and writes the number of components.
-//  assign: one workgroup per band, which (up to kDirectBands bands) sums the earlier
+//  number: one workgroup per band, which (up to kDirectBands bands) sums the earlier
 //          bands' counts itself; its threads take the band's (row, tile) pairs in
 //          raster order, so that a block-wide scan of their counts places each component.
 //          A pair's candidates are the tile's recorded local roots in that row; a
 //          candidate is a component when it is still its own parent (label = own frame
 //          index, flagged). Each component's record is initialised and its root marked
 //          with its number. Bands up to kBandTiles tiles wide list their non-empty tiles
-//          in LDS and deal the pairs out (assign_kernel); wider ones give thread t row
-//          t / 8 and the t % 8-th eighth of the tiles (assign_wide_kernel).
+//          in LDS and deal the pairs out (number_kernel); wider ones give thread t row
+//          t / 8 and the t % 8-th eighth of the tiles (number_wide_kernel).
 // One batch of a thread's tiles (b0 .. b0 + kBandBatch - 1, below tx_hi) in row y (row rr
 // of the band; band_bits: the band's bitmap words): comps[u] gets the bits of tile
 // b0 + u's recorded local roots in that row
@@ -849,7 +849,7 @@ __device__ __forceinline__ int band_start(const int32_t *band_count, int band, i
   return sum;
 }
 
-__global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(
+__global__ __launch_bounds__(kBandThreads) void number_wide_kernel(
     int W, int H, int64_t frame_px, Tiles T, const uint32_t *tile_bits,
     const uint32_t *rec_roots, int32_t *label, const int32_t *band_count, int direct,
     int32_t n_bands, int32_t *n_components, Comp *comp, int32_t max_components,
@@ -887,7 +887,7 @@ __global__ __launch_bounds__(kBandThreads) void assign_wide_kernel(
 // runs of c = ceil(32 nl / kBandThreads) to the threads, so that thread order is raster
 // order and a thread usually has one pair. A pair's candidates are the tile's recorded
 // local roots in that row; the label loads of up to kPairBatch pairs are issued together.
-__global__ __launch_bounds__(kBandThreads) void assign_kernel(
+__global__ __launch_bounds__(kBandThreads) void number_kernel(
     int W, int64_t frame_px, Tiles T, const uint32_t *tile_bits, const uint32_t *rec_roots,
     int32_t *label, const int32_t *band_count, int direct, int32_t n_bands,
     int32_t *n_components, Comp *comp, int32_t max_components, uint32_t *status) {
@@ -1245,11 +1245,11 @@ extern "C" int tg_mask_rois(const tg_mask_rois_args *a, void *stream) {
   const dim3 bands(static_cast<uint32_t>(n_bands));
   const int32_t nb = static_cast<int32_t>(n_bands);
   if (T.tiles_x <= kBandTiles)
-    hipLaunchKernelGGL(assign_kernel, bands, dim3(kBandThreads), 0, s, W, frame_px, T,
+    hipLaunchKernelGGL(number_kernel, bands, dim3(kBandThreads), 0, s, W, frame_px, T,
                        L.tile_bits, L.rec_roots, L.label, L.band_first, direct, nb,
                        a->n_components, L.comp, a->max_components, status);
   else
-    hipLaunchKernelGGL(assign_wide_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
+    hipLaunchKernelGGL(number_wide_kernel, bands, dim3(kBandThreads), 0, s, W, H, frame_px, T,
                        L.tile_bits, L.rec_roots, L.label, L.band_first, direct, nb,
                        a->n_components, L.comp, a->max_components, status);
   hipLaunchKernelGGL(boxes_kernel, entry_groups, dim3(kEntryThreads), 0, s, W, frame_px, T,
