@@ -414,13 +414,15 @@ size_t tg_merge_workspace_bytes(int32_t n_max, int32_t n_frames);
  * area = max(0, x2 - x1) * max(0, y2 - y1), union = (area_a + area_b) - inter,
  * suppressed when inter > iou_threshold * union. Detections whose frame is outside
  * [0, n_frames) are dropped. Kept detections are written to out in input order and their
- * count to *n_kept. Every frame is merged, whatever its number of detections (frames of up
- * to 1024 are ranked and walked in on-chip memory, larger ones in the workspace). The
+ * count to *n_kept. Every frame is merged, whatever its number of detections (the walk's
+ * decisions are reached in parallel rounds over a spatial index of the frame's boxes,
+ * kept in the workspace, with the same result). The
  * coordinates are not expected to be NaN (tg_unstitch never keeps such a box); if one is,
  * min and max ignore the NaN operand. Enqueued on `stream`; the library allocates nothing.
  * Returns TG_E_INVAL (null pointer, negative size, NaN threshold), TG_E_WORKSPACE,
  * TG_E_HIP. With n_max == 0 only *n_kept = 0 is written.
- * *n_kept = TG_E_INTERNAL reports a device-side failure of the compaction.
+ * *n_kept = TG_E_INTERNAL reports a device-side failure (a compaction that could not
+ * complete, or a frame whose rounds overran their bound; neither happens on a correct run).
  */
 int tg_merge(const tg_merge_args *args, void *stream);
 

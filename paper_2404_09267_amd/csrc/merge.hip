@@ -9,7 +9,7 @@
 // IoU > threshold, decided as inter > threshold * union in binary32 with every operation
 // rounded on its own. Kept detections are written in input order.
 //
-// Six launches on the caller's stream, all on device data (the detection count comes from
+// Eight launches on the caller's stream, all on device data (the detection count comes from
 // tg_unstitch's n_out on the device):
 //  1. clear the per-frame counters and look-back words;
 //  2. count detections per frame (LDS histograms, one global atomic per frame and
@@ -17,19 +17,17 @@
 //  3. exclusive scan of the counts (one workgroup);
 //  4. scatter detection indices into frame groups (ranks inside a workgroup from LDS, one
 //     range per frame and workgroup from a global cursor; the order inside a group does
-//     not matter, the ranking below is a total order);
-//  5. one 1024-thread workgroup per frame: bitonic sort of 64-bit keys (score, box), then
-//     the greedy pass 64 candidates at a time (all threads test the chunk against the
-//     detections kept so far and fill the chunk's 64 x 64 suppression bits; one wave walks
-//     the chunk). Frames of up to 1024 detections do all of it in LDS. Larger frames sort
-//     in the workspace (global bitonic passes for the long strides, LDS tiles of up to 4096
-//     keys for the short ones) and index their ranked boxes by a grid of up to 32 x 32 cells
-//     over the frame's boxes: a candidate is tested only against the earlier kept
-//     detections registered in the cells its box touches, plus a "wide" list (see
-//     large_frame for why this finds every suppressor);
-//  6. stable compaction of the kept detections (decoupled look-back, 1024 per workgroup).
+//     not matter, the ranking below is a total order), with each detection's ranking key
+//     (score, box), box and patch at its place in the group;
+//  5-7. the greedy decided in rounds, with no sort: a spatial index of each frame's boxes
+//     (one workgroup per frame), each detection's suppressors ranked above it (over the
+//     whole grid), then per frame rounds in which a detection is suppressed once one of
+//     them is kept and kept once all of them are suppressed (see "the greedy of a frame"
+//     for why this is the greedy walk's result and why the index finds every suppressor);
+//  8. stable compaction of the kept detections (decoupled look-back, 1024 per workgroup).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "lookback.h"
@@ -42,7 +40,6 @@
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxPerFrame = 1024;  // frames ranked and walked in LDS; larger: workspace
 constexpr int kPerThread = 4;  // compaction: consecutive detections per thread
 constexpr int kCompactBlock = kThreads * kPerThread;
 constexpr int kScanThreads = 1024;
@@ -63,19 +60,25 @@ struct MergeParams {
   int32_t *frame_begin;  // [n_frames + 1]
   int32_t *grouped;      // [n_max]
   uint32_t *ticket;
+  uint32_t *status;      // set when a frame's rounds overrun (cannot happen)
   uint64_t *state;       // [compaction workgroups]
-  // Scratch of frames over kMaxPerFrame detections; frame f (first detection lo, n of
-  // them) owns [2 lo, 2 (lo + n)) of the key arrays and [lo, lo + n) (times kCellsMax for
-  // the cell lists) of the others, so frames never share a word.
-  uint64_t *big_key;     // [2 n_max] ranking keys
-  int32_t *big_det;      // [2 n_max] detection index of each key
-  float4 *rbox;          // [n_max] ranked boxes
-  int32_t *rroi;         // [n_max] ranked patch ids
-  uint32_t *rcell;       // [n_max] ranked cell ranges (kWide, kEmpty or packed)
-  float4 *ebox;          // [kCellsMax n_max] kept boxes listed per cell, then the wide list
-  int32_t *eroi;         // [kCellsMax n_max] their patch ids
-  float4 *kbox;          // [n_max] all kept boxes, in rank order
-  int32_t *kroi;         // [n_max] their patch ids
+  // Per detection, at its position in its frame group: frame f (first detection lo, n of
+  // them) owns [lo, lo + n) of these (times kCellsMax for the cell lists), so frames
+  // never share a word.
+  uint64_t *rkey;        // [n_max] ranking keys
+  float4 *rbox;          // [n_max] boxes
+  int32_t *rroi;         // [n_max] patch ids
+  uint32_t *rcell;       // [n_max] cell ranges (kWide, kEmpty or packed)
+  int32_t *rstate;       // [n_max] kUndecided, kKept or kSuppressed
+  int32_t *rlist;        // [2 (kCellsMax + 1) n_max] the lists to search: starts, sizes
+  int32_t *rpred;        // [kPredSlots n_max] suppressors ranked above (positions)
+  int32_t *rnpred;       // [n_max] how many
+  int32_t *rovf;         // [n_max] a longer list's start in ovf, or -1: search again
+  int32_t *ovf;          // [kOvfPerDet n_max] the whole lists of detections with more
+  int64_t ovf_cap;
+  unsigned long long *ovf_used;  // entries of ovf handed out
+  float4 *ebox;          // [kCellsMax n_max] boxes listed per cell, then the wide list
+  int4 *eaux;            // [kCellsMax n_max] their patch ids, keys and positions
 };
 
 __device__ __forceinline__ int count_of(const MergeParams &P) {
@@ -87,7 +90,7 @@ __global__ void clear_kernel(MergeParams P, int32_t n_words32, int32_t n_words64
   if (i < n_words32) {
     P.counts[i] = 0;  // counts and cursor are contiguous
   }
-  if (i < n_words64) reinterpret_cast<uint64_t *>(P.ticket)[i] = 0;  // ticket + states
+  if (i < n_words64) reinterpret_cast<uint64_t *>(P.ticket)[i] = 0;  // ticket, cursor, states
 }
 
 // Detections per frame. Up to kHistMax frames a workgroup first counts in LDS and then
@@ -142,34 +145,6 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const MergeParams P)
   if (tid == 0) P.frame_begin[P.n_frames] = carry;
 }
 
-// Detection indices into frame groups. Up to kHistMax frames a workgroup ranks its
-// detections per frame in LDS and reserves one range per non-empty frame.
-__global__ __launch_bounds__(kThreads) void scatter_kernel(const MergeParams P) {
-  __shared__ int hist[kHistMax];
-  const int tid = threadIdx.x;
-  const bool local = P.n_frames <= kHistMax;
-  if (local)
-    for (int f = tid; f < P.n_frames; f += kThreads) hist[f] = 0;
-  __syncthreads();
-  const int i = blockIdx.x * kThreads + tid;
-  int f = -1, rank = 0;
-  if (i < count_of(P)) {
-    f = P.dets[i].frame;
-    if (f < 0 || f >= P.n_frames)
-      f = -1;
-    else if (local)
-      rank = atomicAdd(&hist[f], 1);
-    else
-      P.grouped[P.frame_begin[f] + atomicAdd(&P.cursor[f], 1)] = i;
-  }
-  if (!local) return;
-  __syncthreads();
-  for (int g = tid; g < P.n_frames; g += kThreads)  // this workgroup's range of frame g
-    if (hist[g]) hist[g] = P.frame_begin[g] + atomicAdd(&P.cursor[g], hist[g]);
-  __syncthreads();
-  if (f >= 0) P.grouped[hist[f] + rank] = i;
-}
-
 // Ranking key, ascending = higher score first, then lower box index. NaN ranks as -inf;
 // -0 and +0 are the same score.
 __device__ __forceinline__ uint64_t rank_key(float s, int32_t box) {
@@ -178,6 +153,44 @@ __device__ __forceinline__ uint64_t rank_key(float s, int32_t box) {
   uint32_t b = __float_as_uint(s);
   b ^= (b & 0x80000000u) ? 0xFFFFFFFFu : 0x80000000u;  // ascending order of floats
   return (static_cast<uint64_t>(~b) << 32) | static_cast<uint32_t>(box);
+}
+
+// Detection indices into frame groups, with each detection's ranking key, box and patch
+// at its position in the group. Up to kHistMax frames a workgroup ranks its detections per
+// frame in LDS and reserves one range per non-empty frame.
+__global__ __launch_bounds__(kThreads) void scatter_kernel(const MergeParams P) {
+  __shared__ int hist[kHistMax];
+  const int tid = threadIdx.x;
+  const bool local = P.n_frames <= kHistMax;
+  if (local)
+    for (int f = tid; f < P.n_frames; f += kThreads) hist[f] = 0;
+  __syncthreads();
+  const int i = blockIdx.x * kThreads + tid;
+  int f = -1, rank = 0, pos = -1;
+  tg_det d;
+  if (i < count_of(P)) {
+    d = P.dets[i];
+    f = d.frame;
+    if (f < 0 || f >= P.n_frames)
+      f = -1;
+    else if (local)
+      rank = atomicAdd(&hist[f], 1);
+    else
+      pos = P.frame_begin[f] + atomicAdd(&P.cursor[f], 1);
+  }
+  if (local) {
+    __syncthreads();
+    for (int g = tid; g < P.n_frames; g += kThreads)  // this workgroup's range of frame g
+      if (hist[g]) hist[g] = P.frame_begin[g] + atomicAdd(&P.cursor[g], hist[g]);
+    __syncthreads();
+    if (f >= 0) pos = hist[f] + rank;
+  }
+  if (pos < 0) return;
+  P.grouped[pos] = i;
+  const float s = (d.box >= 0 && d.box < P.n_scores) ? P.scores[d.box] : __builtin_nanf("");
+  P.rkey[pos] = rank_key(s, d.box);
+  P.rbox[pos] = make_float4(d.x1, d.y1, d.x2, d.y2);
+  P.rroi[pos] = d.roi;
 }
 
 // Whether box a suppresses box b (x1, y1, x2, y2 in .x .y .z .w).
@@ -191,122 +204,46 @@ __device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
   return inter > __fmul_rn(thr, uni);
 }
 
-// LDS of one frame: ranking keys and detection ids for the sort, then the ranked boxes,
-// patches and flags, the list of detections kept so far and one chunk's bit matrix.
-constexpr int kChunk = 64;  // candidates decided per round
-constexpr int kFrameThreads = 1024;  // one workgroup per frame
-static_assert(kChunk * kChunk % kFrameThreads == 0 && 32 % (kChunk * kChunk / kFrameThreads) == 0,
-              "a thread's columns lie in one 32-bit word");
-constexpr size_t kOffKey = 0;                                          // u64 [kMaxPerFrame]
-constexpr size_t kOffDet = kOffKey + sizeof(uint64_t) * kMaxPerFrame;  // i32 [kMaxPerFrame]
-constexpr size_t kOffBox = kOffDet + sizeof(int32_t) * kMaxPerFrame;   // float4 [kMaxPerFrame]
-constexpr size_t kOffRoi = kOffBox + sizeof(float4) * kMaxPerFrame;    // i32 [kMaxPerFrame]
-constexpr size_t kOffKeptBox = kOffRoi + sizeof(int32_t) * kMaxPerFrame;  // float4 [kMaxPerFrame]
-constexpr size_t kOffKeptRoi = kOffKeptBox + sizeof(float4) * kMaxPerFrame;  // i32 [kMaxPerFrame]
-constexpr size_t kOffBits = kOffKeptRoi + sizeof(int32_t) * kMaxPerFrame;   // u32 [64][2]
-constexpr size_t kOffAlive = kOffBits + sizeof(uint32_t) * 2 * kChunk; // u8 [kMaxPerFrame]
-constexpr size_t kLdsBytes = kOffAlive + kMaxPerFrame;
-
-
-// Step (2) of a chunk (all threads): bit b of row a (bits[2a], bits[2a+1]) is set when
-// candidate a suppresses candidate b, for a < b < m; bits must be zero on entry.
-__device__ __forceinline__ void chunk_bits(const MergeParams &P, const float4 *box,
-                                           const int32_t *roi, int m, uint32_t *bits) {
-  constexpr int kCols = kChunk * kChunk / kFrameThreads;  // columns per thread
-  const int tid = threadIdx.x;
-  const int a = tid / (kChunk / kCols), q = tid % (kChunk / kCols);  // row a, columns
-  uint32_t part = 0;                                                 // [kCols q, +kCols)
-  if (a < m) {
-    const float4 ba = box[a];
-    const int ra = roi[a];
-    for (int b = max(kCols * q, a + 1); b < min(kCols * q + kCols, m); ++b)
-      if ((!P.cross_only || roi[b] != ra) && suppresses(ba, box[b], P.thr))
-        part |= 1u << (b & 31);
-    if (part) atomicOr(&bits[2 * a + ((kCols * q) >> 5)], part);
-  }
-}
-
-// Step (3) of a chunk (one wave, row a of the bits in lane a): walks the m candidates in
-// rank order, skipping the ones already dead (alive[a] == 0) or removed by a candidate
-// kept before them; returns the mask of kept candidates (bit a = candidate a).
-__device__ __forceinline__ uint64_t chunk_walk(const uint8_t *alive, const uint32_t *bits,
-                                               int m) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t row_lo = lane < m ? bits[2 * lane] : 0;
-  const uint32_t row_hi = lane < m ? bits[2 * lane + 1] : 0;
-  uint64_t removed = __ballot(lane < m && !alive[lane]) | (m < 64 ? ~uint64_t(0) << m : 0);
-  // only candidates that suppress someone in the chunk can change `removed`: visit those
-  // in rank order (a later one's row cannot affect an earlier candidate)
-  for (uint64_t rows = __ballot((row_lo | row_hi) != 0); rows != 0; rows &= rows - 1) {
-    const int a = __builtin_ctzll(rows);
-    if ((removed >> a) & 1) continue;
-    // readlane returns int: widen through uint32_t so bit 31 does not sign-extend
-    const uint32_t lo32 = static_cast<uint32_t>(__builtin_amdgcn_readlane(row_lo, a));
-    const uint32_t hi32 = static_cast<uint32_t>(__builtin_amdgcn_readlane(row_hi, a));
-    removed |= (static_cast<uint64_t>(hi32) << 32) | lo32;
-  }
-  return __ballot(lane < m && !((removed >> lane) & 1));
-}
-
-// ---- frames of more than kMaxPerFrame detections ---------------------------------------
-
-constexpr int kTileKeys = 4096;  // keys per LDS tile of the large-frame sort
-constexpr int kGridMax = 32;     // cells per axis of the large-frame index
-constexpr int kCellsMax = 4;     // cells a box may touch before it goes on the wide list
-constexpr uint32_t kWide = 0xFFFFFFFFu;   // tested against every kept detection
-constexpr uint32_t kEmpty = 0xFFFFFFFEu;  // x2 < x1 or y2 < y1: overlaps nothing
-
-__device__ __forceinline__ void cmpx(uint64_t *key, int32_t *det, int i, int j, bool up) {
-  const uint64_t ki = key[i], kj = key[j];
-  if ((ki > kj) == up) {
-    key[i] = kj;
-    key[j] = ki;
-    const int32_t d = det[i];
-    det[i] = det[j];
-    det[j] = d;
-  }
-}
-
-// Ascending bitonic sort of gk[0, pw) (payload gd), pw a power of two: the strides of a
-// tile (min(pw, kTileKeys) keys) and more are passes over global memory, the shorter ones
-// run tile by tile in LDS (tk, td). Each compare-exchange is the one of the plain network.
-__device__ __forceinline__ void sort_large(uint64_t *gk, int32_t *gd, int pw, uint64_t *tk,
-                                           int32_t *td) {
-  const int tid = threadIdx.x;
-  const int tile = min(pw, kTileKeys);
-  for (int size = tile; size <= pw; size <<= 1) {
-    for (int stride = size >> 1; stride >= tile; stride >>= 1) {
-      for (int t = tid; t < pw / 2; t += kFrameThreads) {
-        const int i = 2 * t - (t & (stride - 1));
-        cmpx(gk, gd, i, i + stride, (i & size) == 0);
-      }
-      __syncthreads();
-    }
-    // the first round sorts every tile through sizes 2 .. tile; later rounds finish size
-    // `size` with the strides below the tile
-    for (int base = 0; base < pw; base += tile) {
-      for (int k = tid; k < tile; k += kFrameThreads) {
-        tk[k] = gk[base + k];
-        td[k] = gd[base + k];
-      }
-      __syncthreads();
-      for (int sz = size == tile ? 2 : size; sz <= size; sz <<= 1) {
-        for (int stride = min(sz, tile) >> 1; stride > 0; stride >>= 1) {
-          for (int t = tid; t < tile / 2; t += kFrameThreads) {
-            const int i = 2 * t - (t & (stride - 1));
-            cmpx(tk, td, i, i + stride, ((base + i) & sz) == 0);
-          }
-          __syncthreads();
-        }
-      }
-      for (int k = tid; k < tile; k += kFrameThreads) {
-        gk[base + k] = tk[k];
-        gd[base + k] = td[k];
-      }
-      __syncthreads();
-    }
-  }
-}
+// ---- the greedy of a frame, decided in rounds -----------------------------------------
+//
+// The greedy walk keeps a detection exactly when no detection ranked above it that
+// suppresses it is kept (by induction over the ranking). So no sorted ranking is needed:
+// given each detection's suppressors ranked above it, rounds decide the frame -- a
+// detection is suppressed once one of them is kept, kept once all of them are suppressed.
+// The best-ranked undecided detection of a round has only decided suppressors, so every
+// round decides at least one: a frame of n detections needs at most n rounds (two to four
+// in practice, where chains of boxes suppressing each other are short). Three launches:
+//  index:   one workgroup per frame lists every box in a grid of up to kGridMax x kGridMax
+//           cells over the frame's boxes (cells about twice the mean box size) and gives
+//           each detection its lists to search;
+//  search:  kScanLanes lanes per detection, over all detections at once, find its
+//           suppressors ranked above it in those lists (kPredSlots of them are kept; a
+//           detection with more is searched again when it is decided);
+//  resolve: one workgroup per frame runs the rounds on the suppressor lists.
+// Why the cells find every suppressor: with a threshold t >= 0, a suppresses b only if
+// inter > t * union >= 0 (a union is never negative), so inter > 0 and both clipped widths
+// are positive: min(x2a, x2b) > max(x1a, x1b) and likewise in y. The point
+// (max(x1a, x1b), max(y1a, y1b)) then lies in both boxes, and since cell_of is
+// non-decreasing its cell lies in the cell ranges of both: a and b share a cell. Every box
+// is listed in the cells it touches; boxes with a NaN coordinate (where min and max ignore
+// the NaN operand), boxes touching more than kCellsMax cells, and every box when t < 0, are
+// "wide": listed once in a wide list that every detection searches, and themselves
+// searching the whole frame. Boxes with x2 < x1 or y2 < y1 have no positive width with
+// anything, so when t >= 0 they neither suppress nor are suppressed: kept from the start
+// and listed nowhere.
+constexpr int kFrameThreads = 1024;  // index: one workgroup per frame
+constexpr int kResolveThreads = 512; // resolve: one workgroup per frame
+constexpr int kGridMax = 32;         // cells per axis
+constexpr int kCellsMax = 4;         // cells a box may touch before it goes on the wide list
+constexpr int kLists = kCellsMax + 1;
+constexpr uint32_t kWide = 0xFFFFFFFFu;
+constexpr uint32_t kEmpty = 0xFFFFFFFEu;
+constexpr int32_t kUndecided = 0, kKept = 1, kSuppressed = 2;
+constexpr int kPredSlots = 16;  // suppressors kept in place per detection
+constexpr int kOvfPerDet = 16;  // overflow area for longer lists: kOvfPerDet n_max entries
+constexpr int kScanLanes = 8;  // lanes per detection in the search
+constexpr int kBatch = 8;      // list entries whose loads a lane issues together
+constexpr int kSearchDets = kThreads / kScanLanes;  // detections per search workgroup
 
 __device__ __forceinline__ float wave_minf(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
@@ -328,87 +265,48 @@ __device__ __forceinline__ int cell_of(float v, float e0, float sc, int g) {
   return static_cast<int>(t);
 }
 
-static_assert(kLdsBytes >= (sizeof(uint64_t) + sizeof(int32_t)) * kTileKeys,
-              "the large-frame sort tile fits in the frame's LDS");
-
-struct LargeLds {
+struct FrameLds {
   float ex0, sx, ey0, sy;
-  int gx, gy, all_wide, kept;
+  int gx, gy, all_wide;
   float red[4][kFrameThreads / 64];
   float sum[2][kFrameThreads / 64];
   int off[kGridMax * kGridMax + 2];  // list starts (cells, then the wide list), then the end
-  int cur[kGridMax * kGridMax + 1];  // list sizes while counting, then kept entries so far
-  float4 cbox[kChunk];
-  int32_t croi[kChunk];
-  uint32_t crange[kChunk];
-  uint8_t calive[kChunk];
-  uint32_t bits[2 * kChunk];
-  // step (1): candidate q's lists to scan (start in ebox, or -1 for the kept list; length)
-  int sstart[kChunk][kCellsMax + 1], slen[kChunk][kCellsMax + 1];
+  int cur[kGridMax * kGridMax + 1];  // list sizes while counting, then while filling
+  int cnt[kGridMax * kGridMax + 1];  // list sizes
 };
+constexpr int kIdx = 4;  // detections per thread and step of the index, loads issued together
 
-// One frame of n > kMaxPerFrame detections (grouped[lo, lo + n)), by one workgroup.
-//
-// Why the cell index finds every suppressor: with a threshold t >= 0, a suppresses b only
-// if inter > t * union >= 0 (the union of two boxes is never negative), so inter > 0 and
-// both clipped widths are positive: min(x2a, x2b) > max(x1a, x1b) and likewise in y. The
-// point (max(x1a, x1b), max(y1a, y1b)) then lies in both boxes, and since cell_of is
-// non-decreasing, its cell lies in the cell ranges of both: a and b share a cell. Boxes
-// with a NaN coordinate (where min and max ignore the NaN operand), boxes touching more
-// than kCellsMax cells, and every box when t < 0, are "wide": a wide candidate is tested
-// against the whole kept list, and every candidate also scans the list of wide boxes.
-// Boxes with x2 < x1 or y2 < y1 have no positive width with anything, so when t >= 0
-// they neither suppress nor are suppressed and are registered nowhere.
-static_assert(sizeof(LargeLds) <= kLdsBytes, "the large-frame state fits in the frame's LDS");
-
-__device__ __forceinline__ void large_frame(const MergeParams &P, int lo, int n, uint8_t *lds) {
+__global__ __launch_bounds__(kFrameThreads) void index_kernel(const MergeParams P) {
+  __shared__ FrameLds S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  uint64_t *gk = P.big_key + 2 * static_cast<int64_t>(lo);
-  int32_t *gd = P.big_det + 2 * static_cast<int64_t>(lo);
-  float4 *rbox = P.rbox + lo;
-  int32_t *rroi = P.rroi + lo;
-  uint32_t *rcell = P.rcell + lo;
-  float4 *ebox = P.ebox + static_cast<int64_t>(kCellsMax) * lo;
-  int32_t *eroi = P.eroi + static_cast<int64_t>(kCellsMax) * lo;
-  float4 *kbox = P.kbox + lo;
-  int32_t *kroi = P.kroi + lo;
+  const int lo = P.frame_begin[blockIdx.x];
+  const int n = P.frame_begin[blockIdx.x + 1] - lo;
+  if (n <= 0) return;
+  const int64_t ent0 = static_cast<int64_t>(kCellsMax) * lo;  // the frame's list entries
 
-  // 1. Ranking: keys in the workspace, sorted.
-  int pw = 1;
-  while (pw < n) pw <<= 1;  // < 2 n
-  for (int k = tid; k < pw; k += kFrameThreads) {
-    if (k < n) {
-      const int i = P.grouped[lo + k];
-      const int32_t b = P.dets[i].box;
-      const float s = (b >= 0 && b < P.n_scores) ? P.scores[b] : __builtin_nanf("");
-      gk[k] = rank_key(s, b);
-      gd[k] = i;
-    } else {
-      gk[k] = ~uint64_t(0);
-      gd[k] = -1;
-    }
-  }
-  __syncthreads();
-  sort_large(gk, gd, pw, reinterpret_cast<uint64_t *>(lds),
-             reinterpret_cast<int32_t *>(lds + sizeof(uint64_t) * kTileKeys));
-
-  // 2. Ranked boxes, and the frame's extent and mean box size for the grid.
-  LargeLds &S = *reinterpret_cast<LargeLds *>(lds);
+  // the frame's extent and mean box size
   float xlo = __builtin_inff(), xhi = -__builtin_inff(), ylo = xlo, yhi = xhi;
   float sw = 0.0f, sh = 0.0f;
-  for (int r = tid; r < n; r += kFrameThreads) {
-    const tg_det d = P.dets[gd[r]];
-    rbox[r] = make_float4(d.x1, d.y1, d.x2, d.y2);
-    rroi[r] = d.roi;
-    if (__builtin_isfinite(d.x1) && __builtin_isfinite(d.x2) && d.x2 >= d.x1) {
-      xlo = fminf(xlo, d.x1);
-      xhi = fmaxf(xhi, d.x2);
-      sw += d.x2 - d.x1;
+  for (int p0 = tid; p0 < n; p0 += kIdx * kFrameThreads) {
+    float4 bb[kIdx];
+#pragma unroll
+    for (int u = 0; u < kIdx; ++u) {
+      const int p = p0 + u * kFrameThreads;
+      bb[u] = p < n ? P.rbox[lo + p] : make_float4(0.0f, 0.0f, -1.0f, -1.0f);
     }
-    if (__builtin_isfinite(d.y1) && __builtin_isfinite(d.y2) && d.y2 >= d.y1) {
-      ylo = fminf(ylo, d.y1);
-      yhi = fmaxf(yhi, d.y2);
-      sh += d.y2 - d.y1;
+#pragma unroll
+    for (int u = 0; u < kIdx; ++u) {
+      const float4 b = bb[u];
+      if (__builtin_isfinite(b.x) && __builtin_isfinite(b.z) && b.z >= b.x) {
+        xlo = fminf(xlo, b.x);
+        xhi = fmaxf(xhi, b.z);
+        sw += b.z - b.x;
+      }
+      if (__builtin_isfinite(b.y) && __builtin_isfinite(b.w) && b.w >= b.y) {
+        ylo = fminf(ylo, b.y);
+        yhi = fmaxf(yhi, b.w);
+        sh += b.w - b.y;
+      }
     }
   }
   xlo = wave_minf(xlo);
@@ -452,34 +350,45 @@ __device__ __forceinline__ void large_frame(const MergeParams &P, int lo, int n,
     S.sx = (__builtin_isfinite(scx) && scx > 0.0f) ? scx : 0.0f;
     S.sy = (__builtin_isfinite(scy) && scy > 0.0f) ? scy : 0.0f;
     S.all_wide = !(P.thr >= 0.0f);
-    S.kept = 0;
   }
   for (int c = tid; c < kGridMax * kGridMax + 1; c += kFrameThreads) S.cur[c] = 0;
   __syncthreads();
 
-  // 3. Cell index: each ranked box's cell range, then counts, offsets and the entries.
+  // each box's cell range; the lists' sizes
   const int gx = S.gx, gy = S.gy, n_cells = gx * gy;
-  for (int r = tid; r < n; r += kFrameThreads) {
-    const float4 b = rbox[r];
-    uint32_t cr;
-    if (S.all_wide || b.x != b.x || b.y != b.y || b.z != b.z || b.w != b.w) {
-      cr = kWide;
-    } else if (b.z < b.x || b.w < b.y) {
-      cr = kEmpty;
-    } else {
-      const int cx0 = cell_of(b.x, S.ex0, S.sx, gx), cx1 = cell_of(b.z, S.ex0, S.sx, gx);
-      const int cy0 = cell_of(b.y, S.ey0, S.sy, gy), cy1 = cell_of(b.w, S.ey0, S.sy, gy);
-      cr = (cx1 - cx0 + 1) * (cy1 - cy0 + 1) > kCellsMax
-               ? kWide
-               : static_cast<uint32_t>(cx0 | cx1 << 8 | cy0 << 16 | cy1 << 24);
+  for (int p0 = tid; p0 < n; p0 += kIdx * kFrameThreads) {
+    float4 bb[kIdx];
+#pragma unroll
+    for (int u = 0; u < kIdx; ++u) {
+      const int p = p0 + u * kFrameThreads;
+      bb[u] = p < n ? P.rbox[lo + p] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
-    rcell[r] = cr;
-    if (cr == kWide) {
-      atomicAdd(&S.cur[n_cells], 1);
-    } else if (cr != kEmpty) {
-      for (int cy = (cr >> 16) & 0xFF; cy <= static_cast<int>(cr >> 24); ++cy)
-        for (int cx = cr & 0xFF; cx <= static_cast<int>((cr >> 8) & 0xFF); ++cx)
-          atomicAdd(&S.cur[cy * gx + cx], 1);
+#pragma unroll
+    for (int u = 0; u < kIdx; ++u) {
+      const int p = p0 + u * kFrameThreads;
+      if (p >= n) continue;
+      const float4 b = bb[u];
+      uint32_t cr;
+      if (S.all_wide || b.x != b.x || b.y != b.y || b.z != b.z || b.w != b.w) {
+        cr = kWide;
+      } else if (b.z < b.x || b.w < b.y) {
+        cr = kEmpty;
+      } else {
+        const int cx0 = cell_of(b.x, S.ex0, S.sx, gx), cx1 = cell_of(b.z, S.ex0, S.sx, gx);
+        const int cy0 = cell_of(b.y, S.ey0, S.sy, gy), cy1 = cell_of(b.w, S.ey0, S.sy, gy);
+        cr = (cx1 - cx0 + 1) * (cy1 - cy0 + 1) > kCellsMax
+                ? kWide
+                : static_cast<uint32_t>(cx0 | cx1 << 8 | cy0 << 16 | cy1 << 24);
+      }
+      P.rcell[lo + p] = cr;
+      P.rstate[lo + p] = cr == kEmpty ? kKept : kUndecided;
+        if (cr == kWide) {
+        atomicAdd(&S.cur[n_cells], 1);
+      } else if (cr != kEmpty) {
+        for (int cy = (cr >> 16) & 0xFF; cy <= static_cast<int>(cr >> 24); ++cy)
+          for (int cx = cr & 0xFF; cx <= static_cast<int>((cr >> 8) & 0xFF); ++cx)
+            atomicAdd(&S.cur[cy * gx + cx], 1);
+      }
     }
   }
   __syncthreads();
@@ -497,239 +406,300 @@ __device__ __forceinline__ void large_frame(const MergeParams &P, int lo, int n,
     for (int c = c0; c < c1; ++c) {
       const int k = S.cur[c];
       S.off[c] = at;
-      S.cur[c] = 0;  // from here on: kept detections listed so far
+      S.cnt[c] = k;
+      S.cur[c] = 0;  // from here on: entries filled so far
       at += k;
     }
     if (lane == 63) S.off[n_cells + 1] = incl;
   }
   __syncthreads();
-
-  // 4. The greedy, kChunk candidates per round as for small frames. A kept detection is
-  // appended, box and patch inline, to the lists of the cells its box touches (or to the
-  // wide list) -- each list has room for every detection registered in it -- and to the
-  // kept list; step (1) scans, for each candidate, only the lists that can hold a
-  // suppressor of it, all candidates' entries flattened over the workgroup.
-  // the first chunk's candidates; each round loads the next one's while it works
-  float4 nb = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-  uint32_t ncr = kEmpty;
-  int nroi = 0;
-  if (tid < min(kChunk, n)) {
-    nb = rbox[tid];
-    ncr = rcell[tid];
-    nroi = rroi[tid];
-  }
-  for (int c0 = 0; c0 < n; c0 += kChunk) {
-    const int m = min(kChunk, n - c0);
-    const int K = S.kept;
-    if (tid < m) {
-      const float4 b = nb;
-      const uint32_t cr = ncr;
-      S.cbox[tid] = b;
-      S.croi[tid] = nroi;
-      S.crange[tid] = cr;
-      S.calive[tid] = 1;
-      int ns = 0;
+  // the entries (each listed box, its patch, ranking key and position) and each
+  // detection's lists to search: absolute entry starts and sizes (a wide box: the frame's
+  // first position and its size, searched as positions)
+  for (int p0 = tid; p0 < n; p0 += kIdx * kFrameThreads) {
+    uint32_t cc[kIdx];
+    float4 bb[kIdx];
+    uint64_t kk[kIdx];
+    int rr[kIdx];
+#pragma unroll
+    for (int u = 0; u < kIdx; ++u) {
+      const int p = p0 + u * kFrameThreads;
+      const bool in = p < n;
+      cc[u] = in ? P.rcell[lo + p] : kEmpty;
+      bb[u] = in ? P.rbox[lo + p] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      kk[u] = in ? P.rkey[lo + p] : 0;
+      rr[u] = in ? P.rroi[lo + p] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kIdx; ++u) {
+      const int p = p0 + u * kFrameThreads;
+      if (p >= n) continue;
+      const uint32_t cr = cc[u];
+      const int4 aux = make_int4(rr[u], static_cast<int>(static_cast<uint32_t>(kk[u])),
+                                 static_cast<int>(static_cast<uint32_t>(kk[u] >> 32)), lo + p);
+      int32_t *L = P.rlist + 2 * kLists * static_cast<int64_t>(lo + p);
+      int k = 0;
       if (cr == kWide) {
-        S.sstart[tid][0] = -1;
-        S.slen[tid][0] = K;
-        ns = 1;
+        const int64_t at = ent0 + S.off[n_cells] + atomicAdd(&S.cur[n_cells], 1);
+        P.ebox[at] = bb[u];
+        P.eaux[at] = aux;
+        L[0] = lo;
+        L[kLists] = n;
+        k = 1;
       } else if (cr != kEmpty) {
         for (int cy = (cr >> 16) & 0xFF; cy <= static_cast<int>(cr >> 24); ++cy)
-          for (int cx = cr & 0xFF; cx <= static_cast<int>((cr >> 8) & 0xFF); ++cx, ++ns) {
-            S.sstart[tid][ns] = S.off[cy * gx + cx];
-            S.slen[tid][ns] = S.cur[cy * gx + cx];
+          for (int cx = cr & 0xFF; cx <= static_cast<int>((cr >> 8) & 0xFF); ++cx, ++k) {
+            const int c = cy * gx + cx;
+            const int64_t at = ent0 + S.off[c] + atomicAdd(&S.cur[c], 1);
+            P.ebox[at] = bb[u];
+            P.eaux[at] = aux;
+            L[k] = static_cast<int32_t>(ent0) + S.off[c];
+            L[kLists + k] = S.cnt[c];
           }
-        S.sstart[tid][ns] = S.off[n_cells];
-        S.slen[tid][ns] = S.cur[n_cells];
-        ++ns;
+        L[k] = static_cast<int32_t>(ent0) + S.off[n_cells];
+        L[kLists + k] = S.cnt[n_cells];
+        ++k;
       }
-      for (; ns <= kCellsMax; ++ns) S.slen[tid][ns] = 0;
-    }
-    if (tid < 2 * kChunk) S.bits[tid] = 0;
-    __syncthreads();
-    if (tid < min(kChunk, n - c0 - kChunk)) {  // next round's candidates
-      nb = rbox[c0 + kChunk + tid];
-      ncr = rcell[c0 + kChunk + tid];
-      nroi = rroi[c0 + kChunk + tid];
-    }
-    // (1) 16 threads per candidate over its lists, up to 8 entries each per pass with the
-    // loads issued together
-    {
-      constexpr int kSub = kFrameThreads / kChunk, kBatch = 8;
-      const int q = tid / kSub, sub = tid % kSub;
-      if (q < m) {
-        int st[kCellsMax + 1], ln[kCellsMax + 1], tq = 0;
-#pragma unroll
-        for (int k = 0; k <= kCellsMax; ++k) {
-          st[k] = S.sstart[q][k];
-          ln[k] = S.slen[q][k];
-          tq += ln[k];
-        }
-        const float4 bq = S.cbox[q];
-        const int rq = S.croi[q];
-        bool dead = false;
-        for (int t0 = sub; t0 < tq; t0 += kSub * kBatch) {
-          float4 kb[kBatch];
-          int kr[kBatch];
-#pragma unroll
-          for (int u = 0; u < kBatch; ++u) {
-            int j = t0 + u * kSub;
-            if (j >= tq) continue;
-            int at = st[0], k = 0;
-#pragma unroll
-            for (int kk = 0; kk < kCellsMax; ++kk)  // which list: step over the earlier ones
-              if (k == kk && j >= ln[kk]) {
-                j -= ln[kk];
-                k = kk + 1;
-                at = st[kk + 1];
-              }
-            kb[u] = at < 0 ? kbox[j] : ebox[at + j];
-            kr[u] = at < 0 ? kroi[j] : eroi[at + j];
-          }
-#pragma unroll
-          for (int u = 0; u < kBatch; ++u)
-            if (t0 + u * kSub < tq && (!P.cross_only || kr[u] != rq) &&
-                suppresses(kb[u], bq, P.thr))
-              dead = true;
-        }
-        if (dead) S.calive[q] = 0;  // every writer stores 0
+      for (; k < kLists; ++k) {
+        L[k] = 0;
+        L[kLists + k] = 0;
       }
     }
-    __syncthreads();
-    chunk_bits(P, S.cbox, S.croi, m, S.bits);
-    __syncthreads();
-    if (tid < 64) {
-      const uint64_t kb = chunk_walk(S.calive, S.bits, m);
-      const bool keep_me = (kb >> lane) & 1;
-      if (lane < m) P.keep[gd[c0 + lane]] = keep_me ? 1 : 0;
-      if (keep_me) {
-        const float4 b = S.cbox[lane];
-        const int roi = S.croi[lane];
-        const uint32_t cr = S.crange[lane];
-        const int slot = K + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                                 static_cast<uint32_t>(kb >> 32),
-                                 __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(kb), 0u)));
-        kbox[slot] = b;
-        kroi[slot] = roi;
-        if (cr == kWide) {
-          const int at = S.off[n_cells] + atomicAdd(&S.cur[n_cells], 1);
-          ebox[at] = b;
-          eroi[at] = roi;
-        } else if (cr != kEmpty) {
-          for (int cy = (cr >> 16) & 0xFF; cy <= static_cast<int>(cr >> 24); ++cy)
-            for (int cx = cr & 0xFF; cx <= static_cast<int>((cr >> 8) & 0xFF); ++cx) {
-              const int at = S.off[cy * gx + cx] + atomicAdd(&S.cur[cy * gx + cx], 1);
-              ebox[at] = b;
-              eroi[at] = roi;
-            }
-        }
-      }
-      if (lane == 0) S.kept = K + __popcll(kb);
-    }
-    __syncthreads();
   }
 }
 
-__global__ __launch_bounds__(kFrameThreads) void frame_kernel(const MergeParams P) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
-  __shared__ int s_kept;
-  uint64_t *key = reinterpret_cast<uint64_t *>(lds + kOffKey);
-  int32_t *det = reinterpret_cast<int32_t *>(lds + kOffDet);
-  float4 *box = reinterpret_cast<float4 *>(lds + kOffBox);
-  int32_t *roi = reinterpret_cast<int32_t *>(lds + kOffRoi);
-  float4 *kept_box = reinterpret_cast<float4 *>(lds + kOffKeptBox);
-  int32_t *kept_roi = reinterpret_cast<int32_t *>(lds + kOffKeptRoi);
-  uint32_t *bits = reinterpret_cast<uint32_t *>(lds + kOffBits);  // row a: bits[2a], bits[2a+1]
-  uint8_t *alive = lds + kOffAlive;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int f = blockIdx.x;
-  const int lo = P.frame_begin[f];
-  const int n = P.frame_begin[f + 1] - lo;
-  if (n <= 0) return;
-  if (n > kMaxPerFrame) {
-    large_frame(P, lo, n, lds);
-    return;
+// A detection's lists to search, in registers: starts st[k] and sizes ln[k].
+struct Lists {
+  int st[kLists], ln[kLists], total;
+};
+__device__ __forceinline__ Lists lists_of(const MergeParams &P, int a) {
+  const int32_t *L = P.rlist + 2 * kLists * static_cast<int64_t>(a);
+  Lists l;
+  l.total = 0;
+#pragma unroll
+  for (int k = 0; k < kLists; ++k) {
+    l.st[k] = L[k];
+    l.ln[k] = L[kLists + k];
+    l.total += l.ln[k];
   }
-  int pw = 1;
-  while (pw < n) pw <<= 1;
-  for (int k = tid; k < pw; k += kFrameThreads) {
-    if (k < n) {
-      const int i = P.grouped[lo + k];
-      const int32_t b = P.dets[i].box;
-      const float s = (b >= 0 && b < P.n_scores) ? P.scores[b] : __builtin_nanf("");
-      key[k] = rank_key(s, b);
-      det[k] = i;
+  return l;
+}
+
+// One step of a search: candidates t0, t0 + stride, ... (kBatch of them, below l.total) of
+// a detection's lists, loaded together; returns a mask of those that are suppressors of
+// it (box bp, key kp, patch rp) ranked above it (bit u: candidate t0 + u * stride), and
+// their positions in q.
+__device__ __forceinline__ uint32_t search_step(const MergeParams &P, const Lists &l, bool wide,
+                                                int t0, int stride, float4 bp, uint64_t kp,
+                                                int rp, int q[kBatch]) {
+  float4 bq[kBatch];
+  uint64_t kq[kBatch];
+  int rq[kBatch];
+  uint32_t hits = 0;
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) {
+    int t = t0 + u * stride;
+    q[u] = -1;
+    if (t >= l.total) continue;
+    if (wide) {
+      q[u] = l.st[0] + t;
+      bq[u] = P.rbox[q[u]];
+      kq[u] = P.rkey[q[u]];
+      rq[u] = P.rroi[q[u]];
     } else {
-      key[k] = ~uint64_t(0);  // padding sorts last
-      det[k] = -1;
-    }
-  }
-  if (tid == 0) s_kept = 0;
-  __syncthreads();
-  // Bitonic sort of pw keys, ascending.
-  for (int size = 2; size <= pw; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int t = tid; t < pw / 2; t += kFrameThreads) {
-        const int i = 2 * t - (t & (stride - 1));
-        const int j = i + stride;
-        const bool up = (i & size) == 0;
-        const uint64_t ki = key[i], kj = key[j];
-        if ((ki > kj) == up) {
-          key[i] = kj;
-          key[j] = ki;
-          const int32_t d = det[i];
-          det[i] = det[j];
-          det[j] = d;
+      int at = l.st[0], k = 0;
+#pragma unroll
+      for (int kk = 0; kk < kCellsMax; ++kk)  // which list: step over the earlier ones
+        if (k == kk && t >= l.ln[kk]) {
+          t -= l.ln[kk];
+          k = kk + 1;
+          at = l.st[kk + 1];
         }
-      }
-      __syncthreads();
+      const int4 e = P.eaux[at + t];
+      bq[u] = P.ebox[at + t];
+      kq[u] = static_cast<uint64_t>(static_cast<uint32_t>(e.z)) << 32 | static_cast<uint32_t>(e.y);
+      rq[u] = e.x;
+      q[u] = e.w;
     }
   }
-  for (int k = tid; k < n; k += kFrameThreads) {
-    const tg_det d = P.dets[det[k]];
-    box[k] = make_float4(d.x1, d.y1, d.x2, d.y2);
-    roi[k] = d.roi;
-    alive[k] = 1;
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u)
+    if (q[u] >= 0 && kq[u] < kp && !(P.cross_only && rq[u] == rp) && suppresses(bq[u], bp, P.thr))
+      hits |= 1u << u;
+  return hits;
+}
+
+// The suppressors ranked above each detection: kScanLanes consecutive lanes per detection,
+// detections in frame-group order over the whole grid. The first kPredSlots go in place;
+// a workgroup whose detections have more reserves room for their whole lists in the
+// overflow area (one atomic for all of them) and searches those again to fill it; a
+// list that does not fit is left to be searched in the rounds.
+__global__ __launch_bounds__(kThreads) void search_kernel(const MergeParams P) {
+  static_assert(kSearchDets * kScanLanes == kThreads, "whole detections per workgroup");
+  __shared__ int s_np[kSearchDets], s_fill[kSearchDets], s_at[kSearchDets];
+  const int tid = threadIdx.x, j = tid / kScanLanes, sub = tid % kScanLanes;
+  const int a = blockIdx.x * kSearchDets + j;
+  const bool valid = a < P.frame_begin[P.n_frames] && P.rcell[a] != kEmpty;
+  if (sub == 0) {
+    s_np[j] = 0;
+    s_fill[j] = 0;
   }
   __syncthreads();
-  // Greedy over the ranking, kChunk candidates per round: (1) candidates overlapped by a
-  // detection kept in an earlier round die -- lane l of every wave holds candidate l, the
-  // waves share out the kept list; (2) the chunk's own suppression bits; (3) one wave walks
-  // the chunk in rank order with row a of the bits in lane a. Equal to walking candidate
-  // by candidate.
-  const int wave = tid >> 6;
-  for (int c0 = 0; c0 < n; c0 += kChunk) {
-    const int m = min(kChunk, n - c0);
-    const int K = s_kept;
-    if (lane < m) {
-      const float4 bj = box[c0 + lane];
-      const int rj = roi[c0 + lane];
-      bool dead = false;
-#pragma unroll 4
-      for (int e = wave; e < K; e += kFrameThreads / 64)
-        dead |= (!P.cross_only || kept_roi[e] != rj) && suppresses(kept_box[e], bj, P.thr);
-      if (dead) alive[c0 + lane] = 0;  // every writer stores 0
-    }
-    if (tid < 2 * kChunk) bits[tid] = 0;
-    __syncthreads();
-    chunk_bits(P, box + c0, roi + c0, m, bits);
-    __syncthreads();
-    if (tid < 64) {
-      const uint64_t kb = chunk_walk(alive + c0, bits, m);
-      const bool keep_me = (kb >> lane) & 1;
-      if (keep_me) {
-        const int slot = K + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-                                 static_cast<uint32_t>(kb >> 32),
-                                 __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(kb), 0u)));
-        kept_box[slot] = box[c0 + lane];
-        kept_roi[slot] = roi[c0 + lane];
+  Lists l;
+  float4 bp;
+  uint64_t kp = 0;
+  int rp = 0;
+  bool wide = false;
+  if (valid) {
+    l = lists_of(P, a);
+    bp = P.rbox[a];
+    kp = P.rkey[a];
+    rp = P.rroi[a];
+    wide = P.rcell[a] == kWide;
+    for (int t0 = sub; t0 < l.total; t0 += kScanLanes * kBatch) {
+      int q[kBatch];
+      for (uint32_t h = search_step(P, l, wide, t0, kScanLanes, bp, kp, rp, q); h; h &= h - 1) {
+        const int slot = atomicAdd(&s_np[j], 1);
+        if (slot < kPredSlots) P.rpred[kPredSlots * static_cast<int64_t>(a) + slot] = q[__builtin_ctz(h)];
       }
-      if (lane < m) alive[c0 + lane] = keep_me ? 1 : 0;
-      if (lane == 0) s_kept = K + __popcll(kb);
     }
-    __syncthreads();
   }
-  for (int k = tid; k < n; k += kFrameThreads) P.keep[det[k]] = alive[k];
+  __syncthreads();
+  const int np = s_np[j];
+  if (valid && sub == 0) P.rnpred[a] = np;
+  if (tid == 0) {
+    int64_t need = 0;
+    for (int k = 0; k < kSearchDets; ++k)
+      if (s_np[k] > kPredSlots) need += s_np[k];
+    int64_t at = need > 0 ? static_cast<int64_t>(atomicAdd(P.ovf_used, static_cast<unsigned long long>(need)))
+                          : 0;
+    for (int k = 0; k < kSearchDets; ++k) {
+      s_at[k] = -1;
+      if (s_np[k] <= kPredSlots) continue;
+      if (at + s_np[k] <= P.ovf_cap) s_at[k] = static_cast<int>(at);
+      at += s_np[k];
+    }
+  }
+  __syncthreads();
+  if (!valid || np <= kPredSlots) return;
+  const int at = s_at[j];
+  if (sub == 0) P.rovf[a] = at;
+  if (at < 0) return;
+  for (int t0 = sub; t0 < l.total; t0 += kScanLanes * kBatch) {
+    int q[kBatch];
+    for (uint32_t h = search_step(P, l, wide, t0, kScanLanes, bp, kp, rp, q); h; h &= h - 1)
+      P.ovf[at + atomicAdd(&s_fill[j], 1)] = q[__builtin_ctz(h)];
+  }
+}
+
+// This round's decision for an undecided detection a with more suppressors than its
+// kPredSlots and no room for them in the overflow area (many boxes crowded on one spot):
+// its lists searched again, kBatch candidates at a time -- kSuppressed when one of its
+// suppressors is kept, kUndecided when one is still undecided, else kKept.
+__device__ __forceinline__ int32_t decide_searching(const MergeParams &P, int a) {
+  const Lists l = lists_of(P, a);
+  const bool wide = P.rcell[a] == kWide;
+  const float4 bp = P.rbox[a];
+  const uint64_t kp = P.rkey[a];
+  const int rp = P.rroi[a];
+  bool pending = false;
+  for (int t0 = 0; t0 < l.total; t0 += kBatch) {
+    int q[kBatch];
+    const uint32_t h = search_step(P, l, wide, t0, 1, bp, kp, rp, q);
+    int32_t s[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) s[u] = (h >> u & 1u) ? P.rstate[q[u]] : kSuppressed;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (s[u] == kKept) return kSuppressed;
+      pending |= s[u] == kUndecided;
+    }
+  }
+  return pending ? kUndecided : kKept;
+}
+
+// The rounds of one frame, then its keep flags.
+__global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergeParams P) {
+  const int tid = threadIdx.x;
+  const int lo = P.frame_begin[blockIdx.x];
+  const int n = P.frame_begin[blockIdx.x + 1] - lo;
+  if (n <= 0) return;
+  constexpr int kRes = 4;  // detections per thread and step, their loads issued together
+  for (int round = 0;; ++round) {
+    int pending = 0;
+    for (int a0 = lo + tid; a0 < lo + n; a0 += kRes * kResolveThreads) {
+      int32_t st[kRes], np[kRes];
+#pragma unroll
+      for (int u = 0; u < kRes; ++u) {
+        const int a = a0 + u * kResolveThreads;
+        st[u] = a < lo + n ? P.rstate[a] : kKept;
+        np[u] = st[u] == kUndecided ? P.rnpred[a] : 0;
+      }
+      // the states of their first kFirst suppressors, loaded together; the rest one by one
+      constexpr int kFirst = 4;
+      int32_t ps[kRes][kFirst];
+#pragma unroll
+      for (int u = 0; u < kRes; ++u)
+#pragma unroll
+        for (int k = 0; k < kFirst; ++k)
+          ps[u][k] = st[u] == kUndecided && k < np[u] && np[u] <= kPredSlots
+                         ? P.rstate[P.rpred[kPredSlots * static_cast<int64_t>(a0 + u * kResolveThreads) + k]]
+                         : kSuppressed;
+      uint32_t search = 0;  // detections with more suppressors than their slots
+#pragma unroll
+      for (int u = 0; u < kRes; ++u) {
+        if (st[u] != kUndecided) continue;
+        const int a = a0 + u * kResolveThreads;
+        // the list: in place, in the overflow area, or not kept (search again)
+        const int32_t *list = P.rpred + kPredSlots * static_cast<int64_t>(a);
+        if (np[u] > kPredSlots) {
+          const int at = P.rovf[a];
+          if (at < 0) {
+            search |= 1u << u;
+            continue;
+          }
+          list = P.ovf + at;
+        }
+        bool kept = false, und = false;
+#pragma unroll
+        for (int k = 0; k < kFirst; ++k) {
+          kept |= ps[u][k] == kKept;
+          und |= ps[u][k] == kUndecided;
+        }
+        for (int k0 = np[u] > kPredSlots ? 0 : kFirst; k0 < np[u] && !kept; k0 += kFirst) {
+          int32_t sk[kFirst];
+#pragma unroll
+          for (int k = 0; k < kFirst; ++k)
+            sk[k] = k0 + k < np[u] ? P.rstate[list[k0 + k]] : kSuppressed;
+#pragma unroll
+          for (int k = 0; k < kFirst; ++k) {
+            kept |= sk[k] == kKept;
+            und |= sk[k] == kUndecided;
+          }
+        }
+        if (kept || !und)
+          P.rstate[a] = kept ? kSuppressed : kKept;
+        else
+          pending = 1;
+      }
+      for (; search != 0; search &= search - 1) {
+        const int a = a0 + __builtin_ctz(search) * kResolveThreads;
+        const int32_t d = decide_searching(P, a);
+        if (d != kUndecided)
+          P.rstate[a] = d;
+        else
+          pending = 1;
+      }
+    }
+    __syncthreads();  // this round's decisions are visible to the next
+    if (!__syncthreads_or(pending)) break;
+    if (round >= n) {  // cannot happen (each round decides one); reported, not spun on
+      if (tid == 0) *P.status = 1;
+      break;
+    }
+  }
+  for (int a = lo + tid; a < lo + n; a += kResolveThreads)
+    P.keep[P.grouped[a]] = P.rstate[a] == kKept ? 1 : 0;
 }
 
 __global__ __launch_bounds__(kThreads) void compact_kernel(const MergeParams P) {
@@ -767,7 +737,11 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const MergeParams P) 
     const int prefix = tg_detail::lookback_prefix(P.state, blk, total, &failed);
     if (lane == 0) {
       s_prefix = prefix;
-      if (blk == static_cast<int>(gridDim.x) - 1) *P.n_kept = failed ? TG_E_INTERNAL : prefix + total;
+      if (blk == static_cast<int>(gridDim.x) - 1)
+        *P.n_kept = failed || __hip_atomic_load(P.status, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT) != 0
+                        ? TG_E_INTERNAL
+                        : prefix + total;
     }
   }
   __syncthreads();
@@ -784,27 +758,32 @@ int compact_blocks(int32_t n_max) { return (n_max + kCompactBlock - 1) / kCompac
 // Workspace layout, in bytes from the (16-byte aligned) start.
 struct Layout {
   size_t state, counts, cursor, begin, grouped;
-  size_t big_key, big_det, rbox, rroi, rcell, ebox, eroi, kbox, kroi, total;
+  size_t rkey, rbox, rroi, rcell, rstate, rlist, rpred, rnpred, rovf, ovf, ebox, eaux, total;
 };
 size_t round16(size_t v) { return (v + 15) / 16 * 16; }
 Layout layout(int32_t n_max, int32_t n_frames) {
   Layout L;
   const size_t n = static_cast<size_t>(n_max);
-  L.state = 0;  // ticket word + one look-back word per compaction workgroup
-  L.counts = sizeof(uint64_t) * (1 + static_cast<size_t>(compact_blocks(n_max)));
+  // ticket and status word, the overflow area's cursor, one look-back word per compaction
+  // workgroup
+  L.state = 0;
+  L.counts = sizeof(uint64_t) * (2 + static_cast<size_t>(compact_blocks(n_max)));
   L.cursor = L.counts + sizeof(int32_t) * static_cast<size_t>(n_frames);
   L.begin = L.cursor + sizeof(int32_t) * static_cast<size_t>(n_frames);
   L.grouped = L.begin + sizeof(int32_t) * (static_cast<size_t>(n_frames) + 1);
-  L.big_key = round16(L.grouped + sizeof(int32_t) * n);
-  L.big_det = L.big_key + sizeof(uint64_t) * 2 * n;
-  L.rbox = round16(L.big_det + sizeof(int32_t) * 2 * n);
-  L.rroi = L.rbox + sizeof(float4) * n;
+  L.rbox = round16(L.grouped + sizeof(int32_t) * n);
+  L.rkey = L.rbox + sizeof(float4) * n;
+  L.rroi = L.rkey + sizeof(uint64_t) * n;
   L.rcell = L.rroi + sizeof(int32_t) * n;
-  L.ebox = round16(L.rcell + sizeof(uint32_t) * n);
-  L.eroi = L.ebox + sizeof(float4) * kCellsMax * n;
-  L.kbox = round16(L.eroi + sizeof(int32_t) * kCellsMax * n);
-  L.kroi = L.kbox + sizeof(float4) * n;
-  L.total = L.kroi + sizeof(int32_t) * n;
+  L.rstate = L.rcell + sizeof(uint32_t) * n;
+  L.rlist = L.rstate + sizeof(int32_t) * n;
+  L.rpred = L.rlist + sizeof(int32_t) * 2 * (kCellsMax + 1) * n;
+  L.rnpred = L.rpred + sizeof(int32_t) * kPredSlots * n;
+  L.rovf = L.rnpred + sizeof(int32_t) * n;
+  L.ovf = L.rovf + sizeof(int32_t) * n;
+  L.ebox = round16(L.ovf + sizeof(int32_t) * kOvfPerDet * n);
+  L.eaux = L.ebox + sizeof(float4) * kCellsMax * n;
+  L.total = L.eaux + sizeof(int4) * kCellsMax * n;
   return L;
 }
 
@@ -846,23 +825,29 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   P.out = a->out;
   P.n_kept = a->n_kept;
   P.ticket = reinterpret_cast<uint32_t *>(ws + L.state);
-  P.state = reinterpret_cast<uint64_t *>(ws + L.state) + 1;
+  P.status = reinterpret_cast<uint32_t *>(ws + L.state) + 1;
+  P.ovf_used = reinterpret_cast<unsigned long long *>(ws + L.state) + 1;
+  P.state = reinterpret_cast<uint64_t *>(ws + L.state) + 2;
   P.counts = reinterpret_cast<int32_t *>(ws + L.counts);
   P.cursor = reinterpret_cast<int32_t *>(ws + L.cursor);
   P.frame_begin = reinterpret_cast<int32_t *>(ws + L.begin);
   P.grouped = reinterpret_cast<int32_t *>(ws + L.grouped);
-  P.big_key = reinterpret_cast<uint64_t *>(ws + L.big_key);
-  P.big_det = reinterpret_cast<int32_t *>(ws + L.big_det);
+  P.rkey = reinterpret_cast<uint64_t *>(ws + L.rkey);
   P.rbox = reinterpret_cast<float4 *>(ws + L.rbox);
   P.rroi = reinterpret_cast<int32_t *>(ws + L.rroi);
   P.rcell = reinterpret_cast<uint32_t *>(ws + L.rcell);
+  P.rstate = reinterpret_cast<int32_t *>(ws + L.rstate);
+  P.rlist = reinterpret_cast<int32_t *>(ws + L.rlist);
+  P.rpred = reinterpret_cast<int32_t *>(ws + L.rpred);
+  P.rnpred = reinterpret_cast<int32_t *>(ws + L.rnpred);
+  P.rovf = reinterpret_cast<int32_t *>(ws + L.rovf);
+  P.ovf = reinterpret_cast<int32_t *>(ws + L.ovf);
+  P.ovf_cap = std::min<int64_t>(int64_t(kOvfPerDet) * a->n_max, 0x7FFFFFFF);
   P.ebox = reinterpret_cast<float4 *>(ws + L.ebox);
-  P.eroi = reinterpret_cast<int32_t *>(ws + L.eroi);
-  P.kbox = reinterpret_cast<float4 *>(ws + L.kbox);
-  P.kroi = reinterpret_cast<int32_t *>(ws + L.kroi);
+  P.eaux = reinterpret_cast<int4 *>(ws + L.eaux);
 
   const int32_t words32 = 2 * a->n_frames;  // counts + cursor
-  const int32_t words64 = 1 + compact_blocks(a->n_max);
+  const int32_t words64 = 2 + compact_blocks(a->n_max);
   const int32_t clear_n = words32 > words64 ? words32 : words64;
   const uint32_t per = static_cast<uint32_t>((a->n_max + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(clear_kernel, dim3((clear_n + kThreads - 1) / kThreads), dim3(kThreads), 0,
@@ -870,9 +855,15 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   hipLaunchKernelGGL(count_kernel, dim3(per), dim3(kThreads), 0, s, P);
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, s, P);
   hipLaunchKernelGGL(scatter_kernel, dim3(per), dim3(kThreads), 0, s, P);
-  if (a->n_frames > 0)
-    hipLaunchKernelGGL(frame_kernel, dim3(static_cast<uint32_t>(a->n_frames)), dim3(kFrameThreads), 0,
-                       s, P);
+  if (a->n_frames > 0) {
+    hipLaunchKernelGGL(index_kernel, dim3(static_cast<uint32_t>(a->n_frames)), dim3(kFrameThreads),
+                       0, s, P);
+    hipLaunchKernelGGL(search_kernel,
+                       dim3(static_cast<uint32_t>((a->n_max + kSearchDets - 1) / kSearchDets)),
+                       dim3(kThreads), 0, s, P);
+    hipLaunchKernelGGL(resolve_kernel, dim3(static_cast<uint32_t>(a->n_frames)),
+                       dim3(kResolveThreads), 0, s, P);
+  }
   hipLaunchKernelGGL(compact_kernel, dim3(static_cast<uint32_t>(compact_blocks(a->n_max))),
                      dim3(kThreads), 0, s, P);
   return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;

@@ -90,9 +90,8 @@ def test_after_unstitch_on_device(torch, name):
 
 
 def test_large_frames(torch):
-    """Frames on both sides of the on-chip limit (1024 detections) and far past it: 1024,
-    1025, 2048, 2049, 5000 and 20000 detections in one frame next to a small frame, in
-    crowded and sparse layouts, with and without cross_only."""
+    """Large frames: 1024, 1025, 2048, 2049, 5000 and 20000 detections in one frame next
+    to a small frame, in crowded and sparse layouts, with and without cross_only."""
     rng = np.random.default_rng(9)
     for big, span, thr, cross in [(1024, 400.0, 0.5, True), (1025, 400.0, 0.5, True),
                                   (1025, 100.0, 0.3, False), (2048, 600.0, 0.5, True),
@@ -106,8 +105,11 @@ def test_large_frames(torch):
 
 def test_large_frames_special_boxes(torch):
     """A 3000-detection frame with the cases the cell index treats apart: boxes with
-    infinite corners, inverted boxes, boxes wider than the frame, duplicates of one box,
-    and a negative threshold (every pair suppresses)."""
+    infinite corners, inverted boxes, boxes wider than the frame, duplicates of one box
+    (up to 239 suppressors each: their whole lists go to the overflow area), and a
+    negative threshold (every pair suppresses: the lists need about 4.5 M entries, far
+    past the overflow area's 48,000, so most detections search their lists again in
+    the rounds)."""
     rng = np.random.default_rng(19)
     dets, scores = random_dets(rng, 3000, 1, 12, span=800.0)
     k = rng.permutation(3000)
@@ -124,7 +126,7 @@ def test_large_frames_special_boxes(torch):
 
 
 def test_frames_around_the_matrix_limit(torch):
-    """Frames of 437 and 439 detections (the bit matrix fits), 448 and 513 (it does not)."""
+    """Frames of 437, 439, 448 and 513 detections side by side."""
     rng = np.random.default_rng(12)
     sizes = [437, 439, 448, 513]
     dets, scores = random_dets(rng, sum(sizes), len(sizes), 8, span=400.0)
