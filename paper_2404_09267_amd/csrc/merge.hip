@@ -231,8 +231,9 @@ __device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
 // searching the whole frame. Boxes with x2 < x1 or y2 < y1 have no positive width with
 // anything, so when t >= 0 they neither suppress nor are suppressed: kept from the start
 // and listed nowhere.
-constexpr int kFrameThreads = 1024;  // index: one workgroup per frame
-constexpr int kResolveThreads = 512; // resolve: one workgroup per frame
+// index and resolve: one workgroup per frame, of 1024 threads (index) and 512 (resolve),
+// or of kSmallFrame when the frames average at most kSmallFrame detections
+constexpr int kSmallFrame = 256;
 constexpr int kGridMax = 32;         // cells per axis
 constexpr int kCellsMax = 4;         // cells a box may touch before it goes on the wide list
 constexpr int kLists = kCellsMax + 1;
@@ -268,14 +269,15 @@ __device__ __forceinline__ int cell_of(float v, float e0, float sc, int g) {
 struct FrameLds {
   float ex0, sx, ey0, sy;
   int gx, gy, all_wide;
-  float red[4][kFrameThreads / 64];
-  float sum[2][kFrameThreads / 64];
+  float red[4][1024 / 64];
+  float sum[2][1024 / 64];
   int off[kGridMax * kGridMax + 2];  // list starts (cells, then the wide list), then the end
   int cur[kGridMax * kGridMax + 1];  // list sizes while counting, then while filling
   int cnt[kGridMax * kGridMax + 1];  // list sizes
 };
 constexpr int kIdx = 4;  // detections per thread and step of the index, loads issued together
 
+template <int kFrameThreads>
 __global__ __launch_bounds__(kFrameThreads) void index_kernel(const MergeParams P) {
   __shared__ FrameLds S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -619,6 +621,7 @@ __device__ __forceinline__ int32_t decide_searching(const MergeParams &P, int a)
 }
 
 // The rounds of one frame, then its keep flags.
+template <int kResolveThreads>
 __global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergeParams P) {
   const int tid = threadIdx.x;
   const int lo = P.frame_begin[blockIdx.x];
@@ -856,13 +859,19 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, s, P);
   hipLaunchKernelGGL(scatter_kernel, dim3(per), dim3(kThreads), 0, s, P);
   if (a->n_frames > 0) {
-    hipLaunchKernelGGL(index_kernel, dim3(static_cast<uint32_t>(a->n_frames)), dim3(kFrameThreads),
-                       0, s, P);
+    const bool small = a->n_max <= int64_t(kSmallFrame) * a->n_frames;
+    const dim3 frames(static_cast<uint32_t>(a->n_frames));
+    if (small)
+      hipLaunchKernelGGL(index_kernel<kSmallFrame>, frames, dim3(kSmallFrame), 0, s, P);
+    else
+      hipLaunchKernelGGL(index_kernel<1024>, frames, dim3(1024), 0, s, P);
     hipLaunchKernelGGL(search_kernel,
                        dim3(static_cast<uint32_t>((a->n_max + kSearchDets - 1) / kSearchDets)),
                        dim3(kThreads), 0, s, P);
-    hipLaunchKernelGGL(resolve_kernel, dim3(static_cast<uint32_t>(a->n_frames)),
-                       dim3(kResolveThreads), 0, s, P);
+    if (small)
+      hipLaunchKernelGGL(resolve_kernel<kSmallFrame>, frames, dim3(kSmallFrame), 0, s, P);
+    else
+      hipLaunchKernelGGL(resolve_kernel<512>, frames, dim3(512), 0, s, P);
   }
   hipLaunchKernelGGL(compact_kernel, dim3(static_cast<uint32_t>(compact_blocks(a->n_max))),
                      dim3(kThreads), 0, s, P);
