@@ -286,7 +286,7 @@ def merge_cost(tg, W, torch, uargs, ubufs, name, n_frames, with_oracle: bool,
     out = {"input": f"tg_unstitch output of {name} ({n_dets} detections, {n_frames} frames, "
                     f"up to {int(per_frame.max())} per frame), IoU 0.5 across patches",
            "kept": int(mb.n_kept.item()), "us_per_call": round(us, 2),
-           "bound": "latency: 6 launches, one workgroup per frame"}
+           "bound": "latency: 8 launches (frame index and suppression rounds), about 0.3 KB per detection"}
     if with_oracle:
         from oracle import merge
 
@@ -494,7 +494,7 @@ def main():
     boxes_d = torch.from_numpy(boxes).to(dev)
     canv_d = torch.from_numpy(canv).to(dev)
     out = torch.empty((J, 3, wl.canvas, wl.canvas), dtype=torch.float16, device=dev)
-    ubufs = tg.UnstitchBuffers(n_boxes)
+    ubufs = tg.UnstitchBuffers(n_boxes, n_rois)
     batches = [tg.batch_range(J, wl.batch_cap, k) for k in range(tg.batch_count(J, wl.batch_cap))]
 
     # device plan arrays, refreshed every step from double-buffered pinned staging

@@ -327,14 +327,19 @@ typedef struct {
   int32_t *roi_of_box;        /* device out [n_boxes]: RoI id or -1 */
   tg_det *dets;               /* device out [n_boxes]: kept boxes, first *n_out valid */
   int32_t *n_out;             /* device out, one int32 */
-  void *workspace;            /* device scratch, >= tg_unstitch_workspace_bytes(n_boxes) */
+  void *workspace;            /* device scratch, 16-byte aligned,
+                                 >= tg_unstitch_workspace_bytes(n_boxes, n_rois) */
   size_t workspace_bytes;
   int32_t rule;               /* 0: the patch holding the box centre (default);
                                  1: the patch the box overlaps most, see tg_unstitch */
 } tg_unstitch_args;
 
-/* Device scratch tg_unstitch needs for n_boxes boxes (0 when n_boxes <= 0). */
-size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
+/*
+ * Device scratch tg_unstitch needs for n_boxes boxes over a plan of n_rois RoIs (0 when
+ * n_boxes <= 0): the compaction's look-back words (8 bytes per 1024 boxes and one more,
+ * rounded up to 16) and 24 bytes of patch record per RoI.
+ */
+size_t tg_unstitch_workspace_bytes(int32_t n_boxes, int32_t n_rois);
 
 /*
  * Unstitch: box b with canvas c = box_canvas[b]; its centre is
@@ -355,20 +360,23 @@ size_t tg_unstitch_workspace_bytes(int32_t n_boxes);
  * box with a NaN coordinate or no overlap is dropped (Alg. 1 assigns RoIs to zones by
  * largest overlap in the same way, Sec. III-A).
  * Returns TG_E_INVAL on null pointers (unless n_boxes == 0, which only writes
- * *n_out = 0) or n_boxes < 0, TG_E_WORKSPACE when the workspace is too small,
- * TG_E_HIP on launch failure, TG_E_INVAL for a rule other than 0 or 1.
+ * *n_out = 0) or n_boxes < 0, TG_E_WORKSPACE when the workspace is too small or not
+ * 16-byte aligned, TG_E_HIP on launch failure, TG_E_INVAL for a rule other than 0 or 1.
  * *n_out = TG_E_INTERNAL reports a device-side failure of the compaction.
  */
 int tg_unstitch(const tg_unstitch_args *args, void *stream);
 
 /* Largest n_boxes tg_unstitch_noalloc accepts. */
 #define TG_UNSTITCH_NOALLOC_MAX_BOXES (1 << 24)
+/* Largest plan (n_rois) for which tg_unstitch_noalloc keeps patch records in its
+ * scratch array; larger plans are read without them, with the same results. */
+#define TG_UNSTITCH_NOALLOC_MAX_ROIS (1 << 17)
 
 /*
  * tg_unstitch for callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the same operation and
  * results as tg_unstitch, but a->workspace and a->workspace_bytes are ignored. Instead the
- * call uses a scratch array the library holds in device memory, one per GPU: 131 KB that
+ * call uses a scratch array the library holds in device memory, one per GPU: 3.3 MB that
  * each GPU the library runs on keeps until the process ends. The first call on a device
  * looks the array up (hipGetSymbolAddress); no call allocates or frees memory. The kernels
  * clear what they need themselves, so the array's contents from the previous call do not

@@ -139,4 +139,4 @@ extern "C" int32_t tg_stitch_units(int32_t canvas_w, int32_t canvas_h, int32_t c
   return g.n_units;
 }
 
-extern "C" int32_t tg_abi_version(void) { return 7; }
+extern "C" int32_t tg_abi_version(void) { return 8; }

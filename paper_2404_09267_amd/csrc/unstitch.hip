@@ -6,12 +6,18 @@
 // right and bottom edges); it is optionally clipped to that patch and shifted by the
 // patch's frame offset minus its canvas offset.
 //
-// Two launches on the caller's stream:
+// Launches on the caller's stream:
+//  0. pack (calls whose boxes test many patches in all): one 24-byte patch record per
+//     plan position -- the placed rectangle of RoI order[k] in binary32, its canvas and
+//     its id -- so that the assign reads a canvas's patches as consecutive records
+//     instead of gathering placements and RoIs by id. Those gathers (two cache lines per
+//     patch and box) bound the assign by the L2's request rate when many boxes meet
+//     canvases of many patches.
 //  1. assign: LPB lanes per box test the box canvas's patches LPB at a time; a wave
 //     ballot picks the (unique) patch containing the centre and roi_of_box[b] is
 //     written. With the overlap rule each lane scores its patch's overlap area and the
-//     lanes of the box take the largest (ties: lower RoI id) with xor shuffles. The same
-//     launch clears the look-back state of launch 2.
+//     lanes of the box take the largest (ties: lower RoI id) with xor shuffles. The first
+//     launch also clears the look-back state of the emit launch.
 //  2. emit: four consecutive boxes per thread, 1024 per workgroup. Kept boxes are
 //     ranked inside the workgroup with a wave prefix sum of per-thread counts, the
 //     workgroup's offset comes from a single-pass decoupled look-back over earlier
@@ -20,6 +26,7 @@
 //     box index -- a stable compaction whose output does not depend on scheduling.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstdint>
 
@@ -35,6 +42,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kBoxesPerThread = 4;                  // emit: consecutive boxes per thread
 constexpr int kEmitBoxes = kThreads * kBoxesPerThread;
+// Calls whose boxes test at least this many patches in all read the plan through patch
+// records (one pack launch more); smaller ones gather it directly.
+constexpr int64_t kRecordsMinTests = int64_t(1) << 21;
 
 struct UnstitchParams {
   const tg_box *boxes;
@@ -51,12 +61,57 @@ struct UnstitchParams {
   uint32_t *ticket;
   uint64_t *state;  // one word per emit workgroup
   int32_t n_state_words;  // ticket word + state words, in uint64 units
+  float4 *rect;  // patch records (null: the assign gathers the plan directly) ...
+  int2 *meta;    // ... and their (canvas, RoI id)
 };
 
-template <int LPB>
+// Patch records, one per plan position k: the placed rectangle of RoI order[k] as
+// binary32 (dx, dy, dx + w, dy + h) and (its canvas, its id); an id out of range gets
+// canvas -1, which no box names. Also clears the look-back state of the emit launch.
+__global__ __launch_bounds__(kThreads) void pack_kernel(const UnstitchParams P) {
+  const int64_t k = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+  if (k < P.n_state_words) reinterpret_cast<uint64_t *>(P.ticket)[k] = 0;
+  if (k >= P.n_rois) return;
+  const int id = P.order[k];
+  float4 r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  int canvas = -1;
+  if (id >= 0 && id < P.n_rois) {
+    const tg_place pl = P.place[id];
+    const tg_roi ro = P.rois[id];
+    r = make_float4(float(pl.x), float(pl.y), float(pl.x + ro.w), float(pl.y + ro.h));
+    canvas = pl.canvas;
+  }
+  P.rect[k] = r;
+  P.meta[k] = make_int2(canvas, id);
+}
+
+// The patch at plan position k as the assign tests it: its placed rectangle, its canvas
+// (-1 when order[k] is not a RoI id) and order[k] -- from the records or from the plan.
+template <bool kRecords>
+__device__ __forceinline__ void patch_at(const UnstitchParams &P, int k, float4 &r, int &canvas,
+                                         int &id) {
+  if (kRecords) {
+    r = P.rect[k];
+    const int2 m = P.meta[k];
+    canvas = m.x;
+    id = m.y;
+    return;
+  }
+  id = P.order[k];
+  r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  canvas = -1;
+  if (id >= 0 && id < P.n_rois) {
+    const tg_place pl = P.place[id];
+    const tg_roi ro = P.rois[id];
+    r = make_float4(float(pl.x), float(pl.y), float(pl.x + ro.w), float(pl.y + ro.h));
+    canvas = pl.canvas;
+  }
+}
+
+template <int LPB, bool kRecords>
 __global__ __launch_bounds__(kThreads) void assign_kernel(const UnstitchParams P) {
   const int gtid = blockIdx.x * kThreads + threadIdx.x;
-  if (gtid < P.n_state_words) reinterpret_cast<uint64_t *>(P.ticket)[gtid] = 0;
+  if (!kRecords && gtid < P.n_state_words) reinterpret_cast<uint64_t *>(P.ticket)[gtid] = 0;
 
   constexpr int kBoxesPerBlock = kThreads / LPB;
   const int lane = threadIdx.x & 63;
@@ -89,17 +144,13 @@ __global__ __launch_bounds__(kThreads) void assign_kernel(const UnstitchParams P
       float a = 0.0f;
       int id = -1;
       if (k < k_hi) {
-        id = P.order[k];
-        if (id >= 0 && id < P.n_rois) {
-          const tg_place pl = P.place[id];
-          const tg_roi r = P.rois[id];
-          if (pl.canvas == c) {
-            const float ow = fmaxf(0.0f, __fsub_rn(fminf(box.x2, float(pl.x + r.w)),
-                                                   fmaxf(box.x1, float(pl.x))));
-            const float oh = fmaxf(0.0f, __fsub_rn(fminf(box.y2, float(pl.y + r.h)),
-                                                   fmaxf(box.y1, float(pl.y))));
-            a = __fmul_rn(ow, oh);
-          }
+        float4 r;
+        int pc;
+        patch_at<kRecords>(P, k, r, pc, id);
+        if (pc == c) {
+          const float ow = fmaxf(0.0f, __fsub_rn(fminf(box.x2, r.z), fmaxf(box.x1, r.x)));
+          const float oh = fmaxf(0.0f, __fsub_rn(fminf(box.y2, r.w), fmaxf(box.y1, r.y)));
+          a = __fmul_rn(ow, oh);
         }
       }
 #pragma unroll
@@ -124,13 +175,10 @@ __global__ __launch_bounds__(kThreads) void assign_kernel(const UnstitchParams P
     bool hit = false;
     int id = -1;
     if (k < k_hi) {
-      id = P.order[k];
-      if (id >= 0 && id < P.n_rois) {
-        const tg_place pl = P.place[id];
-        const tg_roi r = P.rois[id];
-        hit = pl.canvas == c && float(pl.x) <= cx && cx < float(pl.x + r.w) &&
-              float(pl.y) <= cy && cy < float(pl.y + r.h);
-      }
+      float4 r;
+      int pc;
+      patch_at<kRecords>(P, k, r, pc, id);
+      hit = pc == c && r.x <= cx && cx < r.z && r.y <= cy && cy < r.w;
     }
     const uint64_t m = (__ballot(hit) >> seg_shift) & seg_mask;
     if (m) {
@@ -223,12 +271,26 @@ __global__ void zero_count_kernel(int32_t *n_out) { *n_out = 0; }
 
 int emit_blocks(int32_t n) { return (n + kEmitBoxes - 1) / kEmitBoxes; }
 
-// Workspace of the allocation-free entry point: the ticket word and one look-back word
-// per emit workgroup for up to TG_UNSTITCH_NOALLOC_MAX_BOXES boxes (131 KB). Each GPU the
-// library runs on holds its own copy until the process ends; host code reaches it only
-// through the address hipGetSymbolAddress returns for the current device.
-constexpr int kScratchWords = 1 + (TG_UNSTITCH_NOALLOC_MAX_BOXES + kEmitBoxes - 1) / kEmitBoxes;
-__device__ __align__(256) uint64_t scratch[kScratchWords];
+// Bytes of the ticket and look-back words for n boxes, rounded up to 16 so that the
+// patch records after them are aligned.
+size_t lookback_bytes(int32_t n) {
+  return (sizeof(uint64_t) * (1 + static_cast<size_t>(emit_blocks(n))) + 15) & ~size_t(15);
+}
+
+// Bytes of the patch records of a plan of n_rois RoIs: a float4 and an int2 each.
+size_t record_bytes(int32_t n_rois) {
+  return n_rois > 0 ? 24 * static_cast<size_t>(n_rois) : 0;
+}
+
+// Workspace of the allocation-free entry point: the ticket and look-back words for up
+// to TG_UNSTITCH_NOALLOC_MAX_BOXES boxes, then patch records for plans of up to
+// TG_UNSTITCH_NOALLOC_MAX_ROIS RoIs (3.3 MB in all). Each GPU the library runs on holds
+// its own copy until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchLookback =
+    (8 * (1 + size_t(TG_UNSTITCH_NOALLOC_MAX_BOXES + kEmitBoxes - 1) / kEmitBoxes) + 15) & ~size_t(15);
+constexpr size_t kScratchBytes = kScratchLookback + 24 * size_t(TG_UNSTITCH_NOALLOC_MAX_ROIS);
+__device__ __align__(256) uint64_t scratch[kScratchBytes / 8];
 
 // Device address of `scratch` on the current device, looked up once per device id (null
 // when the lookup fails).
@@ -255,9 +317,22 @@ int check_args(const tg_unstitch_args *a) {
   return TG_OK;
 }
 
-// Enqueues both launches with `ws` (device, 8-byte aligned, tg_unstitch_workspace_bytes
-// bytes) as the ticket and look-back words; the assign launch clears them first.
-int launch(const tg_unstitch_args *a, void *ws, hipStream_t s) {
+template <bool kRecords>
+void launch_assign(int lpb, int32_t n_boxes, hipStream_t s, const UnstitchParams &P) {
+  const int64_t per_block = kThreads / lpb;
+  const dim3 grid(static_cast<uint32_t>((int64_t(n_boxes) + per_block - 1) / per_block));
+  if (lpb == 16)
+    hipLaunchKernelGGL((assign_kernel<16, kRecords>), grid, dim3(kThreads), 0, s, P);
+  else if (lpb == 32)
+    hipLaunchKernelGGL((assign_kernel<32, kRecords>), grid, dim3(kThreads), 0, s, P);
+  else
+    hipLaunchKernelGGL((assign_kernel<64, kRecords>), grid, dim3(kThreads), 0, s, P);
+}
+
+// Enqueues the launches with `words` (device, 8-byte aligned, lookback_bytes(n_boxes)
+// bytes) as the ticket and look-back words -- cleared by the first launch -- and
+// `records` (16-byte aligned, record_bytes(n_rois) bytes, or null) for the patch records.
+int launch(const tg_unstitch_args *a, void *words, void *records, hipStream_t s) {
   if (a->n_boxes == 0) {
     hipLaunchKernelGGL(zero_count_kernel, dim3(1), dim3(1), 0, s, a->n_out);
     return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
@@ -277,26 +352,28 @@ int launch(const tg_unstitch_args *a, void *ws, hipStream_t s) {
   P.roi_of_box = a->roi_of_box;
   P.dets = a->dets;
   P.n_out = a->n_out;
-  P.ticket = static_cast<uint32_t *>(ws);
-  P.state = static_cast<uint64_t *>(ws) + 1;
+  P.ticket = static_cast<uint32_t *>(words);
+  P.state = static_cast<uint64_t *>(words) + 1;
   P.n_state_words = 1 + emit_blocks(a->n_boxes);
-
   // Lanes per box: about the mean number of patches per canvas, so one ballot round
   // usually settles a box.
   const int64_t per_canvas = a->n_canvases > 0 ? (int64_t(a->n_rois) + a->n_canvases - 1) /
                                                      a->n_canvases
                                                : 1;
   const int lpb = per_canvas <= 16 ? 16 : per_canvas <= 32 ? 32 : 64;
-  const int64_t boxes_per_block = kThreads / lpb;
-  const int64_t assign_blocks = (int64_t(a->n_boxes) + boxes_per_block - 1) / boxes_per_block;
-  if (assign_blocks > 0x7FFFFFFF) return TG_E_INVAL;
-  const dim3 g1(static_cast<uint32_t>(assign_blocks));
-  if (lpb == 16)
-    hipLaunchKernelGGL(assign_kernel<16>, g1, dim3(kThreads), 0, s, P);
-  else if (lpb == 32)
-    hipLaunchKernelGGL(assign_kernel<32>, g1, dim3(kThreads), 0, s, P);
-  else
-    hipLaunchKernelGGL(assign_kernel<64>, g1, dim3(kThreads), 0, s, P);
+  // Patch records when the boxes test many patches in all (about n_boxes * per_canvas).
+  const bool use_records = records && a->n_rois > 0 &&
+                           int64_t(a->n_boxes) * per_canvas >= kRecordsMinTests;
+  P.rect = use_records ? static_cast<float4 *>(records) : nullptr;
+  P.meta = use_records ? reinterpret_cast<int2 *>(P.rect + a->n_rois) : nullptr;
+  if (use_records) {
+    const int64_t pack_threads = std::max<int64_t>(a->n_rois, P.n_state_words);
+    hipLaunchKernelGGL(pack_kernel, dim3(static_cast<uint32_t>((pack_threads + kThreads - 1) / kThreads)),
+                       dim3(kThreads), 0, s, P);
+    launch_assign<true>(lpb, a->n_boxes, s, P);
+  } else {
+    launch_assign<false>(lpb, a->n_boxes, s, P);
+  }
   if (hipGetLastError() != hipSuccess) return TG_E_HIP;
   hipLaunchKernelGGL(emit_kernel, dim3(static_cast<uint32_t>(emit_blocks(a->n_boxes))),
                      dim3(kThreads), 0, s, P);
@@ -305,28 +382,31 @@ int launch(const tg_unstitch_args *a, void *ws, hipStream_t s) {
 
 }  // namespace
 
-extern "C" size_t tg_unstitch_workspace_bytes(int32_t n_boxes) {
+extern "C" size_t tg_unstitch_workspace_bytes(int32_t n_boxes, int32_t n_rois) {
   if (n_boxes <= 0) return 0;
-  return sizeof(uint64_t) * (1 + static_cast<size_t>(emit_blocks(n_boxes)));
+  return lookback_bytes(n_boxes) + record_bytes(n_rois);
 }
 
 extern "C" int tg_unstitch(const tg_unstitch_args *a, void *stream) {
   const int rc = check_args(a);
   if (rc != TG_OK) return rc;
-  if (a->n_boxes > 0) {
-    const size_t need = tg_unstitch_workspace_bytes(a->n_boxes);
-    if (!a->workspace || a->workspace_bytes < need ||
-        reinterpret_cast<uintptr_t>(a->workspace) % 8 != 0)
-      return TG_E_WORKSPACE;
-  }
-  return launch(a, a->workspace, static_cast<hipStream_t>(stream));
+  if (a->n_boxes == 0) return launch(a, nullptr, nullptr, static_cast<hipStream_t>(stream));
+  const size_t need = tg_unstitch_workspace_bytes(a->n_boxes, a->n_rois);
+  if (!a->workspace || a->workspace_bytes < need ||
+      reinterpret_cast<uintptr_t>(a->workspace) % 16 != 0)
+    return TG_E_WORKSPACE;
+  char *ws = static_cast<char *>(a->workspace);
+  return launch(a, ws, ws + lookback_bytes(a->n_boxes), static_cast<hipStream_t>(stream));
 }
 
 extern "C" int tg_unstitch_noalloc(const tg_unstitch_args *a, void *stream) {
   const int rc = check_args(a);
   if (rc != TG_OK) return rc;
   if (a->n_boxes > TG_UNSTITCH_NOALLOC_MAX_BOXES) return TG_E_WORKSPACE;
-  void *ws = a->n_boxes > 0 ? scratch_address() : nullptr;
-  if (a->n_boxes > 0 && !ws) return TG_E_HIP;
-  return launch(a, ws, static_cast<hipStream_t>(stream));
+  if (a->n_boxes == 0) return launch(a, nullptr, nullptr, static_cast<hipStream_t>(stream));
+  char *ws = static_cast<char *>(scratch_address());
+  if (!ws) return TG_E_HIP;
+  // plans larger than the records area are gathered directly (same results)
+  void *records = a->n_rois <= TG_UNSTITCH_NOALLOC_MAX_ROIS ? ws + kScratchLookback : nullptr;
+  return launch(a, ws, records, static_cast<hipStream_t>(stream));
 }

@@ -152,7 +152,7 @@ def lib() -> ctypes.CDLL:
         L.tg_stitch_norm_uses_table.restype = _i32
         L.tg_stitch_units.argtypes = [_i32, _i32, _i32]
         L.tg_stitch_units.restype = _i32
-        L.tg_unstitch_workspace_bytes.argtypes = [_i32]
+        L.tg_unstitch_workspace_bytes.argtypes = [_i32, _i32]
         L.tg_unstitch_workspace_bytes.restype = ctypes.c_size_t
         L.tg_unstitch.argtypes = [ctypes.POINTER(UnstitchArgs), _vp]
         L.tg_unstitch.restype = ctypes.c_int
@@ -400,8 +400,8 @@ def stitch_raw(args: StitchArgs, stream=None) -> int:
     return int(lib().tg_stitch(ctypes.byref(args), _stream_handle(stream)))
 
 
-def unstitch_workspace_bytes(n_boxes: int) -> int:
-    return int(lib().tg_unstitch_workspace_bytes(n_boxes))
+def unstitch_workspace_bytes(n_boxes: int, n_rois: int) -> int:
+    return int(lib().tg_unstitch_workspace_bytes(n_boxes, n_rois))
 
 
 class PartitionBuffers:
@@ -451,17 +451,18 @@ def partition(boxes, frame_begin, frame_w, frame_h, zones_x, zones_y, bufs: Part
 
 
 class UnstitchBuffers:
-    """Caller-owned device outputs and scratch for tg_unstitch."""
+    """Caller-owned device outputs and scratch for tg_unstitch of n_boxes boxes over a plan
+    of n_rois RoIs."""
 
-    def __init__(self, n_boxes: int, device="cuda"):
+    def __init__(self, n_boxes: int, n_rois: int, device="cuda"):
         import torch
 
-        self.n_boxes = n_boxes
+        self.n_boxes, self.n_rois = n_boxes, n_rois
         self.roi_of_box = torch.empty(n_boxes, dtype=torch.int32, device=device)
         self.dets = torch.empty((n_boxes, DET_WORDS), dtype=torch.int32, device=device)
         self.n_out = torch.empty(1, dtype=torch.int32, device=device)
-        ws = unstitch_workspace_bytes(n_boxes)
-        self.workspace = torch.empty(max(ws, 8), dtype=torch.uint8, device=device)
+        ws = unstitch_workspace_bytes(n_boxes, n_rois)
+        self.workspace = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
         self.workspace_bytes = ws
 
     def dets_numpy(self) -> np.ndarray:
@@ -477,6 +478,8 @@ def unstitch_args(boxes, box_canvas, dplan: DevicePlan, clip, bufs: UnstitchBuff
     n = bufs.n_boxes
     _check(boxes, torch.float32, (n, 4), "boxes")
     _check(box_canvas, torch.int32, (n,), "box_canvas")
+    if bufs.n_rois < dplan.n_rois:
+        raise ValueError(f"UnstitchBuffers sized for {bufs.n_rois} RoIs, the plan has {dplan.n_rois}")
     a = UnstitchArgs()
     a.boxes, a.box_canvas, a.n_boxes = boxes.data_ptr(), box_canvas.data_ptr(), n
     a.rois, a.place = dplan.rois.data_ptr(), dplan.place.data_ptr()
@@ -504,6 +507,7 @@ def unstitch_raw(args: UnstitchArgs, stream=None) -> int:
 
 
 UNSTITCH_NOALLOC_MAX_BOXES = 1 << 24
+UNSTITCH_NOALLOC_MAX_ROIS = 1 << 17
 
 
 def unstitch_noalloc_raw(args: UnstitchArgs, stream=None) -> int:

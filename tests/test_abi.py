@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version():
-    assert tg.lib().tg_abi_version() == 7
+    assert tg.lib().tg_abi_version() == 8
 
 
 def test_strerror():
@@ -67,6 +67,8 @@ int main(void) {
   F(tg_unstitch_args, n_rois); F(tg_unstitch_args, clip); F(tg_unstitch_args, roi_of_box);
   F(tg_unstitch_args, n_out); F(tg_unstitch_args, workspace); F(tg_unstitch_args, workspace_bytes);
   F(tg_unstitch_args, rule);
+  printf("noalloc_max_boxes %d\nnoalloc_max_rois %d\n", TG_UNSTITCH_NOALLOC_MAX_BOXES,
+         TG_UNSTITCH_NOALLOC_MAX_ROIS);
   printf("tg_gmm_params %zu\ntg_gmm_args %zu\ntg_mask_rois_args %zu\n", sizeof(tg_gmm_params),
          sizeof(tg_gmm_args), sizeof(tg_mask_rois_args));
   F(tg_gmm_params, alpha); F(tg_gmm_params, var_threshold_gen); F(tg_gmm_params, var_max);
@@ -95,6 +97,8 @@ def test_struct_layout_matches_header(tmp_path):
     assert c["tg_pack_params"] == ctypes.sizeof(tg.PackParams)
     assert c["tg_stitch_args"] == ctypes.sizeof(tg.StitchArgs)
     assert c["tg_unstitch_args"] == ctypes.sizeof(tg.UnstitchArgs)
+    assert c["noalloc_max_boxes"] == tg.UNSTITCH_NOALLOC_MAX_BOXES
+    assert c["noalloc_max_rois"] == tg.UNSTITCH_NOALLOC_MAX_ROIS
     assert c["tg_slo_patch"] == tg.SLO_PATCH_DTYPE.itemsize == 24
     assert c["tg_slo_params"] == ctypes.sizeof(tg.SloParams)
     assert c["tg_invocation"] == tg.INVOCATION_DTYPE.itemsize == 40
@@ -174,12 +178,17 @@ def test_unstitch_validation_without_gpu():
     a.boxes = a.box_canvas = a.roi_of_box = a.dets = 0x2000
     a.rois = a.place = a.order = a.canvas_begin = 0x3000
     a.n_rois, a.n_canvases = 3, 1
-    a.workspace, a.workspace_bytes = 0x4000, tg.unstitch_workspace_bytes(10) - 1
+    a.workspace, a.workspace_bytes = 0x4000, tg.unstitch_workspace_bytes(10, 3) - 1
     assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.n_rois, a.workspace_bytes = 4, tg.unstitch_workspace_bytes(10, 3)  # records for 3 only
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.n_rois = 3
     a.workspace = None
     a.workspace_bytes = 1 << 20
     assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
     a.workspace = 0x4004  # misaligned
+    assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
+    a.workspace = 0x4008  # 8-byte but not 16-byte aligned (the patch records are float4)
     assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_WORKSPACE
     a.workspace = 0x4000
     a.rois = None
@@ -187,13 +196,17 @@ def test_unstitch_validation_without_gpu():
 
 
 def test_workspace_sizes():
-    assert tg.unstitch_workspace_bytes(0) == 0
-    assert tg.unstitch_workspace_bytes(-5) == 0
-    # one ticket word and one look-back word per 1024 boxes
-    assert tg.unstitch_workspace_bytes(1) == 16
-    assert tg.unstitch_workspace_bytes(1024) == 16
-    assert tg.unstitch_workspace_bytes(1025) == 24
-    assert tg.unstitch_workspace_bytes(200000) == 8 * (1 + 196)
+    assert tg.unstitch_workspace_bytes(0, 100) == 0
+    assert tg.unstitch_workspace_bytes(-5, 100) == 0
+    # one ticket word and one look-back word per 1024 boxes, rounded up to 16 bytes, then
+    # 24 bytes of patch record per RoI
+    assert tg.unstitch_workspace_bytes(1, 0) == 16
+    assert tg.unstitch_workspace_bytes(1024, 0) == 16
+    assert tg.unstitch_workspace_bytes(1025, 0) == 32
+    assert tg.unstitch_workspace_bytes(200000, 0) == 1584  # 8 * (1 + 196), rounded up
+    assert tg.unstitch_workspace_bytes(1, 3) == 16 + 72
+    assert tg.unstitch_workspace_bytes(200000, 115200) == 1584 + 24 * 115200
+    assert tg.unstitch_workspace_bytes(10, -1) == 16
 
 
 def test_gmm_and_mask_rois_validation_without_gpu():

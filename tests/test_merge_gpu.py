@@ -76,7 +76,7 @@ def test_after_unstitch_on_device(torch, name):
     plan = tg.plan_pack(rois, wl.canvas, wl.canvas, wl.frame_w, wl.frame_h, wl.n_frames, 0)
     boxes, canv = W.make_boxes(wl, plan.n_canvases)
     dplan = tg.DevicePlan(rois, plan)
-    ub = tg.UnstitchBuffers(len(boxes))
+    ub = tg.UnstitchBuffers(len(boxes), len(rois))
     tg.unstitch(torch.from_numpy(boxes).cuda(), torch.from_numpy(canv).cuda(), dplan, 1, ub)
     scores = np.random.default_rng(2).uniform(0, 1, len(boxes)).astype(np.float32)
     mb = tg.MergeBuffers(len(boxes), wl.n_frames)

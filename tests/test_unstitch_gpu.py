@@ -25,7 +25,7 @@ def run_unstitch(torch, boxes, box_canvas, rois, plan, clip, dplan=None, rule=0)
     n = boxes.shape[0]
     b_d = torch.from_numpy(np.ascontiguousarray(boxes, np.float32).reshape(n, 4)).cuda()
     c_d = torch.from_numpy(np.ascontiguousarray(box_canvas, np.int32)).cuda()
-    bufs = tg.UnstitchBuffers(n)
+    bufs = tg.UnstitchBuffers(n, dplan.n_rois)
     bufs.roi_of_box.fill_(-7)
     bufs.n_out.fill_(-7)
     tg.unstitch(b_d, c_d, dplan, clip, bufs, rule=rule)
@@ -116,7 +116,7 @@ def test_zero_boxes_and_no_canvases(torch):
     rois = np.array([[0, 0, 0, 4, 4]])
     plan = tg.plan_pack(rois, 8, 8, 8, 8, 1, 0)
     say("zero boxes")
-    bufs = tg.UnstitchBuffers(0)
+    bufs = tg.UnstitchBuffers(0, 1)
     bufs.n_out.fill_(-5)
     dplan = tg.DevicePlan(rois, plan)
     tg.unstitch(torch.empty((0, 4), dtype=torch.float32, device="cuda"),
@@ -163,3 +163,26 @@ def test_workload_boxes_overlap_rule(torch, name):
     boxes, canv = W.make_boxes(wl, plan.n_canvases)
     say("workload overlap rule", name)
     check(torch, boxes, canv, rois, plan, 1, rule=1)
+
+
+def test_patch_records_switch(torch):
+    """The calls on either side of the switch to patch records (at 2^21 box-patch tests,
+    about n_boxes times the mean patches per canvas) agree with the oracle and with each
+    other on their common boxes: the direct gathers and the records give one result."""
+    rng = np.random.default_rng(91)
+    rois = W.random_rois(rng, 9000, 4, 800, 600, 5, 11, 11)
+    plan = tg.plan_pack(rois, 200, 200, 800, 600, 4, tg.SHELF_FFDH)
+    per_canvas = -(-len(rois) // plan.n_canvases)
+    n_switch = -(-(1 << 21) // per_canvas)
+    n = n_switch + 100
+    cx, cy = rng.uniform(-4, 204, n), rng.uniform(-4, 204, n)
+    bw, bh = rng.uniform(0, 20, n), rng.uniform(0, 20, n)
+    boxes = np.stack([cx - bw / 2, cy - bh / 2, cx + bw / 2, cy + bh / 2], 1).astype(np.float32)
+    boxes[:500] = np.round(boxes[:500])
+    canv = rng.integers(-1, plan.n_canvases + 1, n).astype(np.int32)
+    dplan = tg.DevicePlan(rois, plan)
+    for rule in (0, 1):
+        say("records switch", per_canvas, n_switch, "rule", rule)
+        lo = check(torch, boxes[:n_switch - 1], canv[:n_switch - 1], rois, plan, 1, dplan, rule)
+        hi = check(torch, boxes, canv, rois, plan, 1, dplan, rule)
+        np.testing.assert_array_equal(lo[0], hi[0][:n_switch - 1])

@@ -41,7 +41,7 @@ def _case(torch, seed, n_boxes, rule):
 
 
 def _run(torch, dplan, boxes_d, canv_d, rule, noalloc):
-    bufs = tg.UnstitchBuffers(boxes_d.shape[0])
+    bufs = tg.UnstitchBuffers(boxes_d.shape[0], dplan.n_rois)
     bufs.roi_of_box.fill_(-7)
     bufs.dets.fill_(-7)
     bufs.n_out.fill_(-7)
@@ -68,9 +68,32 @@ def test_noalloc_matches_unstitch_twice(torch, rule):
         assert got[1].tobytes() == want[1].tobytes()
 
 
+def test_noalloc_plan_beyond_record_area(torch):
+    """A plan of more RoIs than the scratch array's patch records hold: the allocation-free
+    entry reads it directly and still matches tg_unstitch (which uses records there)."""
+    rng = np.random.default_rng(14)
+    n_rois = tg.UNSTITCH_NOALLOC_MAX_ROIS + 5000
+    rois = W.random_rois(rng, n_rois, 8, 3840, 2160, 4, 12, 12)
+    plan = tg.plan_pack(rois, 640, 640, 3840, 2160, 8, tg.SHELF_FFDH)
+    dplan = tg.DevicePlan(rois, plan)
+    n = 4_000  # about 25 million box-patch tests: records in tg_unstitch
+    cx, cy = rng.uniform(0, 640, n), rng.uniform(0, 640, n)
+    boxes = np.stack([cx - 3, cy - 3, cx + 3, cy + 3], 1).astype(np.float32)
+    canv = rng.integers(0, plan.n_canvases, n).astype(np.int32)
+    boxes_d = torch.from_numpy(boxes).cuda()
+    canv_d = torch.from_numpy(canv).cuda()
+    for rule in (0, 1):
+        say("noalloc large plan", n_rois, plan.n_canvases, rule)
+        want = _run(torch, dplan, boxes_d, canv_d, rule, noalloc=False)
+        got = _run(torch, dplan, boxes_d, canv_d, rule, noalloc=True)
+        np.testing.assert_array_equal(got[0], want[0])
+        assert got[2] == want[2] and got[2] > 0
+        assert got[1].tobytes() == want[1].tobytes()
+
+
 def test_noalloc_limits(torch):
     dplan, boxes_d, canv_d = _case(torch, 13, 10, 0)
-    bufs = tg.UnstitchBuffers(10)
+    bufs = tg.UnstitchBuffers(10, dplan.n_rois)
     a = tg.unstitch_args(boxes_d, canv_d, dplan, 1, bufs, 0)
     a.n_boxes = tg.UNSTITCH_NOALLOC_MAX_BOXES + 1  # refused before anything is enqueued
     assert tg.unstitch_noalloc_raw(a) == tg.E_WORKSPACE
