@@ -172,7 +172,6 @@ size_t tg_partition_workspace_bytes(int32_t n_frames);
  * another frame id are skipped (zone -1). Enqueued on `stream`; the library allocates
  * nothing. Returns TG_E_INVAL (null pointer, negative count, bad sizes, more than 1024
  * zones), TG_E_WORKSPACE, TG_E_HIP. With n_frames == 0 only *n_patches = 0 is written.
- * *n_patches = TG_E_INTERNAL reports a device-side failure of the compaction.
  */
 int tg_partition(const tg_partition_args *args, void *stream);
 

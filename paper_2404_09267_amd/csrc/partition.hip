@@ -9,26 +9,32 @@
 // an overlap tie goes to the lower number; patches are listed frame by frame, zones in
 // row-major order.
 //
-// Two launches on the caller's stream:
-//  1. clear: zeroes the ticket and look-back words of launch 2.
-//  2. zones: one 256-thread workgroup per frame, frames taken in ticket order. Each
-//     thread scores its RoIs against the zones they touch and folds them into the winning
-//     zone's enclosing rectangle with LDS atomic min/max; the workgroup then counts its
-//     non-empty zones (ballot + mbcnt), finds its output offset with a single-pass
-//     decoupled look-back over earlier frames, and writes its patches there.
+// Three launches on the caller's stream, with no atomics outside LDS:
+//  1. count: one 256-thread workgroup per frame scores the frame's RoIs against the zones
+//     they touch, folds each into the winning zone's enclosing rectangle with LDS atomic
+//     min/max, and stores the frame's number of non-empty zones.
+//  2. scan: one workgroup turns the counts into each frame's first output position and
+//     writes the total.
+//  3. write: the per-frame pass of launch 1 again, then the frame's non-empty zones are
+//     written from its first position in zone order (ranks from ballots and mbcnt).
+// Launch 3 recomputes the rectangles instead of keeping them: a frame's RoIs are a few
+// hundred bytes, while keeping its rectangles would take workspace by the zone count.
+// (A single launch that orders frames by an atomic ticket and finds each frame's position
+// with a look-back over the earlier frames pays for the ticket instead: one device-scope
+// atomic on one address per frame, which the hardware serialises.)
 #include <hip/hip_runtime.h>
 
 #include <climits>
 #include <cstdint>
 
-#include "lookback.h"
 #include "tg.h"
 
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kMaxZones = 1024;                     // zones per frame, e.g. 32 x 32
+constexpr int kMaxZones = 1024;  // zones per frame, e.g. 32 x 32
+constexpr int kScanThreads = 1024;
 
 struct PartitionParams {
   const tg_roi *boxes;
@@ -37,8 +43,7 @@ struct PartitionParams {
   tg_roi *patches;
   int32_t *zone_of_box;
   int32_t *n_patches;
-  uint32_t *ticket;
-  uint64_t *state;  // one word per frame
+  int32_t *first;  // [n_frames]: count of non-empty zones, then the frame's first position
 };
 
 // First pixel of zone k of n along an axis of `size` pixels.
@@ -50,20 +55,23 @@ __device__ __forceinline__ int zone_of(int p, int n, int size) {
   return static_cast<int>(((static_cast<int64_t>(p) + 1) * n - 1) / size);
 }
 
-__global__ void clear_kernel(uint64_t *words, int32_t n_words) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n_words) words[i] = 0;
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row broadcasts).
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
 }
 
-__global__ __launch_bounds__(kThreads) void zone_kernel(const PartitionParams P) {
-  __shared__ int acc[kMaxZones][4];  // x0, y0, x1, y1 of each zone's enclosing rectangle
-  __shared__ int s_frame, s_prefix;
-  __shared__ int s_wave[kWaves];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Frame f's zone rectangles in acc (x0, y0, x1, y1; an empty zone keeps x0 = INT_MAX),
+// and with `record` each RoI's zone in zone_of_box. Called by the whole workgroup; ends
+// with a barrier.
+__device__ void fold_frame(const PartitionParams &P, int f, int (*acc)[4], bool record) {
+  const int tid = threadIdx.x;
   const int X = P.zones_x, Y = P.zones_y, Z = X * Y, W = P.frame_w, H = P.frame_h;
-  if (tid == 0)
-    s_frame = static_cast<int>(__hip_atomic_fetch_add(P.ticket, 1u, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT));
   for (int r = tid; r < Z; r += kThreads) {
     acc[r][0] = INT_MAX;
     acc[r][1] = INT_MAX;
@@ -71,7 +79,6 @@ __global__ __launch_bounds__(kThreads) void zone_kernel(const PartitionParams P)
     acc[r][3] = INT_MIN;
   }
   __syncthreads();
-  const int f = s_frame;
   const int lo = min(max(P.frame_begin[f], 0), P.n_boxes);
   const int hi = min(max(P.frame_begin[f + 1], lo), P.n_boxes);
   for (int b = lo + tid; b < hi; b += kThreads) {
@@ -98,32 +105,61 @@ __global__ __launch_bounds__(kThreads) void zone_kernel(const PartitionParams P)
       atomicMax(&acc[best][2], x1);
       atomicMax(&acc[best][3], y1);
     }
-    if (P.zone_of_box) P.zone_of_box[b] = best;
+    if (record) P.zone_of_box[b] = best;
   }
   __syncthreads();
+}
 
-  // Non-empty zones of this frame, counted in zone order.
-  int total = 0;
-  for (int base = 0; base < Z; base += kThreads) {
-    const int r = base + tid;
-    const uint64_t used = __ballot(r < Z && acc[r][0] != INT_MAX);
-    if (lane == 0) s_wave[wave] = __popcll(used);
-    __syncthreads();
+__global__ __launch_bounds__(kThreads) void count_kernel(const PartitionParams P) {
+  __shared__ int acc[kMaxZones][4];
+  __shared__ int s_wave[kWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int f = blockIdx.x, Z = P.zones_x * P.zones_y;
+  fold_frame(P, f, acc, false);
+  int used = 0;
+  for (int r = tid; r < Z; r += kThreads) used += acc[r][0] != INT_MAX;
+  for (int o = 32; o > 0; o >>= 1) used += __shfl_xor(used, o);
+  if (lane == 0) s_wave[wave] = used;
+  __syncthreads();
+  if (tid == 0) {
+    int total = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) total += s_wave[w];
-    __syncthreads();
+    P.first[f] = total;
   }
-  if (wave == 0) {
-    bool failed;
-    const int prefix = tg_detail::lookback_prefix(P.state, f, total, &failed);
-    if (lane == 0) {
-      s_prefix = prefix;
-      if (f == P.n_frames - 1) *P.n_patches = failed ? TG_E_INTERNAL : prefix + total;
-    }
-  }
-  __syncthreads();
+}
 
-  int pos = s_prefix;
+// Exclusive prefix sum of the counts, in place, and the total: thread t takes a
+// contiguous chunk of frames.
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(const PartitionParams P) {
+  __shared__ int s_wave[kScanThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int F = P.n_frames;
+  const int chunk = (F + kScanThreads - 1) / kScanThreads;
+  const int a = static_cast<int>(min(int64_t(tid) * chunk, int64_t(F)));
+  const int b = static_cast<int>(min(int64_t(a) + chunk, int64_t(F)));
+  int sum = 0;
+  for (int i = a; i < b; ++i) sum += P.first[i];
+  const int incl = wave_inclusive_sum(sum);
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int run = incl - sum;
+  for (int w = 0; w < wave; ++w) run += s_wave[w];
+  for (int i = a; i < b; ++i) {
+    const int c = P.first[i];
+    P.first[i] = run;
+    run += c;
+  }
+  if (tid == kScanThreads - 1) *P.n_patches = run;
+}
+
+__global__ __launch_bounds__(kThreads) void write_kernel(const PartitionParams P) {
+  __shared__ int acc[kMaxZones][4];
+  __shared__ int s_wave[kWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int f = blockIdx.x, Z = P.zones_x * P.zones_y;
+  fold_frame(P, f, acc, P.zone_of_box != nullptr);
+  int pos = P.first[f];
   for (int base = 0; base < Z; base += kThreads) {
     const int r = base + tid;
     const bool u = r < Z && acc[r][0] != INT_MAX;
@@ -187,14 +223,11 @@ extern "C" int tg_partition(const tg_partition_args *a, void *stream) {
   P.patches = a->patches;
   P.zone_of_box = a->zone_of_box;
   P.n_patches = a->n_patches;
-  P.ticket = static_cast<uint32_t *>(a->workspace);
-  P.state = static_cast<uint64_t *>(a->workspace) + 1;
+  P.first = static_cast<int32_t *>(a->workspace);
 
-  const int32_t words = 1 + a->n_frames;
-  hipLaunchKernelGGL(clear_kernel, dim3((words + kThreads - 1) / kThreads), dim3(kThreads), 0,
-                     s, static_cast<uint64_t *>(a->workspace), words);
-  if (hipGetLastError() != hipSuccess) return TG_E_HIP;
-  hipLaunchKernelGGL(zone_kernel, dim3(static_cast<uint32_t>(a->n_frames)), dim3(kThreads), 0,
-                     s, P);
+  const dim3 frames(static_cast<uint32_t>(a->n_frames));
+  hipLaunchKernelGGL(count_kernel, frames, dim3(kThreads), 0, s, P);
+  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, s, P);
+  hipLaunchKernelGGL(write_kernel, frames, dim3(kThreads), 0, s, P);
   return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
 }
