@@ -25,6 +25,7 @@
 //     them is kept and kept once all of them are suppressed (see "the greedy of a frame"
 //     for why this is the greedy walk's result and why the index finds every suppressor);
 //  8. stable compaction of the kept detections (decoupled look-back, 1024 per workgroup).
+// Inputs of at most kTiny detections (by capacity) take one launch instead (tiny_kernel).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -705,6 +706,122 @@ __global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergePar
     P.keep[P.grouped[a]] = P.rstate[a] == kKept ? 1 : 0;
 }
 
+// ---- small inputs: one workgroup, one launch ------------------------------------------
+//
+// Up to kTiny detections (n_max <= kTiny) are merged by one workgroup: each thread holds
+// one detection, its suppressors (ranked above it in the same frame, with cross_only from
+// another patch, and suppressing it) are a kTiny-bit row in LDS found by testing every
+// pair, the rounds above run on those rows (suppressed once a suppressor is kept, kept
+// once all are suppressed), and a workgroup prefix sum writes the kept detections in input
+// order. On inputs this small the launches of the general path, not their work, are the
+// cost.
+constexpr int kTiny = 512;
+constexpr int kTinyWords = kTiny / 32;
+
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row broadcasts).
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
+// A detection as the pair tests read it: one 32-byte LDS record.
+struct alignas(16) TinyDet {
+  float4 box;
+  uint64_t key;
+  int32_t frame, roi;
+};
+
+__global__ __launch_bounds__(kTiny) void tiny_kernel(const MergeParams P) {
+  __shared__ TinyDet s_det[kTiny];
+  __shared__ uint32_t s_sup[kTiny][kTinyWords + 1];  // odd row stride: rows in distinct banks
+  __shared__ uint32_t s_kept[kTinyWords], s_open[kTinyWords];
+  __shared__ int32_t s_wave[kTiny / 64];
+  const int i = threadIdx.x, lane = i & 63, wave = i >> 6;
+  const int n = count_of(P);
+  tg_det d = {0, 0, -1, 0.0f, 0.0f, 0.0f, 0.0f};
+  int f = -1;
+  uint64_t key = ~uint64_t(0);
+  if (i < n) {
+    d = P.dets[i];
+    if (d.frame >= 0 && d.frame < P.n_frames) f = d.frame;
+    const float s = (d.box >= 0 && d.box < P.n_scores) ? P.scores[d.box] : __builtin_nanf("");
+    key = rank_key(s, d.box);
+  }
+  const float4 box = make_float4(d.x1, d.y1, d.x2, d.y2);
+  s_det[i] = TinyDet{box, key, f, d.roi};
+  __syncthreads();
+
+  // this detection's suppressors: four candidates per step, their records read first; a
+  // row word is stored when its 32 candidates are done (words past n stay unset, and
+  // are only ever tested against masks that are zero there)
+  if (f >= 0) {
+    uint32_t word = 0;
+    for (int j0 = 0; j0 < n; j0 += 4) {
+      TinyDet q[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) q[u] = s_det[min(j0 + u, n - 1)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool c = j0 + u < n && q[u].frame == f && q[u].key < key &&
+                       !(P.cross_only && q[u].roi == d.roi) && suppresses(q[u].box, box, P.thr);
+        word |= static_cast<uint32_t>(c) << ((j0 + u) & 31);
+      }
+      if (((j0 + 4) & 31) == 0 || j0 + 4 >= n) {
+        s_sup[i][j0 >> 5] = word;
+        word = 0;
+      }
+    }
+  }
+
+  // rounds; a detection outside the frames is dropped (never kept, never a suppressor)
+  int st = f >= 0 ? kUndecided : kSuppressed;
+  bool overrun = false;
+  for (int round = 0;; ++round) {
+    const uint64_t kept = __ballot(st == kKept), open = __ballot(st == kUndecided);
+    if (lane == 0) {
+      s_kept[2 * wave] = static_cast<uint32_t>(kept);
+      s_kept[2 * wave + 1] = static_cast<uint32_t>(kept >> 32);
+      s_open[2 * wave] = static_cast<uint32_t>(open);
+      s_open[2 * wave + 1] = static_cast<uint32_t>(open >> 32);
+    }
+    if (!__syncthreads_or(st == kUndecided)) break;
+    if (round > n) {  // each round decides the best-ranked undecided detection
+      overrun = true;
+      break;
+    }
+    if (st == kUndecided) {
+      bool any_kept = false, any_open = false;
+#pragma unroll
+      for (int w = 0; w < kTinyWords; ++w) {
+        const uint32_t r = s_sup[i][w];
+        any_kept = any_kept || (r & s_kept[w]) != 0;
+        any_open = any_open || (r & s_open[w]) != 0;
+      }
+      st = any_kept ? kSuppressed : (any_open ? kUndecided : kKept);
+    }
+    __syncthreads();  // every row has been tested before the masks are rewritten
+  }
+
+  const int k = i < n && st == kKept ? 1 : 0;
+  if (i < n) P.keep[i] = k;
+  const int incl = wave_inclusive_sum(k);
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kTiny / 64; ++w) {
+    if (w < wave) before += s_wave[w];
+    total += s_wave[w];
+  }
+  if (k) P.out[before + incl - 1] = d;
+  if (i == 0) *P.n_kept = overrun ? TG_E_INTERNAL : total;
+}
+
 __global__ __launch_bounds__(kThreads) void compact_kernel(const MergeParams P) {
   __shared__ int s_blk, s_prefix;
   __shared__ int s_wave[kThreads / 64];
@@ -813,6 +930,7 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   if (!a->workspace || a->workspace_bytes < L.total ||
       reinterpret_cast<uintptr_t>(a->workspace) % 16 != 0)
     return TG_E_WORKSPACE;
+  const bool tiny = a->n_max <= kTiny;
 
   uint8_t *ws = static_cast<uint8_t *>(a->workspace);
   MergeParams P;
@@ -849,6 +967,10 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   P.ebox = reinterpret_cast<float4 *>(ws + L.ebox);
   P.eaux = reinterpret_cast<int4 *>(ws + L.eaux);
 
+  if (tiny) {
+    hipLaunchKernelGGL(tiny_kernel, dim3(1), dim3(kTiny), 0, s, P);
+    return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
+  }
   const int32_t words32 = 2 * a->n_frames;  // counts + cursor
   const int32_t words64 = 2 + compact_blocks(a->n_max);
   const int32_t clear_n = words32 > words64 ? words32 : words64;

@@ -156,3 +156,35 @@ def test_partial_count_and_empty(torch):
     assert n_kept == 0
     _, _, n_kept = run_gpu(torch, dets[:0], scores, 5, 0.5, True, n_max=0)
     assert n_kept == 0
+
+
+def test_single_workgroup_path(torch):
+    """Capacities up to 512 take the one-launch path (one workgroup, suppressor rows in
+    LDS): against the oracle, and against the general path run on the same detections
+    with a larger capacity, on frames sharing the 512 slots, NaN scores, frames out of
+    range, special boxes, a negative threshold, and counts of 0, 1, 511 and 512."""
+    from oracle import merge
+
+    rng = np.random.default_rng(21)
+    cases = [(1, 1, 0.5, True), (2, 1, 0.5, False), (41, 1, 0.5, True), (200, 3, 0.4, True),
+             (511, 1, 0.3, False), (512, 1, 0.5, True), (512, 7, 0.5, False),
+             (300, 2, -0.5, False), (300, 2, 0.0, True), (512, 600, 0.5, True)]
+    for n, n_frames, thr, cross in cases:
+        dets, scores = random_dets(rng, n, n_frames, 5, span=150.0)
+        if n >= 300:
+            k = rng.permutation(n)
+            dets["frame"][k[:10]] = n_frames + 2                   # dropped
+            dets["x2"][k[10:20]] = np.inf
+            dets["x1"][k[20:30]], dets["x2"][k[20:30]] = dets["x2"][k[20:30]], dets["x1"][k[20:30]]
+            for c in ("x1", "y1", "x2", "y2"):
+                dets[c][k[30:60]] = dets[c][k[30]]                # duplicates of one box
+        say("single workgroup", n, n_frames, thr, cross)
+        want_keep, want_kept = merge.merge(dets, scores, n_frames, thr, cross)
+        for n_max in (n, 513):
+            keep, kept, n_kept = run_gpu(torch, dets, scores, n_frames, thr, cross, n_max=n_max)
+            np.testing.assert_array_equal(keep, want_keep.astype(np.int32))
+            assert n_kept == len(want_kept)
+            np.testing.assert_array_equal(kept.view(np.int32), want_kept.view(np.int32))
+    _, _, n_kept = run_gpu(torch, np.zeros(0, tg.DET_DTYPE), np.zeros(1, np.float32), 3, 0.5,
+                           True, n_max=100)
+    assert n_kept == 0
