@@ -379,6 +379,82 @@ def gmm_cost(tg, W, torch, with_oracle: bool, warm: int = 8, launches: int = 8):
     return out
 
 
+def replay_chunks(rois, plan, first, count, canvas, frame_stride, row_pitch):
+    """The source byte ranges each stitch unit of a launch reads (canvases [first, first +
+    count)): one range per patch row and 2048-pixel run it meets, as (unit, byte offset
+    into the frames, length), sorted by unit."""
+    lo, hi = int(plan.canvas_begin[first]), int(plan.canvas_begin[first + count])
+    ids = plan.order[lo:hi]
+    pl = plan.place[ids].astype(np.int64)
+    r = rois[ids].astype(np.int64)
+    h = r[:, 4]
+    row = np.repeat(np.arange(len(ids)), h)
+    y = np.arange(int(h.sum())) - np.repeat(np.cumsum(h) - h, h)
+    runs = -(-canvas * canvas // 2048)
+    s = (pl[row, 2] + y) * canvas + pl[row, 1]  # first canvas pixel of the row segment
+    e = s + r[row, 3]
+    src = r[row, 0] * frame_stride + (r[row, 2] + y) * row_pitch + 3 * r[row, 1]
+    split = np.minimum(e, (s // 2048 + 1) * 2048)
+    unit0 = (pl[row, 0] - first) * runs + s // 2048
+    two = split < e
+    unit = np.r_[unit0, unit0[two] + 1]
+    off = np.r_[src, src[two] + 3 * (split[two] - s[two])]
+    ln = np.r_[3 * (split - s), 3 * (e[two] - split[two])]
+    o = np.argsort(unit, kind="stable")
+    begin = np.searchsorted(unit[o], np.arange(count * runs + 1)).astype(np.int32)
+    return off[o].astype(np.int64), ln[o].astype(np.int32), begin, runs
+
+
+def replay_ceiling(torch, frames_d, rois, plan, batches, out, canvas, stitch_us,
+                   launches: int = 40):
+    """The stitch launches' own memory traffic replayed with no work of their own
+    (libtg_probe.so tg_probe_replay): one workgroup per stitch unit reads the source byte
+    ranges that unit reads and writes the unit's run of each fp16 plane, batches
+    alternating as in the steps. The time is what the memory system needs for exactly this
+    access pattern; stitch_frac = replay time / stitch time."""
+    import ctypes
+
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2404_09267_amd", "libtg_probe.so"))
+    L.tg_probe_replay.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                                  ctypes.c_void_p]
+    F, H, Wd, _ = frames_d.shape
+    src_bytes = frames_d.numel()
+    descs = []
+    for first, count in batches:
+        off, ln, begin, runs = replay_chunks(rois, plan, first, count, canvas, H * Wd * 3, Wd * 3)
+        if len(off) and int(((off + ln + 15) // 16 * 16).max()) > (src_bytes + 15) // 16 * 16:
+            raise RuntimeError("replay range outside the frames")
+        descs.append((torch.from_numpy(off).cuda(), torch.from_numpy(ln).cuda(),
+                      torch.from_numpy(begin).cuda(), count * runs, runs,
+                      out[first:first + count]))
+    stream = torch.cuda.current_stream()
+    h = ctypes.c_void_p(stream.cuda_stream)
+
+    def launch(i):
+        off, ln, begin, n_units, runs, dst = descs[i % len(descs)]
+        rc = L.tg_probe_replay(ctypes.c_void_p(frames_d.data_ptr()), src_bytes,
+                               ctypes.c_void_p(off.data_ptr()), ctypes.c_void_p(ln.data_ptr()),
+                               ctypes.c_void_p(begin.data_ptr()), n_units, runs,
+                               ctypes.c_void_p(dst.data_ptr()), canvas * canvas * 2, h)
+        if rc != 0:
+            raise RuntimeError(f"tg_probe_replay: {rc}")
+    for i in range(4):
+        launch(i)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs[0].record(stream)
+    for i in range(launches):
+        launch(i)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = sum(evs[i].elapsed_time(evs[i + 1]) for i in range(launches)) * 1e3 / launches
+    return {"kernel": "stitch traffic replayed, libtg_probe.so tg_probe_replay",
+            "ranges_per_launch": int(np.mean([len(d[0]) for d in descs])),
+            "us": round(us, 2), "stitch_frac": round(us / stitch_us, 4)}
+
+
 def stream_ceiling(torch, read_bytes: int, write_bytes: int, launches: int = 40):
     """A plain streaming kernel (libtg_probe.so) moving the stitch launch's algorithmic
     reads and writes, writes alternating between two outputs and reads cycling through a
@@ -634,6 +710,9 @@ def main():
         ceil = stream_ceiling(torch, int(avg_bytes) - write_bytes, write_bytes)
         ceil["stitch_frac"] = round(achieved / ceil["gbs"], 4)
         ceil["planes3"]["stitch_frac"] = round(achieved / ceil["planes3"]["gbs"], 4)
+        ceil["replay"] = replay_ceiling(torch, frames_d, rois, plan0, batches, out, wl.canvas,
+                                        avg_ms * 1e3)
+        ceil["replay"]["gbs"] = round(avg_bytes / ceil["replay"]["us"] / 1e3, 1)
         result["ceiling"] = ceil
     result["unstitch"] = unstitch_cost(tg, torch, uargs, n_boxes)
     if not args.no_aux:
