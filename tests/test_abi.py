@@ -279,7 +279,7 @@ def test_probe_library_exports_its_header():
     text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "tg_probe.h")).read(),
                   flags=re.S)
     names = sorted(set(re.findall(r"\b(tg_\w+)\s*\(", text)))
-    assert names == ["tg_probe_stream", "tg_probe_stream_planes"]
+    assert names == ["tg_probe_replay", "tg_probe_stream", "tg_probe_stream_planes"]
     L = ctypes.CDLL(os.path.join(ROOT, "paper_2404_09267_amd", "libtg_probe.so"))
     f = L.tg_probe_stream
     f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
@@ -296,6 +296,15 @@ def test_probe_library_exports_its_header():
     assert g(ok, 4096, ok, 4800, 4096, 0, None) == -1        # no planes
     assert g(ok, 4096, ok, 4800, 4096, 5, None) == -1        # too many planes
     assert g(ok, 4096, ok, 4816, 4096, 3, None) == -1        # planes of whole 16-byte words
+    r = L.tg_probe_replay
+    r.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                  ctypes.c_int64, ctypes.c_void_p]
+    assert r(None, 4096, ok, ok, ok, 4, 2, ok, 4096, None) == -1  # null source
+    assert r(ok, 4096, ok, ok, ok, 0, 1, ok, 4096, None) == -1    # no units
+    assert r(ok, 4096, ok, ok, ok, 5, 2, ok, 4096, None) == -1    # not whole canvases
+    assert r(ok, 4096, ok, ok, ok, 4, 2, ok, 4100, None) == -1    # plane not whole words
+    assert r(ok, 4096, ok, ok, ok, 4, 2, ctypes.c_void_p(4104), 4096, None) == -1  # misaligned
 
 
 def test_unstitch_noalloc_validation_without_gpu():
