@@ -594,7 +594,6 @@ def main():
                    for k, (first, count) in enumerate(batches)]
     uargs = tg.unstitch_args(boxes_d, canv_d, dplan, 1, ubufs)
     stitch_events = []
-    unstitch_events = []
     plan_s = []
     timing = {"on": False}
 
@@ -615,26 +614,24 @@ def main():
         if rc != tg.OK or J_buf[0] != J:
             raise tg.TgError("tg_plan_pack", rc)
         plan_d.copy_(staging[buf], non_blocking=True)
-        # One timing event before each tg_stitch launch and one after the last: launch k
-        # runs between events k and k + 1. The first also marks the staging upload as done.
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(stitch_args) + 1)]
+        # Two timing events per step, one before the step's first tg_stitch launch (it also
+        # marks the staging upload as done) and one after its last: every event recorded
+        # between two kernels leaves the GPU idle for a few microseconds, so none is put
+        # between the launches themselves.
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         evs[0].record(stream)
         upload_done[buf] = evs[0]
         h = tg._vp(stream.cuda_stream)
-        for k, a in enumerate(stitch_args):
+        for a in stitch_args:
             rc = tg.lib().tg_stitch(tg.ctypes.byref(a), h)
             if rc != tg.OK:
                 raise tg.TgError("tg_stitch", rc)
-            evs[k + 1].record(stream)
-            if timing["on"]:
-                stitch_events.append((evs[k], evs[k + 1], a.canvas_first, a.canvas_count))
+        evs[1].record(stream)
+        if timing["on"]:
+            stitch_events.append((evs[0], evs[1]))
         rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
         if rc != tg.OK:
             raise tg.TgError("tg_unstitch", rc)
-        if timing["on"]:
-            ue = torch.cuda.Event(enable_timing=True)
-            ue.record(stream)
-            unstitch_events.append((evs[-1], ue))
 
     for s in range(args.warmup):
         step(s)
@@ -656,15 +653,12 @@ def main():
     value = canvas_px / (ms_per_step * 1e-3) / 1e6
 
     # ---- dominant kernel: tg_stitch ------------------------------------------------
-    tot_ms, tot_bytes = 0.0, 0
-    per_batch_bytes = {(f, c): stitch_bytes(rois, plan0, f, c, wl.canvas) for f, c in batches}
-    for e0, e1, f, c in stitch_events:
-        tot_ms += e0.elapsed_time(e1)
-        tot_bytes += per_batch_bytes[(f, c)]
-    n_launch = len(stitch_events)
-    launch_ms = sorted(e0.elapsed_time(e1) for e0, e1, _, _ in stitch_events)
-    avg_ms = tot_ms / n_launch
-    avg_bytes = tot_bytes / n_launch
+    # each step's launches run back to back between its two events: the average launch
+    # is the events' interval over all steps divided by the number of launches
+    step_ms = [e0.elapsed_time(e1) for e0, e1 in stitch_events]
+    n_launch = len(batches) * len(stitch_events)
+    avg_ms = float(np.sum(step_ms)) / n_launch
+    avg_bytes = sum(stitch_bytes(rois, plan0, f, c, wl.canvas) for f, c in batches) / len(batches)
     achieved = avg_bytes / (avg_ms * 1e-3) / 1e9
     traffic = None
     if os.path.exists(counters_path(wl.name)):
@@ -677,7 +671,7 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "stitch_kernel<true, false>", "launches": n_launch,
                 "avg_launch_us": round(avg_ms * 1e3, 2),
-                "median_launch_us": round(launch_ms[n_launch // 2] * 1e3, 2),
+                "median_step_launch_us": round(float(np.median(step_ms)) * 1e3 / len(batches), 2),
                 "algorithmic_bytes_per_launch": int(avg_bytes)}
 
     result = {
@@ -697,12 +691,12 @@ def main():
         "stitch_gbs": round(achieved, 1),
         "stitch_pct_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
         # per step, over the timed steps: the host plan (overlapped with the previous
-        # step's GPU work), the GPU time of all of the step's stitch launches, and of its
-        # tg_unstitch
+        # step's GPU work) and the GPU time of all of the step's stitch launches; then
+        # tg_unstitch, timed alone after the steps (no event inside the steps separates it)
         "step_parts": {
             "plan_ms": round(1e3 * float(np.mean(plan_s)), 4),
-            "stitch_ms": round(tot_ms / args.steps, 4),
-            "unstitch_ms": round(float(np.mean([a.elapsed_time(b) for a, b in unstitch_events])), 4),
+            "stitch_ms": round(float(np.mean(step_ms)), 4),
+            "unstitch_ms": None,
             "stitch_launches": len(batches)},
     }
     if not args.no_aux:
@@ -715,6 +709,7 @@ def main():
         ceil["replay"]["gbs"] = round(avg_bytes / ceil["replay"]["us"] / 1e3, 1)
         result["ceiling"] = ceil
     result["unstitch"] = unstitch_cost(tg, torch, uargs, n_boxes)
+    result["step_parts"]["unstitch_ms"] = round(result["unstitch"]["us_per_call"] / 1e3, 4)
     if not args.no_aux:
         result["invoker"] = invoker_cost(tg, W, not args.no_cpu_baseline)
         result["partition"] = partition_cost(tg, W, torch, not args.no_cpu_baseline)
