@@ -2,7 +2,7 @@
 """Throughput of the patch-stitching path on one MI355X.
 
 One step = one pass of the whole path over one batch of synthetic input:
-  tg_plan_pack (host C++) -> plan uploaded to HBM -> tg_stitch once per batch of
+  tg_plan_pack (host C++) -> plan uploaded to HBM (tg_plan_upload) -> tg_stitch once per batch of
   canvases -> tg_unstitch of every detector box.
 Frames, the RoI table and the boxes are resident in HBM before timing starts. The
 host plan of step s+1 overlaps the GPU work of step s (double-buffered pinned
@@ -613,7 +613,7 @@ def main():
             plan_s.append(time.perf_counter() - tp)
         if rc != tg.OK or J_buf[0] != J:
             raise tg.TgError("tg_plan_pack", rc)
-        plan_d.copy_(staging[buf], non_blocking=True)
+        tg.plan_upload(staging[buf], plan_d, stream)  # one kernel reading the pinned buffer
         # Two timing events per step, one before the step's first tg_stitch launch (it also
         # marks the staging upload as done) and one after its last: every event recorded
         # between two kernels leaves the GPU idle for a few microseconds, so none is put

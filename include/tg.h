@@ -139,6 +139,18 @@ int32_t tg_batch_count(int32_t n_canvases, int32_t batch_cap);
 int tg_batch_range(int32_t n_canvases, int32_t batch_cap, int32_t k, int32_t *first,
                    int32_t *count);
 
+/*
+ * Plan upload (data movement only, no step of the method): copies `bytes` from pinned
+ * host memory `src` (hipHostMalloc, or a torch tensor made with pin_memory=True) to
+ * device memory `dst` with one kernel on `stream` that reads `src` over PCIe -- for a
+ * serving loop that hands each step's plan (tg_plan_pack's place, order, canvas_begin)
+ * to the device. `src` must stay unchanged until the stream has passed the kernel; `dst`
+ * belongs to the caller. Returns TG_OK (bytes == 0 enqueues nothing), TG_E_INVAL for a
+ * null pointer or for `src` that is not pinned memory the device can read (checked with
+ * hipHostGetDevicePointer before anything is enqueued), TG_E_HIP on launch failure.
+ */
+int tg_plan_upload(const void *src, void *dst, size_t bytes, void *stream);
+
 /* ---- Adaptive frame partitioning (Sec. III-A, Alg. 1) ---- */
 
 typedef struct {

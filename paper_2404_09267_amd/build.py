@@ -29,7 +29,8 @@ PROBE_SOURCES = ["probe.hip"]
 ARCH = "gfx950"
 
 HOST_SOURCES = ["plan.cpp", "norm.cpp", "invoker.cpp"]
-HIP_SOURCES = ["stitch.hip", "unstitch.hip", "partition.hip", "merge.hip", "gmm.hip", "rois.hip"]
+HIP_SOURCES = ["stitch.hip", "unstitch.hip", "partition.hip", "merge.hip", "gmm.hip", "rois.hip",
+               "upload.hip"]
 
 # Packed FP32 instructions are kept out of every kernel; scalar code is all we need.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,

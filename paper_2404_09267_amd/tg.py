@@ -98,7 +98,7 @@ GMM_MAX_MIX = 5
 
 EXPORTS = ["tg_gmm_plane_stride", "tg_gmm_state_bytes", "tg_gmm_update",
            "tg_mask_rois_workspace_bytes", "tg_mask_rois", "tg_partition_workspace_bytes", "tg_partition", "tg_plan_pack", "tg_batch_count",
-           "tg_batch_range", "tg_slo_replay", "tg_stitch",
+           "tg_batch_range", "tg_plan_upload", "tg_slo_replay", "tg_stitch",
            "tg_stitch_units", "tg_stitch_norm_uses_table",
            "tg_unstitch_workspace_bytes", "tg_unstitch", "tg_unstitch_noalloc",
            "tg_merge_workspace_bytes", "tg_merge",
@@ -139,6 +139,8 @@ def lib() -> ctypes.CDLL:
         L.tg_batch_count.restype = _i32
         L.tg_batch_range.argtypes = [_i32, _i32, _i32, _vp, _vp]
         L.tg_batch_range.restype = ctypes.c_int
+        L.tg_plan_upload.argtypes = [_vp, _vp, ctypes.c_size_t, _vp]
+        L.tg_plan_upload.restype = ctypes.c_int
         L.tg_partition_workspace_bytes.argtypes = [_i32]
         L.tg_partition_workspace_bytes.restype = ctypes.c_size_t
         L.tg_partition.argtypes = [ctypes.POINTER(PartitionArgs), _vp]
@@ -235,6 +237,24 @@ def batch_range(n_canvases: int, batch_cap: int, k: int):
     if rc != OK:
         raise TgError("tg_batch_range", rc)
     return int(first[0]), int(count[0])
+
+
+def plan_upload(src, dst, stream=None) -> None:
+    """Copies pinned host tensor `src` into device tensor `dst` (same byte size) with
+    tg_plan_upload on `stream` (the current stream by default)."""
+    import torch
+
+    if not src.is_pinned():
+        raise ValueError("plan_upload: the source must be pinned host memory")
+    if not dst.is_cuda or not dst.is_contiguous() or not src.is_contiguous():
+        raise ValueError("plan_upload: a contiguous pinned source and device destination")
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise ValueError("plan_upload: source and destination sizes differ")
+    s = stream or torch.cuda.current_stream()
+    rc = lib().tg_plan_upload(_vp(src.data_ptr()), _vp(dst.data_ptr()), n, _vp(s.cuda_stream))
+    if rc != OK:
+        raise TgError("tg_plan_upload", rc)
 
 
 @dataclass

@@ -195,6 +195,13 @@ def test_unstitch_validation_without_gpu():
     assert int(tg.lib().tg_unstitch(ctypes.byref(a), None)) == tg.E_INVAL
 
 
+def test_plan_upload_validation_without_gpu():
+    L = tg.lib()
+    assert int(L.tg_plan_upload(None, None, 0, None)) == tg.OK         # nothing to move
+    assert int(L.tg_plan_upload(None, ctypes.c_void_p(0x1000), 8, None)) == tg.E_INVAL
+    assert int(L.tg_plan_upload(ctypes.c_void_p(0x1000), None, 8, None)) == tg.E_INVAL
+
+
 def test_workspace_sizes():
     assert tg.unstitch_workspace_bytes(0, 100) == 0
     assert tg.unstitch_workspace_bytes(-5, 100) == 0
