@@ -27,6 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+STITCH_RUN = 6144      # canvas pixels per tg_stitch work unit (include/tg.h, tg_stitch_units)
 METRIC = "stitched canvas Mpixel/s and achieved HBM GB/s (% of peak), 20-cam 4K"
 STITCH_SRC = os.path.join(ROOT, "paper_2404_09267_amd", "csrc", "stitch.hip")
 def counters_path(workload: str) -> str:
@@ -381,8 +382,8 @@ def gmm_cost(tg, W, torch, with_oracle: bool, warm: int = 8, launches: int = 8):
 
 def replay_chunks(rois, plan, first, count, canvas, frame_stride, row_pitch):
     """The source byte ranges each stitch unit of a launch reads (canvases [first, first +
-    count)): one range per patch row and 2048-pixel run it meets, as (unit, byte offset
-    into the frames, length), sorted by unit."""
+    count)): one range per patch row and STITCH_RUN-pixel run it meets, as (unit, byte
+    offset into the frames, length), sorted by unit."""
     lo, hi = int(plan.canvas_begin[first]), int(plan.canvas_begin[first + count])
     ids = plan.order[lo:hi]
     pl = plan.place[ids].astype(np.int64)
@@ -390,12 +391,13 @@ def replay_chunks(rois, plan, first, count, canvas, frame_stride, row_pitch):
     h = r[:, 4]
     row = np.repeat(np.arange(len(ids)), h)
     y = np.arange(int(h.sum())) - np.repeat(np.cumsum(h) - h, h)
-    runs = -(-canvas * canvas // 2048)
+    runs = -(-canvas * canvas // STITCH_RUN)
+    assert int(r[:, 3].max(initial=0)) <= STITCH_RUN  # a patch row meets at most two runs
     s = (pl[row, 2] + y) * canvas + pl[row, 1]  # first canvas pixel of the row segment
     e = s + r[row, 3]
     src = r[row, 0] * frame_stride + (r[row, 2] + y) * row_pitch + 3 * r[row, 1]
-    split = np.minimum(e, (s // 2048 + 1) * 2048)
-    unit0 = (pl[row, 0] - first) * runs + s // 2048
+    split = np.minimum(e, (s // STITCH_RUN + 1) * STITCH_RUN)
+    unit0 = (pl[row, 0] - first) * runs + s // STITCH_RUN
     two = split < e
     unit = np.r_[unit0, unit0[two] + 1]
     off = np.r_[src, src[two] + 3 * (split[two] - s[two])]
@@ -418,9 +420,12 @@ def replay_ceiling(torch, frames_d, rois, plan, batches, out, canvas, stitch_us,
     L.tg_probe_replay.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
-                                  ctypes.c_void_p]
+                                  ctypes.c_int64, ctypes.c_void_p]
     F, H, Wd, _ = frames_d.shape
     src_bytes = frames_d.numel()
+    import paper_2404_09267_amd.tg as tgm
+    if tgm.stitch_units(canvas, canvas, 1) != -(-canvas * canvas // STITCH_RUN):
+        raise RuntimeError("STITCH_RUN differs from the library's unit size")
     descs = []
     for first, count in batches:
         off, ln, begin, runs = replay_chunks(rois, plan, first, count, canvas, H * Wd * 3, Wd * 3)
@@ -437,7 +442,8 @@ def replay_ceiling(torch, frames_d, rois, plan, batches, out, canvas, stitch_us,
         rc = L.tg_probe_replay(ctypes.c_void_p(frames_d.data_ptr()), src_bytes,
                                ctypes.c_void_p(off.data_ptr()), ctypes.c_void_p(ln.data_ptr()),
                                ctypes.c_void_p(begin.data_ptr()), n_units, runs,
-                               ctypes.c_void_p(dst.data_ptr()), canvas * canvas * 2, h)
+                               ctypes.c_void_p(dst.data_ptr()), canvas * canvas * 2,
+                               STITCH_RUN * 2, h)
         if rc != 0:
             raise RuntimeError(f"tg_probe_replay: {rc}")
     for i in range(4):

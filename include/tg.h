@@ -315,10 +315,10 @@ int32_t tg_stitch_norm_uses_table(const float mean[3], const float std[3]);
 
 /*
  * Work units of one tg_stitch launch (host only). Each canvas plane is cut, in raster
- * order, into runs of 2048 pixels (the last run of a canvas may be shorter); one unit =
+ * order, into runs of 6144 pixels (the last run of a canvas may be shorter); one unit =
  * one run of one canvas, written in all three planes by one workgroup. Unit k is run
- * k % runs of canvas canvas_first + k / runs, with runs = ceil(canvas_w * canvas_h / 2048),
- * i.e. canvas pixels [2048 r, min(2048 (r + 1), canvas_w * canvas_h)).
+ * k % runs of canvas canvas_first + k / runs, with runs = ceil(canvas_w * canvas_h / 6144),
+ * i.e. canvas pixels [6144 r, min(6144 (r + 1), canvas_w * canvas_h)).
  * Returns the number of units for canvas_count canvases of canvas_w x canvas_h (0 when
  * canvas_count == 0), or TG_E_INVAL for non-positive sizes, a negative count, or more
  * than 2^31 - 1 units.

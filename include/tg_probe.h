@@ -33,15 +33,15 @@ int tg_probe_stream_planes(const void *src, int64_t read_bytes, void *dst, int64
 /* Replay of one stitch launch's memory traffic with no work of its own: workgroup g
  * (of n_units, units_per_canvas per canvas) reads the 16-byte words of src covering the
  * byte ranges [off[k], off[k] + len[k]) for k in [begin[g], begin[g+1]) (the source rows
- * of the patches in stitch unit g, as tg_stitch reads them), then writes unit g's 4096
- * bytes (the last unit of a canvas: the rest of the plane) of each of its canvas's three
- * planes of plane_bytes, canvases of three planes from dst, with 16-byte nontemporal
+ * of the patches in stitch unit g, as tg_stitch reads them), then writes unit g's
+ * run_bytes (the last unit of a canvas: the rest of the plane) of each of its canvas's
+ * three planes of plane_bytes, canvases of three planes from dst, with 16-byte nontemporal
  * stores. off, len, begin: device; every range must lie in src's first src_bytes, rounded
  * up to 16 (the caller checks). Returns 0, -1 for bad arguments, -2 when the launch
  * fails. */
 int tg_probe_replay(const void *src, int64_t src_bytes, const int64_t *off, const int32_t *len,
                     const int32_t *begin, int32_t n_units, int32_t units_per_canvas, void *dst,
-                    int64_t plane_bytes, void *stream);
+                    int64_t plane_bytes, int64_t run_bytes, void *stream);
 
 #ifdef __cplusplus
 }

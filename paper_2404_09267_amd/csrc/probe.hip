@@ -100,15 +100,16 @@ __global__ __launch_bounds__(kReplayThreads) void replay_kernel(
 extern "C" int tg_probe_replay(const void *src, int64_t src_bytes, const int64_t *off,
                                const int32_t *len, const int32_t *begin, int32_t n_units,
                                int32_t units_per_canvas, void *dst, int64_t plane_bytes,
-                               void *stream) {
+                               int64_t run_bytes, void *stream) {
   if (!src || !off || !len || !begin || !dst || n_units < 1 || units_per_canvas < 1 ||
-      n_units % units_per_canvas || plane_bytes < 16 || plane_bytes % 16 || src_bytes < 0 ||
+      n_units % units_per_canvas || plane_bytes < 16 || plane_bytes % 16 || run_bytes < 16 ||
+      run_bytes % 16 || src_bytes < 0 ||
       reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(dst) % 16)
     return -1;
   (void)src_bytes;  // the caller checks every range against it on the host
   hipLaunchKernelGGL(replay_kernel, dim3(static_cast<uint32_t>(n_units)), dim3(kReplayThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4 *>(src), off, len,
-                     begin, static_cast<u32x4 *>(dst), plane_bytes / 16, int64_t(4096 / 16),
+                     begin, static_cast<u32x4 *>(dst), plane_bytes / 16, run_bytes / 16,
                      units_per_canvas);
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }

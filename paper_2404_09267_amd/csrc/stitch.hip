@@ -7,10 +7,12 @@
 //
 // Design for gfx950 (wave64, HBM-bound, write-dominated: 6 bytes written per canvas
 // pixel, 3 bytes read per covered pixel):
-//  - Work units (stitch_units.h): runs of 2048 canvas pixels in raster order, one
-//    128-thread workgroup each, launched in address order. A run is one 4 KB page of
-//    each fp16 plane, so the workgroups resident on the chip write a compact window of
-//    whole pages that sweeps through the output; HBM absorbs writes fastest that way.
+//  - Work units (stitch_units.h): runs of 6144 canvas pixels in raster order, one
+//    256-thread workgroup each, launched in address order. A run is three whole 4 KB
+//    pages of each fp16 plane, so the workgroups resident on the chip write a compact
+//    window of whole pages that sweeps through the output; HBM absorbs writes fastest
+//    that way. (Runs of 2048 pixels on 128 threads were 6-15 % slower: the per-unit plan
+//    scan, list and barriers are then paid three times as often.)
 //  - A workgroup makes one pass over its run: it prefills its LDS staging row with the
 //    pad pixel (4 bytes per pixel: R, G, B and an unused byte, so that every patch edge
 //    falls on a dword boundary and no two patches ever share a staged dword); lists the
@@ -46,7 +48,7 @@ namespace {
 
 using tg_detail::StitchGeometry;
 
-constexpr int kThreads = 128;
+constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kRun = tg_detail::kStitchRun;  // pixels per unit
 constexpr int kGroups = kRun / 8 / kThreads; // 8-pixel groups per thread

@@ -3,8 +3,8 @@
 //
 // A canvas plane is cut, in raster order, into runs of kStitchRun pixels (the last run
 // of a canvas may be shorter); one unit = one run of one canvas, processed by one
-// workgroup, which writes the run in all three fp16 planes. 2048 pixels are 4 KB of
-// one plane: when a plane starts on a 4 KB boundary, every unit writes whole 4 KB
+// workgroup, which writes the run in all three fp16 planes. 6144 pixels are three 4 KB
+// pages of one plane: when a plane starts on a 4 KB boundary, every unit writes whole
 // pages, and the units of a launch, numbered in address order, sweep the output.
 #ifndef TG_STITCH_UNITS_H
 #define TG_STITCH_UNITS_H
@@ -13,7 +13,7 @@
 
 namespace tg_detail {
 
-constexpr int32_t kStitchRun = 2048;
+constexpr int32_t kStitchRun = 6144;
 
 struct StitchGeometry {
   int64_t plane;   // canvas_w * canvas_h pixels
@@ -21,7 +21,7 @@ struct StitchGeometry {
   int32_t n_units; // canvas_count * runs
 };
 
-// Unit k is run (k % runs) of canvas (k / runs): pixels [2048 r, min(2048 (r + 1), plane))
+// Unit k is run (k % runs) of canvas (k / runs): pixels [6144 r, min(6144 (r + 1), plane))
 // in raster order. False when the sizes are not positive or the count overflows int32.
 inline bool stitch_geometry(int32_t canvas_w, int32_t canvas_h, int32_t canvas_count,
                             StitchGeometry *g) {

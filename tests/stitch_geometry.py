@@ -1,8 +1,8 @@
 """tg_stitch's unit geometry restated from its definition (test infrastructure): each
-canvas plane cut in raster order into runs of 2048 pixels, one unit per run."""
+canvas plane cut in raster order into runs of 6144 pixels, one unit per run."""
 import math
 
-RUN = 2048
+RUN = 6144
 
 
 def geometry(cw, ch, count):

@@ -306,12 +306,13 @@ def test_probe_library_exports_its_header():
     r = L.tg_probe_replay
     r.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                   ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                  ctypes.c_int64, ctypes.c_void_p]
-    assert r(None, 4096, ok, ok, ok, 4, 2, ok, 4096, None) == -1  # null source
-    assert r(ok, 4096, ok, ok, ok, 0, 1, ok, 4096, None) == -1    # no units
-    assert r(ok, 4096, ok, ok, ok, 5, 2, ok, 4096, None) == -1    # not whole canvases
-    assert r(ok, 4096, ok, ok, ok, 4, 2, ok, 4100, None) == -1    # plane not whole words
-    assert r(ok, 4096, ok, ok, ok, 4, 2, ctypes.c_void_p(4104), 4096, None) == -1  # misaligned
+                  ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
+    assert r(None, 4096, ok, ok, ok, 4, 2, ok, 4096, 4096, None) == -1  # null source
+    assert r(ok, 4096, ok, ok, ok, 0, 1, ok, 4096, 4096, None) == -1    # no units
+    assert r(ok, 4096, ok, ok, ok, 5, 2, ok, 4096, 4096, None) == -1    # not whole canvases
+    assert r(ok, 4096, ok, ok, ok, 4, 2, ok, 4100, 4096, None) == -1    # plane not whole words
+    assert r(ok, 4096, ok, ok, ok, 4, 2, ok, 4096, 4100, None) == -1    # run not whole words
+    assert r(ok, 4096, ok, ok, ok, 4, 2, ctypes.c_void_p(4104), 4096, 4096, None) == -1
 
 
 def test_unstitch_noalloc_validation_without_gpu():

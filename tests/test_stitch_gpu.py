@@ -57,22 +57,23 @@ def test_odd_frame_widths_and_mean_std(torch):
 
 
 def test_many_patches_per_run_take_further_lists(torch):
-    """Runs met by more patches than one list holds (the rest take further lists): up to
-    8192 tiny RoIs on a small canvas, including 1 x 1, and exactly 128 and 129."""
+    """Runs met by more patches than one list holds (40; the rest take further lists): up
+    to 8192 tiny RoIs on a small canvas, including 1 x 1, and exactly 40 and 41."""
     rng = np.random.default_rng(5)
-    # expect: the exact maximum of patches per unit, or ">" (over 128), or "<=" (128 or fewer)
+    # expect: the exact maximum of patches per unit, or ">" (over 40), or "<=" (40 or fewer)
     for cw, ch, n, lo, hi, pol, expect in [
-            (256, 3, 129, 1, 1, 1, 129), (256, 3, 128, 1, 1, 1, 128),
-            (256, 32, 8192, 1, 1, 1, ">"), (256, 32, 3000, 1, 4, 2, ">"),
-            (64, 64, 200, 2, 6, 0, "<="), (300, 64, 600, 1, 2, 1, ">"),
-            (1300, 6, 900, 1, 2, 0, ">"), (3000, 5, 700, 1, 3, 2, ">")]:
+            (256, 3, 41, 1, 1, 1, 41), (256, 3, 40, 1, 1, 1, 40),
+            (256, 3, 129, 1, 1, 1, 129), (256, 32, 8192, 1, 1, 1, ">"),
+            (256, 32, 3000, 1, 4, 2, ">"), (64, 64, 30, 2, 6, 0, "<="),
+            (300, 64, 600, 1, 2, 1, ">"), (1300, 6, 900, 1, 2, 0, ">"),
+            (3000, 5, 700, 1, 3, 2, ">")]:
         say("dense", cw, ch, n, lo, hi, pol)
         plan, rois = _case(torch, rng, 2, 50, 60, cw, ch, n, lo, hi, hi, pol, with_rois=True)
         most = max(records_per_unit(rois, plan, 0, plan.n_canvases, cw, ch))
         if expect == ">":
-            assert most > 128
+            assert most > 40
         elif expect == "<=":
-            assert most <= 128
+            assert most <= 40
         else:
             assert most == expect
 

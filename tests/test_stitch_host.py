@@ -21,7 +21,7 @@ def test_unit_count_matches_geometry(cw, ch, count):
 
 def test_unit_count_edges():
     assert tg.stitch_units(1280, 1280, 0) == 0
-    for bad in [(0, 10, 1), (10, 0, 1), (10, 10, -1), (65536, 65536, 1024)]:
+    for bad in [(0, 10, 1), (10, 0, 1), (10, 10, -1), (65536, 65536, 4096)]:  # last: > 2^31 - 1 units
         assert tg.lib().tg_stitch_units(*bad) == tg.E_INVAL
     # the largest launch: 2^31 - 1 units at most
     assert tg.stitch_units(2048, 1, 2 ** 31 - 1) == 2 ** 31 - 1
