@@ -186,3 +186,25 @@ def test_patch_records_switch(torch):
         lo = check(torch, boxes[:n_switch - 1], canv[:n_switch - 1], rois, plan, 1, dplan, rule)
         hi = check(torch, boxes, canv, rois, plan, 1, dplan, rule)
         np.testing.assert_array_equal(lo[0], hi[0][:n_switch - 1])
+
+
+@pytest.mark.parametrize("rule", [0, 1])
+def test_patch_records_with_small_canvases(torch, rule):
+    """Patch records on canvases of about 24 patches (16 lanes per box, two rounds):
+    120,000 boxes, centres on edges, NaN and infinite corners, bad canvases."""
+    rng = np.random.default_rng(95 + rule)
+    rois = W.random_rois(rng, 720, 4, 800, 600, 28, 48, 48)
+    plan = tg.plan_pack(rois, 200, 200, 800, 600, 4, tg.SHELF_FFDH)
+    n = 120_000
+    cx, cy = rng.uniform(-8, 208, n), rng.uniform(-8, 208, n)
+    bw, bh = rng.uniform(0, 60, n), rng.uniform(0, 60, n)
+    boxes = np.stack([cx - bw / 2, cy - bh / 2, cx + bw / 2, cy + bh / 2], 1).astype(np.float32)
+    boxes[:20000] = np.round(boxes[:20000])
+    boxes[20000:20500, 1] = np.nan
+    boxes[20500:21000, 2] = np.inf
+    canv = rng.integers(-2, plan.n_canvases + 2, n).astype(np.int32)
+    per_canvas = -(-len(rois) // plan.n_canvases)
+    assert per_canvas <= 32 and n * per_canvas >= 1 << 21
+    for clip in (0, 1):
+        say("records, small canvases", per_canvas, "rule", rule, "clip", clip)
+        check(torch, boxes, canv, rois, plan, clip, rule=rule)
