@@ -361,12 +361,13 @@ int launch(const tg_unstitch_args *a, void *words, void *records, hipStream_t s)
   // Patch records when the boxes test many patches in all (about n_boxes * per_canvas).
   const bool use_records = records && a->n_rois > 0 &&
                            int64_t(a->n_boxes) * per_canvas >= kRecordsMinTests;
-  // Lanes per box. Gathering the plan directly: about the mean number of patches per
-  // canvas, so one ballot round usually settles a box. Reading records, a round costs
-  // little (consecutive records), so canvases of up to 32 patches take 16 lanes and two
-  // rounds at most (window_64x30, 29 patches per canvas: 38.8 us instead of 44.2 with 32).
-  const int lpb = use_records ? (per_canvas <= 32 ? 16 : 64)
-                              : (per_canvas <= 16 ? 16 : per_canvas <= 32 ? 32 : 64);
+  // Lanes per box. Gathering the plan directly, a round is two dependent gathers: 64
+  // lanes, so one round usually settles a box, unless canvases hold at most 16 patches
+  // (cam20_4k, 32 patches per canvas: 11.6 us with 64 lanes, 12.0 with 32, 14.9 with 16).
+  // Reading records, a round costs little (consecutive records), so canvases of up to 32
+  // patches take 16 lanes and two rounds at most (window_64x30, 29 patches per canvas:
+  // 38.8 us instead of 44.2 with 32).
+  const int lpb = use_records ? (per_canvas <= 32 ? 16 : 64) : (per_canvas <= 16 ? 16 : 64);
   P.rect = use_records ? static_cast<float4 *>(records) : nullptr;
   P.meta = use_records ? reinterpret_cast<int2 *>(P.rect + a->n_rois) : nullptr;
   if (use_records) {
