@@ -24,6 +24,8 @@
 //     whole grid), then per frame rounds in which a detection is suppressed once one of
 //     them is kept and kept once all of them are suppressed (see "the greedy of a frame"
 //     for why this is the greedy walk's result and why the index finds every suppressor);
+//     a frame of at most kSmallMax detections is instead decided by its index workgroup
+//     in LDS, from every pair of its detections;
 //  8. stable compaction of the kept detections (decoupled look-back, 1024 per workgroup).
 // Inputs of at most kTiny detections (by capacity) take one launch instead (tiny_kernel).
 #include <hip/hip_runtime.h>
@@ -278,13 +280,124 @@ struct FrameLds {
 };
 constexpr int kIdx = 4;  // detections per thread and step of the index, loads issued together
 
+// ---- frames that fit one workgroup ------------------------------------------------------
+//
+// A frame of at most kSmallMax detections is decided by its index workgroup alone, in LDS:
+// each thread holds one detection and tests every detection of the frame (four 16-byte
+// boxes per step) for the suppressors ranked above it, a row of bits per detection; the
+// rounds run on those rows (masks of kept and undecided detections rebuilt from ballots
+// each round); the keep flags are written at once. The frame's detections are marked
+// kEmpty, so the search passes them by, and the resolve workgroup of the frame returns at
+// once.
+template <int kN>
+struct SmallFrameLds {
+  float4 box[kN];
+  uint64_t key[kN];
+  int32_t roi[kN];
+  uint32_t sup[kN][kN / 32 + 1];  // odd row stride: rows in distinct banks
+  uint32_t kept[kN / 32], open[kN / 32];
+};
+
+// Frames of at most kSmallMax detections take the LDS path; the pair tests grow with the
+// square of the frame, so larger frames spread their search over the whole grid instead
+// (frames of 300-530 detections in one workgroup each: cam20_4k 55 -> 124 us).
+constexpr int kSmallMax = 256;
+constexpr int kSmallRows = 256;  // row bits (at least kSmallMax, a multiple of 64)
+static_assert(kSmallMax <= kSmallRows && kSmallRows <= kSmallFrame, "one detection per thread");
+
+template <int kN>
+__device__ void small_frame(const MergeParams &P, int lo, int n, SmallFrameLds<kN> &S) {
+  constexpr int kWords = kN / 32;
+  const int i = threadIdx.x, lane = i & 63, wave = i >> 6;
+  const bool mine = i < n;  // n <= kN <= the workgroup's threads
+  float4 box = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  uint64_t key = ~uint64_t(0);
+  int roi = 0;
+  if (mine) {
+    box = P.rbox[lo + i];
+    key = P.rkey[lo + i];
+    roi = P.rroi[lo + i];
+  }
+  if (i < kN) {
+    S.box[i] = box;
+    S.key[i] = key;
+    S.roi[i] = roi;
+  }
+  __syncthreads();
+  if (mine) {
+    uint32_t word = 0;
+    for (int j0 = 0; j0 < n; j0 += 4) {
+      float4 qb[4];
+      uint64_t qk[4];
+      int qr[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = min(j0 + u, n - 1);
+        qb[u] = S.box[j];
+        qk[u] = S.key[j];
+        qr[u] = S.roi[j];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool c = j0 + u < n && qk[u] < key && !(P.cross_only && qr[u] == roi) &&
+                       suppresses(qb[u], box, P.thr);
+        word |= static_cast<uint32_t>(c) << ((j0 + u) & 31);
+      }
+      if (((j0 + 4) & 31) == 0 || j0 + 4 >= n) {  // words past n stay unset, masks are 0 there
+        S.sup[i][j0 >> 5] = word;
+        word = 0;
+      }
+    }
+  }
+  int st = mine ? kUndecided : kSuppressed;
+  bool overrun = false;
+  for (int round = 0;; ++round) {
+    const uint64_t kb = __ballot(st == kKept), ob = __ballot(st == kUndecided);
+    if (lane == 0 && wave < kN / 64) {
+      S.kept[2 * wave] = static_cast<uint32_t>(kb);
+      S.kept[2 * wave + 1] = static_cast<uint32_t>(kb >> 32);
+      S.open[2 * wave] = static_cast<uint32_t>(ob);
+      S.open[2 * wave + 1] = static_cast<uint32_t>(ob >> 32);
+    }
+    if (!__syncthreads_or(st == kUndecided)) break;
+    if (round > n) {  // each round decides the best-ranked undecided detection
+      overrun = true;
+      break;
+    }
+    if (st == kUndecided) {
+      bool any_kept = false, any_open = false;
+#pragma unroll
+      for (int w = 0; w < kWords; ++w) {
+        const uint32_t r = S.sup[i][w];
+        any_kept = any_kept || (r & S.kept[w]) != 0;
+        any_open = any_open || (r & S.open[w]) != 0;
+      }
+      st = any_kept ? kSuppressed : (any_open ? kUndecided : kKept);
+    }
+    __syncthreads();  // every row has been tested before the masks are rewritten
+  }
+  if (mine) {
+    P.keep[P.grouped[lo + i]] = st == kKept ? 1 : 0;
+    P.rcell[lo + i] = kEmpty;
+  }
+  if (overrun && i == 0) *P.status = 1;
+}
+
 template <int kFrameThreads>
 __global__ __launch_bounds__(kFrameThreads) void index_kernel(const MergeParams P) {
-  __shared__ FrameLds S;
+  __shared__ union {
+    FrameLds f;
+    SmallFrameLds<kSmallRows> s;
+  } U;
+  FrameLds &S = U.f;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lo = P.frame_begin[blockIdx.x];
   const int n = P.frame_begin[blockIdx.x + 1] - lo;
   if (n <= 0) return;
+  if (n <= kSmallMax) {
+    small_frame<kSmallRows>(P, lo, n, U.s);
+    return;
+  }
   const int64_t ent0 = static_cast<int64_t>(kCellsMax) * lo;  // the frame's list entries
 
   // the frame's extent and mean box size
@@ -622,12 +735,13 @@ __device__ __forceinline__ int32_t decide_searching(const MergeParams &P, int a)
 }
 
 // The rounds of one frame, then its keep flags.
+// (frames of at most kSmallMax detections were decided by index_kernel)
 template <int kResolveThreads>
 __global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergeParams P) {
   const int tid = threadIdx.x;
   const int lo = P.frame_begin[blockIdx.x];
   const int n = P.frame_begin[blockIdx.x + 1] - lo;
-  if (n <= 0) return;
+  if (n <= kSmallMax) return;
   constexpr int kRes = 4;  // detections per thread and step, their loads issued together
   for (int round = 0;; ++round) {
     int pending = 0;

@@ -126,13 +126,25 @@ def test_large_frames_special_boxes(torch):
 
 
 def test_frames_around_the_matrix_limit(torch):
-    """Frames of 437, 439, 448 and 513 detections side by side."""
+    """Frames of 437, 439, 448, 512 and 513 detections side by side (through the spatial
+    index: frames of up to 256 detections are decided in one workgroup's LDS)."""
     rng = np.random.default_rng(12)
-    sizes = [437, 439, 448, 513]
+    sizes = [437, 439, 448, 512, 513]
     dets, scores = random_dets(rng, sum(sizes), len(sizes), 8, span=400.0)
     dets["frame"] = np.repeat(np.arange(len(sizes)), sizes)
     check(torch, dets, scores, len(sizes), 0.4, True)
     check(torch, dets, scores, len(sizes), 0.6, False)
+
+
+def test_frames_around_the_small_workgroup_limit(torch):
+    """Frames averaging at most 256 detections take 256-thread workgroups: frames of 256
+    are decided in LDS, of 257 through the spatial index, side by side."""
+    rng = np.random.default_rng(14)
+    sizes = [256, 257, 40, 1, 0, 120]
+    dets, scores = random_dets(rng, sum(sizes), len(sizes), 6, span=250.0)
+    dets["frame"] = np.repeat(np.arange(len(sizes)), sizes)
+    check(torch, dets, scores, len(sizes), 0.45, True)
+    check(torch, dets, scores, len(sizes), 0.5, False)
 
 
 def test_many_frames(torch):
