@@ -89,6 +89,71 @@ def calib_copy(mb: int, steps: int):
                       "read_plus_write_gbs": round(2 * n / us / 1e3, 1)}), flush=True)
 
 
+class TimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence: recording it
+    performs no system-scope cache writeback and invalidation. An event torch creates does,
+    and the GPU then idles about 5.7 us after it before the next kernel (kernel trace),
+    which would charge each step for the measurement. Completion order is unchanged, so
+    synchronize() still returns once the work recorded before the event has finished (all
+    the host needs from it: the pinned staging read by the upload is free again); the
+    timed region itself ends with a full device synchronisation. Made through the HIP
+    runtime the process already uses (torch's), so that its streams are valid here."""
+    _hip = None
+
+    @classmethod
+    def hip(cls):
+        if cls._hip is None:
+            import ctypes
+
+            path = next((ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64" in ln),
+                        None)
+            if path is None:
+                raise RuntimeError("the HIP runtime is not loaded")
+            h = ctypes.CDLL(path)
+            h.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                              ctypes.c_void_p]
+            h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = h
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+
+        self.ev = ctypes.c_void_p()
+        rc = self.hip().hipEventCreateWithFlags(ctypes.byref(self.ev), 0x20000000)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags: {rc}")
+
+    def record(self, stream):
+        import ctypes
+
+        rc = self.hip().hipEventRecord(self.ev, ctypes.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord: {rc}")
+
+    def synchronize(self):
+        rc = self.hip().hipEventSynchronize(self.ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventSynchronize: {rc}")
+
+    def elapsed_time(self, end) -> float:
+        """Milliseconds from this event to `end`."""
+        import ctypes
+
+        ms = ctypes.c_float()
+        rc = self.hip().hipEventElapsedTime(ctypes.byref(ms), self.ev, end.ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime: {rc}")
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and self.ev:
+            self._hip.hipEventDestroy(self.ev)
+
+
 def xcd_order(n: int) -> np.ndarray:
     """A launch order of n stitch units in which XCD x (the workgroups b with b % 8 == x,
     dealt round-robin by the dispatcher) runs one contiguous block of units in address
@@ -622,9 +687,9 @@ def main():
         tg.plan_upload(staging[buf], plan_d, stream)  # one kernel reading the pinned buffer
         # Two timing events per step, one before the step's first tg_stitch launch (it also
         # marks the staging upload as done) and one after its last: every event recorded
-        # between two kernels leaves the GPU idle for a few microseconds, so none is put
-        # between the launches themselves.
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        # between two kernels can leave the GPU idle for a few microseconds, so none is put
+        # between the launches themselves (and they are made without a system fence).
+        evs = [TimingEvent() for _ in range(2)]
         evs[0].record(stream)
         upload_done[buf] = evs[0]
         h = tg._vp(stream.cuda_stream)
