@@ -45,7 +45,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="cam20_4k")
     ap.add_argument("--policy", type=int, default=0, help="0 shelf FFDH, 1 shelf arrival, 2 guillotine")
     ap.add_argument("--unit-order", choices=["natural", "xcd"], default="natural",
@@ -78,7 +78,7 @@ def calib_copy(mb: int, steps: int):
     for i in range(2):
         dst[i].copy_(src[i])
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs = [TimingEvent() for _ in range(steps + 1)]
     evs[0].record(stream)
     for i in range(steps):
         dst[i & 1].copy_(src[i & 1])
@@ -294,7 +294,7 @@ def partition_cost(tg, W, torch, with_oracle: bool, launches: int = 50):
     for _ in range(3):
         tg.lib().tg_partition(tg.ctypes.byref(a), h)
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs = [TimingEvent() for _ in range(launches + 1)]
     evs[0].record(stream)
     for i in range(launches):
         rc = tg.lib().tg_partition(tg.ctypes.byref(a), h)
@@ -338,7 +338,7 @@ def merge_cost(tg, W, torch, uargs, ubufs, name, n_frames, with_oracle: bool,
     for _ in range(3):
         tg.lib().tg_merge(tg.ctypes.byref(a), h)
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs = [TimingEvent() for _ in range(launches + 1)]
     evs[0].record(stream)
     for i in range(launches):
         rc = tg.lib().tg_merge(tg.ctypes.byref(a), h)
@@ -389,7 +389,7 @@ def gmm_cost(tg, W, torch, with_oracle: bool, warm: int = 8, launches: int = 8):
         update(t)
     used = torch.zeros(launches + 1, dtype=torch.int64, device="cuda")
     used[0] = model.modes[:n].sum(dtype=torch.int64)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    evs = [(TimingEvent(), TimingEvent())
            for _ in range(launches)]
     for i in range(launches):
         evs[i][0].record(stream)
@@ -416,7 +416,7 @@ def gmm_cost(tg, W, torch, with_oracle: bool, warm: int = 8, launches: int = 8):
     for _ in range(2):
         tg.lib().tg_mask_rois(tg.ctypes.byref(ra), h)
     torch.cuda.synchronize()
-    mevs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    mevs = [TimingEvent() for _ in range(launches + 1)]
     mevs[0].record(stream)
     for i in range(launches):
         rc = tg.lib().tg_mask_rois(tg.ctypes.byref(ra), h)
@@ -514,7 +514,7 @@ def replay_ceiling(torch, frames_d, rois, plan, batches, out, canvas, stitch_us,
     for i in range(4):
         launch(i)
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs = [TimingEvent() for _ in range(launches + 1)]
     evs[0].record(stream)
     for i in range(launches):
         launch(i)
@@ -561,7 +561,7 @@ def stream_ceiling(torch, read_bytes: int, write_bytes: int, launches: int = 40)
             for i in range(4):
                 launch(i)
             torch.cuda.synchronize()
-            evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+            evs = [TimingEvent() for _ in range(launches + 1)]
             evs[0].record(stream)
             for i in range(launches):
                 launch(i)
@@ -589,7 +589,7 @@ def unstitch_cost(tg, torch, uargs, n_boxes, launches: int = 50):
     for _ in range(3):
         tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
     torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    evs = [TimingEvent() for _ in range(launches + 1)]
     evs[0].record(stream)
     for i in range(launches):
         rc = tg.lib().tg_unstitch(tg.ctypes.byref(uargs), h)
