@@ -58,8 +58,9 @@ struct MergeParams {
   int32_t *keep;
   tg_det *out;
   int32_t *n_kept;
-  int32_t *counts;       // [n_frames]
-  int32_t *cursor;       // [n_frames]
+  int32_t *counts;       // frame f at [f * cstride]
+  int32_t *cursor;       // frame f at [f * cstride]
+  int32_t cstride;       // kCounterStride, or 1 for very many frames
   int32_t *frame_begin;  // [n_frames + 1]
   int32_t *grouped;      // [n_max]
   uint32_t *ticket;
@@ -88,10 +89,17 @@ __device__ __forceinline__ int count_of(const MergeParams &P) {
   return min(max(*P.n_dets, 0), P.n_max);
 }
 
-__global__ void clear_kernel(MergeParams P, int32_t n_words32, int32_t n_words64) {
+// Frame counters one 256-byte slot apart: the count and scatter passes add to them with
+// global atomics (many detections per frame), and counters packed into a few cache lines
+// queue on those lines (window_64x30, 1,920 frames: count 20 us, scatter 33 us packed).
+constexpr int kCounterStride = 64;      // int32 words
+constexpr int kPaddedFramesMax = 16384; // beyond: packed (4 MB of slots at most)
+
+__global__ void clear_kernel(MergeParams P, int32_t n_frames, int32_t n_words64) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n_words32) {
-    P.counts[i] = 0;  // counts and cursor are contiguous
+  if (i < n_frames) {
+    P.counts[static_cast<int64_t>(i) * P.cstride] = 0;
+    P.cursor[static_cast<int64_t>(i) * P.cstride] = 0;
   }
   if (i < n_words64) reinterpret_cast<uint64_t *>(P.ticket)[i] = 0;  // ticket, cursor, states
 }
@@ -112,14 +120,14 @@ __global__ __launch_bounds__(kThreads) void count_kernel(const MergeParams P) {
   if (i < count_of(P)) {
     const int f = P.dets[i].frame;
     if (f >= 0 && f < P.n_frames)
-      atomicAdd(local ? &hist[f] : &P.counts[f], 1);
+      atomicAdd(local ? &hist[f] : &P.counts[static_cast<int64_t>(f) * P.cstride], 1);
     else
       P.keep[i] = 0;  // no frame to merge in: dropped
   }
   if (!local) return;
   __syncthreads();
   for (int f = tid; f < P.n_frames; f += kThreads)
-    if (hist[f]) atomicAdd(&P.counts[f], hist[f]);
+    if (hist[f]) atomicAdd(&P.counts[static_cast<int64_t>(f) * P.cstride], hist[f]);
 }
 
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const MergeParams P) {
@@ -128,7 +136,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const MergeParams P)
   int carry = 0;
   for (int base = 0; base < P.n_frames; base += kScanThreads) {
     const int f = base + tid;
-    const int v = f < P.n_frames ? P.counts[f] : 0;
+    const int v = f < P.n_frames ? P.counts[static_cast<int64_t>(f) * P.cstride] : 0;
     int incl = v;
     for (int o = 1; o < 64; o <<= 1) {
       const int t = __shfl_up(incl, o);
@@ -179,12 +187,13 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MergeParams P) 
     else if (local)
       rank = atomicAdd(&hist[f], 1);
     else
-      pos = P.frame_begin[f] + atomicAdd(&P.cursor[f], 1);
+      pos = P.frame_begin[f] + atomicAdd(&P.cursor[static_cast<int64_t>(f) * P.cstride], 1);
   }
   if (local) {
     __syncthreads();
     for (int g = tid; g < P.n_frames; g += kThreads)  // this workgroup's range of frame g
-      if (hist[g]) hist[g] = P.frame_begin[g] + atomicAdd(&P.cursor[g], hist[g]);
+      if (hist[g])
+        hist[g] = P.frame_begin[g] + atomicAdd(&P.cursor[static_cast<int64_t>(g) * P.cstride], hist[g]);
     __syncthreads();
     if (f >= 0) pos = hist[f] + rank;
   }
@@ -989,6 +998,8 @@ __global__ void zero_kernel(int32_t *a) { *a = 0; }
 
 int compact_blocks(int32_t n_max) { return (n_max + kCompactBlock - 1) / kCompactBlock; }
 
+int counter_stride(int32_t n_frames) { return n_frames <= kPaddedFramesMax ? kCounterStride : 1; }
+
 // Workspace layout, in bytes from the (16-byte aligned) start.
 struct Layout {
   size_t state, counts, cursor, begin, grouped;
@@ -1002,8 +1013,9 @@ Layout layout(int32_t n_max, int32_t n_frames) {
   // workgroup
   L.state = 0;
   L.counts = sizeof(uint64_t) * (2 + static_cast<size_t>(compact_blocks(n_max)));
-  L.cursor = L.counts + sizeof(int32_t) * static_cast<size_t>(n_frames);
-  L.begin = L.cursor + sizeof(int32_t) * static_cast<size_t>(n_frames);
+  const size_t slots = static_cast<size_t>(n_frames) * counter_stride(n_frames);
+  L.cursor = L.counts + sizeof(int32_t) * slots;
+  L.begin = L.cursor + sizeof(int32_t) * slots;
   L.grouped = L.begin + sizeof(int32_t) * (static_cast<size_t>(n_frames) + 1);
   L.rbox = round16(L.grouped + sizeof(int32_t) * n);
   L.rkey = L.rbox + sizeof(float4) * n;
@@ -1065,6 +1077,7 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   P.state = reinterpret_cast<uint64_t *>(ws + L.state) + 2;
   P.counts = reinterpret_cast<int32_t *>(ws + L.counts);
   P.cursor = reinterpret_cast<int32_t *>(ws + L.cursor);
+  P.cstride = counter_stride(a->n_frames);
   P.frame_begin = reinterpret_cast<int32_t *>(ws + L.begin);
   P.grouped = reinterpret_cast<int32_t *>(ws + L.grouped);
   P.rkey = reinterpret_cast<uint64_t *>(ws + L.rkey);
@@ -1085,12 +1098,11 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
     hipLaunchKernelGGL(tiny_kernel, dim3(1), dim3(kTiny), 0, s, P);
     return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
   }
-  const int32_t words32 = 2 * a->n_frames;  // counts + cursor
   const int32_t words64 = 2 + compact_blocks(a->n_max);
-  const int32_t clear_n = words32 > words64 ? words32 : words64;
+  const int32_t clear_n = a->n_frames > words64 ? a->n_frames : words64;
   const uint32_t per = static_cast<uint32_t>((a->n_max + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(clear_kernel, dim3((clear_n + kThreads - 1) / kThreads), dim3(kThreads), 0,
-                     s, P, words32, words64);
+                     s, P, a->n_frames, words64);
   hipLaunchKernelGGL(count_kernel, dim3(per), dim3(kThreads), 0, s, P);
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, s, P);
   hipLaunchKernelGGL(scatter_kernel, dim3(per), dim3(kThreads), 0, s, P);
