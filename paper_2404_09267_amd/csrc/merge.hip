@@ -66,6 +66,7 @@ struct MergeParams {
   uint32_t *ticket;
   uint32_t *status;      // set when a frame's rounds overrun (cannot happen)
   uint64_t *state;       // [compaction workgroups]
+  uint32_t *big;         // set when a frame is too large for its index workgroup alone
   // Per detection, at its position in its frame group: frame f (first detection lo, n of
   // them) owns [lo, lo + n) of these (times kCellsMax for the cell lists), so frames
   // never share a word.
@@ -101,7 +102,8 @@ __global__ void clear_kernel(MergeParams P, int32_t n_frames, int32_t n_words64)
     P.counts[static_cast<int64_t>(i) * P.cstride] = 0;
     P.cursor[static_cast<int64_t>(i) * P.cstride] = 0;
   }
-  if (i < n_words64) reinterpret_cast<uint64_t *>(P.ticket)[i] = 0;  // ticket, cursor, states
+  // ticket and status, the overflow cursor, the large-frame flag, the look-back states
+  if (i < n_words64) reinterpret_cast<uint64_t *>(P.ticket)[i] = 0;
 }
 
 // Detections per frame. Up to kHistMax frames a workgroup first counts in LDS and then
@@ -257,6 +259,9 @@ constexpr int kOvfPerDet = 16;  // overflow area for longer lists: kOvfPerDet n_
 constexpr int kScanLanes = 8;  // lanes per detection in the search
 constexpr int kBatch = 8;      // list entries whose loads a lane issues together
 constexpr int kSearchDets = kThreads / kScanLanes;  // detections per search workgroup
+// Workgroups of the search and of the rounds: they step through detections and frames, so
+// that inputs whose frames were all decided in LDS pay for a small launch only.
+constexpr int kGridCap = 2048;
 
 __device__ __forceinline__ float wave_minf(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o));
@@ -296,8 +301,8 @@ constexpr int kIdx = 4;  // detections per thread and step of the index, loads i
 // boxes per step) for the suppressors ranked above it, a row of bits per detection; the
 // rounds run on those rows (masks of kept and undecided detections rebuilt from ballots
 // each round); the keep flags are written at once. The frame's detections are marked
-// kEmpty, so the search passes them by, and the resolve workgroup of the frame returns at
-// once.
+// kEmpty, so the search passes them by, and the rounds skip the frame; when no frame is
+// larger, both return at once.
 template <int kN>
 struct SmallFrameLds {
   float4 box[kN];
@@ -407,6 +412,7 @@ __global__ __launch_bounds__(kFrameThreads) void index_kernel(const MergeParams 
     small_frame<kSmallRows>(P, lo, n, U.s);
     return;
   }
+  if (tid == 0) *P.big = 1;  // the search and the rounds have work
   const int64_t ent0 = static_cast<int64_t>(kCellsMax) * lo;  // the frame's list entries
 
   // the frame's extent and mean box size
@@ -659,12 +665,11 @@ __device__ __forceinline__ uint32_t search_step(const MergeParams &P, const List
 // a workgroup whose detections have more reserves room for their whole lists in the
 // overflow area (one atomic for all of them) and searches those again to fill it; a
 // list that does not fit is left to be searched in the rounds.
-__global__ __launch_bounds__(kThreads) void search_kernel(const MergeParams P) {
-  static_assert(kSearchDets * kScanLanes == kThreads, "whole detections per workgroup");
+__device__ __forceinline__ void search_block(const MergeParams &P, int blk, int n_grouped) {
   __shared__ int s_np[kSearchDets], s_fill[kSearchDets], s_at[kSearchDets];
   const int tid = threadIdx.x, j = tid / kScanLanes, sub = tid % kScanLanes;
-  const int a = blockIdx.x * kSearchDets + j;
-  const bool valid = a < P.frame_begin[P.n_frames] && P.rcell[a] != kEmpty;
+  const int a = blk * kSearchDets + j;
+  const bool valid = a < n_grouped && P.rcell[a] != kEmpty;
   if (sub == 0) {
     s_np[j] = 0;
     s_fill[j] = 0;
@@ -717,6 +722,17 @@ __global__ __launch_bounds__(kThreads) void search_kernel(const MergeParams P) {
   }
 }
 
+__global__ __launch_bounds__(kThreads) void search_kernel(const MergeParams P) {
+  static_assert(kSearchDets * kScanLanes == kThreads, "whole detections per workgroup");
+  if (!*P.big) return;  // every frame was decided in its index workgroup
+  const int n_grouped = P.frame_begin[P.n_frames];
+  const int n_blocks = (n_grouped + kSearchDets - 1) / kSearchDets;
+  for (int blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
+    __syncthreads();  // the previous block's readers of s_np, s_fill and s_at are done
+    search_block(P, blk, n_grouped);
+  }
+}
+
 // This round's decision for an undecided detection a with more suppressors than its
 // kPredSlots and no room for them in the overflow area (many boxes crowded on one spot):
 // its lists searched again, kBatch candidates at a time -- kSuppressed when one of its
@@ -746,11 +762,8 @@ __device__ __forceinline__ int32_t decide_searching(const MergeParams &P, int a)
 // The rounds of one frame, then its keep flags.
 // (frames of at most kSmallMax detections were decided by index_kernel)
 template <int kResolveThreads>
-__global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergeParams P) {
+__device__ __forceinline__ void resolve_frame(const MergeParams &P, int lo, int n) {
   const int tid = threadIdx.x;
-  const int lo = P.frame_begin[blockIdx.x];
-  const int n = P.frame_begin[blockIdx.x + 1] - lo;
-  if (n <= kSmallMax) return;
   constexpr int kRes = 4;  // detections per thread and step, their loads issued together
   for (int round = 0;; ++round) {
     int pending = 0;
@@ -827,6 +840,16 @@ __global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergePar
   }
   for (int a = lo + tid; a < lo + n; a += kResolveThreads)
     P.keep[P.grouped[a]] = P.rstate[a] == kKept ? 1 : 0;
+}
+
+template <int kResolveThreads>
+__global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergeParams P) {
+  if (!*P.big) return;  // every frame was decided in its index workgroup
+  for (int f = blockIdx.x; f < P.n_frames; f += gridDim.x) {
+    const int lo = P.frame_begin[f];
+    const int n = P.frame_begin[f + 1] - lo;
+    if (n > kSmallMax) resolve_frame<kResolveThreads>(P, lo, n);
+  }
 }
 
 // ---- small inputs: one workgroup, one launch ------------------------------------------
@@ -1012,7 +1035,7 @@ Layout layout(int32_t n_max, int32_t n_frames) {
   // ticket and status word, the overflow area's cursor, one look-back word per compaction
   // workgroup
   L.state = 0;
-  L.counts = sizeof(uint64_t) * (2 + static_cast<size_t>(compact_blocks(n_max)));
+  L.counts = sizeof(uint64_t) * (3 + static_cast<size_t>(compact_blocks(n_max)));
   const size_t slots = static_cast<size_t>(n_frames) * counter_stride(n_frames);
   L.cursor = L.counts + sizeof(int32_t) * slots;
   L.begin = L.cursor + sizeof(int32_t) * slots;
@@ -1074,7 +1097,8 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
   P.ticket = reinterpret_cast<uint32_t *>(ws + L.state);
   P.status = reinterpret_cast<uint32_t *>(ws + L.state) + 1;
   P.ovf_used = reinterpret_cast<unsigned long long *>(ws + L.state) + 1;
-  P.state = reinterpret_cast<uint64_t *>(ws + L.state) + 2;
+  P.big = reinterpret_cast<uint32_t *>(ws + L.state) + 4;
+  P.state = reinterpret_cast<uint64_t *>(ws + L.state) + 3;
   P.counts = reinterpret_cast<int32_t *>(ws + L.counts);
   P.cursor = reinterpret_cast<int32_t *>(ws + L.cursor);
   P.cstride = counter_stride(a->n_frames);
@@ -1098,7 +1122,7 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
     hipLaunchKernelGGL(tiny_kernel, dim3(1), dim3(kTiny), 0, s, P);
     return hipGetLastError() == hipSuccess ? TG_OK : TG_E_HIP;
   }
-  const int32_t words64 = 2 + compact_blocks(a->n_max);
+  const int32_t words64 = 3 + compact_blocks(a->n_max);
   const int32_t clear_n = a->n_frames > words64 ? a->n_frames : words64;
   const uint32_t per = static_cast<uint32_t>((a->n_max + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(clear_kernel, dim3((clear_n + kThreads - 1) / kThreads), dim3(kThreads), 0,
@@ -1113,13 +1137,14 @@ extern "C" int tg_merge(const tg_merge_args *a, void *stream) {
       hipLaunchKernelGGL(index_kernel<kSmallFrame>, frames, dim3(kSmallFrame), 0, s, P);
     else
       hipLaunchKernelGGL(index_kernel<1024>, frames, dim3(1024), 0, s, P);
-    hipLaunchKernelGGL(search_kernel,
-                       dim3(static_cast<uint32_t>((a->n_max + kSearchDets - 1) / kSearchDets)),
+    const int search_blocks = (a->n_max + kSearchDets - 1) / kSearchDets;
+    hipLaunchKernelGGL(search_kernel, dim3(static_cast<uint32_t>(std::min(search_blocks, kGridCap))),
                        dim3(kThreads), 0, s, P);
+    const dim3 resolve(static_cast<uint32_t>(std::min(a->n_frames, kGridCap)));
     if (small)
-      hipLaunchKernelGGL(resolve_kernel<kSmallFrame>, frames, dim3(kSmallFrame), 0, s, P);
+      hipLaunchKernelGGL(resolve_kernel<kSmallFrame>, resolve, dim3(kSmallFrame), 0, s, P);
     else
-      hipLaunchKernelGGL(resolve_kernel<512>, frames, dim3(512), 0, s, P);
+      hipLaunchKernelGGL(resolve_kernel<512>, resolve, dim3(512), 0, s, P);
   }
   hipLaunchKernelGGL(compact_kernel, dim3(static_cast<uint32_t>(compact_blocks(a->n_max))),
                      dim3(kThreads), 0, s, P);

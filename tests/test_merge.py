@@ -172,22 +172,22 @@ def test_merge_argument_checks():
     assert call(workspace_bytes=a.workspace_bytes - 1) == tg.E_WORKSPACE
     assert call(workspace=0x8008) == tg.E_WORKSPACE  # not 16-byte aligned
     assert L.tg_merge_workspace_bytes(0, 4) == 0
-    # ticket and status, the overflow cursor, one look-back word (24), counts and cursors
-    # one 256-byte slot apart (3 + 3 slots of 64 int32), starts (4 int32), grouped ids
-    # (4 n); then, 16-byte aligned, per detection its
-    # box (16), ranking key (8), patch id, cell range and state (4 each), its lists to
+    # ticket and status, the overflow cursor, the large-frame flag, one look-back word
+    # (32), counts and cursors one 256-byte slot apart (3 + 3 slots of 64 int32), starts
+    # (4 int32), grouped ids (4 n); then, 16-byte aligned, per detection its box (16),
+    # ranking key (8), patch id, cell range and state (4 each), its lists to
     # search (5 starts and 5 sizes: 40), 16 suppressors in place, their count and the
     # start of a longer list (72), and 16 entries of the overflow area (64); then, 16-byte
     # aligned, the cell lists (4 n entries of a box and an int4: 32 bytes)
     n = 1024
-    small = 8 * 3 + 4 * (64 * (3 + 3) + 4) + 4 * n
+    small = 8 * 4 + 4 * (64 * (3 + 3) + 4) + 4 * n
     per_det = 16 + 8 + 4 + 4 + 4 + 40 + 72 + 64
     assert L.tg_merge_workspace_bytes(n, 3) == \
         ((small + 15) // 16 * 16 + per_det * n + 15) // 16 * 16 + 4 * 32 * n
     # past 16,384 frames the counters are packed, one int32 each
-    packed = 8 * 3 + 4 * (2 * 20000 + 20001) + 4 * n
+    packed = 8 * 4 + 4 * (2 * 20000 + 20001) + 4 * n
     assert L.tg_merge_workspace_bytes(n, 20000) == \
         ((packed + 15) // 16 * 16 + per_det * n + 15) // 16 * 16 + 4 * 32 * n
-    padded = 8 * 3 + 4 * (64 * 2 * 16384 + 16385) + 4 * n
+    padded = 8 * 4 + 4 * (64 * 2 * 16384 + 16385) + 4 * n
     assert L.tg_merge_workspace_bytes(n, 16384) == \
         ((padded + 15) // 16 * 16 + per_det * n + 15) // 16 * 16 + 4 * 32 * n

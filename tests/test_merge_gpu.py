@@ -154,6 +154,32 @@ def test_many_frames(torch):
     check(torch, dets, scores, 5000, 0.5, True)
 
 
+def test_many_frames_with_large_ones(torch):
+    """3,000 frames of 25 detections with four of 257-600 among them, the large ones on
+    both sides of frame 2048 (the rounds step through frames 2048 apart) and more than
+    65,536 detections (the search steps through them 65,536 apart). Frames are merged
+    independently, so the oracle checks the large frames and 200 others on their own; the
+    compacted output is the kept detections in input order."""
+    from oracle import merge
+
+    rng = np.random.default_rng(15)
+    sizes = np.full(3000, 25)
+    big = [5, 2100, 2101, 2999]
+    sizes[big] = [300, 400, 257, 600]
+    dets, scores = random_dets(rng, int(sizes.sum()), 3000, 6, span=300.0)
+    dets["frame"] = np.repeat(np.arange(3000), sizes)
+    dets = dets[rng.permutation(len(dets))]
+    say("merge, many frames with large ones", len(dets))
+    keep, kept, n_kept = run_gpu(torch, dets, scores, 3000, 0.5, True)
+    frames = np.r_[big, rng.choice(np.setdiff1d(np.arange(3000), big), 200, replace=False)]
+    sub = np.nonzero(np.isin(dets["frame"], frames))[0]
+    want_keep, _ = merge.merge(dets[sub], scores, 3000, 0.5, True)
+    np.testing.assert_array_equal(keep[sub], want_keep.astype(np.int32))
+    assert set(np.unique(keep)) <= {0, 1}
+    assert n_kept == int(keep.sum())
+    np.testing.assert_array_equal(kept.view(np.int32), dets[keep == 1].view(np.int32))
+
+
 def test_partial_count_and_empty(torch):
     rng = np.random.default_rng(4)
     dets, scores = random_dets(rng, 800, 5, 4)
