@@ -207,15 +207,27 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const MergeParams P) 
   P.rroi[pos] = d.roi;
 }
 
-// Whether box a suppresses box b (x1, y1, x2, y2 in .x .y .z .w).
-__device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
+// Area of a box (x1, y1, x2, y2 in .x .y .z .w), empty and inverted boxes 0.
+__device__ __forceinline__ float box_area(float4 a) {
+  return __fmul_rn(fmaxf(0.0f, __fsub_rn(a.z, a.x)), fmaxf(0.0f, __fsub_rn(a.w, a.y)));
+}
+
+// Whether boxes a and b, of areas area_a and area_b, overlap by more than thr of their
+// union. The result does not depend on the order of a and b: the minima and maxima, the
+// product and the sum are commutative, NaN operands included, and a difference of zeros
+// differs in sign only, which no comparison sees.
+__device__ __forceinline__ bool overlap_above(float4 a, float4 b, float area_a, float area_b,
+                                              float thr) {
   const float w = fmaxf(0.0f, __fsub_rn(fminf(a.z, b.z), fmaxf(a.x, b.x)));
   const float h = fmaxf(0.0f, __fsub_rn(fminf(a.w, b.w), fmaxf(a.y, b.y)));
   const float inter = __fmul_rn(w, h);
-  const float area_a = __fmul_rn(fmaxf(0.0f, __fsub_rn(a.z, a.x)), fmaxf(0.0f, __fsub_rn(a.w, a.y)));
-  const float area_b = __fmul_rn(fmaxf(0.0f, __fsub_rn(b.z, b.x)), fmaxf(0.0f, __fsub_rn(b.w, b.y)));
   const float uni = __fsub_rn(__fadd_rn(area_a, area_b), inter);
   return inter > __fmul_rn(thr, uni);
+}
+
+// Whether box a suppresses box b when a is ranked above b.
+__device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
+  return overlap_above(a, b, box_area(a), box_area(b), thr);
 }
 
 // ---- the greedy of a frame, decided in rounds -----------------------------------------
@@ -308,6 +320,7 @@ struct SmallFrameLds {
   float4 box[kN];
   uint64_t key[kN];
   int32_t roi[kN];
+  float area[kN];
   uint32_t sup[kN][kN / 32 + 1];  // odd row stride: rows in distinct banks
   uint32_t kept[kN / 32], open[kN / 32];
 };
@@ -336,33 +349,45 @@ __device__ void small_frame(const MergeParams &P, int lo, int n, SmallFrameLds<k
     S.box[i] = box;
     S.key[i] = key;
     S.roi[i] = roi;
+    S.area[i] = box_area(box);
+#pragma unroll
+    for (int w = 0; w < kWords; ++w) S.sup[i][w] = 0;
   }
   __syncthreads();
+  // Each pair once: thread i tests the detections 1 .. n/2 places after it, cyclically (at
+  // n/2 exactly, for even n, only the first half of the threads), and the pair's bit goes
+  // into the row of whichever of the two is ranked below.
   if (mine) {
-    uint32_t word = 0;
-    for (int j0 = 0; j0 < n; j0 += 4) {
+    const float area = S.area[i];
+    const int last = (n % 2 == 0 && i < n / 2) ? n / 2 : (n - 1) / 2;
+    for (int d0 = 1; d0 <= last; d0 += 4) {
       float4 qb[4];
       uint64_t qk[4];
-      int qr[4];
+      int qr[4], qj[4];
+      float qa[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int j = min(j0 + u, n - 1);
-        qb[u] = S.box[j];
-        qk[u] = S.key[j];
-        qr[u] = S.roi[j];
+        const int j = i + min(d0 + u, last);  // < 2n
+        qj[u] = j >= n ? j - n : j;
+        qb[u] = S.box[qj[u]];
+        qk[u] = S.key[qj[u]];
+        qr[u] = S.roi[qj[u]];
+        qa[u] = S.area[qj[u]];
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const bool c = j0 + u < n && qk[u] < key && !(P.cross_only && qr[u] == roi) &&
-                       suppresses(qb[u], box, P.thr);
-        word |= static_cast<uint32_t>(c) << ((j0 + u) & 31);
-      }
-      if (((j0 + 4) & 31) == 0 || j0 + 4 >= n) {  // words past n stay unset, masks are 0 there
-        S.sup[i][j0 >> 5] = word;
-        word = 0;
+        if (d0 + u <= last && !(P.cross_only && qr[u] == roi) &&
+            overlap_above(qb[u], box, qa[u], area, P.thr)) {
+          const int j = qj[u];
+          if (qk[u] < key)
+            atomicOr(&S.sup[i][j >> 5], 1u << (j & 31));
+          else if (key < qk[u])
+            atomicOr(&S.sup[j][i >> 5], 1u << (i & 31));
+        }
       }
     }
   }
+  __syncthreads();
   int st = mine ? kUndecided : kSuppressed;
   bool overrun = false;
   for (int round = 0;; ++round) {

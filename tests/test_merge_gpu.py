@@ -147,6 +147,27 @@ def test_frames_around_the_small_workgroup_limit(torch):
     check(torch, dets, scores, len(sizes), 0.5, False)
 
 
+def test_small_frames_special_boxes(torch):
+    """Frames of 1-256 detections (decided in LDS, each pair of boxes tested once) with
+    NaN, infinite and signed-zero corners, inverted and empty boxes, duplicates of one box
+    and equal scores, for thresholds of both signs, with and without cross_only."""
+    rng = np.random.default_rng(23)
+    sizes = [1, 2, 3, 4, 63, 64, 65, 128, 129, 200, 255, 256]
+    dets, scores = random_dets(rng, sum(sizes), len(sizes), 4, span=120.0)
+    dets["frame"] = np.repeat(np.arange(len(sizes)), sizes)
+    k = rng.permutation(len(dets))
+    special = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0], np.float32)
+    for c in ("x1", "y1", "x2", "y2"):
+        pick = k[rng.integers(0, 150, 20)]
+        dets[c][pick] = rng.choice(special, 20)
+    dets["x1"][k[150:170]], dets["x2"][k[150:170]] = dets["x2"][k[150:170]], dets["x1"][k[150:170]]
+    dets["y2"][k[170:190]] = dets["y1"][k[170:190]]  # empty
+    for c in ("x1", "y1", "x2", "y2"):
+        dets[c][k[190:260]] = dets[c][k[190]]  # duplicates, spread over frames
+    for thr, cross in [(0.5, True), (0.3, False), (0.0, False), (-0.5, True), (1.0, False)]:
+        check(torch, dets, scores, len(sizes), thr, cross)
+
+
 def test_many_frames(torch):
     """More frames than the LDS histograms hold (4096): direct global counters."""
     rng = np.random.default_rng(13)
