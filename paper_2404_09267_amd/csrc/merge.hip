@@ -25,7 +25,7 @@
 //     them is kept and kept once all of them are suppressed (see "the greedy of a frame"
 //     for why this is the greedy walk's result and why the index finds every suppressor);
 //     a frame of at most kSmallMax detections is instead decided by its index workgroup
-//     in LDS, from every pair of its detections;
+//     in LDS, each pair of its detections tested once;
 //  8. stable compaction of the kept detections (decoupled look-back, 1024 per workgroup).
 // Inputs of at most kTiny detections (by capacity) take one launch instead (tiny_kernel).
 #include <hip/hip_runtime.h>
@@ -245,7 +245,9 @@ __device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
 //  search:  kScanLanes lanes per detection, over all detections at once, find its
 //           suppressors ranked above it in those lists (kPredSlots of them are kept; a
 //           detection with more is searched again when it is decided);
-//  resolve: one workgroup per frame runs the rounds on the suppressor lists.
+//  resolve: one workgroup per frame (stepping through the frames when there are more than
+//           kGridCap) runs the rounds on the suppressor lists.
+// Search and resolve return at once when no frame was too large for the LDS path.
 // Why the cells find every suppressor: with a threshold t >= 0, a suppresses b only if
 // inter > t * union >= 0 (a union is never negative), so inter > 0 and both clipped widths
 // are positive: min(x2a, x2b) > max(x1a, x1b) and likewise in y. The point
@@ -257,8 +259,8 @@ __device__ __forceinline__ bool suppresses(float4 a, float4 b, float thr) {
 // searching the whole frame. Boxes with x2 < x1 or y2 < y1 have no positive width with
 // anything, so when t >= 0 they neither suppress nor are suppressed: kept from the start
 // and listed nowhere.
-// index and resolve: one workgroup per frame, of 1024 threads (index) and 512 (resolve),
-// or of kSmallFrame when the frames average at most kSmallFrame detections
+// index and resolve: workgroups of 1024 threads (index) and 512 (resolve), or of
+// kSmallFrame when the frames average at most kSmallFrame detections
 constexpr int kSmallFrame = 256;
 constexpr int kGridMax = 32;         // cells per axis
 constexpr int kCellsMax = 4;         // cells a box may touch before it goes on the wide list
