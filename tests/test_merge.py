@@ -146,6 +146,24 @@ def test_oracle_closed_forms():
     assert not keep[dets["frame"] >= 2].any()  # frames outside [0, n_frames)
 
 
+def test_cyclic_pair_schedule_covers_each_pair_once():
+    """The LDS path of frames up to 256 detections tests each unordered pair once: thread i
+    takes the detections 1 .. last(i) places after it, cyclically, where last(i) is n/2 for
+    even n and i < n/2, else (n - 1)/2. Every pair of distinct detections must come up
+    exactly once, for every frame size."""
+    for n in range(1, 258):
+        seen = {}
+        for i in range(n):
+            last = n // 2 if (n % 2 == 0 and i < n // 2) else (n - 1) // 2
+            for d in range(1, last + 1):
+                j = i + d
+                j = j - n if j >= n else j
+                assert j != i and 0 <= j < n
+                key = (min(i, j), max(i, j))
+                seen[key] = seen.get(key, 0) + 1
+        assert len(seen) == n * (n - 1) // 2 and set(seen.values()) <= {1}, n
+
+
 def test_merge_argument_checks():
     L = tg.lib()
     a = tg.MergeArgs()
