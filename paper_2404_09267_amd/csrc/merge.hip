@@ -883,8 +883,8 @@ __global__ __launch_bounds__(kResolveThreads) void resolve_kernel(const MergePar
 //
 // Up to kTiny detections (n_max <= kTiny) are merged by one workgroup: each thread holds
 // one detection, its suppressors (ranked above it in the same frame, with cross_only from
-// another patch, and suppressing it) are a kTiny-bit row in LDS found by testing every
-// pair, the rounds above run on those rows (suppressed once a suppressor is kept, kept
+// another patch, and suppressing it) are a kTiny-bit row in LDS found by testing each
+// pair once, the rounds above run on those rows (suppressed once a suppressor is kept, kept
 // once all are suppressed), and a workgroup prefix sum writes the kept detections in input
 // order. On inputs this small the launches of the general path, not their work, are the
 // cost.
@@ -911,6 +911,7 @@ struct alignas(16) TinyDet {
 
 __global__ __launch_bounds__(kTiny) void tiny_kernel(const MergeParams P) {
   __shared__ TinyDet s_det[kTiny];
+  __shared__ float s_area[kTiny];
   __shared__ uint32_t s_sup[kTiny][kTinyWords + 1];  // odd row stride: rows in distinct banks
   __shared__ uint32_t s_kept[kTinyWords], s_open[kTinyWords];
   __shared__ int32_t s_wave[kTiny / 64];
@@ -926,30 +927,44 @@ __global__ __launch_bounds__(kTiny) void tiny_kernel(const MergeParams P) {
     key = rank_key(s, d.box);
   }
   const float4 box = make_float4(d.x1, d.y1, d.x2, d.y2);
+  const float area = box_area(box);
   s_det[i] = TinyDet{box, key, f, d.roi};
+  s_area[i] = area;
+#pragma unroll
+  for (int w = 0; w < kTinyWords; ++w) s_sup[i][w] = 0;
   __syncthreads();
 
-  // this detection's suppressors: four candidates per step, their records read first; a
-  // row word is stored when its 32 candidates are done (words past n stay unset, and
-  // are only ever tested against masks that are zero there)
+  // the suppressor rows, each pair tested once (as in the LDS path of small frames: thread
+  // i takes the detections 1 .. n/2 places after it, cyclically, four records per step,
+  // and the bit goes into the row of whichever of the two is ranked below); a pair with a
+  // detection outside the frames sets no bit, so such a thread skips its share
   if (f >= 0) {
-    uint32_t word = 0;
-    for (int j0 = 0; j0 < n; j0 += 4) {
+    const int last = (n % 2 == 0 && i < n / 2) ? n / 2 : (n - 1) / 2;
+    for (int d0 = 1; d0 <= last; d0 += 4) {
       TinyDet q[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) q[u] = s_det[min(j0 + u, n - 1)];
+      float qa[4];
+      int qj[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const bool c = j0 + u < n && q[u].frame == f && q[u].key < key &&
-                       !(P.cross_only && q[u].roi == d.roi) && suppresses(q[u].box, box, P.thr);
-        word |= static_cast<uint32_t>(c) << ((j0 + u) & 31);
+        const int j = i + min(d0 + u, last);  // < 2n
+        qj[u] = j >= n ? j - n : j;
+        q[u] = s_det[qj[u]];
+        qa[u] = s_area[qj[u]];
       }
-      if (((j0 + 4) & 31) == 0 || j0 + 4 >= n) {
-        s_sup[i][j0 >> 5] = word;
-        word = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (d0 + u <= last && q[u].frame == f && !(P.cross_only && q[u].roi == d.roi) &&
+            overlap_above(q[u].box, box, qa[u], area, P.thr)) {
+          const int j = qj[u];
+          if (q[u].key < key)
+            atomicOr(&s_sup[i][j >> 5], 1u << (j & 31));
+          else if (key < q[u].key)
+            atomicOr(&s_sup[j][i >> 5], 1u << (i & 31));
+        }
       }
     }
   }
+  __syncthreads();
 
   // rounds; a detection outside the frames is dropped (never kept, never a suppressor)
   int st = f >= 0 ? kUndecided : kSuppressed;
